@@ -1,0 +1,229 @@
+"""Seeded synthetic inputs for the FPO hot path.
+
+This module only draws random numbers and rounds them to the storage dtype.
+It holds none of the method's arithmetic (no softmax, no projection, no norm
+VJP, no outer products, no optimizer): the GPU path and the CPU oracle both
+receive exactly the arrays produced here, and nothing else is shared between
+them.
+
+Workloads (shapes follow the models the paper adapts, Sec. 4 "Models and target
+layers"; the last quarter of layers is the paper's model-level summary window,
+Sec. 2.3):
+
+  id  name           dtype  d     d_ff   V       T     L   targets
+  0   tiny-fp32      f32    256   688    4096    128   2   uniform
+  1   olmo2-7b       bf16   4096  11008  100352  2048  8   Zipf(1.1)
+  2   qwen3-8b       bf16   4096  12288  151936  4096  9   Zipf(1.1)
+  3   falcon3-7b     bf16   3072  23040  131072  4096  7   Zipf(1.1), 1% outlier channels x20
+  4   qwen3-8b-diag  bf16   4096  12288  151936  8192  36  Zipf(1.1), reference-gradient noise
+
+Distributions: final-norm input x ~ N(0,1); RMSNorm gain 1 + N(0, 0.1^2);
+W_U ~ N(0, 0.02^2); cached MLP activation a = SiLU(q) * u with q, u ~ N(0,1)
+(q and u are also the gate / up values the full-MLP mode differentiates
+through); down-projection masters ~ N(0, 0.02^2).
+
+Every tensor is drawn from its own counter-addressed stream:
+SeedSequence(entropy=260814563, spawn_key=(cfg, tensor, layer, block)), in
+blocks of 2**20 elements, so any block can be regenerated on its own and the
+result does not depend on the number of threads used to draw it.
+"""
+from __future__ import annotations
+
+import os
+from concurrent.futures import ThreadPoolExecutor
+from dataclasses import dataclass, replace
+
+import numpy as np
+
+ENTROPY = 260814563
+BLOCK = 1 << 20
+
+# tensor ids inside the spawn key
+T_X, T_GAMMA, T_WU, T_TARGETS, T_Q, T_U, T_W, T_OUTLIER, T_REFNOISE, T_XIN, T_W1, T_W2, T_G, T_STATE, T_MISC = range(15)
+
+
+@dataclass(frozen=True)
+class Config:
+    cid: int
+    name: str
+    dtype: str          # "f32" or "bf16": storage / operand dtype of the inputs
+    d: int
+    d_ff: int
+    V: int
+    T: int
+    L: int
+    zipf: bool
+    outliers: bool
+    diag: bool = False
+    eps: float = 1e-6
+    min_rms: float = 0.5
+    lr: float = 1e-4
+    clip_frac: float = 0.01
+
+    def shrink(self, **kw) -> "Config":
+        return replace(self, **kw)
+
+
+CONFIGS = {
+    0: Config(0, "tiny-fp32", "f32", 256, 688, 4096, 128, 2, zipf=False, outliers=False),
+    1: Config(1, "olmo2-7b", "bf16", 4096, 11008, 100352, 2048, 8, zipf=True, outliers=False),
+    2: Config(2, "qwen3-8b", "bf16", 4096, 12288, 151936, 4096, 9, zipf=True, outliers=False),
+    3: Config(3, "falcon3-7b", "bf16", 3072, 23040, 131072, 4096, 7, zipf=True, outliers=True),
+    4: Config(4, "qwen3-8b-diag", "bf16", 4096, 12288, 151936, 8192, 36, zipf=True, outliers=False, diag=True),
+}
+
+_POOL_WORKERS = max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def _rng(cfg: int, tensor: int, layer: int, block: int) -> np.random.Generator:
+    ss = np.random.SeedSequence(entropy=ENTROPY, spawn_key=(cfg, tensor, layer, block))
+    return np.random.Generator(np.random.PCG64(ss))
+
+
+def normal(cfg: int, tensor: int, layer: int, n: int, std: float = 1.0, mean: float = 0.0) -> np.ndarray:
+    """n float32 draws of N(mean, std^2) from the (cfg, tensor, layer) stream."""
+    out = np.empty(n, dtype=np.float32)
+    nblk = (n + BLOCK - 1) // BLOCK
+
+    def fill(b):
+        lo, hi = b * BLOCK, min(n, (b + 1) * BLOCK)
+        _rng(cfg, tensor, layer, b).standard_normal(hi - lo, dtype=np.float32, out=out[lo:hi])
+        if std != 1.0:
+            out[lo:hi] *= np.float32(std)
+        if mean != 0.0:
+            out[lo:hi] += np.float32(mean)
+
+    if nblk == 1:
+        fill(0)
+    else:
+        with ThreadPoolExecutor(_POOL_WORKERS) as ex:
+            list(ex.map(fill, range(nblk)))
+    return out
+
+
+def uniform01(cfg: int, tensor: int, layer: int, n: int) -> np.ndarray:
+    return _rng(cfg, tensor, layer, 0).random(n)
+
+
+# ---------------------------------------------------------------- rounding
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """float32 -> bfloat16 bit patterns (uint16), round to nearest even.
+    Inputs here are finite (no NaN handling needed)."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
+    return (bits.astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def to_storage(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Return the storage array: float32 as is, or bf16 bit patterns (uint16)."""
+    if dtype == "f32":
+        return np.ascontiguousarray(x, dtype=np.float32)
+    if dtype == "bf16":
+        return bf16_bits(x)
+    raise ValueError(dtype)
+
+
+def storage_to_f64(s: np.ndarray) -> np.ndarray:
+    """Exact upcast of a storage array to float64."""
+    if s.dtype == np.uint16:
+        return bf16_to_f32(s).astype(np.float64)
+    return s.astype(np.float64)
+
+
+# ---------------------------------------------------------------- targets
+def zipf_cdf(V: int, s: float = 1.1) -> np.ndarray:
+    """CDF of the bounded Zipf law P(k) ~ k^-s, k = 1..V (token id = k-1)."""
+    w = np.arange(1, V + 1, dtype=np.float64) ** (-s)
+    c = np.cumsum(w)
+    return c / c[-1]
+
+
+def targets(cfg: Config, T: int | None = None) -> np.ndarray:
+    T = cfg.T if T is None else T
+    u = uniform01(cfg.cid, T_TARGETS, 0, T)
+    if cfg.zipf:
+        t = np.searchsorted(zipf_cdf(cfg.V), u, side="right")
+    else:
+        t = np.floor(u * cfg.V).astype(np.int64)
+    return np.minimum(t, cfg.V - 1).astype(np.int32)
+
+
+# ---------------------------------------------------------------- tensors
+def hidden(cfg: Config) -> np.ndarray:
+    """Cached final-norm input x [T, d] (storage dtype)."""
+    return to_storage(normal(cfg.cid, T_X, 0, cfg.T * cfg.d).reshape(cfg.T, cfg.d), cfg.dtype)
+
+
+def gain(cfg: Config) -> np.ndarray:
+    """Final RMSNorm gain [d] = 1 + N(0, 0.1^2) (storage dtype)."""
+    return to_storage(normal(cfg.cid, T_GAMMA, 0, cfg.d, std=0.1, mean=1.0), cfg.dtype)
+
+
+def unembedding(cfg: Config) -> np.ndarray:
+    """W_U [V, d] ~ N(0, 0.02^2) (storage dtype)."""
+    return to_storage(normal(cfg.cid, T_WU, 0, cfg.V * cfg.d, std=0.02).reshape(cfg.V, cfg.d), cfg.dtype)
+
+
+def _silu32(q: np.ndarray) -> np.ndarray:
+    # forward-pass activation used only to synthesise the cached MLP input
+    return q / (np.float32(1.0) + np.exp(-q))
+
+
+def outlier_channels(cfg: Config, layer: int) -> np.ndarray:
+    k = int(round(0.01 * cfg.d_ff))
+    return _rng(cfg.cid, T_OUTLIER, layer, 0).choice(cfg.d_ff, size=k, replace=False)
+
+
+def mlp_cache(cfg: Config, layer: int):
+    """(q, u, a) for one target layer, each [T, d_ff] in storage dtype.
+
+    q, u ~ N(0,1) are rounded to storage first; a = SiLU(q) * u is formed in
+    float32 from the rounded values (with the outlier channels scaled x20 when
+    the workload asks for them) and then rounded to storage."""
+    n = cfg.T * cfg.d_ff
+    q = to_storage(normal(cfg.cid, T_Q, layer, n).reshape(cfg.T, cfg.d_ff), cfg.dtype)
+    u = to_storage(normal(cfg.cid, T_U, layer, n).reshape(cfg.T, cfg.d_ff), cfg.dtype)
+    if cfg.dtype == "bf16":
+        qf, uf = bf16_to_f32(q), bf16_to_f32(u)
+    else:
+        qf, uf = q, u
+    a = _silu32(qf) * uf
+    if cfg.outliers:
+        a[:, outlier_channels(cfg, layer)] *= np.float32(20.0)
+    return q, u, to_storage(a, cfg.dtype)
+
+
+def activation(cfg: Config, layer: int) -> np.ndarray:
+    return mlp_cache(cfg, layer)[2]
+
+
+def master_weight(cfg: Config, layer: int, tensor: int = T_W, shape=None) -> np.ndarray:
+    """fp32 master weight, N(0, 0.02^2). Down-projection W3 is [d, d_ff]."""
+    shape = (cfg.d, cfg.d_ff) if shape is None else shape
+    return normal(cfg.cid, tensor, layer, int(np.prod(shape)), std=0.02).reshape(shape)
+
+
+def full_mlp_extra(cfg: Config, layer: int):
+    """Inputs of the full-MLP mode for one layer: x_in [T, d] (storage dtype),
+    W1 (gate) and W2 (up) masters [d_ff, d] fp32. W3_init is the layer's
+    down-projection master, rounded to storage."""
+    x_in = to_storage(normal(cfg.cid, T_XIN, layer, cfg.T * cfg.d).reshape(cfg.T, cfg.d), cfg.dtype)
+    W1 = master_weight(cfg, layer, T_W1, (cfg.d_ff, cfg.d))
+    W2 = master_weight(cfg, layer, T_W2, (cfg.d_ff, cfg.d))
+    return x_in, W1, W2
+
+
+def ref_noise(cfg: Config, layer: int) -> np.ndarray:
+    """N(0,1) [d, d_ff] float32 for the diagnostic's reference gradient
+    R = D + sigma * N, sigma = sqrt(3) * ||D||_F / sqrt(d * d_ff)."""
+    return normal(cfg.cid, T_REFNOISE, layer, cfg.d * cfg.d_ff).reshape(cfg.d, cfg.d_ff)
+
+
+def synthetic_signal(cfg: Config, std: float = 0.02, tensor: int = T_G) -> np.ndarray:
+    """A seeded stand-in for the pseudogradient signal g~ [T, d] (storage
+    dtype), used to exercise the outer-product call on its own at full size."""
+    return to_storage(normal(cfg.cid, tensor, 0, cfg.T * cfg.d, std=std).reshape(cfg.T, cfg.d), cfg.dtype)

@@ -1,0 +1,69 @@
+"""Seeded input generator: reproducibility, distributions, rounding."""
+import math
+
+import numpy as np
+import torch
+
+from paper_2608_14563_amd import inputs as I
+
+
+def test_reproducible_bit_exact():
+    c = I.CONFIGS[0]
+    a1, a2 = I.hidden(c), I.hidden(c)
+    assert np.array_equal(a1, a2)
+    q1 = I.mlp_cache(c, 1)
+    q2 = I.mlp_cache(c, 1)
+    for u, v in zip(q1, q2):
+        assert np.array_equal(u, v)
+    assert not np.array_equal(I.activation(c, 0), I.activation(c, 1))
+
+
+def test_block_streams_independent_of_length():
+    # a longer draw starts with the same values as a shorter one
+    a = I.normal(9, 1, 0, 3 * I.BLOCK + 5)
+    b = I.normal(9, 1, 0, I.BLOCK + 7)
+    assert np.array_equal(a[:I.BLOCK + 7], b)
+
+
+def test_moments():
+    c = I.CONFIGS[0]
+    x = I.hidden(c).astype(np.float64)
+    assert abs(x.mean()) < 0.02 and abs(x.std() - 1) < 0.02
+    W = I.unembedding(c).astype(np.float64)
+    assert abs(W.std() - 0.02) < 5e-4
+    g = I.gain(c).astype(np.float64)
+    assert abs(g.mean() - 1) < 0.03 and abs(g.std() - 0.1) < 0.02
+
+
+def test_zipf_cdf_against_direct_sum():
+    V = 1000
+    cdf = I.zipf_cdf(V)
+    Z = math.fsum(k ** -1.1 for k in range(1, V + 1))
+    for k in (1, 2, 10, 500, 1000):
+        direct = math.fsum(j ** -1.1 for j in range(1, k + 1)) / Z
+        assert abs(cdf[k - 1] - direct) < 1e-13
+
+
+def test_zipf_targets_in_range_and_skewed():
+    c = I.CONFIGS[1].shrink(T=20000)
+    y = I.targets(c)
+    assert y.min() >= 0 and y.max() < c.V
+    p0 = (y == 0).mean()
+    Z = np.sum(np.arange(1, c.V + 1, dtype=np.float64) ** -1.1)
+    assert abs(p0 - 1 / Z) < 0.01
+
+
+def test_outlier_channels():
+    c = I.CONFIGS[3].shrink(T=4, d_ff=23040)
+    idx = I.outlier_channels(c, 0)
+    assert len(idx) == 230 and len(set(idx.tolist())) == 230
+
+
+def test_bf16_rounding_matches_torch_rne():
+    r = np.random.default_rng(0)
+    x = (r.standard_normal(100000) * np.exp(r.uniform(-20, 20, 100000))).astype(np.float32)
+    ours = I.bf16_bits(x)
+    ref = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ours, ref)
+    back = I.bf16_to_f32(ours)
+    assert np.array_equal(back, torch.from_numpy(x).to(torch.bfloat16).float().numpy())
