@@ -1,0 +1,261 @@
+#!/usr/bin/env python3
+"""FPO hot-path throughput on one MI355X.
+
+One step = one pass of the whole hot path over one batch of T tokens:
+fpo_output_error (final-norm recompute, vocabulary-chunked logits + online
+softmax + error, projection through W_U, clamped RMSNorm VJP) followed by
+fpo_pseudograd with the fused update (per-layer outer products for every
+target layer, relative 1% clip, SGD-momentum on fp32 masters, bf16 copy).
+Inputs are seeded synthetic tensors of the workload's shapes, resident in HBM
+before timing starts. Prints one JSON line on stdout; progress goes to stderr.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes as C
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "FPO update tokens/sec at 8B shapes; % bf16 MFMA peak; HBM GB/s on VJP/update"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=1, help="workload id (paper_2608_14563_amd.inputs.CONFIGS)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=16, help="tokens in the oracle's timed sample")
+    return ap.parse_args()
+
+
+def prof_lib():
+    from paper_2608_14563_amd import _lib
+    lib = _lib.load()
+    lib.fpo_prof_enable.argtypes = [C.c_char_p]
+    lib.fpo_prof_read.argtypes = [C.c_int, C.c_char_p, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
+    return lib
+
+
+def prof_read(lib):
+    n = 64
+    names = C.create_string_buffer(32 * n)
+    ms = (C.c_double * n)()
+    cnt = (C.c_int64 * n)()
+    k = lib.fpo_prof_read(n, names, ms, cnt)
+    if k < 0:
+        raise RuntimeError("fpo_prof_read failed")
+    return {names.raw[32 * i:32 * i + 32].split(b"\0")[0].decode(): (ms[i], cnt[i]) for i in range(k)}
+
+
+def kernel_work(name, c, steps, nchunk):
+    """Algorithmic work of one kernel over `steps` steps: (amount, unit, bound).
+    Flops count only the method's contractions; bytes count each operand once."""
+    T, d, V, dff, L = c.T, c.d, c.V, c.d_ff, c.L
+    if name in ("logits_chunk", "proj_chunk"):
+        return 2.0 * T * V * d * steps, "flop", "mfma"
+    if name == "outer":
+        return 2.0 * T * d * dff * L * steps, "flop", "mfma"
+    if name == "update":
+        # SGD momentum, step > 1: dW r, buf r/w, W r/w (fp32) + bf16 copy w
+        return 22.0 * L * d * dff * steps, "byte", "hbm"
+    if name == "chunk_stats":
+        return 4.0 * T * V * steps, "byte", "hbm"  # staged p~ read + write (bf16)
+    if name == "finalize_vjp":
+        return (T * d * (4 + 2 + 2 + 4 + 2)) * steps, "byte", "hbm"
+    return None
+
+
+def cpu_baseline(c, tokens, x, gam, W_U, y, acts, W0):
+    """The oracle, timed on a bounded sample of the same workload: the first
+    `tokens` tokens through the output error and every layer's outer product,
+    plus the optimizer step of one layer; scaled to the full step."""
+    import numpy as np
+
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        thr = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        thr = len(os.sched_getaffinity(0))
+    ts = min(tokens, c.T)
+    t0 = time.perf_counter()
+    out = O.output_error(x[:ts], gam, W_U, y[:ts], eps=c.eps, min_rms=c.min_rms, vocab_chunk=8192)
+    t1 = time.perf_counter()
+    for a in acts:
+        D = O.pseudograd(out["g_tilde"], a[:ts], scale=1.0 / c.T)
+    t2 = time.perf_counter()
+    D = O.pseudograd(out["g_tilde"], acts[0][:ts], scale=1.0 / c.T)
+    s = O.clip_scale(float((D * D).sum()), float((W0.astype(np.float64) ** 2).sum()), c.clip_frac)
+    O.sgd_momentum(W0, np.zeros_like(D), s * D, c.lr, 0.9, step=2)
+    t3 = time.perf_counter()
+    upd_one = t3 - t2
+    per_tok = (t2 - t0) / ts
+    est = per_tok * c.T + upd_one * c.L
+    return {"value": c.T / est, "unit": "tokens/s", "cores": int(thr), "kind": "oracle",
+            "sample": (f"first {ts} of {c.T} tokens through output error (full V={c.V}) and all {c.L} "
+                       f"layer outer products ({t2 - t0:.1f} s) plus one layer's clipped SGD-momentum step "
+                       f"({upd_one:.1f} s); full step estimated as per-token time x T + per-layer update x L "
+                       f"= {est:.1f} s"),
+            "seconds": round(t3 - t0, 2)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build has no "
+              "multi-GPU path: run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2608_14563_amd import api
+    from paper_2608_14563_amd import inputs as I
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    c = I.CONFIGS[args.config]
+    if c.diag or c.dtype != "bf16":
+        print("bench workloads are the bf16 training configurations 1-3", file=sys.stderr)
+        sys.exit(2)
+    log(f"[bench] workload {c.name}: T={c.T} d={c.d} d_ff={c.d_ff} V={c.V} L={c.L}; generating inputs")
+    tg0 = time.perf_counter()
+    x, gam, W_U, y = I.hidden(c), I.gain(c), I.unembedding(c), I.targets(c)
+    acts = [I.activation(c, l) for l in range(c.L)]
+    Wm_host = [I.master_weight(c, l) for l in range(c.L)]
+    log(f"[bench] inputs generated in {time.perf_counter() - tg0:.1f} s; uploading")
+
+    def t(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    tx, tgam, tW, ty = t(x), t(gam), t(W_U), t(y)
+    tacts = [t(a) for a in acts]
+    Wm = [t(w) for w in Wm_host]
+    s1 = [torch.zeros_like(w) for w in Wm]
+    Wlp = [w.to(torch.bfloat16) for w in Wm]
+    Wsq = torch.tensor([float((w.astype(np.float64) ** 2).sum()) for w in Wm_host], dtype=torch.float64, device=dev)
+    T, d = c.T, c.d
+    g_t = torch.empty(T, d, device=dev)
+    g_lp = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
+    lse = torch.empty(T, device=dev)
+    loss = torch.empty(T, device=dev)
+    amax = torch.empty(T, dtype=torch.int32, device=dev)
+    bad = torch.empty(1, dtype=torch.int32, device=dev)
+    dW = [torch.empty(d, c.d_ff, device=dev) for _ in range(c.L)]
+    ss = torch.empty(c.L, dtype=torch.float64, device=dev)
+    ws_oe = api.workspace(api.fpo_output_error_workspace(T, d, c.V, torch.bfloat16), dev)
+    ws_pg = api.workspace(api.fpo_pseudograd_workspace(T, d, c.d_ff, c.L, torch.bfloat16), dev)
+    torch.cuda.synchronize()
+    step_no = [0]
+
+    def step():
+        step_no[0] += 1
+        api.fpo_output_error(tx, tgam, tW, ty, g_t, g_tilde_lp=g_lp, lse=lse, loss=loss, argmax=amax,
+                             bad_targets=bad, ws=ws_oe, eps=c.eps, min_rms=c.min_rms)
+        api.fpo_pseudograd(g_lp, tacts, dW3=dW, sumsq=ss,
+                           opt=api.OptConfig(lr=c.lr, clip_frac=c.clip_frac, step=step_no[0]),
+                           W_master=Wm, W_lp=Wlp, state1=s1, W_sumsq=Wsq, ws=ws_pg)
+
+    lib = prof_lib()
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    # one untimed step with every kernel timed, to find the dominant kernel
+    lib.fpo_prof_reset()
+    lib.fpo_prof_enable(b"")
+    step()
+    torch.cuda.synchronize()
+    lib.fpo_prof_disable()
+    per_kernel = prof_read(lib)
+    lib.fpo_prof_reset()
+    dom = max(per_kernel, key=lambda k: per_kernel[k][0])
+    log("[bench] per-kernel ms in one step: " + ", ".join(f"{k}={v[0]:.3f}/{v[1]}" for k, v in sorted(per_kernel.items(), key=lambda kv: -kv[1][0])))
+    # timed region: K steps, the dominant kernel bracketed by events on its stream
+    lib.fpo_prof_enable(dom.encode())
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    lib.fpo_prof_disable()
+    ms_total = e0.elapsed_time(e1)
+    dom_stats = prof_read(lib)[dom]
+    lib.fpo_prof_reset()
+    ms_step = ms_total / args.steps
+    tok_s = c.T / (ms_step / 1000.0)
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step, {tok_s:.0f} tokens/s; dominant kernel {dom}: "
+        f"{dom_stats[0] / dom_stats[1]:.3f} ms avg over {dom_stats[1]} launches")
+    nchunk = None
+    w = kernel_work(dom, c, args.steps, nchunk)
+    roof = None
+    if w is not None:
+        amount, unit, bound = w
+        secs = dom_stats[0] / 1000.0
+        if unit == "flop":
+            ach = amount / secs / 1e12
+            roof = {"bound": bound, "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None, "kernel": dom,
+                    "avg_launch_ms": round(dom_stats[0] / dom_stats[1], 4), "launches": dom_stats[1]}
+        else:
+            ach = amount / secs / 1e9
+            roof = {"bound": bound, "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None, "kernel": dom,
+                    "avg_launch_ms": round(dom_stats[0] / dom_stats[1], 4), "launches": dom_stats[1]}
+    kernels = {}
+    for k, (ms, n) in per_kernel.items():
+        wk = kernel_work(k, c, 1, nchunk)
+        e = {"ms_per_step": round(ms, 4), "launches": n}
+        if wk is not None:
+            amount, unit, bound = wk
+            if unit == "flop":
+                e["tflops"] = round(amount / (ms / 1e3) / 1e12, 1)
+                e["mfma_frac"] = round(amount / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+            else:
+                e["gbs"] = round(amount / (ms / 1e3) / 1e9, 1)
+                e["hbm_frac"] = round(amount / (ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)
+        kernels[k] = e
+    flops_step = 4.0 * c.T * c.V * c.d + 2.0 * c.T * c.d * c.d_ff * c.L
+    res = {
+        "metric": METRIC, "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{c.name}-shaped FPO step: T={c.T} tokens, d={c.d}, d_ff={c.d_ff}, V={c.V}, "
+                               f"{c.L} target layers (W3), bf16 operands / fp32 accumulate, SGD-momentum on fp32 "
+                               f"masters, 1% relative clip", "T": c.T, "d": c.d, "d_ff": c.d_ff, "V": c.V, "L": c.L},
+        "step_mfma_frac": round(flops_step / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] timing the CPU oracle on a {args.cpu_tokens}-token sample")
+        res["cpu_baseline"] = cpu_baseline(c, args.cpu_tokens, x, gam, W_U, y, acts, Wm_host[0])
+    else:
+        res["cpu_baseline"] = None
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

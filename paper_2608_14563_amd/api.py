@@ -1,0 +1,193 @@
+"""Python binding of libfpo: the four calls of include/fpo.h under the same
+names, taking torch tensors. Argument marshalling only: every step of the
+path runs in the HIP library; torch supplies device memory and the stream.
+
+All tensors must be on the same CUDA (HIP) device and contiguous. The
+operand dtype follows h_final / g_tilde_lp: torch.bfloat16 (FPO_BF16) or
+torch.float32 (FPO_F32). Work is enqueued on torch's current stream.
+"""
+from __future__ import annotations
+
+import ctypes as C
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import torch
+
+from . import _lib as L
+
+__all__ = [
+    "fpo_abi_version", "fpo_output_error", "fpo_output_error_workspace", "fpo_pseudograd",
+    "fpo_pseudograd_workspace", "fpo_apply_update", "fpo_apply_update_workspace", "fpo_cosine",
+    "fpo_cosine_workspace", "OptConfig", "workspace", "dtype_code",
+]
+
+
+def dtype_code(t: torch.dtype) -> int:
+    if t == torch.bfloat16:
+        return L.FPO_BF16
+    if t == torch.float32:
+        return L.FPO_F32
+    raise TypeError(f"unsupported dtype {t}")
+
+
+def _p(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libfpo must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(dev: torch.device) -> int:
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+class _Keep:
+    """Builds [host] pointer arrays and keeps them alive for one call."""
+
+    def __init__(self):
+        self.refs = []
+
+    def arr(self, tensors: Optional[Sequence[Optional[torch.Tensor]]]):
+        if tensors is None:
+            return None
+        a = (C.c_void_p * max(1, len(tensors)))()
+        for i, t in enumerate(tensors):
+            a[i] = _p(t)
+        self.refs.append(a)
+        return C.cast(a, L.PP)
+
+    def i64(self, vals):
+        a = (C.c_int64 * len(vals))(*vals)
+        self.refs.append(a)
+        return a
+
+
+def workspace(nbytes: int, device) -> torch.Tensor:
+    """Caller-owned scratch (torch allocations are 256-byte aligned)."""
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def fpo_abi_version() -> int:
+    return L.load().fpo_abi_version()
+
+
+# --------------------------------------------------------------------- output error
+def _oe_desc(T, d, V, dtype, eps, min_rms, vocab_chunk):
+    return L.OeDesc(T, d, V, dtype, eps, min_rms, vocab_chunk)
+
+
+def fpo_output_error_workspace(T: int, d: int, V: int, dtype: torch.dtype, vocab_chunk: int = 0) -> int:
+    desc = _oe_desc(T, d, V, dtype_code(dtype), 0.0, 0.0, vocab_chunk)
+    return L.load().fpo_output_error_workspace(C.byref(desc))
+
+
+def fpo_output_error(h_final, gamma, W_U, targets, g_tilde, g_tilde_lp=None, g_pre=None, lse=None,
+                     loss=None, argmax=None, bad_targets=None, ws=None, eps=1e-6, min_rms=0.5,
+                     vocab_chunk=0):
+    T, d = h_final.shape
+    V = W_U.shape[0]
+    desc = _oe_desc(T, d, V, dtype_code(h_final.dtype), eps, min_rms, vocab_chunk)
+    lib = L.load()
+    if ws is None:
+        ws = workspace(lib.fpo_output_error_workspace(C.byref(desc)), h_final.device)
+    L.check(lib.fpo_output_error(
+        C.byref(desc), _p(h_final), _p(gamma), _p(W_U), _p(targets), _p(g_tilde), _p(g_tilde_lp),
+        _p(g_pre), _p(lse), _p(loss), _p(argmax), _p(bad_targets), _p(ws), ws.numel(),
+        _stream(h_final.device)))
+    return ws
+
+
+# --------------------------------------------------------------------- optimizer
+@dataclass
+class OptConfig:
+    kind: int = L.FPO_OPT_SGD
+    lr: float = 1e-4
+    momentum: float = 0.9
+    beta1: float = 0.9
+    beta2: float = 0.999
+    adam_eps: float = 1e-8
+    weight_decay: float = 0.01
+    clip_frac: float = 0.01
+    step: int = 1
+
+    def c(self) -> L.Opt:
+        return L.Opt(self.kind, self.lr, self.momentum, self.beta1, self.beta2, self.adam_eps,
+                     self.weight_decay, self.clip_frac, self.step)
+
+
+def _upd_bufs(keep: _Keep, W_master, W_lp, state1, state2, W_sumsq, clip_scale):
+    return L.UpdateBufs(keep.arr(W_master), keep.arr(W_lp), keep.arr(state1), keep.arr(state2),
+                        _p(W_sumsq), _p(clip_scale))
+
+
+# --------------------------------------------------------------------- pseudograd
+def fpo_pseudograd_workspace(T, d, d_ff, Lyr, dtype: torch.dtype, full_mlp=False) -> int:
+    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(dtype), L.FPO_MODE_FULL_MLP if full_mlp else L.FPO_MODE_W3, 1.0)
+    return L.load().fpo_pseudograd_workspace(C.byref(desc))
+
+
+def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, ref_sumsq=None,
+                   W3_init=None, gate=None, up=None, x_in=None, dW1=None, dW2=None, scale=None,
+                   opt: Optional[OptConfig] = None, W_master=None, W_lp=None, state1=None,
+                   state2=None, W_sumsq=None, clip_scale=None, ws=None):
+    T, d = g_tilde_lp.shape
+    Lyr = len(a)
+    d_ff = a[0].shape[1]
+    full = W3_init is not None
+    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(g_tilde_lp.dtype),
+                    L.FPO_MODE_FULL_MLP if full else L.FPO_MODE_W3,
+                    (1.0 / T) if scale is None else scale)
+    lib = L.load()
+    if ws is None:
+        ws = workspace(lib.fpo_pseudograd_workspace(C.byref(desc)), g_tilde_lp.device)
+    k = _Keep()
+    o = opt.c() if opt is not None else None
+    ub = _upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale) if opt is not None else None
+    L.check(lib.fpo_pseudograd(
+        C.byref(desc), _p(g_tilde_lp), k.arr(a), k.arr(W3_init), k.arr(gate), k.arr(up),
+        k.arr(x_in), k.arr(dW3), k.arr(dW1), k.arr(dW2), _p(sumsq), k.arr(ref), _p(ref_dot),
+        _p(ref_sumsq), C.byref(o) if o is not None else None, C.byref(ub) if ub is not None else None,
+        _p(ws), ws.numel(), _stream(g_tilde_lp.device)))
+    return ws
+
+
+# --------------------------------------------------------------------- update
+def fpo_apply_update_workspace(numels: Sequence[int]) -> int:
+    k = _Keep()
+    return L.load().fpo_apply_update_workspace(len(numels), k.i64(list(numels)))
+
+
+def fpo_apply_update(opt: OptConfig, grad, grad_sumsq, W_master, state1, W_sumsq, W_lp=None,
+                     state2=None, clip_scale=None, lp_dtype: torch.dtype = torch.bfloat16, ws=None):
+    n = len(grad)
+    k = _Keep()
+    numel = k.i64([g.numel() for g in grad])
+    lib = L.load()
+    if ws is None:
+        ws = workspace(lib.fpo_apply_update_workspace(n, numel), grad[0].device)
+    o = opt.c()
+    ub = _upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale)
+    L.check(lib.fpo_apply_update(C.byref(o), n, numel, k.arr(grad), _p(grad_sumsq), C.byref(ub),
+                                 dtype_code(lp_dtype), _p(ws), ws.numel(), _stream(grad[0].device)))
+    return ws
+
+
+# --------------------------------------------------------------------- cosine
+def fpo_cosine_workspace(numels: Sequence[int]) -> int:
+    k = _Keep()
+    return L.load().fpo_cosine_workspace(len(numels), k.i64(list(numels)))
+
+
+def fpo_cosine(A, B=None, dot=None, sumsq_A=None, sumsq_B=None, cos=None, ws=None):
+    n = len(A)
+    k = _Keep()
+    numel = k.i64([t.numel() for t in A])
+    lib = L.load()
+    if ws is None:
+        ws = workspace(lib.fpo_cosine_workspace(n, numel), A[0].device)
+    dt = dtype_code(B[0].dtype) if B is not None else L.FPO_F32
+    L.check(lib.fpo_cosine(n, numel, k.arr(A), k.arr(B), dt, _p(dot), _p(sumsq_A), _p(sumsq_B),
+                           _p(cos), _p(ws), ws.numel(), _stream(A[0].device)))
+    return ws

@@ -1,0 +1,459 @@
+// C-ABI layer of libfpo: argument validation, workspace planning and carving,
+// and the launch sequence of each call on the caller's stream. No device
+// memory is allocated here and nothing synchronises with the host.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/fpo.h"
+#include "launch.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+  return fail(FPO_ERR_HIP, "%s: %s (%d)", where, hipGetErrorString(e), (int)e);
+}
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+inline bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
+
+constexpr int64_t kIntMax = 0x7fffffff;
+constexpr size_t kAlign = 256;
+
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base((char*)b) {}
+  template <typename T>
+  T* take(int64_t n) {
+    T* p = base ? (T*)(base + off) : nullptr;
+    off += round_up((int64_t)(n * sizeof(T)), kAlign);
+    return p;
+  }
+};
+
+// ------------------------------------------------------------------ plans
+struct OePlan {
+  int64_t Vc = 0, nb = 0;
+  int nsplit = 1;
+};
+
+OePlan plan_oe(const fpo_oe_desc& d) {
+  const bool bf16 = d.dtype == FPO_BF16;
+  const int64_t BM = bf16 ? 256 : 128, BN = BM, WTN = bf16 ? 128 : 64;
+  // staged p~ budget: 32M elements per chunk
+  int64_t vmax = d.vocab_chunk > 0 ? round_up(d.vocab_chunk, 256)
+                                   : std::max<int64_t>(256, ((int64_t)32 * 1024 * 1024 / d.T) / 256 * 256);
+  vmax = std::min(vmax, round_up(d.V, 256));
+  const int64_t nchunk = ceil_div(d.V, vmax);
+  OePlan p;
+  p.Vc = round_up(ceil_div(d.V, nchunk), 256);
+  p.nb = p.Vc / WTN;
+  const int64_t tiles = ceil_div(d.T, BM) * ceil_div(d.d, BN);
+  int64_t ns = ceil_div(512, tiles);
+  ns = std::min<int64_t>(ns, 8);
+  ns = std::min<int64_t>(ns, std::max<int64_t>(1, p.nb / 2));
+  p.nsplit = (int)std::max<int64_t>(1, ns);
+  return p;
+}
+
+size_t carve_oe(const fpo_oe_desc& d, const OePlan& p, void* ws, fpo::OeLaunch* L) {
+  const int64_t esz = d.dtype == FPO_BF16 ? 2 : 4;
+  Carver c(ws);
+  void* y = c.take<char>(d.T * d.d * esz);
+  void* P = c.take<char>(d.T * p.Vc * esz);
+  float* blk_m = c.take<float>(d.T * p.nb);
+  float* blk_s = c.take<float>(d.T * p.nb);
+  int32_t* blk_i = c.take<int32_t>(d.T * p.nb);
+  float* fout = c.take<float>(d.T * p.nsplit);
+  float* alpha = c.take<float>(d.T);
+  float* runM = c.take<float>(d.T);
+  float* runS = c.take<float>(d.T);
+  int32_t* runA = c.take<int32_t>(d.T);
+  float* ztgt = c.take<float>(d.T);
+  float* G = c.take<float>((int64_t)p.nsplit * d.T * d.d);
+  if (L) {
+    L->y = y;
+    L->P = P;
+    L->blk_m = blk_m;
+    L->blk_s = blk_s;
+    L->blk_i = blk_i;
+    L->fout = fout;
+    L->alpha = alpha;
+    L->runM = runM;
+    L->runS = runS;
+    L->runA = runA;
+    L->ztgt = ztgt;
+    L->G = G;
+  }
+  return c.off;
+}
+
+int check_oe_desc(const fpo_oe_desc* d) {
+  if (!d) return fail(FPO_ERR_NULL, "fpo_output_error: desc is NULL");
+  if (d->dtype != FPO_F32 && d->dtype != FPO_BF16)
+    return fail(FPO_ERR_DTYPE, "fpo_output_error: unknown dtype %d", (int)d->dtype);
+  if (d->T <= 0 || d->d <= 0 || d->V <= 0 || d->T > kIntMax || d->d > kIntMax || d->V > kIntMax)
+    return fail(FPO_ERR_SHAPE, "fpo_output_error: sizes must be in [1, 2^31): T=%lld d=%lld V=%lld",
+                (long long)d->T, (long long)d->d, (long long)d->V);
+  if (d->d % 8 || d->V % 8)
+    return fail(FPO_ERR_SHAPE, "fpo_output_error: d and V must be multiples of 8 (d=%lld V=%lld)",
+                (long long)d->d, (long long)d->V);
+  if (!(d->eps >= 0.f) || !std::isfinite(d->eps))
+    return fail(FPO_ERR_ARG, "fpo_output_error: eps must be finite and >= 0");
+  if (!(d->min_rms >= 0.f) || !std::isfinite(d->min_rms))
+    return fail(FPO_ERR_ARG, "fpo_output_error: min_rms must be finite and >= 0");
+  if (d->vocab_chunk < 0) return fail(FPO_ERR_ARG, "fpo_output_error: vocab_chunk must be >= 0");
+  return FPO_OK;
+}
+
+struct PgPlan {
+  int64_t Tp = 0, ntiles = 0, upd_blocks = 0;
+  int nmats = 0;
+};
+
+PgPlan plan_pg(const fpo_pg_desc& d) {
+  PgPlan p;
+  const bool bf16 = d.dtype == FPO_BF16;
+  p.Tp = round_up(d.T, 64);
+  p.ntiles = fpo::pseudograd_tiles(bf16, d.d, d.d_ff);
+  const bool full = d.mode == FPO_MODE_FULL_MLP;
+  p.nmats = (int)(full ? 3 * d.L : d.L);
+  p.upd_blocks = p.nmats * fpo::update_blocks(d.d * d.d_ff);
+  return p;
+}
+
+size_t carve_pg(const fpo_pg_desc& d, const PgPlan& p, void* ws, fpo::PgLaunch* L,
+                double** upd_part) {
+  const int64_t esz = d.dtype == FPO_BF16 ? 2 : 4;
+  const bool full = d.mode == FPO_MODE_FULL_MLP;
+  Carver c(ws);
+  void* gT = c.take<char>(d.d * p.Tp * esz);
+  void* dq = full ? c.take<char>(d.d_ff * p.Tp * esz) : nullptr;
+  void* du = full ? c.take<char>(d.d_ff * p.Tp * esz) : nullptr;
+  double* part = c.take<double>(std::max<int64_t>(d.L, 2) * p.ntiles * 3);
+  double* up = c.take<double>(p.upd_blocks);
+  if (L) {
+    L->gT = gT;
+    L->dq_T = dq;
+    L->du_T = du;
+    L->part = part;
+  }
+  if (upd_part) *upd_part = up;
+  return c.off;
+}
+
+int check_pg_desc(const fpo_pg_desc* d) {
+  if (!d) return fail(FPO_ERR_NULL, "fpo_pseudograd: desc is NULL");
+  if (d->dtype != FPO_F32 && d->dtype != FPO_BF16)
+    return fail(FPO_ERR_DTYPE, "fpo_pseudograd: unknown dtype %d", (int)d->dtype);
+  if (d->mode != FPO_MODE_W3 && d->mode != FPO_MODE_FULL_MLP)
+    return fail(FPO_ERR_ARG, "fpo_pseudograd: unknown mode %d", (int)d->mode);
+  if (d->T <= 0 || d->d <= 0 || d->d_ff <= 0 || d->L <= 0 || d->T > kIntMax || d->d > kIntMax ||
+      d->d_ff > kIntMax)
+    return fail(FPO_ERR_SHAPE, "fpo_pseudograd: sizes must be in [1, 2^31): T=%lld d=%lld d_ff=%lld L=%lld",
+                (long long)d->T, (long long)d->d, (long long)d->d_ff, (long long)d->L);
+  if (d->L > fpo::kMaxMats)
+    return fail(FPO_ERR_SHAPE, "fpo_pseudograd: at most %d layers per call (L=%lld)", fpo::kMaxMats,
+                (long long)d->L);
+  if (d->d % 8 || d->d_ff % 8)
+    return fail(FPO_ERR_SHAPE, "fpo_pseudograd: d and d_ff must be multiples of 8");
+  if (!std::isfinite(d->scale)) return fail(FPO_ERR_ARG, "fpo_pseudograd: scale must be finite");
+  return FPO_OK;
+}
+
+int check_opt(const fpo_opt* o) {
+  if (!o) return fail(FPO_ERR_NULL, "optimizer description is NULL");
+  if (o->kind != FPO_OPT_SGD && o->kind != FPO_OPT_ADAMW)
+    return fail(FPO_ERR_ARG, "unknown optimizer kind %d", (int)o->kind);
+  if (!(o->lr >= 0.f) || !std::isfinite(o->lr)) return fail(FPO_ERR_ARG, "lr must be finite and >= 0");
+  if (o->step < 1) return fail(FPO_ERR_ARG, "step is 1-based (got %lld)", (long long)o->step);
+  if (!std::isfinite(o->clip_frac)) return fail(FPO_ERR_ARG, "clip_frac must be finite");
+  if (o->kind == FPO_OPT_SGD && !(o->momentum >= 0.f && o->momentum <= 1.f))
+    return fail(FPO_ERR_ARG, "momentum must be in [0, 1]");
+  if (o->kind == FPO_OPT_ADAMW) {
+    if (!(o->beta1 >= 0.f && o->beta1 < 1.f) || !(o->beta2 >= 0.f && o->beta2 < 1.f))
+      return fail(FPO_ERR_ARG, "AdamW betas must be in [0, 1)");
+    if (!(o->adam_eps > 0.f)) return fail(FPO_ERR_ARG, "AdamW eps must be > 0");
+    if (!(o->weight_decay >= 0.f)) return fail(FPO_ERR_ARG, "weight_decay must be >= 0");
+  }
+  return FPO_OK;
+}
+
+int check_ws(void* ws, size_t have, size_t need, const char* who) {
+  if (need == 0) return FPO_OK;
+  if (!ws) return fail(FPO_ERR_WORKSPACE, "%s: workspace is NULL (%zu bytes needed)", who, need);
+  if (!aligned(ws, kAlign)) return fail(FPO_ERR_WORKSPACE, "%s: workspace not 256-byte aligned", who);
+  if (have < need)
+    return fail(FPO_ERR_WORKSPACE, "%s: workspace %zu bytes < %zu needed", who, have, need);
+  return FPO_OK;
+}
+
+int fill_update(const fpo_opt* opt, int64_t n, const int64_t* numel, const float* const* grad,
+                const double* grad_sumsq, const fpo_update_bufs* upd, int32_t lp_dtype,
+                fpo::UpdLaunch* U) {
+  if (int e = check_opt(opt)) return e;
+  if (!upd) return fail(FPO_ERR_NULL, "update buffers are NULL");
+  if (n <= 0 || n > fpo::kMaxMats) return fail(FPO_ERR_SHAPE, "n_mats must be in [1, %d]", fpo::kMaxMats);
+  if (!numel || !grad || !grad_sumsq || !upd->W_master || !upd->state1 || !upd->W_sumsq)
+    return fail(FPO_ERR_NULL, "update: numel, grad, grad_sumsq, W_master, state1 and W_sumsq are required");
+  if (opt->kind == FPO_OPT_ADAMW && !upd->state2)
+    return fail(FPO_ERR_NULL, "update: AdamW needs state2");
+  if (lp_dtype != FPO_F32 && lp_dtype != FPO_BF16)
+    return fail(FPO_ERR_DTYPE, "update: unknown low-precision dtype %d", (int)lp_dtype);
+  U->kind = opt->kind;
+  U->lr = opt->lr;
+  U->momentum = opt->momentum;
+  U->beta1 = opt->beta1;
+  U->beta2 = opt->beta2;
+  U->adam_eps = opt->adam_eps;
+  U->weight_decay = opt->weight_decay;
+  U->clip_frac = opt->clip_frac;
+  U->step = opt->step;
+  U->n = (int)n;
+  U->lp_bf16 = lp_dtype == FPO_BF16;
+  for (int64_t m = 0; m < n; ++m) {
+    if (numel[m] <= 0 || numel[m] % 4)
+      return fail(FPO_ERR_SHAPE, "update: numel[%lld]=%lld must be a positive multiple of 4",
+                  (long long)m, (long long)numel[m]);
+    if (!grad[m] || !upd->W_master[m] || !upd->state1[m] ||
+        (opt->kind == FPO_OPT_ADAMW && !upd->state2[m]))
+      return fail(FPO_ERR_NULL, "update: NULL buffer for matrix %lld", (long long)m);
+    if (!aligned(grad[m], 16) || !aligned(upd->W_master[m], 16) || !aligned(upd->state1[m], 16))
+      return fail(FPO_ERR_ARG, "update: buffers of matrix %lld must be 16-byte aligned", (long long)m);
+    U->numel[m] = numel[m];
+    U->grad[m] = grad[m];
+    U->W[m] = upd->W_master[m];
+    U->W_lp[m] = upd->W_lp ? upd->W_lp[m] : nullptr;
+    U->s1[m] = upd->state1[m];
+    U->s2[m] = upd->state2 ? upd->state2[m] : nullptr;
+  }
+  U->grad_sumsq = grad_sumsq;
+  U->W_sumsq = upd->W_sumsq;
+  U->clip_scale = upd->clip_scale;
+  return FPO_OK;
+}
+
+size_t update_ws(int64_t n, const int64_t* numel) {
+  int64_t blocks = 0;
+  for (int64_t m = 0; m < n; ++m) blocks += fpo::update_blocks(numel[m]);
+  return (size_t)round_up(blocks * 8, kAlign);
+}
+
+}  // namespace
+
+extern "C" {
+
+int fpo_abi_version(void) { return FPO_ABI_VERSION; }
+
+const char* fpo_last_error(void) { return g_err.c_str(); }
+
+size_t fpo_output_error_workspace(const fpo_oe_desc* desc) {
+  if (check_oe_desc(desc)) return 0;
+  return carve_oe(*desc, plan_oe(*desc), nullptr, nullptr);
+}
+
+int fpo_output_error(const fpo_oe_desc* desc, const void* h_final, const void* gamma,
+                     const void* W_U, const int32_t* targets, float* g_tilde, void* g_tilde_lp,
+                     float* g_pre, float* lse, float* loss, int32_t* argmax, int32_t* bad_targets,
+                     void* ws, size_t ws_bytes, void* stream) {
+  if (int e = check_oe_desc(desc)) return e;
+  if (!h_final || !gamma || !W_U || !targets || !g_tilde)
+    return fail(FPO_ERR_NULL, "fpo_output_error: h_final, gamma, W_U, targets and g_tilde are required");
+  const void* ptrs[] = {h_final, gamma, W_U, g_tilde, g_tilde_lp, g_pre};
+  for (const void* p : ptrs)
+    if (p && !aligned(p, 16)) return fail(FPO_ERR_ARG, "fpo_output_error: tensors must be 16-byte aligned");
+  const OePlan p = plan_oe(*desc);
+  const size_t need = carve_oe(*desc, p, nullptr, nullptr);
+  if (int e = check_ws(ws, ws_bytes, need, "fpo_output_error")) return e;
+  fpo::OeLaunch L{};
+  L.bf16 = desc->dtype == FPO_BF16;
+  L.T = desc->T;
+  L.d = desc->d;
+  L.V = desc->V;
+  L.Vc = p.Vc;
+  L.nsplit = p.nsplit;
+  L.eps = desc->eps;
+  L.min_rms = desc->min_rms;
+  L.h_final = h_final;
+  L.gamma = gamma;
+  L.W_U = W_U;
+  L.targets = targets;
+  L.g_tilde = g_tilde;
+  L.g_tilde_lp = g_tilde_lp;
+  L.g_pre = g_pre;
+  L.lse = lse;
+  L.loss = loss;
+  L.argmax = argmax;
+  L.bad_targets = bad_targets;
+  L.stream = stream;
+  carve_oe(*desc, p, ws, &L);
+  hipError_t e = fpo::launch_output_error(L);
+  if (e != hipSuccess) return hip_fail(e, "fpo_output_error launch");
+  return FPO_OK;
+}
+
+size_t fpo_pseudograd_workspace(const fpo_pg_desc* desc) {
+  if (check_pg_desc(desc)) return 0;
+  return carve_pg(*desc, plan_pg(*desc), nullptr, nullptr, nullptr);
+}
+
+int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* const* a,
+                   const void* const* W3_init, const void* const* gate, const void* const* up,
+                   const void* const* x_in, float* const* dW3, float* const* dW1, float* const* dW2,
+                   double* sumsq, const float* const* ref, double* ref_dot, double* ref_sumsq,
+                   const fpo_opt* opt, const fpo_update_bufs* upd, void* ws, size_t ws_bytes,
+                   void* stream) {
+  if (int e = check_pg_desc(desc)) return e;
+  const bool full = desc->mode == FPO_MODE_FULL_MLP;
+  const int L = (int)desc->L;
+  if (!g_tilde_lp || !a) return fail(FPO_ERR_NULL, "fpo_pseudograd: g_tilde_lp and a are required");
+  if (!dW3 && !ref) return fail(FPO_ERR_NULL, "fpo_pseudograd: dW3 may be NULL only with ref");
+  if (ref && (!ref_dot || !ref_sumsq))
+    return fail(FPO_ERR_NULL, "fpo_pseudograd: ref needs ref_dot and ref_sumsq");
+  if (full && (!W3_init || !gate || !up || !x_in || !dW1 || !dW2))
+    return fail(FPO_ERR_NULL, "fpo_pseudograd: full-MLP mode needs W3_init, gate, up, x_in, dW1, dW2");
+  if ((opt == nullptr) != (upd == nullptr))
+    return fail(FPO_ERR_ARG, "fpo_pseudograd: opt and upd must both be given or both be NULL");
+  if (opt && (!dW3 || !sumsq))
+    return fail(FPO_ERR_NULL, "fpo_pseudograd: the fused update needs dW3 and sumsq");
+  if (!aligned(g_tilde_lp, 16)) return fail(FPO_ERR_ARG, "fpo_pseudograd: g_tilde_lp must be 16-byte aligned");
+  fpo::PgLaunch P{};
+  P.bf16 = desc->dtype == FPO_BF16;
+  P.full_mlp = full;
+  P.T = desc->T;
+  P.d = desc->d;
+  P.d_ff = desc->d_ff;
+  P.L = L;
+  P.scale = desc->scale;
+  P.g_lp = g_tilde_lp;
+  for (int l = 0; l < L; ++l) {
+    if (!a[l]) return fail(FPO_ERR_NULL, "fpo_pseudograd: a[%d] is NULL", l);
+    if (!aligned(a[l], 16)) return fail(FPO_ERR_ARG, "fpo_pseudograd: a[%d] not 16-byte aligned", l);
+    P.a[l] = a[l];
+    P.dW3[l] = dW3 ? dW3[l] : nullptr;
+    if (dW3 && !dW3[l]) return fail(FPO_ERR_NULL, "fpo_pseudograd: dW3[%d] is NULL", l);
+    if (P.dW3[l] && !aligned(P.dW3[l], 16)) return fail(FPO_ERR_ARG, "fpo_pseudograd: dW3[%d] not aligned", l);
+    P.ref[l] = ref ? ref[l] : nullptr;
+    if (ref && !ref[l]) return fail(FPO_ERR_NULL, "fpo_pseudograd: ref[%d] is NULL", l);
+    if (full) {
+      if (!W3_init[l] || !gate[l] || !up[l] || !x_in[l] || !dW1[l] || !dW2[l])
+        return fail(FPO_ERR_NULL, "fpo_pseudograd: full-MLP buffer of layer %d is NULL", l);
+      P.W3i[l] = W3_init[l];
+      P.q[l] = gate[l];
+      P.u[l] = up[l];
+      P.x_in[l] = x_in[l];
+      P.dW1[l] = dW1[l];
+      P.dW2[l] = dW2[l];
+    }
+  }
+  P.sumsq = sumsq;
+  P.ref_dot = ref_dot;
+  P.ref_sumsq = ref_sumsq;
+  P.stream = stream;
+  const PgPlan pl = plan_pg(*desc);
+  P.Tp = pl.Tp;
+  const size_t need = carve_pg(*desc, pl, nullptr, nullptr, nullptr);
+  if (int e = check_ws(ws, ws_bytes, need, "fpo_pseudograd")) return e;
+  double* upart = nullptr;
+  carve_pg(*desc, pl, ws, &P, &upart);
+  fpo::UpdLaunch U{};
+  if (opt) {
+    const int n = pl.nmats;
+    if (n > fpo::kMaxMats) return fail(FPO_ERR_SHAPE, "fpo_pseudograd: fused update limited to %d matrices", fpo::kMaxMats);
+    int64_t numel[fpo::kMaxMats];
+    const float* grads[fpo::kMaxMats];
+    for (int m = 0; m < n; ++m) {
+      const int l = m % L, kind = m / L;
+      numel[m] = desc->d * desc->d_ff;
+      grads[m] = kind == 0 ? dW3[l] : (kind == 1 ? dW1[l] : dW2[l]);
+    }
+    if (int e = fill_update(opt, n, numel, grads, sumsq, upd, desc->dtype, &U)) return e;
+    U.part = upart;
+    U.stream = stream;
+  }
+  hipError_t e = fpo::launch_pseudograd(P);
+  if (e != hipSuccess) return hip_fail(e, "fpo_pseudograd launch");
+  if (opt) {
+    e = fpo::launch_update(U);
+    if (e != hipSuccess) return hip_fail(e, "fpo_pseudograd update launch");
+  }
+  return FPO_OK;
+}
+
+size_t fpo_apply_update_workspace(int64_t n_mats, const int64_t* numel) {
+  if (n_mats <= 0 || !numel) return 0;
+  return update_ws(n_mats, numel);
+}
+
+int fpo_apply_update(const fpo_opt* opt, int64_t n_mats, const int64_t* numel,
+                     const float* const* grad, const double* grad_sumsq,
+                     const fpo_update_bufs* upd, int32_t lp_dtype, void* ws, size_t ws_bytes,
+                     void* stream) {
+  fpo::UpdLaunch U{};
+  if (int e = fill_update(opt, n_mats, numel, grad, grad_sumsq, upd, lp_dtype, &U)) return e;
+  if (int e = check_ws(ws, ws_bytes, update_ws(n_mats, numel), "fpo_apply_update")) return e;
+  U.part = (double*)ws;
+  U.stream = stream;
+  hipError_t e = fpo::launch_update(U);
+  if (e != hipSuccess) return hip_fail(e, "fpo_apply_update launch");
+  return FPO_OK;
+}
+
+size_t fpo_cosine_workspace(int64_t n_pairs, const int64_t* numel) {
+  if (n_pairs <= 0 || !numel) return 0;
+  int64_t blocks = 0;
+  for (int64_t m = 0; m < n_pairs; ++m) blocks += fpo::cosine_blocks(numel[m]);
+  return (size_t)round_up(blocks * 3 * 8, kAlign);
+}
+
+int fpo_cosine(int64_t n_pairs, const int64_t* numel, const float* const* A, const void* const* B,
+               int32_t dtype_B, double* dot, double* sumsq_A, double* sumsq_B, float* cos,
+               void* ws, size_t ws_bytes, void* stream) {
+  if (n_pairs <= 0 || n_pairs > fpo::kMaxMats)
+    return fail(FPO_ERR_SHAPE, "fpo_cosine: n_pairs must be in [1, %d]", fpo::kMaxMats);
+  if (!numel || !A) return fail(FPO_ERR_NULL, "fpo_cosine: numel and A are required");
+  if (dtype_B != FPO_F32 && dtype_B != FPO_BF16)
+    return fail(FPO_ERR_DTYPE, "fpo_cosine: unknown dtype %d", (int)dtype_B);
+  fpo::CosLaunch C{};
+  C.n = (int)n_pairs;
+  C.b_bf16 = dtype_B == FPO_BF16;
+  for (int64_t m = 0; m < n_pairs; ++m) {
+    if (numel[m] <= 0 || numel[m] % 4)
+      return fail(FPO_ERR_SHAPE, "fpo_cosine: numel[%lld] must be a positive multiple of 4", (long long)m);
+    if (!A[m] || (B && !B[m])) return fail(FPO_ERR_NULL, "fpo_cosine: NULL pointer for pair %lld", (long long)m);
+    if (!aligned(A[m], 16) || (B && !aligned(B[m], 16)))
+      return fail(FPO_ERR_ARG, "fpo_cosine: pair %lld not 16-byte aligned", (long long)m);
+    C.numel[m] = numel[m];
+    C.A[m] = A[m];
+    C.B[m] = B ? B[m] : nullptr;
+  }
+  if (int e = check_ws(ws, ws_bytes, fpo_cosine_workspace(n_pairs, numel), "fpo_cosine")) return e;
+  C.dot = dot;
+  C.sa = sumsq_A;
+  C.sb = sumsq_B;
+  C.cos = cos;
+  C.part = (double*)ws;
+  C.stream = stream;
+  hipError_t e = fpo::launch_cosine(C);
+  if (e != hipSuccess) return hip_fail(e, "fpo_cosine launch");
+  return FPO_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,366 @@
+// Output-error path (Sec. 3.1 steps 2-4; eq. gproj; App. E eq. rmsnorm-vjp):
+//   rms_forward  : rho_t and y_t = gamma * x_t / rho_t            (HBM bound)
+//   logits_chunk : z = y W_c^T for one vocabulary chunk (MFMA), per-block
+//                  row statistics, p~ = exp(z - block max) staged  (MFMA bound)
+//   chunk_stats  : running max / partition function / argmax per token;
+//                  staged p~ brought to one reference per split
+//   proj_chunk   : G_s <- rescale(G_s) + p~ W_c (MFMA), one partial per split
+//   finalize_vjp : g = sum_s G_s / S - W_U[y]; clamped RMSNorm VJP  (HBM bound)
+// The T x V logits never reach HBM; only one chunk of p~ is staged.
+#include "gemm.hpp"
+#include "launch.hpp"
+#include "prof.hpp"
+
+namespace fpo {
+
+// ------------------------------------------------------------------ forward
+template <typename T>
+__global__ __launch_bounds__(256) void rms_forward_kernel(const T* __restrict__ x,
+                                                          const T* __restrict__ gamma, int d,
+                                                          float eps, T* __restrict__ y,
+                                                          int32_t* __restrict__ bad) {
+  __shared__ float red[16];
+  const int64_t row = blockIdx.x;
+  const T* xr = x + row * d;
+  float ss = 0.f;
+  for (int k = threadIdx.x * 4; k < d; k += 1024) {
+    f32x4 v = ld4(xr, k);
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  ss = block_sum(ss, red);
+  const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  for (int k = threadIdx.x * 4; k < d; k += 1024) {
+    f32x4 v = ld4(xr, k), g = ld4(gamma, k);
+    st4(y + row * d, k, f32x4{g.x * v.x * inv, g.y * v.y * inv, g.z * v.z * inv, g.w * v.w * inv});
+  }
+  if (bad && row == 0 && threadIdx.x == 0) *bad = 0;
+}
+
+// ------------------------------------------------------------------ logits
+// One workgroup: BM tokens x BN vocabulary columns of the chunk; each wave's
+// WTN columns form one statistics block b (block max m, sum of exp(z - m),
+// first arg-max). Columns at or beyond `vc_valid` are masked out.
+template <class E>
+__global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
+    const typename E::T* __restrict__ y, const typename E::T* __restrict__ Wc, int T, int d,
+    int vc_valid, int v0, const int32_t* __restrict__ targets, typename E::T* __restrict__ P,
+    int64_t ldp, int nb, float* __restrict__ blk_m, float* __restrict__ blk_s,
+    int32_t* __restrict__ blk_i, float* __restrict__ ztgt) {
+  using TT = Tile<E>;
+  __shared__ GemmSmem<E> sm;
+  f32x4 acc[E::FM][E::FN];
+  zero_acc<E>(acc);
+  const int m0 = blockIdx.x * TT::BM, n0 = blockIdx.y * TT::BN;
+  gemm_mainloop<E, false>(sm, acc, y, d, T, Wc, d, vc_valid, d, m0, n0, 0,
+                          (d + TT::BK - 1) / TT::BK, NoHook{});
+  const AccMap<E> mp;
+  const int lr = threadIdx.x & 15;
+  const int b = n0 / TT::WTN + ((threadIdx.x >> 6) & 1);  // this wave's block
+#pragma unroll
+  for (int f = 0; f < E::FM; ++f) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = m0 + mp.row(f, r);
+      const int c0 = n0 + mp.col(0);
+      float z[E::FN];
+      float m = -INFINITY;
+      int mi = 0x7fffffff;
+#pragma unroll
+      for (int i = 0; i < E::FN; ++i) {
+        z[i] = acc[f][i][r];
+        if (c0 + i < vc_valid && z[i] > m) {
+          m = z[i];
+          mi = c0 + i;
+        }
+      }
+      // lowest column among equal maxima across the 16 lanes of the row
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        const float m2 = __shfl_xor(m, o, 64);
+        const int i2 = __shfl_xor(mi, o, 64);
+        if (m2 > m || (m2 == m && i2 < mi)) {
+          m = m2;
+          mi = i2;
+        }
+      }
+      float p[E::FN];
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < E::FN; ++i) {
+        p[i] = (c0 + i < vc_valid) ? __expf(z[i] - m) : 0.f;
+        s += p[i];
+      }
+      s = wave_sum<16>(s);
+      if (row < T) {
+        typename E::T* pr = P + (int64_t)row * ldp + c0;
+#pragma unroll
+        for (int i = 0; i < E::FN; i += 4) st4(pr, i, f32x4{p[i], p[i + 1], p[i + 2], p[i + 3]});
+        if (lr == 0 && b < nb) {
+          const int64_t o = (int64_t)row * nb + b;
+          blk_m[o] = m;
+          blk_s[o] = s;
+          blk_i[o] = (mi == 0x7fffffff) ? mi : v0 + mi;
+        }
+        const int64_t tg = (int64_t)targets[row] - v0 - c0;
+        if (tg >= 0 && tg < E::FN && c0 + tg < vc_valid) {
+#pragma unroll
+          for (int i = 0; i < E::FN; ++i)
+            if (i == tg) ztgt[row] = z[i];
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ stats
+// One wave per token. Folds the chunk's block statistics (block max m_b, sum
+// of exp(z - m_b), first arg-max) into the running max M, partition S and
+// argmax, and brings the staged p~ of every block to one reference per split
+// of the chunk: ref_s = max of the split's block maxima, p~ <- p~ exp(m_b - ref_s).
+// The projection accumulates split s in scale ref_s and stores
+//   G_s <- acc * exp(ref_s - M_new) + G_s * exp(M_old - M_new),
+// so every factor is <= 1 and nothing can overflow.
+constexpr int kMaxSplit = 8;
+
+template <typename PT>
+__global__ __launch_bounds__(256) void chunk_stats_kernel(
+    int T, int nb, int bps, int nsplit, int first, int blkw, int vc_valid,
+    const float* __restrict__ blk_m, const float* __restrict__ blk_s,
+    const int32_t* __restrict__ blk_i, float* __restrict__ runM, float* __restrict__ runS,
+    int32_t* __restrict__ runA, float* __restrict__ fout, float* __restrict__ alpha,
+    PT* __restrict__ P, int64_t ldp) {
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + w;
+  if (row >= T) return;  // whole wave exits together; no barrier below
+  const float* bm = blk_m + (int64_t)row * nb;
+  const float* bs = blk_s + (int64_t)row * nb;
+  const int32_t* bi = blk_i + (int64_t)row * nb;
+  float mc = -INFINITY;
+  for (int b = l; b < nb; b += 64) mc = fmaxf(mc, bm[b]);
+  mc = wave_max(mc);
+  int ai = 0x7fffffff;
+  for (int b = l; b < nb; b += 64)
+    if (bm[b] == mc) ai = min(ai, bi[b]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) ai = min(ai, __shfl_xor(ai, o, 64));
+  const float Mold = first ? -INFINITY : runM[row];
+  const float Mnew = fmaxf(Mold, mc);
+  float ref[kMaxSplit];
+#pragma unroll
+  for (int sp = 0; sp < kMaxSplit; ++sp) {
+    float r = -INFINITY;
+    if (sp < nsplit) {
+      for (int b = sp * bps + l; b < min(nb, (sp + 1) * bps); b += 64) r = fmaxf(r, bm[b]);
+      r = wave_max(r);
+    }
+    ref[sp] = r;
+  }
+  // partition function of the chunk relative to M_new
+  float s = 0.f;
+  for (int b = l; b < nb; b += 64) s += bs[b] * __expf(bm[b] - Mnew);
+  s = wave_sum(s);
+  // rescale staged p~ to its split's reference (16-byte chunks)
+  constexpr int EPC = 16 / sizeof(PT);
+  PT* pr = P + (int64_t)row * ldp;
+  const int ncv = (vc_valid + EPC - 1) / EPC;
+  for (int c = l; c < ncv; c += 64) {
+    const int b = (c * EPC) / blkw;
+    const int sp = b / bps;
+    float rs = ref[0];
+#pragma unroll
+    for (int k = 1; k < kMaxSplit; ++k)
+      if (k == sp) rs = ref[k];
+    const float m = bm[b];
+    if (m == rs) continue;
+    const float f = __expf(m - rs);
+    u32x4* q = reinterpret_cast<u32x4*>(pr) + c;
+    if constexpr (sizeof(PT) == 2) {
+      u32x4 v = *q;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = pack_bf16x2(bf16_lo(v[e]) * f, bf16_hi(v[e]) * f);
+      *q = v;
+    } else {
+      f32x4 v = __builtin_bit_cast(f32x4, *q) * f;
+      *q = __builtin_bit_cast(u32x4, v);
+    }
+  }
+  if (l < nsplit) {
+    float fo = 0.f;
+#pragma unroll
+    for (int sp = 0; sp < kMaxSplit; ++sp)
+      if (sp == l) fo = __expf(ref[sp] - Mnew);  // 0 for a split without blocks
+    fout[(int64_t)row * nsplit + l] = fo;
+  }
+  if (l == 0) {
+    const float a = first ? 0.f : __expf(Mold - Mnew);
+    runS[row] = (first ? 0.f : runS[row] * a) + s;
+    runM[row] = Mnew;
+    alpha[row] = a;
+    if (first || mc > Mold) runA[row] = ai;
+  }
+}
+
+// ------------------------------------------------------------------ projection
+// G_s[t, :] (one partial per split s of the chunk's blocks) holds
+// sum_v exp(z_tv - M_t) W_U[v, :] over the vocabulary processed so far; the
+// split's products are accumulated in scale ref_s and merged in the epilogue.
+template <class E>
+__global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
+    const typename E::T* __restrict__ P, int64_t ldp, const typename E::T* __restrict__ Wc,
+    int T, int d, int vc_valid, int nb, int bps, int blkw, int first,
+    const float* __restrict__ fout, const float* __restrict__ alpha, float* __restrict__ G,
+    int64_t split_stride) {
+  using TT = Tile<E>;
+  __shared__ GemmSmem<E> sm;
+  f32x4 acc[E::FM][E::FN];
+  zero_acc<E>(acc);
+  const int m0 = blockIdx.x * TT::BM, n0 = blockIdx.y * TT::BN, sp = blockIdx.z;
+  const int nsplit = gridDim.z;
+  float* Gs = G + sp * split_stride;
+  const int tpb = blkw / TT::BK;
+  const int nkt = (vc_valid + TT::BK - 1) / TT::BK;
+  const int kt0 = min(sp * bps * tpb, nkt), kt1 = min(min(nb, (sp + 1) * bps) * tpb, nkt);
+  gemm_mainloop<E, true>(sm, acc, P, ldp, T, Wc, d, d, vc_valid, m0, n0, kt0, kt1, NoHook{});
+  const AccMap<E> mp;
+#pragma unroll
+  for (int f = 0; f < E::FM; ++f)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = m0 + mp.row(f, r);
+      const int c = n0 + mp.col(0);
+      if (row >= T || c >= d) continue;
+      const float so = fout[(int64_t)row * nsplit + sp];
+      const float sa = first ? 0.f : alpha[row];
+#pragma unroll
+      for (int i = 0; i < E::FN; i += 4) {
+        float* gp = Gs + (int64_t)row * d + c + i;
+        f32x4 o = {acc[f][i][r] * so, acc[f][i + 1][r] * so, acc[f][i + 2][r] * so,
+                   acc[f][i + 3][r] * so};
+        if (!first) o += *reinterpret_cast<const f32x4*>(gp) * sa;
+        *reinterpret_cast<f32x4*>(gp) = o;
+      }
+    }
+}
+
+// ------------------------------------------------------------------ finalize
+// One workgroup per token: g = sum_s G_s / S - W_U[y] (zero for a target
+// outside [0, V)), then the clamped VJP
+//   rho~ = max(sqrt(mean x^2 + eps), min_rms); x^ = x / rho~;
+//   c = (1/d) <x^, gamma * g>;  g~ = (gamma * g - c x^) / rho~.
+template <typename T>
+__global__ __launch_bounds__(256) void finalize_vjp_kernel(
+    int d, int V, int nsplit, int64_t split_stride, const float* __restrict__ G,
+    const float* __restrict__ runM, const float* __restrict__ runS,
+    const int32_t* __restrict__ runA, const float* __restrict__ ztgt,
+    const int32_t* __restrict__ targets, const T* __restrict__ W_U, const T* __restrict__ x,
+    const T* __restrict__ gamma, float eps, float min_rms, float* __restrict__ g_tilde,
+    T* __restrict__ g_tilde_lp, float* __restrict__ g_pre, float* __restrict__ lse,
+    float* __restrict__ loss, int32_t* __restrict__ argmax, int32_t* __restrict__ bad) {
+  __shared__ float red[16];
+  const int64_t row = blockIdx.x;
+  const int tg = targets[row];
+  const bool valid = tg >= 0 && tg < V;
+  const float S = runS[row];
+  const float invS = 1.0f / S;
+  const T* xr = x + row * d;
+  float* gt = g_tilde + row * d;
+  float ss = 0.f, cd = 0.f;
+  for (int k = threadIdx.x * 4; k < d; k += 1024) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < nsplit; ++s) acc += *reinterpret_cast<const f32x4*>(G + s * split_stride + row * d + k);
+    f32x4 g = {0.f, 0.f, 0.f, 0.f};
+    if (valid) {
+      f32x4 wy = ld4(W_U + (int64_t)tg * d, k);
+      g = acc * invS - wy;
+    }
+    if (g_pre) *reinterpret_cast<f32x4*>(g_pre + row * d + k) = g;
+    *reinterpret_cast<f32x4*>(gt + k) = g;
+    f32x4 xv = ld4(xr, k), gm = ld4(gamma, k);
+    ss += xv.x * xv.x + xv.y * xv.y + xv.z * xv.z + xv.w * xv.w;
+    cd += xv.x * gm.x * g.x + xv.y * gm.y * g.y + xv.z * gm.z * g.z + xv.w * gm.w * g.w;
+  }
+  ss = block_sum(ss, red);
+  cd = block_sum(cd, red);
+  const float rho = sqrtf(ss / (float)d + eps);
+  const float rt = fmaxf(rho, min_rms);
+  const float irt = 1.0f / rt;
+  const float c = cd * irt / (float)d;  // (1/d) <x / rho~, gamma * g>
+  for (int k = threadIdx.x * 4; k < d; k += 1024) {
+    f32x4 g = *reinterpret_cast<const f32x4*>(gt + k);
+    f32x4 xv = ld4(xr, k), gm = ld4(gamma, k);
+    f32x4 o;
+    o.x = (gm.x * g.x - c * xv.x * irt) * irt;
+    o.y = (gm.y * g.y - c * xv.y * irt) * irt;
+    o.z = (gm.z * g.z - c * xv.z * irt) * irt;
+    o.w = (gm.w * g.w - c * xv.w * irt) * irt;
+    *reinterpret_cast<f32x4*>(gt + k) = o;
+    if (g_tilde_lp) st4(g_tilde_lp + row * d, k, o);
+  }
+  if (threadIdx.x == 0) {
+    const float l_se = runM[row] + logf(S);
+    if (lse) lse[row] = l_se;
+    if (loss) loss[row] = valid ? l_se - ztgt[row] : 0.f;
+    if (argmax) argmax[row] = runA[row];
+    if (!valid && bad) atomicAdd(bad, 1);
+  }
+}
+
+// ------------------------------------------------------------------ launchers
+#define FPO_CHECK_LAUNCH()                       \
+  do {                                           \
+    hipError_t e_ = hipGetLastError();           \
+    if (e_ != hipSuccess) return e_;             \
+  } while (0)
+
+template <class E>
+static hipError_t run_output_error(const OeLaunch& a) {
+  using T = typename E::T;
+  using TT = Tile<E>;
+  hipStream_t st = (hipStream_t)a.stream;
+  const T* x = (const T*)a.h_final;
+  const T* gamma = (const T*)a.gamma;
+  const T* W = (const T*)a.W_U;
+  T* y = (T*)a.y;
+  T* P = (T*)a.P;
+  FPO_LAUNCH("rms_forward", st,
+             rms_forward_kernel<T><<<dim3((unsigned)a.T), dim3(256), 0, st>>>(x, gamma, (int)a.d, a.eps, y,
+                                                                   a.bad_targets));
+  FPO_CHECK_LAUNCH();
+  const int nchunk = (int)((a.V + a.Vc - 1) / a.Vc);
+  const int gm = (int)((a.T + TT::BM - 1) / TT::BM);
+  for (int c = 0; c < nchunk; ++c) {
+    const int64_t v0 = (int64_t)c * a.Vc;
+    const int vc_valid = (int)std::min<int64_t>(a.Vc, a.V - v0);
+    const int gn = (vc_valid + TT::BN - 1) / TT::BN;
+    const int nbv = (vc_valid + TT::WTN - 1) / TT::WTN;  // blocks holding a valid column
+    FPO_LAUNCH("logits_chunk", st,
+               logits_chunk_kernel<E><<<dim3(gm, gn), dim3(256), 0, st>>>(
+        y, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, (int)v0, a.targets, P, a.Vc, nbv,
+        a.blk_m, a.blk_s, a.blk_i, a.ztgt));
+    FPO_CHECK_LAUNCH();
+    const int bps = (nbv + a.nsplit - 1) / a.nsplit;
+    FPO_LAUNCH("chunk_stats", st,
+               chunk_stats_kernel<T><<<dim3((unsigned)((a.T + 3) / 4)), dim3(256), 0, st>>>(
+        (int)a.T, nbv, bps, a.nsplit, c == 0, TT::WTN, vc_valid, a.blk_m, a.blk_s, a.blk_i,
+        a.runM, a.runS, a.runA, a.fout, a.alpha, P, a.Vc));
+    FPO_CHECK_LAUNCH();
+    FPO_LAUNCH("proj_chunk", st,
+               proj_chunk_kernel<E><<<dim3(gm, (unsigned)((a.d + TT::BN - 1) / TT::BN), a.nsplit), dim3(256), 0, st>>>(
+        P, a.Vc, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, nbv, bps, TT::WTN, c == 0, a.fout,
+        a.alpha, a.G, a.T * a.d));
+    FPO_CHECK_LAUNCH();
+  }
+  FPO_LAUNCH("finalize_vjp", st,
+             finalize_vjp_kernel<T><<<dim3((unsigned)a.T), dim3(256), 0, st>>>(
+      (int)a.d, (int)a.V, a.nsplit, a.T * a.d, a.G, a.runM, a.runS, a.runA, a.ztgt, a.targets, W,
+      x, gamma, a.eps, a.min_rms, a.g_tilde, (T*)a.g_tilde_lp, a.g_pre, a.lse, a.loss, a.argmax,
+      a.bad_targets));
+  FPO_CHECK_LAUNCH();
+  return hipSuccess;
+}
+
+hipError_t launch_output_error(const OeLaunch& a) {
+  return a.bf16 ? run_output_error<TileBF16>(a) : run_output_error<TileF32>(a);
+}
+
+}  // namespace fpo

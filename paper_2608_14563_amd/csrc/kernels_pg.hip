@@ -1,0 +1,254 @@
+// Per-layer outer products (eq. w3update; App. A divisor) and the full-MLP
+// feedback path (eq. errh):
+//   transpose_pad : g~ [T, d] -> g~^T [d, Tp] (zero columns t >= T) so that the
+//                   token axis, the contraction axis, is contiguous
+//   outer_kernel  : C_m = scale * A_m B_m for a list of matrices (MFMA),
+//                   A_m [M, Tp] token-contiguous, B_m [T, N] row-major; epilogue
+//                   writes C and per-tile ||C||^2 (and <C, R>, ||R||^2)
+//   errh_kernel   : E = g~ W3_init (MFMA); du = E*SiLU(q), dq = E*u*SiLU'(q),
+//                   stored token-contiguous for the W1/W2 outer products
+//   reduce_parts  : fixed-order float64 sums of the tile partials
+#include "gemm.hpp"
+#include "launch.hpp"
+#include "prof.hpp"
+
+namespace fpo {
+
+template <typename T>
+__global__ __launch_bounds__(256) void transpose_pad_kernel(const T* __restrict__ src, int64_t R,
+                                                            int64_t C, T* __restrict__ dst,
+                                                            int64_t ldd, int64_t Rp) {
+  // src [R, C] -> dst [C, ldd] with dst[c, r] = src[r, c] for r < R, 0 for R <= r < Rp
+  __shared__ float tile[64][65];
+  const int64_t r0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64;
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int rr = e / 64, cc = e % 64;
+    const int64_t r = r0 + rr, c = c0 + cc;
+    tile[rr][cc] = (r < R && c < C) ? ld_as_f32(src, r * C + c) : 0.f;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int cc = e / 64, rr = e % 64;
+    const int64_t r = r0 + rr, c = c0 + cc;
+    if (c < C && r < Rp) st_from_f32(dst, c * ldd + r, tile[rr][cc]);
+  }
+}
+
+struct OuterArgs {
+  const void* A[kMaxMats];
+  const void* B[kMaxMats];
+  float* C[kMaxMats];
+  const float* R[kMaxMats];
+};
+
+template <class E>
+__global__ __launch_bounds__(256, 1) void outer_kernel(OuterArgs args, int M, int N, int K,
+                                                       int64_t lda, int64_t ldb, float scale,
+                                                       int ntm, double* __restrict__ part) {
+  using TT = Tile<E>;
+  using T = typename E::T;
+  __shared__ GemmSmem<E> sm;
+  __shared__ double red[3][4];
+  const int mat = blockIdx.y;
+  const int tile = blockIdx.x;
+  const int tm = tile % ntm, tn = tile / ntm;
+  const int m0 = tm * TT::BM, n0 = tn * TT::BN;
+  f32x4 acc[E::FM][E::FN];
+  zero_acc<E>(acc);
+  gemm_mainloop<E, true>(sm, acc, (const T*)args.A[mat], lda, M, (const T*)args.B[mat], ldb, N, K,
+                         m0, n0, 0, (K + TT::BK - 1) / TT::BK, NoHook{});
+  float* C = args.C[mat];
+  const float* R = args.R[mat];
+  const AccMap<E> mp;
+  float ss = 0.f, dt = 0.f, rr = 0.f;
+#pragma unroll
+  for (int f = 0; f < E::FM; ++f)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = m0 + mp.row(f, r);
+      const int c = n0 + mp.col(0);
+      if (row >= M || c >= N) continue;  // N % 8 == 0: a lane's FN columns are all in or all out
+#pragma unroll
+      for (int i = 0; i < E::FN; i += 4) {
+        f32x4 v = {acc[f][i][r] * scale, acc[f][i + 1][r] * scale, acc[f][i + 2][r] * scale,
+                   acc[f][i + 3][r] * scale};
+        const int64_t o = (int64_t)row * N + c + i;
+        if (C) *reinterpret_cast<f32x4*>(C + o) = v;
+        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+        if (R) {
+          f32x4 q = *reinterpret_cast<const f32x4*>(R + o);
+          dt += v.x * q.x + v.y * q.y + v.z * q.z + v.w * q.w;
+          rr += q.x * q.x + q.y * q.y + q.z * q.z + q.w * q.w;
+        }
+      }
+    }
+  double s0 = wave_sum_d((double)ss), s1 = wave_sum_d((double)dt), s2 = wave_sum_d((double)rr);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    red[0][w] = s0;
+    red[1][w] = s1;
+    red[2][w] = s2;
+  }
+  __syncthreads();
+  if (threadIdx.x < 3) {
+    const int k = threadIdx.x;
+    const double v = red[k][0] + red[k][1] + red[k][2] + red[k][3];
+    part[((int64_t)mat * gridDim.x + tile) * 3 + k] = v;
+  }
+}
+
+// E = g~ W3_init for one layer; writes du^T and dq^T [d_ff, Tp] (rows t < Tp;
+// t >= T give zero because the A rows load as zero and q, u are not read).
+template <class E>
+__global__ __launch_bounds__(256, 1) void errh_kernel(const typename E::T* __restrict__ g,
+                                                      const typename E::T* __restrict__ W3i,
+                                                      const typename E::T* __restrict__ q,
+                                                      const typename E::T* __restrict__ u, int T,
+                                                      int Tp, int d, int d_ff,
+                                                      typename E::T* __restrict__ dq_T,
+                                                      typename E::T* __restrict__ du_T) {
+  using TT = Tile<E>;
+  using TE = typename E::T;
+  __shared__ GemmSmem<E> sm;
+  f32x4 acc[E::FM][E::FN];
+  zero_acc<E>(acc);
+  const int m0 = blockIdx.x * TT::BM, n0 = blockIdx.y * TT::BN;
+  gemm_mainloop<E, true>(sm, acc, g, d, T, W3i, d_ff, d_ff, d, m0, n0, 0,
+                         (d + TT::BK - 1) / TT::BK, NoHook{});
+  const AccMap<E> mp;
+#pragma unroll
+  for (int f = 0; f < E::FM; ++f) {
+    const int t0 = m0 + mp.row(f, 0);  // 4 consecutive tokens t0..t0+3
+    if (t0 >= Tp) continue;            // Tp % 4 == 0
+#pragma unroll
+    for (int i = 0; i < E::FN; ++i) {
+      const int j = n0 + mp.col(i);
+      if (j >= d_ff) continue;
+      float vq[4], vu[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int t = t0 + r;
+        const float e = acc[f][i][r];
+        float dqv = 0.f, duv = 0.f;
+        if (t < T) {
+          const float qq = ld_as_f32(q, (int64_t)t * d_ff + j);
+          const float uu = ld_as_f32(u, (int64_t)t * d_ff + j);
+          const float sg = 1.0f / (1.0f + __expf(-qq));
+          duv = e * qq * sg;
+          dqv = e * uu * sg * (1.0f + qq * (1.0f - sg));
+        }
+        vq[r] = dqv;
+        vu[r] = duv;
+      }
+      st4<TE>(dq_T + (int64_t)j * Tp + t0, 0, f32x4{vq[0], vq[1], vq[2], vq[3]});
+      st4<TE>(du_T + (int64_t)j * Tp + t0, 0, f32x4{vu[0], vu[1], vu[2], vu[3]});
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void reduce_parts_kernel(const double* __restrict__ part,
+                                                           int ntiles, int mat_base,
+                                                           double* __restrict__ sumsq,
+                                                           double* __restrict__ dot,
+                                                           double* __restrict__ refsq) {
+  __shared__ double red[16];
+  const int mat = blockIdx.x;
+  const double* p = part + (int64_t)mat * ntiles * 3;
+  double a = 0.0, b = 0.0, c = 0.0;
+  for (int t = threadIdx.x; t < ntiles; t += 256) {
+    a += p[3 * t];
+    b += p[3 * t + 1];
+    c += p[3 * t + 2];
+  }
+  a = block_sum_d(a, red);
+  b = block_sum_d(b, red);
+  c = block_sum_d(c, red);
+  if (threadIdx.x == 0) {
+    if (sumsq) sumsq[mat_base + mat] = a;
+    if (dot) dot[mat] = b;
+    if (refsq) refsq[mat] = c;
+  }
+}
+
+int64_t pseudograd_tiles(bool bf16, int64_t M, int64_t N) {
+  const int BM = bf16 ? TileBF16::BM : TileF32::BM, BN = bf16 ? TileBF16::BN : TileF32::BN;
+  return ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+}
+
+#define FPO_CHECK_LAUNCH()             \
+  do {                                 \
+    hipError_t e_ = hipGetLastError(); \
+    if (e_ != hipSuccess) return e_;   \
+  } while (0)
+
+template <class E>
+static hipError_t run_pseudograd(const PgLaunch& a) {
+  using T = typename E::T;
+  using TT = Tile<E>;
+  hipStream_t st = (hipStream_t)a.stream;
+  // token-contiguous copy of the signal
+  FPO_LAUNCH("transpose_pad", st,
+             transpose_pad_kernel<T><<<dim3((unsigned)(a.Tp / 64), (unsigned)((a.d + 63) / 64)), dim3(256), 0, st>>>(
+      (const T*)a.g_lp, a.T, a.d, (T*)a.gT, a.Tp, a.Tp));
+  FPO_CHECK_LAUNCH();
+  // W3 outer products: M = d, N = d_ff, K = T
+  {
+    OuterArgs oa{};
+    for (int l = 0; l < a.L; ++l) {
+      oa.A[l] = a.gT;
+      oa.B[l] = a.a[l];
+      oa.C[l] = a.dW3[l];
+      oa.R[l] = a.ref[l];
+    }
+    const int ntm = (int)((a.d + TT::BM - 1) / TT::BM);
+    const int ntiles = (int)pseudograd_tiles(a.bf16, a.d, a.d_ff);
+    FPO_LAUNCH("outer", st,
+               outer_kernel<E><<<dim3(ntiles, a.L), dim3(256), 0, st>>>(oa, (int)a.d, (int)a.d_ff, (int)a.T,
+                                                           a.Tp, a.d_ff, a.scale, ntm, a.part));
+    FPO_CHECK_LAUNCH();
+    FPO_LAUNCH("reduce_parts", st,
+               reduce_parts_kernel<<<dim3(a.L), dim3(256), 0, st>>>(a.part, ntiles, 0, a.sumsq, a.ref_dot,
+                                                         a.ref_sumsq));
+    FPO_CHECK_LAUNCH();
+  }
+  if (a.full_mlp) {
+    const int ntm = (int)((a.d_ff + TT::BM - 1) / TT::BM);
+    const int ntiles = (int)pseudograd_tiles(a.bf16, a.d_ff, a.d);
+    for (int l = 0; l < a.L; ++l) {
+      FPO_LAUNCH("errh", st,
+                 errh_kernel<E><<<dim3((unsigned)((a.Tp + TT::BM - 1) / TT::BM), (unsigned)((a.d_ff + TT::BN - 1) / TT::BN)), dim3(256), 0, st>>>(
+          (const T*)a.g_lp, (const T*)a.W3i[l], (const T*)a.q[l], (const T*)a.u[l], (int)a.T,
+          (int)a.Tp, (int)a.d, (int)a.d_ff, (T*)a.dq_T, (T*)a.du_T));
+      FPO_CHECK_LAUNCH();
+      OuterArgs oa{};
+      oa.A[0] = a.dq_T;
+      oa.B[0] = a.x_in[l];
+      oa.C[0] = a.dW1[l];
+      oa.A[1] = a.du_T;
+      oa.B[1] = a.x_in[l];
+      oa.C[1] = a.dW2[l];
+      FPO_LAUNCH("outer", st,
+                 outer_kernel<E><<<dim3(ntiles, 2), dim3(256), 0, st>>>(oa, (int)a.d_ff, (int)a.d, (int)a.T,
+                                                           a.Tp, a.d, a.scale, ntm, a.part));
+      FPO_CHECK_LAUNCH();
+      // matrices W1(l) and W2(l) sit at a.L + l and 2 a.L + l of sumsq
+      if (a.sumsq) {
+        FPO_LAUNCH("reduce_parts", st,
+                   reduce_parts_kernel<<<dim3(1), dim3(256), 0, st>>>(a.part, ntiles, a.L + l, a.sumsq,
+                                                           nullptr, nullptr));
+        FPO_CHECK_LAUNCH();
+        FPO_LAUNCH("reduce_parts", st,
+                   reduce_parts_kernel<<<dim3(1), dim3(256), 0, st>>>(a.part + (int64_t)ntiles * 3, ntiles,
+                                                           2 * a.L + l, a.sumsq, nullptr, nullptr));
+        FPO_CHECK_LAUNCH();
+      }
+    }
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_pseudograd(const PgLaunch& a) {
+  return a.bf16 ? run_pseudograd<TileBF16>(a) : run_pseudograd<TileF32>(a);
+}
+
+}  // namespace fpo

@@ -1,0 +1,114 @@
+// Host-side launch descriptors shared between the C-ABI layer and the kernel
+// translation units. Every pointer is a device pointer; the ABI layer has
+// validated sizes and carved the workspace before filling these.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+namespace fpo {
+
+constexpr int kMaxMats = 64;
+
+struct OeLaunch {
+  bool bf16;
+  int64_t T, d, V, Vc;
+  int nsplit;
+  float eps, min_rms;
+  const void* h_final;
+  const void* gamma;
+  const void* W_U;
+  const int32_t* targets;
+  float* g_tilde;
+  void* g_tilde_lp;
+  float* g_pre;
+  float* lse;
+  float* loss;
+  int32_t* argmax;
+  int32_t* bad_targets;
+  // workspace
+  void* y;
+  void* P;
+  float* blk_m;
+  float* blk_s;
+  int32_t* blk_i;
+  float* fout;
+  float* alpha;
+  float* runM;
+  float* runS;
+  int32_t* runA;
+  float* ztgt;
+  float* G;
+  void* stream;
+};
+hipError_t launch_output_error(const OeLaunch& a);
+
+struct PgLaunch {
+  bool bf16;
+  bool full_mlp;
+  int64_t T, d, d_ff, Tp;
+  int L;
+  float scale;
+  const void* g_lp;                 // [T, d]
+  const void* a[kMaxMats];          // [T, d_ff]
+  const void* W3i[kMaxMats];        // [d, d_ff]
+  const void* q[kMaxMats];
+  const void* u[kMaxMats];
+  const void* x_in[kMaxMats];       // [T, d]
+  float* dW3[kMaxMats];
+  float* dW1[kMaxMats];
+  float* dW2[kMaxMats];
+  const float* ref[kMaxMats];
+  double* sumsq;                    // [n_mats] or null
+  double* ref_dot;
+  double* ref_sumsq;
+  // workspace
+  void* gT;                         // [d, Tp] transposed signal
+  void* dq_T;                       // [d_ff, Tp] full-MLP gate error (transposed)
+  void* du_T;                       // [d_ff, Tp] full-MLP up error (transposed)
+  double* part;                     // per-tile partials
+  void* stream;
+};
+hipError_t launch_pseudograd(const PgLaunch& a);
+int64_t pseudograd_tiles(bool bf16, int64_t M, int64_t N);
+
+struct UpdLaunch {
+  int kind;
+  float lr, momentum, beta1, beta2, adam_eps, weight_decay, clip_frac;
+  int64_t step;
+  int n;
+  int64_t numel[kMaxMats];
+  const float* grad[kMaxMats];
+  float* W[kMaxMats];
+  void* W_lp[kMaxMats];
+  bool lp_bf16;
+  float* s1[kMaxMats];
+  float* s2[kMaxMats];
+  const double* grad_sumsq;
+  double* W_sumsq;
+  float* clip_scale;
+  double* part;
+  void* stream;
+};
+hipError_t launch_update(const UpdLaunch& a);
+int64_t update_blocks(int64_t numel);
+
+struct CosLaunch {
+  int n;
+  int64_t numel[kMaxMats];
+  const float* A[kMaxMats];
+  const void* B[kMaxMats];
+  bool b_bf16;
+  double* dot;
+  double* sa;
+  double* sb;
+  float* cos;
+  double* part;
+  void* stream;
+};
+hipError_t launch_cosine(const CosLaunch& a);
+int64_t cosine_blocks(int64_t numel);
+
+}  // namespace fpo

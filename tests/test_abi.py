@@ -1,0 +1,176 @@
+"""C-ABI surface of libfpo: loading, exported symbols, workspace queries and
+every host-side validation error. Nothing here launches a kernel (each error
+path returns before any HIP call), so it runs without a GPU."""
+import ctypes as C
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2608_14563_amd import _lib as L
+from paper_2608_14563_amd import inputs as I
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HDR = os.path.join(ROOT, "include", "fpo.h")
+FAKE = 0x100000  # aligned, never dereferenced: every call below fails validation first
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(L.LIB_PATH):
+        pytest.fail("libfpo.so is not built (run __graft_entry__.build())")
+    return L.load()
+
+
+def header_functions(path=HDR):
+    txt = open(path).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(fpo_[a-z_]+)\s*\(", txt)))
+
+
+def all_header_functions():
+    inc = os.path.join(ROOT, "include")
+    names = []
+    for f in sorted(os.listdir(inc)):
+        if f.endswith(".h"):
+            names += header_functions(os.path.join(inc, f))
+    return sorted(set(names))
+
+
+def test_header_declares_the_abi():
+    names = header_functions()
+    assert set(names) == set(L.EXPORTS), names
+
+
+def test_library_exports_every_header_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", L.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    exported = {ln.split()[-1] for ln in out.splitlines() if ln.strip()}
+    names = all_header_functions()
+    assert "fpo_prof_read" in names
+    for name in names:
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_abi_version(lib):
+    assert lib.fpo_abi_version() == 1
+
+
+def oe(T=128, d=256, V=4096, dtype=L.FPO_BF16, eps=1e-6, min_rms=0.5, chunk=0):
+    return L.OeDesc(T, d, V, dtype, eps, min_rms, chunk)
+
+
+def test_workspace_queries_for_every_workload(lib):
+    for c in I.CONFIGS.values():
+        dt = L.FPO_BF16 if c.dtype == "bf16" else L.FPO_F32
+        ws = lib.fpo_output_error_workspace(C.byref(oe(c.T, c.d, c.V, dt)))
+        assert ws >= c.T * c.d * (2 if dt else 4)
+        pg = L.PgDesc(c.T, c.d, c.d_ff, c.L, dt, L.FPO_MODE_W3, 1.0 / c.T)
+        assert lib.fpo_pseudograd_workspace(C.byref(pg)) >= c.d * c.T * (2 if dt else 4)
+        pgf = L.PgDesc(c.T, c.d, c.d_ff, min(c.L, 21), dt, L.FPO_MODE_FULL_MLP, 1.0 / c.T)
+        assert lib.fpo_pseudograd_workspace(C.byref(pgf)) > lib.fpo_pseudograd_workspace(C.byref(pg)) or c.L > 21
+    n = (C.c_int64 * 2)(1024, 4096)
+    assert lib.fpo_apply_update_workspace(2, n) >= 16
+    assert lib.fpo_cosine_workspace(2, n) >= 48
+
+
+def test_invalid_descriptions_give_zero_workspace(lib):
+    assert lib.fpo_output_error_workspace(None) == 0
+    assert lib.fpo_output_error_workspace(C.byref(oe(d=250))) == 0
+    assert lib.fpo_output_error_workspace(C.byref(oe(dtype=7))) == 0
+
+
+def call_oe(lib, desc, ws=FAKE, ws_bytes=1 << 40, **over):
+    args = dict(h=FAKE, g=FAKE, W=FAKE, t=FAKE, gt=FAKE)
+    args.update(over)
+    return lib.fpo_output_error(C.byref(desc) if desc is not None else None, args["h"], args["g"], args["W"],
+                                args["t"], args["gt"], None, None, None, None, None, None, ws, ws_bytes, None)
+
+
+def test_output_error_validation(lib):
+    assert call_oe(lib, None) == L.FPO_ERR_NULL
+    assert call_oe(lib, oe(dtype=3)) == L.FPO_ERR_DTYPE
+    assert call_oe(lib, oe(T=0)) == L.FPO_ERR_SHAPE
+    assert call_oe(lib, oe(d=12)) == L.FPO_ERR_SHAPE
+    assert call_oe(lib, oe(V=4100)) == L.FPO_ERR_SHAPE
+    assert call_oe(lib, oe(V=1 << 31)) == L.FPO_ERR_SHAPE
+    assert call_oe(lib, oe(eps=-1.0)) == L.FPO_ERR_ARG
+    assert call_oe(lib, oe(min_rms=float("nan"))) == L.FPO_ERR_ARG
+    assert call_oe(lib, oe(chunk=-5)) == L.FPO_ERR_ARG
+    assert call_oe(lib, oe(), h=None) == L.FPO_ERR_NULL
+    assert call_oe(lib, oe(), gt=None) == L.FPO_ERR_NULL
+    assert call_oe(lib, oe(), W=FAKE + 4) == L.FPO_ERR_ARG
+    assert call_oe(lib, oe(), ws=None) == L.FPO_ERR_WORKSPACE
+    assert call_oe(lib, oe(), ws=FAKE + 64) == L.FPO_ERR_WORKSPACE
+    assert call_oe(lib, oe(), ws_bytes=100) == L.FPO_ERR_WORKSPACE
+    msg = lib.fpo_last_error().decode()
+    assert "workspace" in msg and "needed" in msg
+
+
+def arr(vals):
+    a = (C.c_void_p * len(vals))(*vals)
+    return C.cast(a, L.PP), a
+
+
+def test_pseudograd_validation(lib):
+    a, ka = arr([FAKE, FAKE])
+    dw, kd = arr([FAKE, FAKE])
+
+    def call(desc, A=a, dW3=dw, ref=None, ref_dot=None, opt=None, upd=None, ws_bytes=1 << 40, g=FAKE):
+        return lib.fpo_pseudograd(C.byref(desc) if desc is not None else None, g, A, None, None, None, None,
+                                  dW3, None, None, None, ref, ref_dot, None, opt, upd, FAKE, ws_bytes, None)
+
+    good = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_W3, 1 / 128)
+    assert call(None) == L.FPO_ERR_NULL
+    assert call(L.PgDesc(128, 256, 688, 2, 5, 0, 1.0)) == L.FPO_ERR_DTYPE
+    assert call(L.PgDesc(128, 256, 688, 2, 1, 9, 1.0)) == L.FPO_ERR_ARG
+    assert call(L.PgDesc(128, 256, 690, 2, 1, 0, 1.0)) == L.FPO_ERR_SHAPE
+    assert call(L.PgDesc(128, 256, 688, 65, 1, 0, 1.0)) == L.FPO_ERR_SHAPE
+    assert call(L.PgDesc(128, 256, 688, 2, 1, 0, float("inf"))) == L.FPO_ERR_ARG
+    assert call(good, g=None) == L.FPO_ERR_NULL
+    assert call(good, dW3=None) == L.FPO_ERR_NULL
+    r, kr = arr([FAKE, FAKE])
+    assert call(good, dW3=None, ref=r) == L.FPO_ERR_NULL  # ref needs ref_dot / ref_sumsq
+    o = L.Opt(0, 1e-4, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)
+    assert call(good, opt=C.byref(o)) == L.FPO_ERR_ARG  # opt without upd
+    full = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_FULL_MLP, 1 / 128)
+    assert call(full) == L.FPO_ERR_NULL
+    assert call(good, ws_bytes=16) == L.FPO_ERR_WORKSPACE
+    b, kb = arr([FAKE, None])
+    assert call(good, A=b) == L.FPO_ERR_NULL
+
+
+def test_apply_update_validation(lib):
+    g, kg = arr([FAKE])
+    W, kw = arr([FAKE])
+    s1, k1 = arr([FAKE])
+    n = (C.c_int64 * 1)(1024)
+    ub = L.UpdateBufs(W, None, s1, None, FAKE, None)
+
+    def call(o, n_mats=1, numel=n, upd=ub, lp=L.FPO_BF16, ws_bytes=1 << 20):
+        return lib.fpo_apply_update(C.byref(o) if o is not None else None, n_mats, numel, g, FAKE,
+                                    C.byref(upd) if upd is not None else None, lp, FAKE, ws_bytes, None)
+
+    sgd = L.Opt(0, 1e-4, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)
+    assert call(None) == L.FPO_ERR_NULL
+    assert call(L.Opt(4, 1e-4, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)) == L.FPO_ERR_ARG
+    assert call(L.Opt(0, -1.0, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)) == L.FPO_ERR_ARG
+    assert call(L.Opt(0, 1e-4, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 0)) == L.FPO_ERR_ARG
+    assert call(L.Opt(1, 1e-4, 0.9, 1.0, 0.999, 1e-8, 0.01, 0.01, 1)) == L.FPO_ERR_ARG
+    assert call(L.Opt(1, 1e-4, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)) == L.FPO_ERR_NULL  # AdamW needs state2
+    assert call(sgd, upd=None) == L.FPO_ERR_NULL
+    assert call(sgd, n_mats=0) == L.FPO_ERR_SHAPE
+    assert call(sgd, numel=(C.c_int64 * 1)(1022)) == L.FPO_ERR_SHAPE
+    assert call(sgd, lp=9) == L.FPO_ERR_DTYPE
+    assert call(sgd, ws_bytes=8) == L.FPO_ERR_WORKSPACE
+
+
+def test_cosine_validation(lib):
+    A, ka = arr([FAKE])
+    n = (C.c_int64 * 1)(1024)
+    assert lib.fpo_cosine(0, n, A, None, 0, None, None, None, None, FAKE, 1 << 20, None) == L.FPO_ERR_SHAPE
+    assert lib.fpo_cosine(1, None, A, None, 0, None, None, None, None, FAKE, 1 << 20, None) == L.FPO_ERR_NULL
+    assert lib.fpo_cosine(1, n, A, None, 3, None, None, None, None, FAKE, 1 << 20, None) == L.FPO_ERR_DTYPE
+    assert lib.fpo_cosine(1, (C.c_int64 * 1)(6), A, None, 0, None, None, None, None, FAKE, 1 << 20, None) == L.FPO_ERR_SHAPE
+    assert lib.fpo_cosine(1, n, A, None, 0, None, None, None, None, FAKE, 8, None) == L.FPO_ERR_WORKSPACE

@@ -1,0 +1,146 @@
+"""GPU parity of fpo_apply_update (relative clip + SGD-momentum / AdamW on
+fp32 masters) and of fpo_cosine against the fp64 oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2608_14563_amd import api
+from paper_2608_14563_amd import inputs as I
+from tests._util import assert_close, bf16_rne_bits, dev_tensor, ulp_diff_f32
+
+pytestmark = pytest.mark.gpu
+
+
+def make(shapes, seed, gscale):
+    r = np.random.default_rng(seed)
+    W = [(0.02 * r.standard_normal(s)).astype(np.float32) for s in shapes]
+    G = [[(gscale * r.standard_normal(s)).astype(np.float32) for s in shapes] for _ in range(3)]
+    return W, G
+
+
+@pytest.mark.parametrize("kind", ["sgd", "adamw"])
+@pytest.mark.parametrize("clip,gscale", [(0.01, 1e-2), (0.01, 1e-5), (0.0, 1e-3), (1.0, 1e-3)])
+def test_three_steps(dev, kind, clip, gscale):
+    shapes = [(256, 688), (64, 100), (8, 4)]
+    W, Gs = make(shapes, 7, gscale)
+    n = len(shapes)
+    tW = [torch.from_numpy(w.copy()).to(dev) for w in W]
+    s1 = [torch.zeros_like(w) for w in tW]
+    s2 = [torch.zeros_like(w) for w in tW] if kind == "adamw" else None
+    lp = [torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in tW]
+    Wsq = torch.tensor([float((w.astype(np.float64) ** 2).sum()) for w in W], dtype=torch.float64, device=dev)
+    clipv = torch.empty(n, device=dev)
+    # oracle state (fp64), fed the same gradients
+    oW = [w.astype(np.float64) for w in W]
+    ob = [np.zeros(s) for s in shapes]
+    om = [np.zeros(s) for s in shapes]
+    ov = [np.zeros(s) for s in shapes]
+    lr = 1e-3 if kind == "adamw" else 1e-2
+    for step in range(1, 4):
+        G = Gs[step - 1]
+        tg = [torch.from_numpy(g).to(dev) for g in G]
+        gsq = torch.tensor([float((g.astype(np.float64) ** 2).sum()) for g in G], dtype=torch.float64, device=dev)
+        Wprev = [w.cpu().numpy().copy() for w in tW]
+        opt = api.OptConfig(kind=0 if kind == "sgd" else 1, lr=lr, clip_frac=clip, step=step)
+        api.fpo_apply_update(opt, tg, gsq, tW, s1, Wsq, W_lp=lp, state2=s2, clip_scale=clipv)
+        torch.cuda.synchronize()
+        for m in range(n):
+            wsq_in = float((Wprev[m].astype(np.float64) ** 2).sum())
+            s = O.clip_scale(float(gsq[m]), wsq_in, clip)
+            assert abs(float(clipv[m]) - s) <= 1e-5 * s
+            Gh = s * G[m].astype(np.float64)
+            if kind == "sgd":
+                oW[m], ob[m] = O.sgd_momentum(oW[m], ob[m], Gh, lr, 0.9, step)
+                assert_close("momentum", s1[m].cpu().numpy(), ob[m], "f32")
+                b = s1[m].cpu().numpy().astype(np.float64)
+                expect = (Wprev[m].astype(np.float64) - np.float64(np.float32(lr)) * b).astype(np.float32)
+            else:
+                oW[m], om[m], ov[m] = O.adamw(oW[m], om[m], ov[m], Gh, lr, step)
+                assert_close("exp_avg", s1[m].cpu().numpy(), om[m], "f32")
+                assert_close("exp_avg_sq", s2[m].cpu().numpy(), ov[m], "f32")
+                mg = s1[m].cpu().numpy().astype(np.float64)
+                vg = s2[m].cpu().numpy().astype(np.float64)
+                lr32 = np.float64(np.float32(lr))
+                decay = np.float64(np.float32(1.0) - np.float32(lr) * np.float32(0.01))
+                expect = (Wprev[m].astype(np.float64) * decay
+                          - lr32 * (mg / (1 - 0.9 ** step)) / (np.sqrt(vg / (1 - 0.999 ** step)) + 1e-8)).astype(np.float32)
+            Wg = tW[m].cpu().numpy()
+            tol_ulp = 1 if kind == "sgd" else 4
+            assert ulp_diff_f32(Wg, expect).max() <= tol_ulp
+            # the master moved as the oracle says, to its own precision
+            assert np.max(np.abs(Wg - oW[m])) <= 1e-6 * max(1.0, np.max(np.abs(oW[m])))
+            assert np.array_equal(lp[m].view(torch.int16).cpu().numpy().view(np.uint16), bf16_rne_bits(Wg))
+            assert abs(float(Wsq[m]) - float((Wg.astype(np.float64) ** 2).sum())) <= 1e-6 * float(Wsq[m])
+
+
+def test_clip_edge_cases(dev):
+    W = torch.full((4, 4), 0.5, device=dev)
+    z = torch.zeros(4, 4, device=dev)
+    s1 = torch.zeros(4, 4, device=dev)
+    Wsq = torch.tensor([4.0], dtype=torch.float64, device=dev)
+    cs = torch.empty(1, device=dev)
+    api.fpo_apply_update(api.OptConfig(lr=1.0, clip_frac=0.01), [z], torch.zeros(1, dtype=torch.float64, device=dev),
+                         [W], [s1], Wsq, clip_scale=cs, lp_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert float(cs[0]) == 1.0 and torch.all(W == 0.5)
+    assert not torch.isnan(W).any()
+
+
+@pytest.mark.parametrize("bdtype", ["f32", "bf16"])
+def test_cosine(dev, bdtype):
+    r = np.random.default_rng(3)
+    A = [r.standard_normal((300, 100)).astype(np.float32) for _ in range(3)] + [np.zeros((8, 8), np.float32)]
+    B = [a + 0.5 * r.standard_normal(a.shape).astype(np.float32) for a in A]
+    B[1] = -A[1]
+    Bs = [b if bdtype == "f32" else I.bf16_bits(b) for b in B]
+    tA = [torch.from_numpy(a).to(dev) for a in A]
+    tB = [dev_tensor(b, dev) for b in Bs]
+    n = len(A)
+    dot, sa, sb = (torch.empty(n, dtype=torch.float64, device=dev) for _ in range(3))
+    cs = torch.empty(n, device=dev)
+    api.fpo_cosine(tA, tB, dot=dot, sumsq_A=sa, sumsq_B=sb, cos=cs)
+    torch.cuda.synchronize()
+    for m in range(n):
+        d0, na, nb, c0 = O.cosine(A[m], Bs[m])
+        if na == 0:
+            assert float(cs[m]) == 0.0
+            continue
+        assert_close("dot", float(dot[m]), d0, "f32")
+        assert_close("sa", float(sa[m]), na, "f32")
+        assert_close("sb", float(sb[m]), nb, "f32")
+        assert abs(float(cs[m]) - c0) <= 1e-6
+    assert abs(float(cs[1]) + 1.0) <= 1e-6
+    # norms-only mode
+    api.fpo_cosine(tA, None, sumsq_A=sa)
+    torch.cuda.synchronize()
+    assert_close("sa", float(sa[0]), O.cosine(A[0], A[0])[1], "f32")
+
+
+def test_fused_update_matches_separate_calls(dev):
+    c = I.CONFIGS[1].shrink(T=256, d=256, d_ff=512, L=2)
+    g = dev_tensor(I.synthetic_signal(c), dev)
+    acts = [dev_tensor(I.activation(c, l), dev) for l in range(2)]
+    W0 = [torch.from_numpy(I.master_weight(c, l)).to(dev) for l in range(2)]
+
+    def fresh():
+        W = [w.clone() for w in W0]
+        return W, [torch.zeros_like(w) for w in W], [torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in W], \
+            torch.tensor([float((w.double() ** 2).sum()) for w in W], dtype=torch.float64, device=dev)
+
+    opt = api.OptConfig(lr=1e-2, clip_frac=0.01, step=1)
+    # separate
+    W, s1, lp, Wsq = fresh()
+    dW = [torch.empty(256, 512, device=dev) for _ in range(2)]
+    ss = torch.empty(2, dtype=torch.float64, device=dev)
+    api.fpo_pseudograd(g, acts, dW3=dW, sumsq=ss)
+    api.fpo_apply_update(opt, dW, ss, W, s1, Wsq, W_lp=lp)
+    # fused
+    Wf, s1f, lpf, Wsqf = fresh()
+    dWf = [torch.empty(256, 512, device=dev) for _ in range(2)]
+    ssf = torch.empty(2, dtype=torch.float64, device=dev)
+    api.fpo_pseudograd(g, acts, dW3=dWf, sumsq=ssf, opt=opt, W_master=Wf, W_lp=lpf, state1=s1f, W_sumsq=Wsqf)
+    torch.cuda.synchronize()
+    for a, b in zip(W + s1 + dW, Wf + s1f + dWf):
+        assert torch.equal(a, b)
+    assert torch.equal(Wsq, Wsqf)
