@@ -155,13 +155,13 @@ def main():
     Wlp = [w.to(torch.bfloat16) for w in Wm]
     Wsq = torch.tensor([float((w.astype(np.float64) ** 2).sum()) for w in Wm_host], dtype=torch.float64, device=dev)
     T, d = c.T, c.d
-    g_t = torch.empty(T, d, device=dev)
+    g_t = torch.empty(T, d, dtype=torch.float32, device=dev)
     g_lp = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
-    lse = torch.empty(T, device=dev)
-    loss = torch.empty(T, device=dev)
+    lse = torch.empty(T, dtype=torch.float32, device=dev)
+    loss = torch.empty(T, dtype=torch.float32, device=dev)
     amax = torch.empty(T, dtype=torch.int32, device=dev)
     bad = torch.empty(1, dtype=torch.int32, device=dev)
-    dW = [torch.empty(d, c.d_ff, device=dev) for _ in range(c.L)]
+    dW = [torch.empty(d, c.d_ff, dtype=torch.float32, device=dev) for _ in range(c.L)]
     ss = torch.empty(c.L, dtype=torch.float64, device=dev)
     ws_oe = api.workspace(api.fpo_output_error_workspace(T, d, c.V, torch.bfloat16), dev)
     ws_pg = api.workspace(api.fpo_pseudograd_workspace(T, d, c.d_ff, c.L, torch.bfloat16), dev)

@@ -101,10 +101,14 @@ typedef struct {
  *   AdamW: beta1, beta2, adam_eps, decoupled weight_decay (0.01 in the
  *          paper), bias correction with the 1-based `step`.
  *   clip_frac  relative clip ||s*dW||_F <= clip_frac * ||W||_F applied to the
- *          gradient before the step (0.01 in the paper); <= 0 disables it. */
+ *          gradient before the step (0.01 in the paper); <= 0 disables it.
+ * Hyperparameters are double; the derived factors (1 - beta, 1 - lr * wd,
+ * bias corrections) are formed in double on the host and rounded once to
+ * float32 for the device arithmetic. AdamW moments must be zero before step 1;
+ * SGD ignores the buffer's content at step 1. */
 typedef struct {
   int32_t kind; /* fpo_opt_kind */
-  float lr, momentum, beta1, beta2, adam_eps, weight_decay, clip_frac;
+  double lr, momentum, beta1, beta2, adam_eps, weight_decay, clip_frac;
   int64_t step;
 } fpo_opt;
 

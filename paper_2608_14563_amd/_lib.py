@@ -37,9 +37,9 @@ class PgDesc(C.Structure):
 
 
 class Opt(C.Structure):
-    _fields_ = [("kind", C.c_int32), ("lr", C.c_float), ("momentum", C.c_float), ("beta1", C.c_float),
-                ("beta2", C.c_float), ("adam_eps", C.c_float), ("weight_decay", C.c_float),
-                ("clip_frac", C.c_float), ("step", C.c_int64)]
+    _fields_ = [("kind", C.c_int32), ("lr", C.c_double), ("momentum", C.c_double), ("beta1", C.c_double),
+                ("beta2", C.c_double), ("adam_eps", C.c_double), ("weight_decay", C.c_double),
+                ("clip_frac", C.c_double), ("step", C.c_int64)]
 
 
 class UpdateBufs(C.Structure):

@@ -31,12 +31,17 @@ def dtype_code(t: torch.dtype) -> int:
     raise TypeError(f"unsupported dtype {t}")
 
 
-def _p(t: Optional[torch.Tensor]) -> Optional[int]:
+def _p(t: Optional[torch.Tensor], dtype: Optional[torch.dtype] = None) -> Optional[int]:
     if t is None:
         return None
     if not t.is_contiguous():
         raise ValueError("tensors passed to libfpo must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"expected a {dtype} tensor, got {t.dtype}")
     return t.data_ptr()
+
+
+F32, F64, I32 = torch.float32, torch.float64, torch.int32
 
 
 def _stream(dev: torch.device) -> int:
@@ -49,12 +54,12 @@ class _Keep:
     def __init__(self):
         self.refs = []
 
-    def arr(self, tensors: Optional[Sequence[Optional[torch.Tensor]]]):
+    def arr(self, tensors: Optional[Sequence[Optional[torch.Tensor]]], dtype=None):
         if tensors is None:
             return None
         a = (C.c_void_p * max(1, len(tensors)))()
         for i, t in enumerate(tensors):
-            a[i] = _p(t)
+            a[i] = _p(t, dtype)
         self.refs.append(a)
         return C.cast(a, L.PP)
 
@@ -88,13 +93,15 @@ def fpo_output_error(h_final, gamma, W_U, targets, g_tilde, g_tilde_lp=None, g_p
                      vocab_chunk=0):
     T, d = h_final.shape
     V = W_U.shape[0]
-    desc = _oe_desc(T, d, V, dtype_code(h_final.dtype), eps, min_rms, vocab_chunk)
+    op = h_final.dtype
+    desc = _oe_desc(T, d, V, dtype_code(op), eps, min_rms, vocab_chunk)
     lib = L.load()
     if ws is None:
         ws = workspace(lib.fpo_output_error_workspace(C.byref(desc)), h_final.device)
     L.check(lib.fpo_output_error(
-        C.byref(desc), _p(h_final), _p(gamma), _p(W_U), _p(targets), _p(g_tilde), _p(g_tilde_lp),
-        _p(g_pre), _p(lse), _p(loss), _p(argmax), _p(bad_targets), _p(ws), ws.numel(),
+        C.byref(desc), _p(h_final), _p(gamma, op), _p(W_U, op), _p(targets, I32), _p(g_tilde, F32),
+        _p(g_tilde_lp, op), _p(g_pre, F32), _p(lse, F32), _p(loss, F32), _p(argmax, I32),
+        _p(bad_targets, I32), _p(ws), ws.numel(),
         _stream(h_final.device)))
     return ws
 
@@ -117,9 +124,9 @@ class OptConfig:
                      self.weight_decay, self.clip_frac, self.step)
 
 
-def _upd_bufs(keep: _Keep, W_master, W_lp, state1, state2, W_sumsq, clip_scale):
-    return L.UpdateBufs(keep.arr(W_master), keep.arr(W_lp), keep.arr(state1), keep.arr(state2),
-                        _p(W_sumsq), _p(clip_scale))
+def _upd_bufs(keep: _Keep, W_master, W_lp, state1, state2, W_sumsq, clip_scale, lp_dtype):
+    return L.UpdateBufs(keep.arr(W_master, F32), keep.arr(W_lp, lp_dtype), keep.arr(state1, F32),
+                        keep.arr(state2, F32), _p(W_sumsq, F64), _p(clip_scale, F32))
 
 
 # --------------------------------------------------------------------- pseudograd
@@ -143,12 +150,13 @@ def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, 
     if ws is None:
         ws = workspace(lib.fpo_pseudograd_workspace(C.byref(desc)), g_tilde_lp.device)
     k = _Keep()
+    op = g_tilde_lp.dtype
     o = opt.c() if opt is not None else None
-    ub = _upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale) if opt is not None else None
+    ub = _upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale, op) if opt is not None else None
     L.check(lib.fpo_pseudograd(
-        C.byref(desc), _p(g_tilde_lp), k.arr(a), k.arr(W3_init), k.arr(gate), k.arr(up),
-        k.arr(x_in), k.arr(dW3), k.arr(dW1), k.arr(dW2), _p(sumsq), k.arr(ref), _p(ref_dot),
-        _p(ref_sumsq), C.byref(o) if o is not None else None, C.byref(ub) if ub is not None else None,
+        C.byref(desc), _p(g_tilde_lp), k.arr(a, op), k.arr(W3_init, op), k.arr(gate, op), k.arr(up, op),
+        k.arr(x_in, op), k.arr(dW3, F32), k.arr(dW1, F32), k.arr(dW2, F32), _p(sumsq, F64),
+        k.arr(ref, F32), _p(ref_dot, F64), _p(ref_sumsq, F64), C.byref(o) if o is not None else None, C.byref(ub) if ub is not None else None,
         _p(ws), ws.numel(), _stream(g_tilde_lp.device)))
     return ws
 
@@ -168,8 +176,8 @@ def fpo_apply_update(opt: OptConfig, grad, grad_sumsq, W_master, state1, W_sumsq
     if ws is None:
         ws = workspace(lib.fpo_apply_update_workspace(n, numel), grad[0].device)
     o = opt.c()
-    ub = _upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale)
-    L.check(lib.fpo_apply_update(C.byref(o), n, numel, k.arr(grad), _p(grad_sumsq), C.byref(ub),
+    ub = _upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale, lp_dtype)
+    L.check(lib.fpo_apply_update(C.byref(o), n, numel, k.arr(grad, F32), _p(grad_sumsq, F64), C.byref(ub),
                                  dtype_code(lp_dtype), _p(ws), ws.numel(), _stream(grad[0].device)))
     return ws
 
@@ -187,7 +195,8 @@ def fpo_cosine(A, B=None, dot=None, sumsq_A=None, sumsq_B=None, cos=None, ws=Non
     lib = L.load()
     if ws is None:
         ws = workspace(lib.fpo_cosine_workspace(n, numel), A[0].device)
-    dt = dtype_code(B[0].dtype) if B is not None else L.FPO_F32
-    L.check(lib.fpo_cosine(n, numel, k.arr(A), k.arr(B), dt, _p(dot), _p(sumsq_A), _p(sumsq_B),
-                           _p(cos), _p(ws), ws.numel(), _stream(A[0].device)))
+    bdt = B[0].dtype if B is not None else F32
+    dt = dtype_code(bdt)
+    L.check(lib.fpo_cosine(n, numel, k.arr(A, F32), k.arr(B, bdt), dt, _p(dot, F64), _p(sumsq_A, F64),
+                           _p(sumsq_B, F64), _p(cos, F32), _p(ws), ws.numel(), _stream(A[0].device)))
     return ws

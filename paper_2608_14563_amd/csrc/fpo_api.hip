@@ -182,16 +182,16 @@ int check_opt(const fpo_opt* o) {
   if (!o) return fail(FPO_ERR_NULL, "optimizer description is NULL");
   if (o->kind != FPO_OPT_SGD && o->kind != FPO_OPT_ADAMW)
     return fail(FPO_ERR_ARG, "unknown optimizer kind %d", (int)o->kind);
-  if (!(o->lr >= 0.f) || !std::isfinite(o->lr)) return fail(FPO_ERR_ARG, "lr must be finite and >= 0");
+  if (!(o->lr >= 0.0) || !std::isfinite(o->lr)) return fail(FPO_ERR_ARG, "lr must be finite and >= 0");
   if (o->step < 1) return fail(FPO_ERR_ARG, "step is 1-based (got %lld)", (long long)o->step);
   if (!std::isfinite(o->clip_frac)) return fail(FPO_ERR_ARG, "clip_frac must be finite");
-  if (o->kind == FPO_OPT_SGD && !(o->momentum >= 0.f && o->momentum <= 1.f))
+  if (o->kind == FPO_OPT_SGD && !(o->momentum >= 0.0 && o->momentum <= 1.0))
     return fail(FPO_ERR_ARG, "momentum must be in [0, 1]");
   if (o->kind == FPO_OPT_ADAMW) {
-    if (!(o->beta1 >= 0.f && o->beta1 < 1.f) || !(o->beta2 >= 0.f && o->beta2 < 1.f))
+    if (!(o->beta1 >= 0.0 && o->beta1 < 1.0) || !(o->beta2 >= 0.0 && o->beta2 < 1.0))
       return fail(FPO_ERR_ARG, "AdamW betas must be in [0, 1)");
-    if (!(o->adam_eps > 0.f)) return fail(FPO_ERR_ARG, "AdamW eps must be > 0");
-    if (!(o->weight_decay >= 0.f)) return fail(FPO_ERR_ARG, "weight_decay must be >= 0");
+    if (!(o->adam_eps > 0.0)) return fail(FPO_ERR_ARG, "AdamW eps must be > 0");
+    if (!(o->weight_decay >= 0.0)) return fail(FPO_ERR_ARG, "weight_decay must be >= 0");
   }
   return FPO_OK;
 }

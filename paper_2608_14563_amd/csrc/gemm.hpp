@@ -301,6 +301,29 @@ __device__ __forceinline__ void zero_acc(f32x4 (&acc)[E::FM][E::FN]) {
     for (int i = 0; i < E::FN; ++i) acc[f][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 }
 
+// Workgroup -> tile mapping. Consecutive workgroup ids are dispatched
+// round-robin over the 8 XCDs, each with its own L2. xcd_remap gives every
+// XCD a contiguous range of logical tile ids; grouped_tile walks a range in
+// groups of `gm` tile rows, so the workgroups resident on one XCD at a time
+// cover a few tile rows x a few tile columns and share A rows and B columns
+// in that XCD's L2 while they stream through K together.
+constexpr int kXcds = 8;
+
+__device__ __forceinline__ int xcd_remap(int bid, int nblk) {
+  const int xcd = bid % kXcds, slot = bid / kXcds;
+  const int per = nblk / kXcds, rem = nblk % kXcds;
+  return xcd * per + (xcd < rem ? xcd : rem) + slot;
+}
+
+__device__ __forceinline__ void grouped_tile(int id, int ntm, int ntn, int gm, int& tm, int& tn) {
+  const int width = gm * ntn;
+  const int first = (id / width) * gm;
+  const int rows = (ntm - first) < gm ? (ntm - first) : gm;
+  const int r = id % width;
+  tm = first + r % rows;
+  tn = r / rows;
+}
+
 // Output coordinates of accumulator element [f][i][r] (relative to the tile).
 template <class E>
 struct AccMap {

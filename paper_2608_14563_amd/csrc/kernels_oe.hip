@@ -50,7 +50,10 @@ __global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
   __shared__ GemmSmem<E> sm;
   f32x4 acc[E::FM][E::FN];
   zero_acc<E>(acc);
-  const int m0 = blockIdx.x * TT::BM, n0 = blockIdx.y * TT::BN;
+  const int ntm = (T + TT::BM - 1) / TT::BM, ntn = (vc_valid + TT::BN - 1) / TT::BN;
+  int tm, tn;
+  grouped_tile(xcd_remap(blockIdx.x, gridDim.x), ntm, ntn, 8, tm, tn);
+  const int m0 = tm * TT::BM, n0 = tn * TT::BN;
   gemm_mainloop<E, false>(sm, acc, y, d, T, Wc, d, vc_valid, d, m0, n0, 0,
                           (d + TT::BK - 1) / TT::BK, NoHook{});
   const AccMap<E> mp;
@@ -207,15 +210,19 @@ __global__ __launch_bounds__(256) void chunk_stats_kernel(
 template <class E>
 __global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
     const typename E::T* __restrict__ P, int64_t ldp, const typename E::T* __restrict__ Wc,
-    int T, int d, int vc_valid, int nb, int bps, int blkw, int first,
+    int T, int d, int vc_valid, int nb, int bps, int blkw, int first, int nsplit,
     const float* __restrict__ fout, const float* __restrict__ alpha, float* __restrict__ G,
     int64_t split_stride) {
   using TT = Tile<E>;
   __shared__ GemmSmem<E> sm;
   f32x4 acc[E::FM][E::FN];
   zero_acc<E>(acc);
-  const int m0 = blockIdx.x * TT::BM, n0 = blockIdx.y * TT::BN, sp = blockIdx.z;
-  const int nsplit = gridDim.z;
+  // tiles: (token rows) x (split, column); columns of one split are adjacent
+  const int ntm = (T + TT::BM - 1) / TT::BM, ntn = (d + TT::BN - 1) / TT::BN;
+  int tm, tsn;
+  grouped_tile(xcd_remap(blockIdx.x, gridDim.x), ntm, ntn * nsplit, 8, tm, tsn);
+  const int sp = tsn / ntn;
+  const int m0 = tm * TT::BM, n0 = (tsn % ntn) * TT::BN;
   float* Gs = G + sp * split_stride;
   const int tpb = blkw / TT::BK;
   const int nkt = (vc_valid + TT::BK - 1) / TT::BK;
@@ -334,7 +341,7 @@ static hipError_t run_output_error(const OeLaunch& a) {
     const int gn = (vc_valid + TT::BN - 1) / TT::BN;
     const int nbv = (vc_valid + TT::WTN - 1) / TT::WTN;  // blocks holding a valid column
     FPO_LAUNCH("logits_chunk", st,
-               logits_chunk_kernel<E><<<dim3(gm, gn), dim3(256), 0, st>>>(
+               logits_chunk_kernel<E><<<dim3(gm * gn), dim3(256), 0, st>>>(
         y, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, (int)v0, a.targets, P, a.Vc, nbv,
         a.blk_m, a.blk_s, a.blk_i, a.ztgt));
     FPO_CHECK_LAUNCH();
@@ -345,9 +352,9 @@ static hipError_t run_output_error(const OeLaunch& a) {
         a.runM, a.runS, a.runA, a.fout, a.alpha, P, a.Vc));
     FPO_CHECK_LAUNCH();
     FPO_LAUNCH("proj_chunk", st,
-               proj_chunk_kernel<E><<<dim3(gm, (unsigned)((a.d + TT::BN - 1) / TT::BN), a.nsplit), dim3(256), 0, st>>>(
-        P, a.Vc, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, nbv, bps, TT::WTN, c == 0, a.fout,
-        a.alpha, a.G, a.T * a.d));
+               proj_chunk_kernel<E><<<dim3(gm * (unsigned)((a.d + TT::BN - 1) / TT::BN) * a.nsplit), dim3(256), 0, st>>>(
+        P, a.Vc, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, nbv, bps, TT::WTN, c == 0, a.nsplit,
+        a.fout, a.alpha, a.G, a.T * a.d));
     FPO_CHECK_LAUNCH();
   }
   FPO_LAUNCH("finalize_vjp", st,

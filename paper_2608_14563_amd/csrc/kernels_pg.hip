@@ -44,14 +44,19 @@ struct OuterArgs {
 template <class E>
 __global__ __launch_bounds__(256, 1) void outer_kernel(OuterArgs args, int M, int N, int K,
                                                        int64_t lda, int64_t ldb, float scale,
-                                                       int ntm, double* __restrict__ part) {
+                                                       double* __restrict__ part) {
   using TT = Tile<E>;
   using T = typename E::T;
   __shared__ GemmSmem<E> sm;
   __shared__ double red[3][4];
-  const int mat = blockIdx.y;
-  const int tile = blockIdx.x;
-  const int tm = tile % ntm, tn = tile / ntm;
+  // one flat grid over (matrix, tile); each XCD takes a contiguous range
+  const int ntm = (M + TT::BM - 1) / TT::BM, ntn = (N + TT::BN - 1) / TT::BN;
+  const int ntiles = ntm * ntn;
+  const int id = xcd_remap(blockIdx.x, gridDim.x);
+  const int mat = id / ntiles;
+  const int tile = id % ntiles;
+  int tm, tn;
+  grouped_tile(tile, ntm, ntn, 8, tm, tn);
   const int m0 = tm * TT::BM, n0 = tn * TT::BN;
   f32x4 acc[E::FM][E::FN];
   zero_acc<E>(acc);
@@ -93,7 +98,7 @@ __global__ __launch_bounds__(256, 1) void outer_kernel(OuterArgs args, int M, in
   if (threadIdx.x < 3) {
     const int k = threadIdx.x;
     const double v = red[k][0] + red[k][1] + red[k][2] + red[k][3];
-    part[((int64_t)mat * gridDim.x + tile) * 3 + k] = v;
+    part[((int64_t)mat * ntiles + tm + (int64_t)tn * ntm) * 3 + k] = v;
   }
 }
 
@@ -112,7 +117,10 @@ __global__ __launch_bounds__(256, 1) void errh_kernel(const typename E::T* __res
   __shared__ GemmSmem<E> sm;
   f32x4 acc[E::FM][E::FN];
   zero_acc<E>(acc);
-  const int m0 = blockIdx.x * TT::BM, n0 = blockIdx.y * TT::BN;
+  const int ntm = (Tp + TT::BM - 1) / TT::BM, ntn = (d_ff + TT::BN - 1) / TT::BN;
+  int tm, tn;
+  grouped_tile(xcd_remap(blockIdx.x, gridDim.x), ntm, ntn, 8, tm, tn);
+  const int m0 = tm * TT::BM, n0 = tn * TT::BN;
   gemm_mainloop<E, true>(sm, acc, g, d, T, W3i, d_ff, d_ff, d, m0, n0, 0,
                          (d + TT::BK - 1) / TT::BK, NoHook{});
   const AccMap<E> mp;
@@ -200,11 +208,10 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
       oa.C[l] = a.dW3[l];
       oa.R[l] = a.ref[l];
     }
-    const int ntm = (int)((a.d + TT::BM - 1) / TT::BM);
     const int ntiles = (int)pseudograd_tiles(a.bf16, a.d, a.d_ff);
     FPO_LAUNCH("outer", st,
-               outer_kernel<E><<<dim3(ntiles, a.L), dim3(256), 0, st>>>(oa, (int)a.d, (int)a.d_ff, (int)a.T,
-                                                           a.Tp, a.d_ff, a.scale, ntm, a.part));
+               outer_kernel<E><<<dim3(ntiles * a.L), dim3(256), 0, st>>>(oa, (int)a.d, (int)a.d_ff, (int)a.T,
+                                                           a.Tp, a.d_ff, a.scale, a.part));
     FPO_CHECK_LAUNCH();
     FPO_LAUNCH("reduce_parts", st,
                reduce_parts_kernel<<<dim3(a.L), dim3(256), 0, st>>>(a.part, ntiles, 0, a.sumsq, a.ref_dot,
@@ -212,11 +219,10 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
     FPO_CHECK_LAUNCH();
   }
   if (a.full_mlp) {
-    const int ntm = (int)((a.d_ff + TT::BM - 1) / TT::BM);
     const int ntiles = (int)pseudograd_tiles(a.bf16, a.d_ff, a.d);
     for (int l = 0; l < a.L; ++l) {
       FPO_LAUNCH("errh", st,
-                 errh_kernel<E><<<dim3((unsigned)((a.Tp + TT::BM - 1) / TT::BM), (unsigned)((a.d_ff + TT::BN - 1) / TT::BN)), dim3(256), 0, st>>>(
+                 errh_kernel<E><<<dim3((unsigned)(((a.Tp + TT::BM - 1) / TT::BM) * ((a.d_ff + TT::BN - 1) / TT::BN))), dim3(256), 0, st>>>(
           (const T*)a.g_lp, (const T*)a.W3i[l], (const T*)a.q[l], (const T*)a.u[l], (int)a.T,
           (int)a.Tp, (int)a.d, (int)a.d_ff, (T*)a.dq_T, (T*)a.du_T));
       FPO_CHECK_LAUNCH();
@@ -228,8 +234,8 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
       oa.B[1] = a.x_in[l];
       oa.C[1] = a.dW2[l];
       FPO_LAUNCH("outer", st,
-                 outer_kernel<E><<<dim3(ntiles, 2), dim3(256), 0, st>>>(oa, (int)a.d_ff, (int)a.d, (int)a.T,
-                                                           a.Tp, a.d, a.scale, ntm, a.part));
+                 outer_kernel<E><<<dim3(ntiles * 2), dim3(256), 0, st>>>(oa, (int)a.d_ff, (int)a.d, (int)a.T,
+                                                           a.Tp, a.d, a.scale, a.part));
       FPO_CHECK_LAUNCH();
       // matrices W1(l) and W2(l) sit at a.L + l and 2 a.L + l of sumsq
       if (a.sumsq) {

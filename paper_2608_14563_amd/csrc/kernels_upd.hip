@@ -25,10 +25,13 @@ struct UpdArgs {
   int64_t blk0[kUpdBatch + 1];
 };
 
+// Device copies of the hyperparameters: each derived factor is formed in double
+// on the host and rounded once to float.
 struct OptScalars {
   int kind, first, lp_bf16;
-  float lr, momentum, beta1, beta2, adam_eps, weight_decay, clip_frac;
+  float lr, momentum, beta1, one_m_beta1, beta2, one_m_beta2, adam_eps, decay;
   float inv_bc1, inv_sqrt_bc2;  // 1/(1-beta1^t), 1/sqrt(1-beta2^t)
+  double clip_frac;
 };
 
 __device__ __forceinline__ int find_mat(const int64_t* blk0, int n, int64_t b) {
@@ -37,9 +40,9 @@ __device__ __forceinline__ int find_mat(const int64_t* blk0, int n, int64_t b) {
   return m;
 }
 
-__device__ __forceinline__ float clip_factor(double gs, double ws, float frac) {
-  if (frac <= 0.f || gs == 0.0) return 1.0f;
-  const double s = (double)frac * sqrt(ws) / sqrt(gs);
+__device__ __forceinline__ float clip_factor(double gs, double ws, double frac) {
+  if (frac <= 0.0 || gs == 0.0) return 1.0f;
+  const double s = frac * sqrt(ws) / sqrt(gs);
   return (float)(s < 1.0 ? s : 1.0);
 }
 
@@ -81,16 +84,15 @@ __global__ __launch_bounds__(256) void update_kernel(UpdArgs a, int n, OptScalar
     } else {  // AdamW, decoupled weight decay, bias corrected
       f32x4 mv = *reinterpret_cast<const f32x4*>(s1 + i);
       f32x4 vv = *reinterpret_cast<const f32x4*>(s2 + i);
-      const float decay = 1.0f - o.lr * o.weight_decay;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const float ge = gv[e];
-        const float me = o.beta1 * mv[e] + (1.0f - o.beta1) * ge;
-        const float ve = o.beta2 * vv[e] + (1.0f - o.beta2) * ge * ge;
+        const float me = o.beta1 * mv[e] + o.one_m_beta1 * ge;
+        const float ve = o.beta2 * vv[e] + o.one_m_beta2 * ge * ge;
         mv[e] = me;
         vv[e] = ve;
         const float denom = sqrtf(ve) * o.inv_sqrt_bc2 + o.adam_eps;
-        w[e] = w[e] * decay - o.lr * (me * o.inv_bc1) / denom;
+        w[e] = w[e] * o.decay - o.lr * (me * o.inv_bc1) / denom;
       }
       *reinterpret_cast<f32x4*>(s1 + i) = mv;
       *reinterpret_cast<f32x4*>(s2 + i) = vv;
@@ -137,15 +139,17 @@ hipError_t launch_update(const UpdLaunch& a) {
   o.kind = a.kind;
   o.first = a.step <= 1;
   o.lp_bf16 = a.lp_bf16;
-  o.lr = a.lr;
-  o.momentum = a.momentum;
-  o.beta1 = a.beta1;
-  o.beta2 = a.beta2;
-  o.adam_eps = a.adam_eps;
-  o.weight_decay = a.weight_decay;
+  o.lr = (float)a.lr;
+  o.momentum = (float)a.momentum;
+  o.beta1 = (float)a.beta1;
+  o.one_m_beta1 = (float)(1.0 - a.beta1);
+  o.beta2 = (float)a.beta2;
+  o.one_m_beta2 = (float)(1.0 - a.beta2);
+  o.adam_eps = (float)a.adam_eps;
+  o.decay = (float)(1.0 - a.lr * a.weight_decay);
   o.clip_frac = a.clip_frac;
-  const double bc1 = 1.0 - pow((double)a.beta1, (double)a.step);
-  const double bc2 = 1.0 - pow((double)a.beta2, (double)a.step);
+  const double bc1 = 1.0 - pow(a.beta1, (double)a.step);
+  const double bc2 = 1.0 - pow(a.beta2, (double)a.step);
   o.inv_bc1 = (float)(1.0 / bc1);
   o.inv_sqrt_bc2 = (float)(1.0 / sqrt(bc2));
   int64_t part_off = 0;

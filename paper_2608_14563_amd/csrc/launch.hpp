@@ -76,7 +76,7 @@ int64_t pseudograd_tiles(bool bf16, int64_t M, int64_t N);
 
 struct UpdLaunch {
   int kind;
-  float lr, momentum, beta1, beta2, adam_eps, weight_decay, clip_frac;
+  double lr, momentum, beta1, beta2, adam_eps, weight_decay, clip_frac;
   int64_t step;
   int n;
   int64_t numel[kMaxMats];

@@ -19,7 +19,7 @@ import torch
 import oracle as O
 
 GOLD = os.path.join(os.path.dirname(__file__), "golden")
-torch.set_default_dtype(torch.float64)
+
 
 
 def toy(seed=0, T=4, d=6, V=16, d_ff=10, L=2):

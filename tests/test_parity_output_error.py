@@ -19,8 +19,8 @@ def run_gpu(x, gamma, W, y, dtype, dev, eps=1e-6, min_rms=0.5, chunk=0):
     tx = dev_tensor(x, dev)
     tdt = tx.dtype
     out = dict(
-        g_tilde=torch.empty(T, d, device=dev), g_tilde_lp=torch.empty(T, d, dtype=tdt, device=dev),
-        g_pre=torch.empty(T, d, device=dev), lse=torch.empty(T, device=dev), loss=torch.empty(T, device=dev),
+        g_tilde=torch.empty(T, d, dtype=torch.float32, device=dev), g_tilde_lp=torch.empty(T, d, dtype=tdt, device=dev),
+        g_pre=torch.empty(T, d, dtype=torch.float32, device=dev), lse=torch.empty(T, dtype=torch.float32, device=dev), loss=torch.empty(T, dtype=torch.float32, device=dev),
         argmax=torch.empty(T, dtype=torch.int32, device=dev), bad_targets=torch.full((1,), -7, dtype=torch.int32, device=dev))
     api.fpo_output_error(tx, dev_tensor(gamma, dev), dev_tensor(W, dev), dev_tensor(y, dev), eps=eps,
                          min_rms=min_rms, vocab_chunk=chunk, **out)

@@ -21,7 +21,7 @@ def run_w3(c, g, acts, dev, refs=None, store=True):
     T, d = g.shape
     tg = dev_tensor(g, dev)
     ta = [dev_tensor(a, dev) for a in acts]
-    dW = [torch.empty(d, c.d_ff, device=dev) for _ in acts] if store else None
+    dW = [torch.empty(d, c.d_ff, dtype=torch.float32, device=dev) for _ in acts] if store else None
     ss = torch.full((len(acts),), -1.0, dtype=torch.float64, device=dev)
     kw = {}
     if refs is not None:
@@ -86,9 +86,9 @@ def test_full_mlp(dev, cid, T, d, d_ff, L):
     extras = [I.full_mlp_extra(c, l) for l in range(L)]
     W3i = [I.to_storage(I.master_weight(c, l), c.dtype) for l in range(L)]
     tg = dev_tensor(g, dev)
-    dW3 = [torch.empty(d, d_ff, device=dev) for _ in range(L)]
-    dW1 = [torch.empty(d_ff, d, device=dev) for _ in range(L)]
-    dW2 = [torch.empty(d_ff, d, device=dev) for _ in range(L)]
+    dW3 = [torch.empty(d, d_ff, dtype=torch.float32, device=dev) for _ in range(L)]
+    dW1 = [torch.empty(d_ff, d, dtype=torch.float32, device=dev) for _ in range(L)]
+    dW2 = [torch.empty(d_ff, d, dtype=torch.float32, device=dev) for _ in range(L)]
     ss = torch.empty(3 * L, dtype=torch.float64, device=dev)
     api.fpo_pseudograd(tg, [dev_tensor(cc[2], dev) for cc in caches], dW3=dW3, sumsq=ss,
                        W3_init=[dev_tensor(w, dev) for w in W3i], gate=[dev_tensor(cc[0], dev) for cc in caches],
