@@ -8,6 +8,7 @@
 //   finalize_vjp : g = sum_s G_s / S - W_U[y]; clamped RMSNorm VJP  (HBM bound)
 // The T x V logits never reach HBM; only one chunk of p~ is staged.
 #include "gemm.hpp"
+#include "gemm2.hpp"
 #include "launch.hpp"
 #include "prof.hpp"
 
@@ -37,43 +38,35 @@ __global__ __launch_bounds__(256) void rms_forward_kernel(const T* __restrict__ 
 }
 
 // ------------------------------------------------------------------ logits
-// One workgroup: BM tokens x BN vocabulary columns of the chunk; each wave's
-// WTN columns form one statistics block b (block max m, sum of exp(z - m),
-// first arg-max). Columns at or beyond `vc_valid` are masked out.
-template <class E>
-__global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
-    const typename E::T* __restrict__ y, const typename E::T* __restrict__ Wc, int T, int d,
-    int vc_valid, int v0, const int32_t* __restrict__ targets, typename E::T* __restrict__ P,
-    int64_t ldp, int nb, float* __restrict__ blk_m, float* __restrict__ blk_s,
-    int32_t* __restrict__ blk_i, float* __restrict__ ztgt) {
-  using TT = Tile<E>;
-  __shared__ GemmSmem<E> sm;
-  f32x4 acc[E::FM][E::FN];
-  zero_acc<E>(acc);
-  const int ntm = (T + TT::BM - 1) / TT::BM, ntn = (vc_valid + TT::BN - 1) / TT::BN;
-  int tm, tn;
-  grouped_tile(xcd_remap(blockIdx.x, gridDim.x), ntm, ntn, 8, tm, tn);
-  const int m0 = tm * TT::BM, n0 = tn * TT::BN;
-  gemm_mainloop<E, false>(sm, acc, y, d, T, Wc, d, vc_valid, d, m0, n0, 0,
-                          (d + TT::BK - 1) / TT::BK, NoHook{});
-  const AccMap<E> mp;
+// One workgroup: 256 (bf16) / 128 (fp32) tokens x as many vocabulary columns of
+// the chunk; each wave's 128 / 64 columns form one statistics block b (block
+// max m, sum of exp(z - m), first arg-max). Columns at or beyond `vc_valid`
+// are masked out; p~ = exp(z - m) is staged for the projection.
+template <typename PT, int FM, int FN, bool CONTIG, class Map>
+__device__ __forceinline__ void logits_epilogue(f32x4 (&acc)[FM][FN], const Map& mp, int m0,
+                                                int n0, int b, int T, int vc_valid, int v0,
+                                                const int32_t* __restrict__ targets,
+                                                PT* __restrict__ P, int64_t ldp, int nb,
+                                                float* __restrict__ blk_m,
+                                                float* __restrict__ blk_s,
+                                                int32_t* __restrict__ blk_i,
+                                                float* __restrict__ ztgt) {
   const int lr = threadIdx.x & 15;
-  const int b = n0 / TT::WTN + ((threadIdx.x >> 6) & 1);  // this wave's block
 #pragma unroll
-  for (int f = 0; f < E::FM; ++f) {
+  for (int f = 0; f < FM; ++f) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = m0 + mp.row(f, r);
-      const int c0 = n0 + mp.col(0);
-      float z[E::FN];
+      float z[FN];
       float m = -INFINITY;
       int mi = 0x7fffffff;
 #pragma unroll
-      for (int i = 0; i < E::FN; ++i) {
+      for (int i = 0; i < FN; ++i) {  // columns increase with i
+        const int c = n0 + mp.col(i);
         z[i] = acc[f][i][r];
-        if (c0 + i < vc_valid && z[i] > m) {
+        if (c < vc_valid && z[i] > m) {
           m = z[i];
-          mi = c0 + i;
+          mi = c;
         }
       }
       // lowest column among equal maxima across the 16 lanes of the row
@@ -86,32 +79,67 @@ __global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
           mi = i2;
         }
       }
-      float p[E::FN];
+      float p[FN];
       float s = 0.f;
 #pragma unroll
-      for (int i = 0; i < E::FN; ++i) {
-        p[i] = (c0 + i < vc_valid) ? __expf(z[i] - m) : 0.f;
+      for (int i = 0; i < FN; ++i) {
+        p[i] = (n0 + mp.col(i) < vc_valid) ? __expf(z[i] - m) : 0.f;
         s += p[i];
       }
       s = wave_sum<16>(s);
       if (row < T) {
-        typename E::T* pr = P + (int64_t)row * ldp + c0;
+        PT* pr = P + (int64_t)row * ldp + n0;
+        if constexpr (CONTIG) {
 #pragma unroll
-        for (int i = 0; i < E::FN; i += 4) st4(pr, i, f32x4{p[i], p[i + 1], p[i + 2], p[i + 3]});
+          for (int i = 0; i < FN; i += 4)
+            st4(pr, mp.col(i), f32x4{p[i], p[i + 1], p[i + 2], p[i + 3]});
+        } else {
+#pragma unroll
+          for (int i = 0; i < FN; ++i) st_from_f32(pr, mp.col(i), p[i]);
+        }
         if (lr == 0 && b < nb) {
           const int64_t o = (int64_t)row * nb + b;
           blk_m[o] = m;
           blk_s[o] = s;
           blk_i[o] = (mi == 0x7fffffff) ? mi : v0 + mi;
         }
-        const int64_t tg = (int64_t)targets[row] - v0 - c0;
-        if (tg >= 0 && tg < E::FN && c0 + tg < vc_valid) {
+        const int64_t tg = (int64_t)targets[row] - v0 - n0;
 #pragma unroll
-          for (int i = 0; i < E::FN; ++i)
-            if (i == tg) ztgt[row] = z[i];
-        }
+        for (int i = 0; i < FN; ++i)
+          if (tg == mp.col(i) && n0 + mp.col(i) < vc_valid) ztgt[row] = z[i];
       }
     }
+  }
+}
+
+template <class E>
+__global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
+    const typename E::T* __restrict__ y, const typename E::T* __restrict__ Wc, int T, int d,
+    int vc_valid, int v0, const int32_t* __restrict__ targets, typename E::T* __restrict__ P,
+    int64_t ldp, int nb, float* __restrict__ blk_m, float* __restrict__ blk_s,
+    int32_t* __restrict__ blk_i, float* __restrict__ ztgt) {
+  using TT = Tile<E>;
+  const int ntm = (T + TT::BM - 1) / TT::BM, ntn = (vc_valid + TT::BN - 1) / TT::BN;
+  int tm, tn;
+  grouped_tile(xcd_remap(blockIdx.x, gridDim.x), ntm, ntn, 8, tm, tn);
+  const int m0 = tm * TT::BM, n0 = tn * TT::BN;
+  const int b = n0 / TT::WTN + ((threadIdx.x >> 6) & 1);  // this wave's block
+  f32x4 acc[E::FM][E::FN];
+  zero_acc<E>(acc);
+  if constexpr (E::EPC == 8) {
+    __shared__ G2Smem sm;
+    const Operand A{y + (int64_t)m0 * d, d, band_bytes(T - m0, d)};
+    const Operand B{Wc + (int64_t)n0 * d, d, band_bytes(vc_valid - n0, d)};
+    gemm2_mainloop<false>(sm, acc, A, B, T - m0, vc_valid - n0, d, 0, (d + G2::BK - 1) / G2::BK);
+    logits_epilogue<uint16_t, 8, 8, false>(acc, AccMap2<false>(), m0, n0, b, T, vc_valid, v0,
+                                           targets, P, ldp, nb, blk_m, blk_s, blk_i, ztgt);
+  } else {
+    __shared__ GemmSmem<E> sm;
+    gemm_mainloop<E, false>(sm, acc, y, d, T, Wc, d, vc_valid, d, m0, n0, 0,
+                            (d + TT::BK - 1) / TT::BK, NoHook{});
+    logits_epilogue<typename E::T, E::FM, E::FN, true>(acc, AccMap<E>(), m0, n0, b, T, vc_valid,
+                                                       v0, targets, P, ldp, nb, blk_m, blk_s,
+                                                       blk_i, ztgt);
   }
 }
 
@@ -207,39 +235,23 @@ __global__ __launch_bounds__(256) void chunk_stats_kernel(
 // G_s[t, :] (one partial per split s of the chunk's blocks) holds
 // sum_v exp(z_tv - M_t) W_U[v, :] over the vocabulary processed so far; the
 // split's products are accumulated in scale ref_s and merged in the epilogue.
-template <class E>
-__global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
-    const typename E::T* __restrict__ P, int64_t ldp, const typename E::T* __restrict__ Wc,
-    int T, int d, int vc_valid, int nb, int bps, int blkw, int first, int nsplit,
-    const float* __restrict__ fout, const float* __restrict__ alpha, float* __restrict__ G,
-    int64_t split_stride) {
-  using TT = Tile<E>;
-  __shared__ GemmSmem<E> sm;
-  f32x4 acc[E::FM][E::FN];
-  zero_acc<E>(acc);
-  // tiles: (token rows) x (split, column); columns of one split are adjacent
-  const int ntm = (T + TT::BM - 1) / TT::BM, ntn = (d + TT::BN - 1) / TT::BN;
-  int tm, tsn;
-  grouped_tile(xcd_remap(blockIdx.x, gridDim.x), ntm, ntn * nsplit, 8, tm, tsn);
-  const int sp = tsn / ntn;
-  const int m0 = tm * TT::BM, n0 = (tsn % ntn) * TT::BN;
-  float* Gs = G + sp * split_stride;
-  const int tpb = blkw / TT::BK;
-  const int nkt = (vc_valid + TT::BK - 1) / TT::BK;
-  const int kt0 = min(sp * bps * tpb, nkt), kt1 = min(min(nb, (sp + 1) * bps) * tpb, nkt);
-  gemm_mainloop<E, true>(sm, acc, P, ldp, T, Wc, d, d, vc_valid, m0, n0, kt0, kt1, NoHook{});
-  const AccMap<E> mp;
+template <int FM, int FN, class Map>
+__device__ __forceinline__ void proj_epilogue(f32x4 (&acc)[FM][FN], const Map& mp, int m0, int n0,
+                                              int sp, int nsplit, int T, int d, int first,
+                                              const float* __restrict__ fout,
+                                              const float* __restrict__ alpha,
+                                              float* __restrict__ Gs) {
 #pragma unroll
-  for (int f = 0; f < E::FM; ++f)
+  for (int f = 0; f < FM; ++f)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = m0 + mp.row(f, r);
-      const int c = n0 + mp.col(0);
+      const int c = n0 + mp.col(0);  // FN consecutive columns
       if (row >= T || c >= d) continue;
       const float so = fout[(int64_t)row * nsplit + sp];
       const float sa = first ? 0.f : alpha[row];
 #pragma unroll
-      for (int i = 0; i < E::FN; i += 4) {
+      for (int i = 0; i < FN; i += 4) {
         float* gp = Gs + (int64_t)row * d + c + i;
         f32x4 o = {acc[f][i][r] * so, acc[f][i + 1][r] * so, acc[f][i + 2][r] * so,
                    acc[f][i + 3][r] * so};
@@ -247,6 +259,41 @@ __global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
         *reinterpret_cast<f32x4*>(gp) = o;
       }
     }
+}
+
+template <class E>
+__global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
+    const typename E::T* __restrict__ P, int64_t ldp, const typename E::T* __restrict__ Wc,
+    int T, int d, int vc_valid, int nb, int bps, int blkw, int first, int nsplit,
+    const float* __restrict__ fout, const float* __restrict__ alpha, float* __restrict__ G,
+    int64_t split_stride) {
+  using TT = Tile<E>;
+  // tiles: (token rows) x (split, column); columns of one split are adjacent
+  const int ntm = (T + TT::BM - 1) / TT::BM, ntn = (d + TT::BN - 1) / TT::BN;
+  int tm, tsn;
+  grouped_tile(xcd_remap(blockIdx.x, gridDim.x), ntm, ntn * nsplit, 8, tm, tsn);
+  const int sp = tsn / ntn;
+  const int m0 = tm * TT::BM, n0 = (tsn % ntn) * TT::BN;
+  float* Gs = G + sp * split_stride;
+  f32x4 acc[E::FM][E::FN];
+  zero_acc<E>(acc);
+  if constexpr (E::EPC == 8) {
+    __shared__ G2Smem sm;
+    const int tpb = blkw / G2::BK;
+    const int nkt = (vc_valid + G2::BK - 1) / G2::BK;
+    const int kt0 = min(sp * bps * tpb, nkt), kt1 = min(min(nb, (sp + 1) * bps) * tpb, nkt);
+    const Operand A{P + (int64_t)m0 * ldp, ldp, band_bytes(T - m0, ldp)};
+    const Operand B{Wc + n0, d, band_bytes(vc_valid, d, n0)};
+    gemm2_mainloop<true>(sm, acc, A, B, T - m0, d - n0, vc_valid, kt0, kt1);
+    proj_epilogue<8, 8>(acc, AccMap2<true>(), m0, n0, sp, nsplit, T, d, first, fout, alpha, Gs);
+  } else {
+    __shared__ GemmSmem<E> sm;
+    const int tpb = blkw / TT::BK;
+    const int nkt = (vc_valid + TT::BK - 1) / TT::BK;
+    const int kt0 = min(sp * bps * tpb, nkt), kt1 = min(min(nb, (sp + 1) * bps) * tpb, nkt);
+    gemm_mainloop<E, true>(sm, acc, P, ldp, T, Wc, d, d, vc_valid, m0, n0, kt0, kt1, NoHook{});
+    proj_epilogue<E::FM, E::FN>(acc, AccMap<E>(), m0, n0, sp, nsplit, T, d, first, fout, alpha, Gs);
+  }
 }
 
 // ------------------------------------------------------------------ finalize

@@ -9,6 +9,7 @@
 //                   stored token-contiguous for the W1/W2 outer products
 //   reduce_parts  : fixed-order float64 sums of the tile partials
 #include "gemm.hpp"
+#include "gemm2.hpp"
 #include "launch.hpp"
 #include "prof.hpp"
 
@@ -41,40 +42,21 @@ struct OuterArgs {
   const float* R[kMaxMats];
 };
 
-template <class E>
-__global__ __launch_bounds__(256, 1) void outer_kernel(OuterArgs args, int M, int N, int K,
-                                                       int64_t lda, int64_t ldb, float scale,
-                                                       double* __restrict__ part) {
-  using TT = Tile<E>;
-  using T = typename E::T;
-  __shared__ GemmSmem<E> sm;
-  __shared__ double red[3][4];
-  // one flat grid over (matrix, tile); each XCD takes a contiguous range
-  const int ntm = (M + TT::BM - 1) / TT::BM, ntn = (N + TT::BN - 1) / TT::BN;
-  const int ntiles = ntm * ntn;
-  const int id = xcd_remap(blockIdx.x, gridDim.x);
-  const int mat = id / ntiles;
-  const int tile = id % ntiles;
-  int tm, tn;
-  grouped_tile(tile, ntm, ntn, 8, tm, tn);
-  const int m0 = tm * TT::BM, n0 = tn * TT::BN;
-  f32x4 acc[E::FM][E::FN];
-  zero_acc<E>(acc);
-  gemm_mainloop<E, true>(sm, acc, (const T*)args.A[mat], lda, M, (const T*)args.B[mat], ldb, N, K,
-                         m0, n0, 0, (K + TT::BK - 1) / TT::BK, NoHook{});
-  float* C = args.C[mat];
-  const float* R = args.R[mat];
-  const AccMap<E> mp;
+template <int FM, int FN, class Map>
+__device__ __forceinline__ void outer_epilogue(f32x4 (&acc)[FM][FN], const Map& mp, int m0, int n0,
+                                               int M, int N, float scale, float* __restrict__ C,
+                                               const float* __restrict__ R, double* red,
+                                               double* __restrict__ part_out) {
   float ss = 0.f, dt = 0.f, rr = 0.f;
 #pragma unroll
-  for (int f = 0; f < E::FM; ++f)
+  for (int f = 0; f < FM; ++f)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int row = m0 + mp.row(f, r);
-      const int c = n0 + mp.col(0);
-      if (row >= M || c >= N) continue;  // N % 8 == 0: a lane's FN columns are all in or all out
+      const int c = n0 + mp.col(0);  // FN consecutive columns
+      if (row >= M || c >= N) continue;  // N % 8 == 0: a lane's columns are all in or all out
 #pragma unroll
-      for (int i = 0; i < E::FN; i += 4) {
+      for (int i = 0; i < FN; i += 4) {
         f32x4 v = {acc[f][i][r] * scale, acc[f][i + 1][r] * scale, acc[f][i + 2][r] * scale,
                    acc[f][i + 3][r] * scale};
         const int64_t o = (int64_t)row * N + c + i;
@@ -90,46 +72,65 @@ __global__ __launch_bounds__(256, 1) void outer_kernel(OuterArgs args, int M, in
   double s0 = wave_sum_d((double)ss), s1 = wave_sum_d((double)dt), s2 = wave_sum_d((double)rr);
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) {
-    red[0][w] = s0;
-    red[1][w] = s1;
-    red[2][w] = s2;
+    red[w] = s0;
+    red[4 + w] = s1;
+    red[8 + w] = s2;
   }
   __syncthreads();
   if (threadIdx.x < 3) {
     const int k = threadIdx.x;
-    const double v = red[k][0] + red[k][1] + red[k][2] + red[k][3];
-    part[((int64_t)mat * ntiles + tm + (int64_t)tn * ntm) * 3 + k] = v;
+    part_out[k] = red[4 * k] + red[4 * k + 1] + red[4 * k + 2] + red[4 * k + 3];
+  }
+}
+
+template <class E>
+__global__ __launch_bounds__(256, 1) void outer_kernel(OuterArgs args, int M, int N, int K,
+                                                       int64_t lda, int64_t ldb, float scale,
+                                                       double* __restrict__ part) {
+  using TT = Tile<E>;
+  using T = typename E::T;
+  __shared__ double red[12];
+  // one flat grid over (matrix, tile); each XCD takes a contiguous range
+  const int ntm = (M + TT::BM - 1) / TT::BM, ntn = (N + TT::BN - 1) / TT::BN;
+  const int ntiles = ntm * ntn;
+  const int id = xcd_remap(blockIdx.x, gridDim.x);
+  const int mat = id / ntiles;
+  const int tile = id % ntiles;
+  int tm, tn;
+  grouped_tile(tile, ntm, ntn, 8, tm, tn);
+  const int m0 = tm * TT::BM, n0 = tn * TT::BN;
+  const T* Am = (const T*)args.A[mat];
+  const T* Bm = (const T*)args.B[mat];
+  double* po = part + ((int64_t)mat * ntiles + tm + (int64_t)tn * ntm) * 3;
+  f32x4 acc[E::FM][E::FN];
+  zero_acc<E>(acc);
+  if constexpr (E::EPC == 8) {
+    __shared__ G2Smem sm;
+    const Operand A{Am + (int64_t)m0 * lda, lda, band_bytes(M - m0, lda)};
+    const Operand B{Bm + n0, ldb, band_bytes(K, ldb, n0)};
+    gemm2_mainloop<true>(sm, acc, A, B, M - m0, N - n0, K, 0, (K + G2::BK - 1) / G2::BK);
+    outer_epilogue<8, 8>(acc, AccMap2<true>(), m0, n0, M, N, scale, args.C[mat], args.R[mat], red, po);
+  } else {
+    __shared__ GemmSmem<E> sm;
+    gemm_mainloop<E, true>(sm, acc, Am, lda, M, Bm, ldb, N, K, m0, n0, 0, (K + TT::BK - 1) / TT::BK,
+                           NoHook{});
+    outer_epilogue<E::FM, E::FN>(acc, AccMap<E>(), m0, n0, M, N, scale, args.C[mat], args.R[mat], red, po);
   }
 }
 
 // E = g~ W3_init for one layer; writes du^T and dq^T [d_ff, Tp] (rows t < Tp;
 // t >= T give zero because the A rows load as zero and q, u are not read).
-template <class E>
-__global__ __launch_bounds__(256, 1) void errh_kernel(const typename E::T* __restrict__ g,
-                                                      const typename E::T* __restrict__ W3i,
-                                                      const typename E::T* __restrict__ q,
-                                                      const typename E::T* __restrict__ u, int T,
-                                                      int Tp, int d, int d_ff,
-                                                      typename E::T* __restrict__ dq_T,
-                                                      typename E::T* __restrict__ du_T) {
-  using TT = Tile<E>;
-  using TE = typename E::T;
-  __shared__ GemmSmem<E> sm;
-  f32x4 acc[E::FM][E::FN];
-  zero_acc<E>(acc);
-  const int ntm = (Tp + TT::BM - 1) / TT::BM, ntn = (d_ff + TT::BN - 1) / TT::BN;
-  int tm, tn;
-  grouped_tile(xcd_remap(blockIdx.x, gridDim.x), ntm, ntn, 8, tm, tn);
-  const int m0 = tm * TT::BM, n0 = tn * TT::BN;
-  gemm_mainloop<E, true>(sm, acc, g, d, T, W3i, d_ff, d_ff, d, m0, n0, 0,
-                         (d + TT::BK - 1) / TT::BK, NoHook{});
-  const AccMap<E> mp;
+template <typename TE, int FM, int FN, class Map>
+__device__ __forceinline__ void errh_epilogue(f32x4 (&acc)[FM][FN], const Map& mp, int m0, int n0,
+                                              const TE* __restrict__ q, const TE* __restrict__ u,
+                                              int T, int Tp, int d_ff, TE* __restrict__ dq_T,
+                                              TE* __restrict__ du_T) {
 #pragma unroll
-  for (int f = 0; f < E::FM; ++f) {
+  for (int f = 0; f < FM; ++f) {
     const int t0 = m0 + mp.row(f, 0);  // 4 consecutive tokens t0..t0+3
     if (t0 >= Tp) continue;            // Tp % 4 == 0
 #pragma unroll
-    for (int i = 0; i < E::FN; ++i) {
+    for (int i = 0; i < FN; ++i) {
       const int j = n0 + mp.col(i);
       if (j >= d_ff) continue;
       float vq[4], vu[4];
@@ -151,6 +152,35 @@ __global__ __launch_bounds__(256, 1) void errh_kernel(const typename E::T* __res
       st4<TE>(dq_T + (int64_t)j * Tp + t0, 0, f32x4{vq[0], vq[1], vq[2], vq[3]});
       st4<TE>(du_T + (int64_t)j * Tp + t0, 0, f32x4{vu[0], vu[1], vu[2], vu[3]});
     }
+  }
+}
+
+template <class E>
+__global__ __launch_bounds__(256, 1) void errh_kernel(const typename E::T* __restrict__ g,
+                                                      const typename E::T* __restrict__ W3i,
+                                                      const typename E::T* __restrict__ q,
+                                                      const typename E::T* __restrict__ u, int T,
+                                                      int Tp, int d, int d_ff,
+                                                      typename E::T* __restrict__ dq_T,
+                                                      typename E::T* __restrict__ du_T) {
+  using TT = Tile<E>;
+  f32x4 acc[E::FM][E::FN];
+  zero_acc<E>(acc);
+  const int ntm = (Tp + TT::BM - 1) / TT::BM, ntn = (d_ff + TT::BN - 1) / TT::BN;
+  int tm, tn;
+  grouped_tile(xcd_remap(blockIdx.x, gridDim.x), ntm, ntn, 8, tm, tn);
+  const int m0 = tm * TT::BM, n0 = tn * TT::BN;
+  if constexpr (E::EPC == 8) {
+    __shared__ G2Smem sm;
+    const Operand A{g + (int64_t)m0 * d, d, band_bytes(T - m0, d)};
+    const Operand B{W3i + n0, d_ff, band_bytes(d, d_ff, n0)};
+    gemm2_mainloop<true>(sm, acc, A, B, T - m0, d_ff - n0, d, 0, (d + G2::BK - 1) / G2::BK);
+    errh_epilogue<uint16_t, 8, 8>(acc, AccMap2<true>(), m0, n0, q, u, T, Tp, d_ff, dq_T, du_T);
+  } else {
+    __shared__ GemmSmem<E> sm;
+    gemm_mainloop<E, true>(sm, acc, g, d, T, W3i, d_ff, d_ff, d, m0, n0, 0,
+                           (d + TT::BK - 1) / TT::BK, NoHook{});
+    errh_epilogue<typename E::T, E::FM, E::FN>(acc, AccMap<E>(), m0, n0, q, u, T, Tp, d_ff, dq_T, du_T);
   }
 }
 
