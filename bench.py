@@ -41,7 +41,22 @@ def parse():
     ap.add_argument("--config", type=int, default=1, help="workload id (paper_2608_14563_amd.inputs.CONFIGS)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-tokens", type=int, default=16, help="tokens in the oracle's timed sample")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration)")
     return ap.parse_args()
+
+
+def calibrate_copy(mib: int) -> None:
+    """A plain copy of known size: the HBM read/write counters of this
+    dispatch calibrate the FETCH_SIZE / WRITE_SIZE readings of the kernels."""
+    import torch
+    n = mib * (1 << 20)
+    src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes": n}), flush=True)
 
 
 def prof_lib():
@@ -61,6 +76,37 @@ def prof_read(lib):
     if k < 0:
         raise RuntimeError("fpo_prof_read failed")
     return {names.raw[32 * i:32 * i + 32].split(b"\0")[0].decode(): (ms[i], cnt[i]) for i in range(k)}
+
+
+def source_hash() -> str:
+    """Hash of the kernel sources; a profile's traffic figure applies only while
+    the sources it was measured on are unchanged."""
+    import hashlib
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2608_14563_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".hpp")):
+            h.update(f.encode())
+            h.update(open(os.path.join(d, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def profiled_traffic(workload: str, kernel: str):
+    """HBM bytes per dispatch of `kernel` from the committed rocprofv3 counter
+    summary (profiles/*.md, FETCH_SIZE and WRITE_SIZE scaled by the plain-copy
+    calibration), or None when absent or taken on different kernel sources."""
+    pdir = os.path.join(ROOT, "profiles")
+    if not os.path.isdir(pdir):
+        return None
+    want = source_hash()
+    for f in sorted(os.listdir(pdir)):
+        if not f.endswith(".md"):
+            continue
+        for line in open(os.path.join(pdir, f)):
+            p = line.split()
+            if len(p) == 5 and p[0] == "traffic" and p[1] == workload and p[2] == kernel and p[3] == want:
+                return float(p[4])
+    return None
 
 
 def kernel_work(name, c, steps, nchunk):
@@ -117,6 +163,9 @@ def cpu_baseline(c, tokens, x, gam, W_U, y, acts, W0):
 
 def main():
     args = parse()
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build has no "
               "multi-GPU path: run with --gpus 1", file=sys.stderr)
@@ -211,18 +260,19 @@ def main():
     nchunk = None
     w = kernel_work(dom, c, args.steps, nchunk)
     roof = None
+    traffic = profiled_traffic(c.name, dom)
     if w is not None:
         amount, unit, bound = w
         secs = dom_stats[0] / 1000.0
         if unit == "flop":
             ach = amount / secs / 1e12
             roof = {"bound": bound, "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": None, "kernel": dom,
+                    "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": traffic, "kernel": dom,
                     "avg_launch_ms": round(dom_stats[0] / dom_stats[1], 4), "launches": dom_stats[1]}
         else:
             ach = amount / secs / 1e9
             roof = {"bound": bound, "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                    "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None, "kernel": dom,
+                    "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": traffic, "kernel": dom,
                     "avg_launch_ms": round(dom_stats[0] / dom_stats[1], 4), "launches": dom_stats[1]}
     kernels = {}
     for k, (ms, n) in per_kernel.items():
