@@ -86,7 +86,6 @@ size_t carve_oe(const fpo_oe_desc& d, const OePlan& p, void* ws, fpo::OeLaunch* 
   float* runM = c.take<float>(d.T);
   float* runS = c.take<float>(d.T);
   int32_t* runA = c.take<int32_t>(d.T);
-  float* ztgt = c.take<float>(d.T);
   float* G = c.take<float>((int64_t)p.nsplit * d.T * d.d);
   if (L) {
     L->y = y;
@@ -99,7 +98,6 @@ size_t carve_oe(const fpo_oe_desc& d, const OePlan& p, void* ws, fpo::OeLaunch* 
     L->runM = runM;
     L->runS = runS;
     L->runA = runA;
-    L->ztgt = ztgt;
     L->G = G;
   }
   return c.off;

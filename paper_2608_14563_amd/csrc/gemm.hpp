@@ -327,6 +327,8 @@ __device__ __forceinline__ void grouped_tile(int id, int ntm, int ntn, int gm, i
 // Output coordinates of accumulator element [f][i][r] (relative to the tile).
 template <class E>
 struct AccMap {
+  static constexpr int R = 4;     // accumulator elements per (f, i): rows 4 consecutive
+  static constexpr int LPR = 16;  // lanes sharing one output row
   int row0, col0;  // tile-relative row of (f=0, r=0), col of i=0
   __device__ __forceinline__ AccMap() {
     const int l = threadIdx.x & 63, w = threadIdx.x >> 6;

@@ -2,7 +2,9 @@
 // (gfx950 buffer_load_dwordx4 ... lds). One workgroup of 4 waves (2 x 2)
 // computes a 256 x 256 tile of C = A B, A K-contiguous ([M][K]), B either
 // N-contiguous ([K][N]) or K-contiguous ([N][K], "Bt"). K advances 32 per
-// stage, one v_mfma_f32_16x16x32_bf16 K step.
+// stage = two K steps of v_mfma_f32_32x32x16_bf16 (each wave: 4 x 4 blocks of
+// 32 x 32). The 32x32x16 shape sustains ~95% of the bf16 peak in a pure MFMA
+// loop on gfx950 where 16x16x32 reaches ~70% (measured).
 //
 // Pipeline: tiles kt+1..kt+3 are in flight while tile kt is multiplied; the
 // global->LDS copies go straight into LDS (no register staging), each wave
@@ -13,13 +15,18 @@
 //
 // LDS layouts (16-byte chunks):
 //   K-contiguous tile: [rows][4 chunks], chunk c of row r stored at position
-//     c ^ ((r >> 1) & 3) -- fragment reads of 16 consecutive rows are then
-//     bank-conflict free on gfx950 (measured).
+//     c ^ ((r >> 2) & 3) -- fragment reads (32 consecutive rows x 2 chunks)
+//     are then bank-conflict free under every lane-phase model consistent
+//     with ds_read_b128 timings measured on gfx950.
 //   N-contiguous tile: [32 K rows][32 chunks] as in memory (conflict free).
-// Lane layout of the MFMA operands as in gemm.hpp: lane l owns K indices
-// 8*(l>>4) + s of the step. Output columns: for an N-contiguous B the lane owns
-// 8 consecutive columns 8*(l&15) + i of its wave's 128; for a K-contiguous B
-// it owns columns 16*i + (l&15).
+// Lane layout: in K step h (16 wide) lane l owns K indices 16h + 8*(l>>5) + s,
+// s = 0..7, for both operands (the K order inside an MFMA is a summation order
+// only). A fragment f holds rows 32f + (l&31) of the wave's 128. Output
+// columns: for an N-contiguous B the lane owns the 4 consecutive columns
+// 4*(l&31) + i of its wave's 128 (the four B operands i are packed with v_perm
+// from 4-column raw rows, so no LDS transpose is needed); for a K-contiguous B
+// it owns columns 32*i + (l&31). Accumulator acc[f][i] element r holds row
+// 32f + 8*(r>>2) + 4*(l>>5) + (r&3).
 #pragma once
 
 #include "common.hpp"
@@ -39,7 +46,7 @@ struct G2Smem {
   u32x4 s[G2::NST * G2::STAGE_CHUNKS];  // 128 KB
 };
 
-__device__ __forceinline__ int swz4(int row) { return (row >> 1) & 3; }
+__device__ __forceinline__ int swz4(int row) { return (row >> 2) & 3; }
 
 // One 16-byte-per-lane LDS-DMA copy: lane l's 16 bytes at rsrc + voff land at
 // LDS byte address m0 + 16 * l. Issued as inline asm so that the compiler does
@@ -56,9 +63,6 @@ __device__ __forceinline__ void dma16(u32x4 rsrc, uint32_t lds_addr, uint32_t vo
       : "memory", "m0");
 }
 
-__device__ __forceinline__ uint32_t lds_addr_of(const u32x4* p) {
-  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
-}
 
 // s_waitcnt vmcnt(n) leaving lgkmcnt / expcnt unconstrained (gfx9 encoding:
 // vmcnt[3:0] at bits 3:0, vmcnt[5:4] at bits 15:14).
@@ -113,133 +117,223 @@ __device__ __forceinline__ u32x4 make_rsrc(const Operand& o) {
 template <bool BNC>
 struct Pipe2 {
   u32x4 ra, rb;
-  int64_t lda, ldb;
-  int M_rem, N_rem, K;  // rows of A / cols of B left from the band base; K total
+  uint32_t lds_wave;      // LDS byte address of this wave's slice of stage 0 (uniform)
+  uint32_t offA[4], offB[4];  // per-lane byte offsets of this lane's copies at k0 = 0
+  int kA[4], kB[4];           // K index of the chunk / row each copy reads at k0 = 0
+  bool okA[4], okB[4];        // row (A, Bt) or column (B) inside the operand
+  int K;
+  int64_t stepB;              // bytes B advances per K tile (BNC: 32 rows; Bt: 64 bytes)
 
-  // Issue the DMA copies of K tile kt into ring stage st.
-  __device__ __forceinline__ void issue(u32x4* smem, int st, int kt) const {
+  __device__ __forceinline__ void setup(const u32x4* smem, const Operand& A, const Operand& B,
+                                        int M_rem, int N_rem, int K_) {
     const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
-    const int k0 = kt * G2::BK;
-    u32x4* sa = smem + st * G2::STAGE_CHUNKS;
-    u32x4* sb = sa + G2::A_CHUNKS;
+    ra = make_rsrc(A);
+    rb = make_rsrc(B);
+    lds_wave = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem + (uint32_t)w * 4096u);
+    K = K_;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int inst = w * 4 + j;
       const int row = 16 * inst + (l >> 2);
       const int c = (l & 3) ^ swz4(row);
-      const int gk = k0 + 8 * c;
-      const uint32_t off = (row < M_rem && gk < K) ? (uint32_t)(((int64_t)row * lda + gk) * 2) : kOOB;
-      dma16(ra, lds_addr_of(sa + inst * 64), off);
+      kA[j] = 8 * c;
+      okA[j] = row < M_rem;
+      offA[j] = (uint32_t)(((int64_t)row * A.ld + 8 * c) * 2);
+      if constexpr (BNC) {
+        const int krow = 2 * inst + (l >> 5), cb = l & 31;
+        kB[j] = krow;
+        okB[j] = 8 * cb < N_rem;
+        offB[j] = (uint32_t)(((int64_t)krow * B.ld + 8 * cb) * 2);
+      } else {
+        kB[j] = 8 * c;
+        okB[j] = row < N_rem;
+        offB[j] = (uint32_t)(((int64_t)row * B.ld + 8 * c) * 2);
+      }
+    }
+    stepB = BNC ? (int64_t)G2::BK * B.ld * 2 : (int64_t)G2::BK * 2;
+  }
+
+  // DMA copies of K tile kt into ring stage st; tiles at or beyond K (and
+  // out-of-range rows / columns) read as zero.
+  __device__ __forceinline__ void issue(int st, int kt) const {
+    const int k0 = kt * G2::BK;
+    const uint32_t sa = lds_wave + (uint32_t)st * (G2::STAGE_CHUNKS * 16);
+    const uint32_t sb = sa + G2::A_CHUNKS * 16;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool ok = okA[j] && (k0 + kA[j] < K);
+      dma16(ra, sa + 1024u * j, ok ? offA[j] + (uint32_t)(k0 * 2) : kOOB);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int inst = w * 4 + j;
-      uint32_t off;
-      if constexpr (BNC) {
-        const int krow = 2 * inst + (l >> 5), c = l & 31;
-        const int gk = k0 + krow;
-        off = (gk < K && 8 * c < N_rem) ? (uint32_t)(((int64_t)gk * ldb + 8 * c) * 2) : kOOB;
-      } else {
-        const int row = 16 * inst + (l >> 2);
-        const int c = (l & 3) ^ swz4(row);
-        const int gk = k0 + 8 * c;
-        off = (row < N_rem && gk < K) ? (uint32_t)(((int64_t)row * ldb + gk) * 2) : kOOB;
-      }
-      dma16(rb, lds_addr_of(sb + inst * 64), off);
+      const bool ok = okB[j] && (k0 + kB[j] < K);
+      dma16(rb, sb + 1024u * j, ok ? offB[j] + (uint32_t)(kt * stepB) : kOOB);
     }
   }
 
-  __device__ __forceinline__ static void compute(const u32x4* smem, int st, f32x4 (&acc)[8][8]) {
+  // A fragment (32 rows x K step h) f of a stage.
+  __device__ __forceinline__ static u32x4 read_a(const u32x4* stage, int f, int h) {
     const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
-    const int wm = w >> 1, wn = w & 1, lr = l & 15, lg = l >> 4;
-    const u32x4* sa = smem + st * G2::STAGE_CHUNKS;
-    const u32x4* sb = sa + G2::A_CHUNKS;
-    u32x4 af[8];
-#pragma unroll
-    for (int f = 0; f < 8; ++f) {
-      const int row = wm * G2::WTM + 16 * f + lr;
-      af[f] = sa[row * 4 + (lg ^ swz4(row))];
-    }
-    u32x4 bo[8];
+    const int row = (w >> 1) * G2::WTM + 32 * f + (l & 31);
+    return stage[row * 4 + ((2 * h + (l >> 5)) ^ swz4(row))];
+  }
+  // BNC: raw K rows (4 columns, 8 bytes each) of both K steps into raw[h*8+s];
+  // Bt: the operands themselves into bq[i*2+h].
+  __device__ __forceinline__ static void read_b(const u32x4* stage, u32x2 (&raw)[16], u32x4 (&bq)[8]) {
+    const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+    const int wn = w & 1, lc = l & 31, lk = l >> 5;
+    const u32x4* sb = stage + G2::A_CHUNKS;
     if constexpr (BNC) {
-      u32x4 raw[8];
+      const u32x2* sb2 = reinterpret_cast<const u32x2*>(sb);
 #pragma unroll
-      for (int s = 0; s < 8; ++s) raw[s] = sb[(8 * lg + s) * 32 + wn * 16 + lr];
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int q = i >> 1;
-        const uint32_t sel = (i & 1) ? 0x07060302u : 0x05040100u;
-        bo[i] = u32x4{__builtin_amdgcn_perm(raw[1][q], raw[0][q], sel),
-                      __builtin_amdgcn_perm(raw[3][q], raw[2][q], sel),
-                      __builtin_amdgcn_perm(raw[5][q], raw[4][q], sel),
-                      __builtin_amdgcn_perm(raw[7][q], raw[6][q], sel)};
-      }
+        for (int s = 0; s < 8; ++s) raw[h * 8 + s] = sb2[(16 * h + 8 * lk + s) * 64 + wn * 32 + lc];
     } else {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int row = wn * G2::WTN + 16 * i + lr;
-        bo[i] = sb[row * 4 + (lg ^ swz4(row))];
-      }
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int row = wn * G2::WTN + 32 * i + lc;
+          bq[i * 2 + h] = sb[row * 4 + ((2 * h + lk) ^ swz4(row))];
+        }
     }
+  }
+  // B operands (i, h) for i in [i0, i0+2): v_perm packing of K-row pairs (BNC)
+  // or as read (Bt). b[i*2+h].
+  __device__ __forceinline__ static void pack_b(const u32x2 (&raw)[16], const u32x4 (&bq)[8],
+                                                u32x4 (&b)[8], int i0) {
 #pragma unroll
-    for (int f = 0; f < 8; ++f)
+    for (int i = i0; i < i0 + 2; ++i)
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
-        acc[f][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, af[f]),
-                                                            __builtin_bit_cast(bf16x8, bo[i]),
-                                                            acc[f][i], 0, 0, 0);
+      for (int h = 0; h < 2; ++h) {
+        if constexpr (BNC) {
+          const int q = i >> 1;
+          const uint32_t sel = (i & 1) ? 0x07060302u : 0x05040100u;
+          const u32x2* r = raw + h * 8;
+          b[i * 2 + h] = u32x4{__builtin_amdgcn_perm(r[1][q], r[0][q], sel),
+                               __builtin_amdgcn_perm(r[3][q], r[2][q], sel),
+                               __builtin_amdgcn_perm(r[5][q], r[4][q], sel),
+                               __builtin_amdgcn_perm(r[7][q], r[6][q], sel)};
+        } else {
+          b[i * 2 + h] = bq[i * 2 + h];
+        }
+      }
+  }
+  // The four MFMAs of fragment row f in K step h.
+  __device__ __forceinline__ static void mfma_row(u32x4 a, const u32x4 (&b)[8], f32x16 (&acc)[4][4],
+                                                  int f, int h) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      acc[f][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                          __builtin_bit_cast(bf16x8, b[i * 2 + h]),
+                                                          acc[f][i], 0, 0, 0);
   }
 };
 
-// C tile (m0, n0) accumulated over K tiles [kt0, kt1). A_band / B_band point at
-// row m0 of A and at the tile's first column (BNC: element (0, n0); Bt: row n0).
+// One K tile: the 32 MFMAs of the current stage in 8 groups of 4 (K step h,
+// fragment row f) with the packed B operands `bc`; A fragments are read from
+// the current stage two groups ahead. Between the groups: the wait + barrier
+// that make tile i+1 visible, the next tile's B reads and packing into `bn`,
+// and the copies of tile i+3.
 template <bool BNC>
-__device__ __forceinline__ void gemm2_mainloop(G2Smem& sm, f32x4 (&acc)[8][8], const Operand& A,
+__device__ __forceinline__ void gemm2_iter(const Pipe2<BNC>& p, G2Smem& sm, f32x16 (&acc)[4][4],
+                                           const u32x4 (&bc)[8], u32x4 (&bn)[8], u32x2 (&raw)[16],
+                                           u32x4 (&bq)[8], int i, int kt0) {
+  using P = Pipe2<BNC>;
+  const u32x4* cur = sm.s + (i % G2::NST) * G2::STAGE_CHUNKS;
+  const u32x4* nxt = sm.s + ((i + 1) % G2::NST) * G2::STAGE_CHUNKS;
+  u32x4 a0 = P::read_a(cur, 0, 0), a1 = P::read_a(cur, 1, 0);
+  P::mfma_row(a0, bc, acc, 0, 0);
+  u32x4 a2 = P::read_a(cur, 2, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  wait_vmcnt<G2::LOADS_PER_STAGE>();
+  stage_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  P::mfma_row(a1, bc, acc, 1, 0);
+  u32x4 a3 = P::read_a(cur, 3, 0);
+  P::read_b(nxt, raw, bq);
+  __builtin_amdgcn_sched_barrier(0);
+  P::mfma_row(a2, bc, acc, 2, 0);
+  u32x4 a4 = P::read_a(cur, 0, 1);
+  __builtin_amdgcn_sched_barrier(0);
+  p.issue((i + 3) % G2::NST, kt0 + i + 3);
+  __builtin_amdgcn_sched_barrier(0);
+  P::mfma_row(a3, bc, acc, 3, 0);
+  u32x4 a5 = P::read_a(cur, 1, 1);
+  P::pack_b(raw, bq, bn, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  P::mfma_row(a4, bc, acc, 0, 1);
+  u32x4 a6 = P::read_a(cur, 2, 1);
+  P::pack_b(raw, bq, bn, 2);
+  __builtin_amdgcn_sched_barrier(0);
+  P::mfma_row(a5, bc, acc, 1, 1);
+  u32x4 a7 = P::read_a(cur, 3, 1);
+  __builtin_amdgcn_sched_barrier(0);
+  P::mfma_row(a6, bc, acc, 2, 1);
+  P::mfma_row(a7, bc, acc, 3, 1);
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// C tile accumulated over K tiles [kt0, kt1). A and B point at the band of the
+// tile (A: row m0; B: column n0 (N-contiguous) or row n0 (K-contiguous)).
+//
+// Software pipeline over a 4-stage ring: while tile i is multiplied, tile
+// i+1's B operands are read and packed and tile i+3's copies are issued.
+// Copies are issued every iteration (beyond the last tile they read zeros into
+// a stage no longer needed), so the wait before each barrier is a constant
+// vmcnt(8): only tile i+2's copies may still be in flight. A stage is
+// overwritten only after every wave has passed the barrier that follows its
+// last read (its reads feed MFMAs issued before that barrier).
+template <bool BNC>
+__device__ __forceinline__ void gemm2_mainloop(G2Smem& sm, f32x16 (&acc)[4][4], const Operand& A,
                                                const Operand& B, int M_rem, int N_rem, int K,
                                                int kt0, int kt1) {
-  Pipe2<BNC> p;
-  p.ra = make_rsrc(A);
-  p.rb = make_rsrc(B);
-  p.lda = A.ld;
-  p.ldb = B.ld;
-  p.M_rem = M_rem;
-  p.N_rem = N_rem;
-  p.K = K;
   const int n = kt1 - kt0;
   if (n <= 0) return;
-#pragma unroll
-  for (int i = 0; i < G2::NST - 1; ++i)
-    if (i < n) p.issue(sm.s, i, kt0 + i);
+  Pipe2<BNC> p;
+  p.setup(sm.s, A, B, M_rem, N_rem, K);
+  p.issue(0, kt0);
+  p.issue(1, kt0 + 1);
+  p.issue(2, kt0 + 2);
+  wait_vmcnt<2 * G2::LOADS_PER_STAGE>();
+  stage_barrier();
+  u32x4 bc[8], bn[8], bq[8];
+  u32x2 raw[16];
+  Pipe2<BNC>::read_b(sm.s, raw, bq);
+  Pipe2<BNC>::pack_b(raw, bq, bc, 0);
+  Pipe2<BNC>::pack_b(raw, bq, bc, 2);
   for (int i = 0; i < n; ++i) {
-    // tile i's copies are complete once at most the copies of tiles i+1, i+2
-    // (issued after it) are outstanding
-    const int ahead = n - 1 - i;
-    if (ahead >= 2)
-      wait_vmcnt<2 * G2::LOADS_PER_STAGE>();
-    else if (ahead == 1)
-      wait_vmcnt<G2::LOADS_PER_STAGE>();
-    else
-      wait_vmcnt<0>();
-    stage_barrier();
-    if (i + G2::NST - 1 < n) p.issue(sm.s, (i + G2::NST - 1) % G2::NST, kt0 + i + G2::NST - 1);
-    Pipe2<BNC>::compute(sm.s, i % G2::NST, acc);
+    gemm2_iter<BNC>(p, sm, acc, bc, bn, raw, bq, i, kt0);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) bc[j] = bn[j];
   }
+  wait_vmcnt<0>();
   __syncthreads();
 }
 
-// Output coordinates of acc[f][i][r] relative to the tile.
+__device__ __forceinline__ void zero_acc2(f32x16 (&acc)[4][4]) {
+#pragma unroll
+  for (int f = 0; f < 4; ++f)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[f][i] = f32x16{};
+}
+
+// Output coordinates of acc[f][i] element r relative to the tile.
 template <bool BNC>
 struct AccMap2 {
-  int row0, colb, lr;
+  static constexpr int R = 16;    // accumulator elements per (f, i): 4 groups of 4 consecutive rows
+  static constexpr int LPR = 32;  // lanes sharing one output row
+  int row0, colb, lc;
   __device__ __forceinline__ AccMap2() {
     const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
-    lr = l & 15;
-    row0 = (w >> 1) * G2::WTM + 4 * (l >> 4);
+    lc = l & 31;
+    row0 = (w >> 1) * G2::WTM + 4 * (l >> 5);
     colb = (w & 1) * G2::WTN;
   }
-  __device__ __forceinline__ int row(int f, int r) const { return row0 + 16 * f + r; }
+  __device__ __forceinline__ int row(int f, int r) const { return row0 + 32 * f + 8 * (r >> 2) + (r & 3); }
   __device__ __forceinline__ int col(int i) const {
-    return BNC ? colb + 8 * lr + i : colb + 16 * i + lr;
+    return BNC ? colb + 4 * lc + i : colb + 32 * i + lc;
   }
 };
 

@@ -42,20 +42,18 @@ __global__ __launch_bounds__(256) void rms_forward_kernel(const T* __restrict__ 
 // the chunk; each wave's 128 / 64 columns form one statistics block b (block
 // max m, sum of exp(z - m), first arg-max). Columns at or beyond `vc_valid`
 // are masked out; p~ = exp(z - m) is staged for the projection.
-template <typename PT, int FM, int FN, bool CONTIG, class Map>
-__device__ __forceinline__ void logits_epilogue(f32x4 (&acc)[FM][FN], const Map& mp, int m0,
+template <typename PT, bool CONTIG, class Map, class VA, int FM, int FN>
+__device__ __forceinline__ void logits_epilogue(VA (&acc)[FM][FN], const Map& mp, int m0,
                                                 int n0, int b, int T, int vc_valid, int v0,
-                                                const int32_t* __restrict__ targets,
                                                 PT* __restrict__ P, int64_t ldp, int nb,
                                                 float* __restrict__ blk_m,
                                                 float* __restrict__ blk_s,
-                                                int32_t* __restrict__ blk_i,
-                                                float* __restrict__ ztgt) {
-  const int lr = threadIdx.x & 15;
+                                                int32_t* __restrict__ blk_i) {
+  const int lr = threadIdx.x & (Map::LPR - 1);
 #pragma unroll
   for (int f = 0; f < FM; ++f) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < Map::R; ++r) {
       const int row = m0 + mp.row(f, r);
       float z[FN];
       float m = -INFINITY;
@@ -69,9 +67,9 @@ __device__ __forceinline__ void logits_epilogue(f32x4 (&acc)[FM][FN], const Map&
           mi = c;
         }
       }
-      // lowest column among equal maxima across the 16 lanes of the row
+      // lowest column among equal maxima across the lanes of the row
 #pragma unroll
-      for (int o = 1; o < 16; o <<= 1) {
+      for (int o = 1; o < Map::LPR; o <<= 1) {
         const float m2 = __shfl_xor(m, o, 64);
         const int i2 = __shfl_xor(mi, o, 64);
         if (m2 > m || (m2 == m && i2 < mi)) {
@@ -86,7 +84,7 @@ __device__ __forceinline__ void logits_epilogue(f32x4 (&acc)[FM][FN], const Map&
         p[i] = (n0 + mp.col(i) < vc_valid) ? __expf(z[i] - m) : 0.f;
         s += p[i];
       }
-      s = wave_sum<16>(s);
+      s = wave_sum<Map::LPR>(s);
       if (row < T) {
         PT* pr = P + (int64_t)row * ldp + n0;
         if constexpr (CONTIG) {
@@ -103,11 +101,84 @@ __device__ __forceinline__ void logits_epilogue(f32x4 (&acc)[FM][FN], const Map&
           blk_s[o] = s;
           blk_i[o] = (mi == 0x7fffffff) ? mi : v0 + mi;
         }
-        const int64_t tg = (int64_t)targets[row] - v0 - n0;
-#pragma unroll
-        for (int i = 0; i < FN; ++i)
-          if (tg == mp.col(i) && n0 + mp.col(i) < vc_valid) ztgt[row] = z[i];
       }
+    }
+  }
+}
+
+// bf16: the tile is computed transposed, C^T = W_c y^T (rows: 256 vocabulary
+// entries, columns: 256 tokens). Each lane then holds 64 logits of one token
+// per accumulator column block i (vocabulary rows 32f + 8q + 4h + j, h = lane
+// half, j < 4, in increasing order for increasing (f, q, j)); the lane pair
+// (l, l ^ 32) covers the wave's 128 vocabulary entries of that token, so the
+// block statistics need one cross-lane exchange. p~ goes out as 8-byte runs of
+// 4 vocabulary entries.
+template <bool RAGGED>
+__device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], int vt0, int tt0,
+                                                   int T, int vc_valid, int v0,
+                                                   uint16_t* __restrict__ P, int64_t ldp, int nb,
+                                                   float* __restrict__ blk_m,
+                                                   float* __restrict__ blk_s,
+                                                   int32_t* __restrict__ blk_i) {
+  const int l = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lc = l & 31, h = l >> 5;
+  const int vw = vt0 + (w >> 1) * G2::WTM;  // chunk-relative first entry of the wave's block
+  const int b = vw / G2::WTM;
+  const int vl = vw + 4 * h;                // entry of offset 0 in this lane
+  const int lim = vc_valid - vl;            // offset o is in range iff o < lim (RAGGED only)
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int t = tt0 + (w & 1) * G2::WTN + 32 * i + lc;
+    // block maximum, then its first (lowest) entry; offsets o = 32f + 8q + j
+    // increase with (f, r)
+    float m = -INFINITY;
+#pragma unroll
+    for (int f = 0; f < 4; ++f)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int o = 32 * f + 8 * (r >> 2) + (r & 3);
+        if (!RAGGED || o < lim) m = fmaxf(m, acc[f][i][r]);
+      }
+    int mo = 0x7fffffff;
+#pragma unroll
+    for (int f = 3; f >= 0; --f)
+#pragma unroll
+      for (int r = 15; r >= 0; --r) {
+        const int o = 32 * f + 8 * (r >> 2) + (r & 3);
+        if ((!RAGGED || o < lim) && acc[f][i][r] == m) mo = o;
+      }
+    int mi = mo == 0x7fffffff ? mo : vl + mo;
+    {
+      const float m2 = __shfl_xor(m, 32, 64);
+      const int i2 = __shfl_xor(mi, 32, 64);
+      if (m2 > m || (m2 == m && i2 < mi)) {
+        m = m2;
+        mi = i2;
+      }
+    }
+    float s = 0.f;
+    uint16_t* pr = P + (int64_t)t * ldp + vl;
+#pragma unroll
+    for (int f = 0; f < 4; ++f)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float p[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int o = 32 * f + 8 * q + j;
+          p[j] = (!RAGGED || o < lim) ? __expf(acc[f][i][4 * q + j] - m) : 0.f;
+          s += p[j];
+        }
+        if (t < T)
+          *reinterpret_cast<u32x2*>(pr + 32 * f + 8 * q) =
+              u32x2{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])};
+      }
+    s += __shfl_xor(s, 32, 64);
+    if (t < T && h == 0 && b < nb) {
+      const int64_t ob = (int64_t)t * nb + b;
+      blk_m[ob] = m;
+      blk_s[ob] = s;
+      blk_i[ob] = (mi == 0x7fffffff) ? mi : v0 + mi;
     }
   }
 }
@@ -115,31 +186,34 @@ __device__ __forceinline__ void logits_epilogue(f32x4 (&acc)[FM][FN], const Map&
 template <class E>
 __global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
     const typename E::T* __restrict__ y, const typename E::T* __restrict__ Wc, int T, int d,
-    int vc_valid, int v0, const int32_t* __restrict__ targets, typename E::T* __restrict__ P,
-    int64_t ldp, int nb, float* __restrict__ blk_m, float* __restrict__ blk_s,
-    int32_t* __restrict__ blk_i, float* __restrict__ ztgt) {
+    int vc_valid, int v0, typename E::T* __restrict__ P, int64_t ldp, int nb,
+    float* __restrict__ blk_m, float* __restrict__ blk_s, int32_t* __restrict__ blk_i) {
   using TT = Tile<E>;
   const int ntm = (T + TT::BM - 1) / TT::BM, ntn = (vc_valid + TT::BN - 1) / TT::BN;
   int tm, tn;
+  // consecutive workgroups share a vocabulary band and sweep the token tiles
   grouped_tile(xcd_remap(blockIdx.x, gridDim.x), ntm, ntn, 8, tm, tn);
   const int m0 = tm * TT::BM, n0 = tn * TT::BN;
-  const int b = n0 / TT::WTN + ((threadIdx.x >> 6) & 1);  // this wave's block
-  f32x4 acc[E::FM][E::FN];
-  zero_acc<E>(acc);
   if constexpr (E::EPC == 8) {
     __shared__ G2Smem sm;
-    const Operand A{y + (int64_t)m0 * d, d, band_bytes(T - m0, d)};
-    const Operand B{Wc + (int64_t)n0 * d, d, band_bytes(vc_valid - n0, d)};
-    gemm2_mainloop<false>(sm, acc, A, B, T - m0, vc_valid - n0, d, 0, (d + G2::BK - 1) / G2::BK);
-    logits_epilogue<uint16_t, 8, 8, false>(acc, AccMap2<false>(), m0, n0, b, T, vc_valid, v0,
-                                           targets, P, ldp, nb, blk_m, blk_s, blk_i, ztgt);
+    f32x16 acc[4][4];
+    zero_acc2(acc);
+    const Operand A{Wc + (int64_t)n0 * d, d, band_bytes(vc_valid - n0, d)};
+    const Operand B{y + (int64_t)m0 * d, d, band_bytes(T - m0, d)};
+    gemm2_mainloop<false>(sm, acc, A, B, vc_valid - n0, T - m0, d, 0, (d + G2::BK - 1) / G2::BK);
+    if (n0 + ((threadIdx.x >> 7) + 1) * G2::WTM <= vc_valid)  // wave-uniform
+      logits_epilogue_vt<false>(acc, n0, m0, T, vc_valid, v0, P, ldp, nb, blk_m, blk_s, blk_i);
+    else
+      logits_epilogue_vt<true>(acc, n0, m0, T, vc_valid, v0, P, ldp, nb, blk_m, blk_s, blk_i);
   } else {
     __shared__ GemmSmem<E> sm;
+    f32x4 acc[E::FM][E::FN];
+    zero_acc<E>(acc);
+    const int b = n0 / TT::WTN + ((threadIdx.x >> 6) & 1);  // this wave's block
     gemm_mainloop<E, false>(sm, acc, y, d, T, Wc, d, vc_valid, d, m0, n0, 0,
                             (d + TT::BK - 1) / TT::BK, NoHook{});
-    logits_epilogue<typename E::T, E::FM, E::FN, true>(acc, AccMap<E>(), m0, n0, b, T, vc_valid,
-                                                       v0, targets, P, ldp, nb, blk_m, blk_s,
-                                                       blk_i, ztgt);
+    logits_epilogue<typename E::T, true>(acc, AccMap<E>(), m0, n0, b, T, vc_valid, v0, P, ldp, nb,
+                                         blk_m, blk_s, blk_i);
   }
 }
 
@@ -235,8 +309,8 @@ __global__ __launch_bounds__(256) void chunk_stats_kernel(
 // G_s[t, :] (one partial per split s of the chunk's blocks) holds
 // sum_v exp(z_tv - M_t) W_U[v, :] over the vocabulary processed so far; the
 // split's products are accumulated in scale ref_s and merged in the epilogue.
-template <int FM, int FN, class Map>
-__device__ __forceinline__ void proj_epilogue(f32x4 (&acc)[FM][FN], const Map& mp, int m0, int n0,
+template <class Map, class VA, int FM, int FN>
+__device__ __forceinline__ void proj_epilogue(VA (&acc)[FM][FN], const Map& mp, int m0, int n0,
                                               int sp, int nsplit, int T, int d, int first,
                                               const float* __restrict__ fout,
                                               const float* __restrict__ alpha,
@@ -244,7 +318,7 @@ __device__ __forceinline__ void proj_epilogue(f32x4 (&acc)[FM][FN], const Map& m
 #pragma unroll
   for (int f = 0; f < FM; ++f)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < Map::R; ++r) {
       const int row = m0 + mp.row(f, r);
       const int c = n0 + mp.col(0);  // FN consecutive columns
       if (row >= T || c >= d) continue;
@@ -261,6 +335,46 @@ __device__ __forceinline__ void proj_epilogue(f32x4 (&acc)[FM][FN], const Map& m
     }
 }
 
+// bf16 form of the merge: the tile's per-row factors exp(ref_s - M_new) and
+// exp(M_old - M_new) are staged in LDS (the ring is free after the main loop)
+// and each fragment's 16 partial rows are loaded together before use, so the
+// row loads overlap instead of serialising on their latency.
+__device__ __forceinline__ void proj_epilogue2(f32x16 (&acc)[4][4], G2Smem& sm, int m0, int n0,
+                                               int sp, int nsplit, int T, int d, int first,
+                                               const float* __restrict__ fout,
+                                               const float* __restrict__ alpha,
+                                               float* __restrict__ Gs) {
+  float* sf = reinterpret_cast<float*>(sm.s);
+  {
+    const int rr = m0 + (int)threadIdx.x;
+    sf[threadIdx.x] = rr < T ? fout[(int64_t)rr * nsplit + sp] : 0.f;
+    sf[256 + threadIdx.x] = (!first && rr < T) ? alpha[rr] : 0.f;
+  }
+  __syncthreads();
+  const AccMap2<true> mp;
+  const int c = n0 + mp.col(0);  // 4 consecutive columns
+  const bool cok = c < d;        // d % 4 == 0
+#pragma unroll
+  for (int f = 0; f < 4; ++f) {
+    f32x4 old[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = m0 + mp.row(f, r);
+      old[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (!first && cok && row < T) old[r] = *reinterpret_cast<const f32x4*>(Gs + (int64_t)row * d + c);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int lr = mp.row(f, r);
+      const int row = m0 + lr;
+      if (!cok || row >= T) continue;
+      const float so = sf[lr], sa = sf[256 + lr];
+      const f32x4 o = f32x4{acc[f][0][r], acc[f][1][r], acc[f][2][r], acc[f][3][r]} * so + old[r] * sa;
+      *reinterpret_cast<f32x4*>(Gs + (int64_t)row * d + c) = o;
+    }
+  }
+}
+
 template <class E>
 __global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
     const typename E::T* __restrict__ P, int64_t ldp, const typename E::T* __restrict__ Wc,
@@ -275,24 +389,26 @@ __global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
   const int sp = tsn / ntn;
   const int m0 = tm * TT::BM, n0 = (tsn % ntn) * TT::BN;
   float* Gs = G + sp * split_stride;
-  f32x4 acc[E::FM][E::FN];
-  zero_acc<E>(acc);
   if constexpr (E::EPC == 8) {
     __shared__ G2Smem sm;
+    f32x16 acc[4][4];
+    zero_acc2(acc);
     const int tpb = blkw / G2::BK;
     const int nkt = (vc_valid + G2::BK - 1) / G2::BK;
     const int kt0 = min(sp * bps * tpb, nkt), kt1 = min(min(nb, (sp + 1) * bps) * tpb, nkt);
     const Operand A{P + (int64_t)m0 * ldp, ldp, band_bytes(T - m0, ldp)};
     const Operand B{Wc + n0, d, band_bytes(vc_valid, d, n0)};
     gemm2_mainloop<true>(sm, acc, A, B, T - m0, d - n0, vc_valid, kt0, kt1);
-    proj_epilogue<8, 8>(acc, AccMap2<true>(), m0, n0, sp, nsplit, T, d, first, fout, alpha, Gs);
+    proj_epilogue2(acc, sm, m0, n0, sp, nsplit, T, d, first, fout, alpha, Gs);
   } else {
     __shared__ GemmSmem<E> sm;
+    f32x4 acc[E::FM][E::FN];
+    zero_acc<E>(acc);
     const int tpb = blkw / TT::BK;
     const int nkt = (vc_valid + TT::BK - 1) / TT::BK;
     const int kt0 = min(sp * bps * tpb, nkt), kt1 = min(min(nb, (sp + 1) * bps) * tpb, nkt);
     gemm_mainloop<E, true>(sm, acc, P, ldp, T, Wc, d, d, vc_valid, m0, n0, kt0, kt1, NoHook{});
-    proj_epilogue<E::FM, E::FN>(acc, AccMap<E>(), m0, n0, sp, nsplit, T, d, first, fout, alpha, Gs);
+    proj_epilogue(acc, AccMap<E>(), m0, n0, sp, nsplit, T, d, first, fout, alpha, Gs);
   }
 }
 
@@ -305,7 +421,7 @@ template <typename T>
 __global__ __launch_bounds__(256) void finalize_vjp_kernel(
     int d, int V, int nsplit, int64_t split_stride, const float* __restrict__ G,
     const float* __restrict__ runM, const float* __restrict__ runS,
-    const int32_t* __restrict__ runA, const float* __restrict__ ztgt,
+    const int32_t* __restrict__ runA, const T* __restrict__ y,
     const int32_t* __restrict__ targets, const T* __restrict__ W_U, const T* __restrict__ x,
     const T* __restrict__ gamma, float eps, float min_rms, float* __restrict__ g_tilde,
     T* __restrict__ g_tilde_lp, float* __restrict__ g_pre, float* __restrict__ lse,
@@ -318,14 +434,16 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
   const float invS = 1.0f / S;
   const T* xr = x + row * d;
   float* gt = g_tilde + row * d;
-  float ss = 0.f, cd = 0.f;
+  float ss = 0.f, cd = 0.f, zt = 0.f;
   for (int k = threadIdx.x * 4; k < d; k += 1024) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int s = 0; s < nsplit; ++s) acc += *reinterpret_cast<const f32x4*>(G + s * split_stride + row * d + k);
     f32x4 g = {0.f, 0.f, 0.f, 0.f};
     if (valid) {
       f32x4 wy = ld4(W_U + (int64_t)tg * d, k);
+      f32x4 yv = ld4(y + row * d, k);
       g = acc * invS - wy;
+      zt += yv.x * wy.x + yv.y * wy.y + yv.z * wy.z + yv.w * wy.w;  // target logit z_y
     }
     if (g_pre) *reinterpret_cast<f32x4*>(g_pre + row * d + k) = g;
     *reinterpret_cast<f32x4*>(gt + k) = g;
@@ -335,6 +453,7 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
   }
   ss = block_sum(ss, red);
   cd = block_sum(cd, red);
+  zt = block_sum(zt, red);
   const float rho = sqrtf(ss / (float)d + eps);
   const float rt = fmaxf(rho, min_rms);
   const float irt = 1.0f / rt;
@@ -353,7 +472,7 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
   if (threadIdx.x == 0) {
     const float l_se = runM[row] + logf(S);
     if (lse) lse[row] = l_se;
-    if (loss) loss[row] = valid ? l_se - ztgt[row] : 0.f;
+    if (loss) loss[row] = valid ? l_se - zt : 0.f;
     if (argmax) argmax[row] = runA[row];
     if (!valid && bad) atomicAdd(bad, 1);
   }
@@ -389,8 +508,8 @@ static hipError_t run_output_error(const OeLaunch& a) {
     const int nbv = (vc_valid + TT::WTN - 1) / TT::WTN;  // blocks holding a valid column
     FPO_LAUNCH("logits_chunk", st,
                logits_chunk_kernel<E><<<dim3(gm * gn), dim3(256), 0, st>>>(
-        y, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, (int)v0, a.targets, P, a.Vc, nbv,
-        a.blk_m, a.blk_s, a.blk_i, a.ztgt));
+        y, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, (int)v0, P, a.Vc, nbv, a.blk_m, a.blk_s,
+        a.blk_i));
     FPO_CHECK_LAUNCH();
     const int bps = (nbv + a.nsplit - 1) / a.nsplit;
     FPO_LAUNCH("chunk_stats", st,
@@ -406,7 +525,7 @@ static hipError_t run_output_error(const OeLaunch& a) {
   }
   FPO_LAUNCH("finalize_vjp", st,
              finalize_vjp_kernel<T><<<dim3((unsigned)a.T), dim3(256), 0, st>>>(
-      (int)a.d, (int)a.V, a.nsplit, a.T * a.d, a.G, a.runM, a.runS, a.runA, a.ztgt, a.targets, W,
+      (int)a.d, (int)a.V, a.nsplit, a.T * a.d, a.G, a.runM, a.runS, a.runA, y, a.targets, W,
       x, gamma, a.eps, a.min_rms, a.g_tilde, (T*)a.g_tilde_lp, a.g_pre, a.lse, a.loss, a.argmax,
       a.bad_targets));
   FPO_CHECK_LAUNCH();

@@ -42,8 +42,8 @@ struct OuterArgs {
   const float* R[kMaxMats];
 };
 
-template <int FM, int FN, class Map>
-__device__ __forceinline__ void outer_epilogue(f32x4 (&acc)[FM][FN], const Map& mp, int m0, int n0,
+template <class Map, class VA, int FM, int FN>
+__device__ __forceinline__ void outer_epilogue(VA (&acc)[FM][FN], const Map& mp, int m0, int n0,
                                                int M, int N, float scale, float* __restrict__ C,
                                                const float* __restrict__ R, double* red,
                                                double* __restrict__ part_out) {
@@ -51,7 +51,7 @@ __device__ __forceinline__ void outer_epilogue(f32x4 (&acc)[FM][FN], const Map& 
 #pragma unroll
   for (int f = 0; f < FM; ++f)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < Map::R; ++r) {
       const int row = m0 + mp.row(f, r);
       const int c = n0 + mp.col(0);  // FN consecutive columns
       if (row >= M || c >= N) continue;  // N % 8 == 0: a lane's columns are all in or all out
@@ -69,6 +69,54 @@ __device__ __forceinline__ void outer_epilogue(f32x4 (&acc)[FM][FN], const Map& 
         }
       }
     }
+  double s0 = wave_sum_d((double)ss), s1 = wave_sum_d((double)dt), s2 = wave_sum_d((double)rr);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    red[w] = s0;
+    red[4 + w] = s1;
+    red[8 + w] = s2;
+  }
+  __syncthreads();
+  if (threadIdx.x < 3) {
+    const int k = threadIdx.x;
+    part_out[k] = red[4 * k] + red[4 * k + 1] + red[4 * k + 2] + red[4 * k + 3];
+  }
+}
+
+// bf16 form: 16 rows of a fragment are loaded (reference) before use, so
+// the loads overlap; every lane's 4 columns are consecutive.
+__device__ __forceinline__ void outer_epilogue2(const f32x16 (&acc)[4][4], int m0, int n0, int M,
+                                                int N, float scale, float* __restrict__ C,
+                                                const float* __restrict__ R, double* red,
+                                                double* __restrict__ part_out) {
+  const AccMap2<true> mp;
+  const int c = n0 + mp.col(0);
+  const bool cok = c < N;  // N % 4 == 0: a lane's columns are all in or all out
+  float ss = 0.f, dt = 0.f, rr = 0.f;
+#pragma unroll
+  for (int f = 0; f < 4; ++f) {
+    f32x4 q[16];
+    if (R) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + mp.row(f, r);
+        q[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (cok && row < M) q[r] = *reinterpret_cast<const f32x4*>(R + (int64_t)row * N + c);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = m0 + mp.row(f, r);
+      if (!cok || row >= M) continue;
+      const f32x4 v = f32x4{acc[f][0][r], acc[f][1][r], acc[f][2][r], acc[f][3][r]} * scale;
+      if (C) *reinterpret_cast<f32x4*>(C + (int64_t)row * N + c) = v;
+      ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+      if (R) {
+        dt += v.x * q[r].x + v.y * q[r].y + v.z * q[r].z + v.w * q[r].w;
+        rr += q[r].x * q[r].x + q[r].y * q[r].y + q[r].z * q[r].z + q[r].w * q[r].w;
+      }
+    }
+  }
   double s0 = wave_sum_d((double)ss), s1 = wave_sum_d((double)dt), s2 = wave_sum_d((double)rr);
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) {
@@ -102,33 +150,37 @@ __global__ __launch_bounds__(256, 1) void outer_kernel(OuterArgs args, int M, in
   const T* Am = (const T*)args.A[mat];
   const T* Bm = (const T*)args.B[mat];
   double* po = part + ((int64_t)mat * ntiles + tm + (int64_t)tn * ntm) * 3;
-  f32x4 acc[E::FM][E::FN];
-  zero_acc<E>(acc);
   if constexpr (E::EPC == 8) {
     __shared__ G2Smem sm;
+    f32x16 acc[4][4];
+    zero_acc2(acc);
     const Operand A{Am + (int64_t)m0 * lda, lda, band_bytes(M - m0, lda)};
     const Operand B{Bm + n0, ldb, band_bytes(K, ldb, n0)};
     gemm2_mainloop<true>(sm, acc, A, B, M - m0, N - n0, K, 0, (K + G2::BK - 1) / G2::BK);
-    outer_epilogue<8, 8>(acc, AccMap2<true>(), m0, n0, M, N, scale, args.C[mat], args.R[mat], red, po);
+    outer_epilogue2(acc, m0, n0, M, N, scale, args.C[mat], args.R[mat], red, po);
   } else {
     __shared__ GemmSmem<E> sm;
+    f32x4 acc[E::FM][E::FN];
+    zero_acc<E>(acc);
     gemm_mainloop<E, true>(sm, acc, Am, lda, M, Bm, ldb, N, K, m0, n0, 0, (K + TT::BK - 1) / TT::BK,
                            NoHook{});
-    outer_epilogue<E::FM, E::FN>(acc, AccMap<E>(), m0, n0, M, N, scale, args.C[mat], args.R[mat], red, po);
+    outer_epilogue(acc, AccMap<E>(), m0, n0, M, N, scale, args.C[mat], args.R[mat], red, po);
   }
 }
 
 // E = g~ W3_init for one layer; writes du^T and dq^T [d_ff, Tp] (rows t < Tp;
 // t >= T give zero because the A rows load as zero and q, u are not read).
-template <typename TE, int FM, int FN, class Map>
-__device__ __forceinline__ void errh_epilogue(f32x4 (&acc)[FM][FN], const Map& mp, int m0, int n0,
+template <typename TE, class Map, class VA, int FM, int FN>
+__device__ __forceinline__ void errh_epilogue(VA (&acc)[FM][FN], const Map& mp, int m0, int n0,
                                               const TE* __restrict__ q, const TE* __restrict__ u,
                                               int T, int Tp, int d_ff, TE* __restrict__ dq_T,
                                               TE* __restrict__ du_T) {
 #pragma unroll
-  for (int f = 0; f < FM; ++f) {
-    const int t0 = m0 + mp.row(f, 0);  // 4 consecutive tokens t0..t0+3
-    if (t0 >= Tp) continue;            // Tp % 4 == 0
+  for (int f = 0; f < FM; ++f)
+#pragma unroll
+  for (int rg = 0; rg < Map::R; rg += 4) {
+    const int t0 = m0 + mp.row(f, rg);  // 4 consecutive tokens t0..t0+3
+    if (t0 >= Tp) continue;             // Tp % 4 == 0
 #pragma unroll
     for (int i = 0; i < FN; ++i) {
       const int j = n0 + mp.col(i);
@@ -137,7 +189,7 @@ __device__ __forceinline__ void errh_epilogue(f32x4 (&acc)[FM][FN], const Map& m
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int t = t0 + r;
-        const float e = acc[f][i][r];
+        const float e = acc[f][i][rg + r];
         float dqv = 0.f, duv = 0.f;
         if (t < T) {
           const float qq = ld_as_f32(q, (int64_t)t * d_ff + j);
@@ -155,6 +207,53 @@ __device__ __forceinline__ void errh_epilogue(f32x4 (&acc)[FM][FN], const Map& m
   }
 }
 
+// bf16 form: per fragment and group of 4 consecutive tokens, the lane's 4
+// consecutive columns of q and u are loaded as 8-byte runs (all 8 loads before
+// use), and dq^T, du^T go out as 8-byte runs of 4 tokens.
+__device__ __forceinline__ void errh_epilogue2(const f32x16 (&acc)[4][4], int m0, int n0,
+                                               const uint16_t* __restrict__ q,
+                                               const uint16_t* __restrict__ u, int T, int Tp,
+                                               int d_ff, uint16_t* __restrict__ dq_T,
+                                               uint16_t* __restrict__ du_T) {
+  const AccMap2<true> mp;
+  const int j0 = n0 + mp.col(0);
+  if (j0 >= d_ff) return;  // d_ff % 4 == 0: the lane's 4 columns are all in or all out
+#pragma unroll
+  for (int f = 0; f < 4; ++f)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int t0 = m0 + mp.row(f, 4 * g);  // tokens t0..t0+3
+      if (t0 >= Tp) continue;                // Tp % 4 == 0
+      u32x2 qv[4], uv[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        qv[r] = u32x2{0u, 0u};
+        uv[r] = u32x2{0u, 0u};
+        if (t0 + r < T) {
+          qv[r] = *reinterpret_cast<const u32x2*>(q + (int64_t)(t0 + r) * d_ff + j0);
+          uv[r] = *reinterpret_cast<const u32x2*>(u + (int64_t)(t0 + r) * d_ff + j0);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float vq[4], vu[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const uint32_t qw = qv[r][i >> 1], uw = uv[r][i >> 1];
+          const float qq = (i & 1) ? bf16_hi(qw) : bf16_lo(qw);
+          const float uu = (i & 1) ? bf16_hi(uw) : bf16_lo(uw);
+          const float e = acc[f][i][4 * g + r];
+          const float sg = 1.0f / (1.0f + __expf(-qq));
+          const bool in = t0 + r < T;
+          vu[r] = in ? e * qq * sg : 0.f;
+          vq[r] = in ? e * uu * sg * (1.0f + qq * (1.0f - sg)) : 0.f;
+        }
+        st4<uint16_t>(dq_T + (int64_t)(j0 + i) * Tp + t0, 0, f32x4{vq[0], vq[1], vq[2], vq[3]});
+        st4<uint16_t>(du_T + (int64_t)(j0 + i) * Tp + t0, 0, f32x4{vu[0], vu[1], vu[2], vu[3]});
+      }
+    }
+}
+
 template <class E>
 __global__ __launch_bounds__(256, 1) void errh_kernel(const typename E::T* __restrict__ g,
                                                       const typename E::T* __restrict__ W3i,
@@ -164,23 +263,25 @@ __global__ __launch_bounds__(256, 1) void errh_kernel(const typename E::T* __res
                                                       typename E::T* __restrict__ dq_T,
                                                       typename E::T* __restrict__ du_T) {
   using TT = Tile<E>;
-  f32x4 acc[E::FM][E::FN];
-  zero_acc<E>(acc);
   const int ntm = (Tp + TT::BM - 1) / TT::BM, ntn = (d_ff + TT::BN - 1) / TT::BN;
   int tm, tn;
   grouped_tile(xcd_remap(blockIdx.x, gridDim.x), ntm, ntn, 8, tm, tn);
   const int m0 = tm * TT::BM, n0 = tn * TT::BN;
   if constexpr (E::EPC == 8) {
     __shared__ G2Smem sm;
+    f32x16 acc[4][4];
+    zero_acc2(acc);
     const Operand A{g + (int64_t)m0 * d, d, band_bytes(T - m0, d)};
     const Operand B{W3i + n0, d_ff, band_bytes(d, d_ff, n0)};
     gemm2_mainloop<true>(sm, acc, A, B, T - m0, d_ff - n0, d, 0, (d + G2::BK - 1) / G2::BK);
-    errh_epilogue<uint16_t, 8, 8>(acc, AccMap2<true>(), m0, n0, q, u, T, Tp, d_ff, dq_T, du_T);
+    errh_epilogue2(acc, m0, n0, q, u, T, Tp, d_ff, dq_T, du_T);
   } else {
     __shared__ GemmSmem<E> sm;
+    f32x4 acc[E::FM][E::FN];
+    zero_acc<E>(acc);
     gemm_mainloop<E, true>(sm, acc, g, d, T, W3i, d_ff, d_ff, d, m0, n0, 0,
                            (d + TT::BK - 1) / TT::BK, NoHook{});
-    errh_epilogue<typename E::T, E::FM, E::FN>(acc, AccMap<E>(), m0, n0, q, u, T, Tp, d_ff, dq_T, du_T);
+    errh_epilogue<typename E::T>(acc, AccMap<E>(), m0, n0, q, u, T, Tp, d_ff, dq_T, du_T);
   }
 }
 

@@ -39,7 +39,6 @@ struct OeLaunch {
   float* runM;
   float* runS;
   int32_t* runA;
-  float* ztgt;
   float* G;
   void* stream;
 };
