@@ -43,7 +43,7 @@ struct G2 {
 };
 
 struct G2Smem {
-  u32x4 s[G2::NST * G2::STAGE_CHUNKS];  // 128 KB
+  u32x4 s[G2::NST * G2::STAGE_CHUNKS];  // 32 KB per stage
 };
 
 __device__ __forceinline__ int swz4(int row) { return (row >> 2) & 3; }
@@ -153,22 +153,23 @@ struct Pipe2 {
     stepB = BNC ? (int64_t)G2::BK * B.ld * 2 : (int64_t)G2::BK * 2;
   }
 
-  // DMA copies of K tile kt into ring stage st; tiles at or beyond K (and
-  // out-of-range rows / columns) read as zero.
-  __device__ __forceinline__ void issue(int st, int kt) const {
+  // DMA copy j (0..3: A, 4..7: B) of K tile kt into ring stage st; tiles at
+  // or beyond K (and out-of-range rows / columns) read as zero.
+  __device__ __forceinline__ void issue_one(int st, int kt, int j) const {
     const int k0 = kt * G2::BK;
     const uint32_t sa = lds_wave + (uint32_t)st * (G2::STAGE_CHUNKS * 16);
-    const uint32_t sb = sa + G2::A_CHUNKS * 16;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    if (j < 4) {
       const bool ok = okA[j] && (k0 + kA[j] < K);
       dma16(ra, sa + 1024u * j, ok ? offA[j] + (uint32_t)(k0 * 2) : kOOB);
+    } else {
+      const int jb = j - 4;
+      const bool ok = okB[jb] && (k0 + kB[jb] < K);
+      dma16(rb, sa + G2::A_CHUNKS * 16 + 1024u * jb, ok ? offB[jb] + (uint32_t)(kt * stepB) : kOOB);
     }
+  }
+  __device__ __forceinline__ void issue(int st, int kt) const {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const bool ok = okB[j] && (k0 + kB[j] < K);
-      dma16(rb, sb + 1024u * j, ok ? offB[j] + (uint32_t)(kt * stepB) : kOOB);
-    }
+    for (int j = 0; j < 8; ++j) issue_one(st, kt, j);
   }
 
   // A fragment (32 rows x K step h) f of a stage.
@@ -177,21 +178,21 @@ struct Pipe2 {
     const int row = (w >> 1) * G2::WTM + 32 * f + (l & 31);
     return stage[row * 4 + ((2 * h + (l >> 5)) ^ swz4(row))];
   }
-  // BNC: raw K rows (4 columns, 8 bytes each) of both K steps into raw[h*8+s];
-  // Bt: the operands themselves into bq[i*2+h].
-  __device__ __forceinline__ static void read_b(const u32x4* stage, u32x2 (&raw)[16], u32x4 (&bq)[8]) {
+  // BNC: raw K rows (4 columns, 8 bytes each) of K step `part` into
+  // raw[part*8+s]; Bt: the operands (i, h) for i in {2 part, 2 part + 1} into
+  // bq[i*2+h].
+  __device__ __forceinline__ static void read_b(const u32x4* stage, u32x2 (&raw)[16], u32x4 (&bq)[8],
+                                                int part) {
     const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
     const int wn = w & 1, lc = l & 31, lk = l >> 5;
     const u32x4* sb = stage + G2::A_CHUNKS;
     if constexpr (BNC) {
       const u32x2* sb2 = reinterpret_cast<const u32x2*>(sb);
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int s = 0; s < 8; ++s) raw[h * 8 + s] = sb2[(16 * h + 8 * lk + s) * 64 + wn * 32 + lc];
+      for (int s = 0; s < 8; ++s) raw[part * 8 + s] = sb2[(16 * part + 8 * lk + s) * 64 + wn * 32 + lc];
     } else {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 2 * part; i < 2 * part + 2; ++i)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const int row = wn * G2::WTN + 32 * i + lc;
@@ -220,91 +221,131 @@ struct Pipe2 {
         }
       }
   }
-  // The four MFMAs of fragment row f in K step h.
-  __device__ __forceinline__ static void mfma_row(u32x4 a, const u32x4 (&b)[8], f32x16 (&acc)[4][4],
-                                                  int f, int h) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      acc[f][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                          __builtin_bit_cast(bf16x8, b[i * 2 + h]),
-                                                          acc[f][i], 0, 0, 0);
+  // MFMA (f, i) of K step h.
+  __device__ __forceinline__ static void mfma1(u32x4 a, const u32x4 (&b)[8], f32x16 (&acc)[4][4],
+                                               int f, int h, int i) {
+    acc[f][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                        __builtin_bit_cast(bf16x8, b[i * 2 + h]),
+                                                        acc[f][i], 0, 0, 0);
   }
 };
 
 // One K tile: the 32 MFMAs of the current stage in 8 groups of 4 (K step h,
-// fragment row f) with the packed B operands `bc`; A fragments are read from
-// the current stage two groups ahead. Between the groups: the wait + barrier
-// that make tile i+1 visible, the next tile's B reads and packing into `bn`,
-// and the copies of tile i+3.
+// fragment row f) with the packed B operands `bc`. Each group's A fragment is
+// read two groups ahead; the first two of the tile come in `a0`, `a1` from the
+// previous iteration, and the last two groups read those of the next tile.
+// With one wave per SIMD the MFMA pipe idles whenever the wave stalls on other
+// issue, so the remaining work is spread one item between consecutive MFMAs
+// in a fixed order (sched_barrier keeps the compiler from regrouping it): the
+// wait + barrier that make tile i+1 visible (after group 0), the eight copies
+// of tile i + NST - 1, the next tile's B reads and their packing into `bn`.
+#define FPO_SB() __builtin_amdgcn_sched_barrier(0)
 template <bool BNC>
 __device__ __forceinline__ void gemm2_iter(const Pipe2<BNC>& p, G2Smem& sm, f32x16 (&acc)[4][4],
                                            const u32x4 (&bc)[8], u32x4 (&bn)[8], u32x2 (&raw)[16],
-                                           u32x4 (&bq)[8], int i, int kt0) {
+                                           u32x4 (&bq)[8], u32x4& a0, u32x4& a1, int i, int kt0) {
   using P = Pipe2<BNC>;
-  const u32x4* cur = sm.s + (i % G2::NST) * G2::STAGE_CHUNKS;
-  const u32x4* nxt = sm.s + ((i + 1) % G2::NST) * G2::STAGE_CHUNKS;
-  u32x4 a0 = P::read_a(cur, 0, 0), a1 = P::read_a(cur, 1, 0);
-  P::mfma_row(a0, bc, acc, 0, 0);
-  u32x4 a2 = P::read_a(cur, 2, 0);
-  __builtin_amdgcn_sched_barrier(0);
-  wait_vmcnt<G2::LOADS_PER_STAGE>();
-  stage_barrier();
-  __builtin_amdgcn_sched_barrier(0);
-  P::mfma_row(a1, bc, acc, 1, 0);
-  u32x4 a3 = P::read_a(cur, 3, 0);
-  P::read_b(nxt, raw, bq);
-  __builtin_amdgcn_sched_barrier(0);
-  P::mfma_row(a2, bc, acc, 2, 0);
-  u32x4 a4 = P::read_a(cur, 0, 1);
-  __builtin_amdgcn_sched_barrier(0);
-  p.issue((i + 3) % G2::NST, kt0 + i + 3);
-  __builtin_amdgcn_sched_barrier(0);
-  P::mfma_row(a3, bc, acc, 3, 0);
-  u32x4 a5 = P::read_a(cur, 1, 1);
-  P::pack_b(raw, bq, bn, 0);
-  __builtin_amdgcn_sched_barrier(0);
-  P::mfma_row(a4, bc, acc, 0, 1);
-  u32x4 a6 = P::read_a(cur, 2, 1);
-  P::pack_b(raw, bq, bn, 2);
-  __builtin_amdgcn_sched_barrier(0);
-  P::mfma_row(a5, bc, acc, 1, 1);
-  u32x4 a7 = P::read_a(cur, 3, 1);
-  __builtin_amdgcn_sched_barrier(0);
-  P::mfma_row(a6, bc, acc, 2, 1);
-  P::mfma_row(a7, bc, acc, 3, 1);
-  __builtin_amdgcn_sched_barrier(0);
+  constexpr int NST = G2::NST;
+  const u32x4* cur = sm.s + (i % NST) * G2::STAGE_CHUNKS;
+  const u32x4* nxt = sm.s + ((i + 1) % NST) * G2::STAGE_CHUNKS;
+  const int st = (i + NST - 1) % NST, kt = kt0 + i + NST - 1;
+  // group 0: f0 h0
+  P::mfma1(a0, bc, acc, 0, 0, 0); FPO_SB();
+  u32x4 a2 = P::read_a(cur, 2, 0); FPO_SB();
+  P::mfma1(a0, bc, acc, 0, 0, 1); FPO_SB();
+  P::mfma1(a0, bc, acc, 0, 0, 2); FPO_SB();
+  P::mfma1(a0, bc, acc, 0, 0, 3); FPO_SB();
+  wait_vmcnt<(NST - 3) * G2::LOADS_PER_STAGE>();
+  stage_barrier(); FPO_SB();
+  // group 1: f1 h0
+  P::mfma1(a1, bc, acc, 1, 0, 0); FPO_SB();
+  u32x4 a3 = P::read_a(cur, 3, 0); FPO_SB();
+  P::mfma1(a1, bc, acc, 1, 0, 1); FPO_SB();
+  p.issue_one(st, kt, 0); FPO_SB();
+  P::mfma1(a1, bc, acc, 1, 0, 2); FPO_SB();
+  P::read_b(nxt, raw, bq, 0); FPO_SB();
+  P::mfma1(a1, bc, acc, 1, 0, 3); FPO_SB();
+  p.issue_one(st, kt, 1); FPO_SB();
+  // group 2: f2 h0
+  P::mfma1(a2, bc, acc, 2, 0, 0); FPO_SB();
+  u32x4 a4 = P::read_a(cur, 0, 1); FPO_SB();
+  P::mfma1(a2, bc, acc, 2, 0, 1); FPO_SB();
+  p.issue_one(st, kt, 2); FPO_SB();
+  P::mfma1(a2, bc, acc, 2, 0, 2); FPO_SB();
+  P::read_b(nxt, raw, bq, 1); FPO_SB();
+  P::mfma1(a2, bc, acc, 2, 0, 3); FPO_SB();
+  p.issue_one(st, kt, 3); FPO_SB();
+  // group 3: f3 h0
+  P::mfma1(a3, bc, acc, 3, 0, 0); FPO_SB();
+  u32x4 a5 = P::read_a(cur, 1, 1); FPO_SB();
+  P::mfma1(a3, bc, acc, 3, 0, 1); FPO_SB();
+  p.issue_one(st, kt, 4); FPO_SB();
+  P::mfma1(a3, bc, acc, 3, 0, 2); FPO_SB();
+  P::mfma1(a3, bc, acc, 3, 0, 3); FPO_SB();
+  p.issue_one(st, kt, 5); FPO_SB();
+  // group 4: f0 h1
+  P::mfma1(a4, bc, acc, 0, 1, 0); FPO_SB();
+  u32x4 a6 = P::read_a(cur, 2, 1); FPO_SB();
+  P::mfma1(a4, bc, acc, 0, 1, 1); FPO_SB();
+  P::pack_b(raw, bq, bn, 0); FPO_SB();
+  P::mfma1(a4, bc, acc, 0, 1, 2); FPO_SB();
+  p.issue_one(st, kt, 6); FPO_SB();
+  P::mfma1(a4, bc, acc, 0, 1, 3); FPO_SB();
+  // group 5: f1 h1
+  P::mfma1(a5, bc, acc, 1, 1, 0); FPO_SB();
+  u32x4 a7 = P::read_a(cur, 3, 1); FPO_SB();
+  P::mfma1(a5, bc, acc, 1, 1, 1); FPO_SB();
+  P::pack_b(raw, bq, bn, 2); FPO_SB();
+  P::mfma1(a5, bc, acc, 1, 1, 2); FPO_SB();
+  p.issue_one(st, kt, 7); FPO_SB();
+  P::mfma1(a5, bc, acc, 1, 1, 3); FPO_SB();
+  // group 6: f2 h1
+  P::mfma1(a6, bc, acc, 2, 1, 0); FPO_SB();
+  a0 = P::read_a(nxt, 0, 0); FPO_SB();
+  P::mfma1(a6, bc, acc, 2, 1, 1); FPO_SB();
+  P::mfma1(a6, bc, acc, 2, 1, 2); FPO_SB();
+  P::mfma1(a6, bc, acc, 2, 1, 3); FPO_SB();
+  // group 7: f3 h1
+  P::mfma1(a7, bc, acc, 3, 1, 0); FPO_SB();
+  a1 = P::read_a(nxt, 1, 0); FPO_SB();
+  P::mfma1(a7, bc, acc, 3, 1, 1); FPO_SB();
+  P::mfma1(a7, bc, acc, 3, 1, 2); FPO_SB();
+  P::mfma1(a7, bc, acc, 3, 1, 3); FPO_SB();
 }
+#undef FPO_SB
 
 // C tile accumulated over K tiles [kt0, kt1). A and B point at the band of the
 // tile (A: row m0; B: column n0 (N-contiguous) or row n0 (K-contiguous)).
 //
-// Software pipeline over a 4-stage ring: while tile i is multiplied, tile
-// i+1's B operands are read and packed and tile i+3's copies are issued.
+// Software pipeline over an NST-stage ring: while tile i is multiplied, tile
+// i+1's operands are read (B packed) and tile i+NST-1's copies are issued.
 // Copies are issued every iteration (beyond the last tile they read zeros into
 // a stage no longer needed), so the wait before each barrier is a constant
-// vmcnt(8): only tile i+2's copies may still be in flight. A stage is
+// count: only tiles i+2 .. i+NST-2 may still be in flight. A stage is
 // overwritten only after every wave has passed the barrier that follows its
 // last read (its reads feed MFMAs issued before that barrier).
 template <bool BNC>
 __device__ __forceinline__ void gemm2_mainloop(G2Smem& sm, f32x16 (&acc)[4][4], const Operand& A,
                                                const Operand& B, int M_rem, int N_rem, int K,
                                                int kt0, int kt1) {
+  constexpr int NST = G2::NST;
   const int n = kt1 - kt0;
   if (n <= 0) return;
   Pipe2<BNC> p;
   p.setup(sm.s, A, B, M_rem, N_rem, K);
-  p.issue(0, kt0);
-  p.issue(1, kt0 + 1);
-  p.issue(2, kt0 + 2);
-  wait_vmcnt<2 * G2::LOADS_PER_STAGE>();
+#pragma unroll
+  for (int s = 0; s < NST - 1; ++s) p.issue(s, kt0 + s);
+  wait_vmcnt<(NST - 2) * G2::LOADS_PER_STAGE>();
   stage_barrier();
   u32x4 bc[8], bn[8], bq[8];
   u32x2 raw[16];
-  Pipe2<BNC>::read_b(sm.s, raw, bq);
+  Pipe2<BNC>::read_b(sm.s, raw, bq, 0);
+  Pipe2<BNC>::read_b(sm.s, raw, bq, 1);
+  u32x4 a0 = Pipe2<BNC>::read_a(sm.s, 0, 0), a1 = Pipe2<BNC>::read_a(sm.s, 1, 0);
   Pipe2<BNC>::pack_b(raw, bq, bc, 0);
   Pipe2<BNC>::pack_b(raw, bq, bc, 2);
   for (int i = 0; i < n; ++i) {
-    gemm2_iter<BNC>(p, sm, acc, bc, bn, raw, bq, i, kt0);
+    gemm2_iter<BNC>(p, sm, acc, bc, bn, raw, bq, a0, a1, i, kt0);
 #pragma unroll
     for (int j = 0; j < 8; ++j) bc[j] = bn[j];
   }
