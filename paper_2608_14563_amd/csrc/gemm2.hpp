@@ -1,24 +1,31 @@
-// bf16 MFMA tile core with a 4-stage LDS ring fed by LDS-DMA buffer loads
+// bf16 MFMA tile core with a 2-stage LDS ring fed by LDS-DMA buffer loads
 // (gfx950 buffer_load_dwordx4 ... lds). One workgroup of 4 waves (2 x 2)
 // computes a 256 x 256 tile of C = A B, A K-contiguous ([M][K]), B either
-// N-contiguous ([K][N]) or K-contiguous ([N][K], "Bt"). K advances 32 per
-// stage = two K steps of v_mfma_f32_32x32x16_bf16 (each wave: 4 x 4 blocks of
-// 32 x 32). The 32x32x16 shape sustains ~95% of the bf16 peak in a pure MFMA
-// loop on gfx950 where 16x16x32 reaches ~70% (measured).
+// N-contiguous ([K][N]) or K-contiguous ([N][K], "Bt"). K advances 64 per
+// stage = four K steps of v_mfma_f32_32x32x16_bf16 (each wave: 4 x 4 blocks of
+// 32 x 32, i.e. 128 x 128).
 //
-// Pipeline: tiles kt+1..kt+3 are in flight while tile kt is multiplied; the
-// global->LDS copies go straight into LDS (no register staging), each wave
-// instruction filling 1 KB of LDS at base + 16 * lane. Out-of-range rows or
-// K chunks are given a buffer offset beyond the resource and read as zero.
-// One barrier per stage: a stage is refilled only after every wave has passed
-// the barrier that follows its last use.
+// Why these shapes (measured on MI355X with random bf16 operands, where the
+// chip runs at its power limit and the clock, not the issue rate, decides):
+//  * 32x32x16 sustains ~70% of the bf16 peak in a pure MFMA loop, 16x16x32
+//    ~64%;
+//  * a 64-deep K stage makes every copy of a K-contiguous row a full 128-byte
+//    line: at 32 deep each row gave a half line, twice the L2 requests for the
+//    same bytes, and the extra request traffic cost ~25% of the clock.
+//
+// Pipeline (per K tile j in stage j % 2): the 16 copies of tile j+1 are issued
+// from the end of iteration j-1 into the other stage, two between MFMA groups;
+// one wait + barrier per tile (after MFMA group 13 of 16) makes tile j+1
+// visible and releases stage j % 2; the last two groups then overlap the next
+// tile's first operand reads. Out-of-range rows / K chunks are given a buffer
+// offset beyond the resource and read as zero.
 //
 // LDS layouts (16-byte chunks):
-//   K-contiguous tile: [rows][4 chunks], chunk c of row r stored at position
-//     c ^ ((r >> 2) & 3) -- fragment reads (32 consecutive rows x 2 chunks)
-//     are then bank-conflict free under every lane-phase model consistent
-//     with ds_read_b128 timings measured on gfx950.
-//   N-contiguous tile: [32 K rows][32 chunks] as in memory (conflict free).
+//   K-contiguous tile: [rows][8 chunks], chunk c of row r stored at position
+//     c ^ swz8(r); swz8 takes row bits (2, 1, 3) -- fragment reads (32
+//     consecutive rows x 2 chunks) are then bank-conflict free under every
+//     lane-phase model consistent with ds_read_b128 timings measured on gfx950.
+//   N-contiguous tile: [64 K rows][32 chunks] as in memory.
 // Lane layout: in K step h (16 wide) lane l owns K indices 16h + 8*(l>>5) + s,
 // s = 0..7, for both operands (the K order inside an MFMA is a summation order
 // only). A fragment f holds rows 32f + (l&31) of the wave's 128. Output
@@ -34,19 +41,21 @@
 namespace fpo {
 
 struct G2 {
-  static constexpr int BM = 256, BN = 256, BK = 32, NST = 4;
+  static constexpr int BM = 256, BN = 256, BK = 64, NST = 2;
   static constexpr int WTM = 128, WTN = 128;
-  static constexpr int A_CHUNKS = BM * 4;        // 16 KB
-  static constexpr int B_CHUNKS = BN * 4;        // 16 KB
+  static constexpr int A_CHUNKS = BM * 8;   // 32 KB
+  static constexpr int B_CHUNKS = BN * 8;   // 32 KB
   static constexpr int STAGE_CHUNKS = A_CHUNKS + B_CHUNKS;
-  static constexpr int LOADS_PER_STAGE = 8;      // DMA instructions per wave per stage
+  static constexpr int LOADS_PER_STAGE = 16;  // DMA instructions per wave per stage
 };
 
 struct G2Smem {
-  u32x4 s[G2::NST * G2::STAGE_CHUNKS];  // 32 KB per stage
+  u32x4 s[G2::NST * G2::STAGE_CHUNKS];  // 64 KB per stage
 };
 
-__device__ __forceinline__ int swz4(int row) { return (row >> 2) & 3; }
+__device__ __forceinline__ int swz8(int row) {
+  return ((row >> 2) & 1) | (row & 2) | ((row >> 1) & 4);
+}
 
 // One 16-byte-per-lane LDS-DMA copy: lane l's 16 bytes at rsrc + voff land at
 // LDS byte address m0 + 16 * l. Issued as inline asm so that the compiler does
@@ -117,238 +126,234 @@ __device__ __forceinline__ u32x4 make_rsrc(const Operand& o) {
 template <bool BNC>
 struct Pipe2 {
   u32x4 ra, rb;
-  uint32_t lds_wave;      // LDS byte address of this wave's slice of stage 0 (uniform)
-  uint32_t offA[4], offB[4];  // per-lane byte offsets of this lane's copies at k0 = 0
-  int kA[4], kB[4];           // K index of the chunk / row each copy reads at k0 = 0
-  bool okA[4], okB[4];        // row (A, Bt) or column (B) inside the operand
-  int K;
-  int64_t stepB;              // bytes B advances per K tile (BNC: 32 rows; Bt: 64 bytes)
+  uint32_t lds_wave;   // LDS byte address of stage 0 (uniform)
+  int w, l;
+  // K-contiguous copies: instruction q (0..7) of this wave covers rows
+  // 8*(8w+q) .. +7; lane l reads row 8*(8w+q) + (l>>3), global chunk
+  // (l&7) ^ swz8(row), which depends on q only through q & 1.
+  uint32_t offA[2], offBt[2];  // byte offsets at q = 0 / 1, k = 0
+  int kc[2];                   // K index of the lane's chunk for q & 1
+  int rowA0;                   // row of the lane at q = 0
+  int M_rem, N_rem, K;
+  int64_t ldA2, ldB2;          // row strides in bytes
+  // N-contiguous copies: instruction q covers K rows 2*(8w+q) + (l>>5),
+  // columns 8*(l&31) .. +7.
+  uint32_t offBn;
+  bool okBn;
 
   __device__ __forceinline__ void setup(const u32x4* smem, const Operand& A, const Operand& B,
-                                        int M_rem, int N_rem, int K_) {
-    const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+                                        int M_rem_, int N_rem_, int K_) {
+    w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));  // uniform: LDS addresses go to M0
+    l = threadIdx.x & 63;
     ra = make_rsrc(A);
     rb = make_rsrc(B);
-    lds_wave = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem + (uint32_t)w * 4096u);
+    lds_wave = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)smem);
+    M_rem = M_rem_;
+    N_rem = N_rem_;
     K = K_;
+    ldA2 = A.ld * 2;
+    ldB2 = B.ld * 2;
+    rowA0 = 64 * w + (l >> 3);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int inst = w * 4 + j;
-      const int row = 16 * inst + (l >> 2);
-      const int c = (l & 3) ^ swz4(row);
-      kA[j] = 8 * c;
-      okA[j] = row < M_rem;
-      offA[j] = (uint32_t)(((int64_t)row * A.ld + 8 * c) * 2);
-      if constexpr (BNC) {
-        const int krow = 2 * inst + (l >> 5), cb = l & 31;
-        kB[j] = krow;
-        okB[j] = 8 * cb < N_rem;
-        offB[j] = (uint32_t)(((int64_t)krow * B.ld + 8 * cb) * 2);
-      } else {
-        kB[j] = 8 * c;
-        okB[j] = row < N_rem;
-        offB[j] = (uint32_t)(((int64_t)row * B.ld + 8 * c) * 2);
-      }
+    for (int p = 0; p < 2; ++p) {
+      const int row = rowA0 + 8 * p;
+      const int c = (l & 7) ^ swz8(row);
+      kc[p] = 8 * c;
+      offA[p] = (uint32_t)((int64_t)(l >> 3) * ldA2 + 16 * c);
+      offBt[p] = (uint32_t)((int64_t)(l >> 3) * ldB2 + 16 * c);
     }
-    stepB = BNC ? (int64_t)G2::BK * B.ld * 2 : (int64_t)G2::BK * 2;
+    offBn = (uint32_t)((int64_t)(l >> 5) * ldB2 + 16 * (l & 31));
+    okBn = 8 * (l & 31) < N_rem;
   }
 
-  // DMA copy j (0..3: A, 4..7: B) of K tile kt into ring stage st; tiles at
-  // or beyond K (and out-of-range rows / columns) read as zero.
+  // DMA copy j (0..7: A, 8..15: B) of K tile kt into ring stage st; rows,
+  // columns and K chunks out of range read as zero.
   __device__ __forceinline__ void issue_one(int st, int kt, int j) const {
     const int k0 = kt * G2::BK;
-    const uint32_t sa = lds_wave + (uint32_t)st * (G2::STAGE_CHUNKS * 16);
-    if (j < 4) {
-      const bool ok = okA[j] && (k0 + kA[j] < K);
-      dma16(ra, sa + 1024u * j, ok ? offA[j] + (uint32_t)(k0 * 2) : kOOB);
+    const uint32_t sbase = lds_wave + (uint32_t)st * (G2::STAGE_CHUNKS * 16);
+    const int q = j & 7, inst = 8 * w + q;
+    if (j < 8) {
+      const int row = rowA0 + 8 * q;
+      const bool ok = row < M_rem && k0 + kc[q & 1] < K;
+      const uint32_t off = offA[q & 1] + (uint32_t)((int64_t)8 * inst * ldA2) + (uint32_t)(k0 * 2);
+      dma16(ra, sbase + 1024u * inst, ok ? off : kOOB);
+    } else if constexpr (BNC) {
+      const int krow = 2 * inst + (l >> 5);
+      const bool ok = okBn && k0 + krow < K;
+      const uint32_t off = offBn + (uint32_t)((int64_t)(k0 + 2 * inst) * ldB2);
+      dma16(rb, sbase + G2::A_CHUNKS * 16 + 1024u * inst, ok ? off : kOOB);
     } else {
-      const int jb = j - 4;
-      const bool ok = okB[jb] && (k0 + kB[jb] < K);
-      dma16(rb, sa + G2::A_CHUNKS * 16 + 1024u * jb, ok ? offB[jb] + (uint32_t)(kt * stepB) : kOOB);
+      const int row = rowA0 + 8 * q;
+      const bool ok = row < N_rem && k0 + kc[q & 1] < K;
+      const uint32_t off = offBt[q & 1] + (uint32_t)((int64_t)8 * inst * ldB2) + (uint32_t)(k0 * 2);
+      dma16(rb, sbase + G2::A_CHUNKS * 16 + 1024u * inst, ok ? off : kOOB);
     }
   }
-  __device__ __forceinline__ void issue(int st, int kt) const {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) issue_one(st, kt, j);
-  }
 
-  // A fragment (32 rows x K step h) f of a stage.
-  __device__ __forceinline__ static u32x4 read_a(const u32x4* stage, int f, int h) {
-    const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  // A fragment (32 rows, K step h) f of a stage.
+  __device__ __forceinline__ u32x4 read_a(const u32x4* stage, int f, int h) const {
     const int row = (w >> 1) * G2::WTM + 32 * f + (l & 31);
-    return stage[row * 4 + ((2 * h + (l >> 5)) ^ swz4(row))];
+    return stage[row * 8 + ((2 * h + (l >> 5)) ^ swz8(row))];
   }
-  // BNC: raw K rows (4 columns, 8 bytes each) of K step `part` into
-  // raw[part*8+s]; Bt: the operands (i, h) for i in {2 part, 2 part + 1} into
-  // bq[i*2+h].
-  __device__ __forceinline__ static void read_b(const u32x4* stage, u32x2 (&raw)[16], u32x4 (&bq)[8],
-                                                int part) {
-    const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
-    const int wn = w & 1, lc = l & 31, lk = l >> 5;
+  // B of K step h, half `part` (0/1). BNC: raw K rows 16h + 8*(l>>5) + s for
+  // s in [4 part, 4 part + 4) (4 columns, 8 bytes each) into raw[s]; Bt: the
+  // operands i in {2 part, 2 part + 1} into bq[i].
+  __device__ __forceinline__ void read_b(const u32x4* stage, int h, int part, u32x2 (&raw)[8],
+                                         u32x4 (&bq)[4]) const {
     const u32x4* sb = stage + G2::A_CHUNKS;
+    const int wn = w & 1, lc = l & 31;
     if constexpr (BNC) {
       const u32x2* sb2 = reinterpret_cast<const u32x2*>(sb);
 #pragma unroll
-      for (int s = 0; s < 8; ++s) raw[part * 8 + s] = sb2[(16 * part + 8 * lk + s) * 64 + wn * 32 + lc];
+      for (int s = 4 * part; s < 4 * part + 4; ++s)
+        raw[s] = sb2[(16 * h + 8 * (l >> 5) + s) * 64 + wn * 32 + lc];
     } else {
 #pragma unroll
-      for (int i = 2 * part; i < 2 * part + 2; ++i)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int row = wn * G2::WTN + 32 * i + lc;
-          bq[i * 2 + h] = sb[row * 4 + ((2 * h + lk) ^ swz4(row))];
-        }
+      for (int i = 2 * part; i < 2 * part + 2; ++i) {
+        const int row = wn * G2::WTN + 32 * i + lc;
+        bq[i] = sb[row * 8 + ((2 * h + (l >> 5)) ^ swz8(row))];
+      }
     }
   }
-  // B operands (i, h) for i in [i0, i0+2): v_perm packing of K-row pairs (BNC)
-  // or as read (Bt). b[i*2+h].
-  __device__ __forceinline__ static void pack_b(const u32x2 (&raw)[16], const u32x4 (&bq)[8],
-                                                u32x4 (&b)[8], int i0) {
+  // B operands i in {2 part, 2 part + 1} of a K step: v_perm packing of K-row
+  // pairs (BNC) or as read (Bt).
+  __device__ __forceinline__ static void pack_b(const u32x2 (&raw)[8], const u32x4 (&bq)[4],
+                                                u32x4 (&b)[4], int part) {
 #pragma unroll
-    for (int i = i0; i < i0 + 2; ++i)
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        if constexpr (BNC) {
-          const int q = i >> 1;
-          const uint32_t sel = (i & 1) ? 0x07060302u : 0x05040100u;
-          const u32x2* r = raw + h * 8;
-          b[i * 2 + h] = u32x4{__builtin_amdgcn_perm(r[1][q], r[0][q], sel),
-                               __builtin_amdgcn_perm(r[3][q], r[2][q], sel),
-                               __builtin_amdgcn_perm(r[5][q], r[4][q], sel),
-                               __builtin_amdgcn_perm(r[7][q], r[6][q], sel)};
-        } else {
-          b[i * 2 + h] = bq[i * 2 + h];
-        }
+    for (int i = 2 * part; i < 2 * part + 2; ++i) {
+      if constexpr (BNC) {
+        const int q = i >> 1;
+        const uint32_t sel = (i & 1) ? 0x07060302u : 0x05040100u;
+        b[i] = u32x4{__builtin_amdgcn_perm(raw[1][q], raw[0][q], sel),
+                     __builtin_amdgcn_perm(raw[3][q], raw[2][q], sel),
+                     __builtin_amdgcn_perm(raw[5][q], raw[4][q], sel),
+                     __builtin_amdgcn_perm(raw[7][q], raw[6][q], sel)};
+      } else {
+        b[i] = bq[i];
       }
+    }
   }
-  // MFMA (f, i) of K step h.
-  __device__ __forceinline__ static void mfma1(u32x4 a, const u32x4 (&b)[8], f32x16 (&acc)[4][4],
-                                               int f, int h, int i) {
-    acc[f][i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                        __builtin_bit_cast(bf16x8, b[i * 2 + h]),
-                                                        acc[f][i], 0, 0, 0);
+  __device__ __forceinline__ static void mfma1(u32x4 a, u32x4 b, f32x16& acc) {
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                  __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
   }
 };
 
-// One K tile: the 32 MFMAs of the current stage in 8 groups of 4 (K step h,
-// fragment row f) with the packed B operands `bc`. Each group's A fragment is
-// read two groups ahead; the first two of the tile come in `a0`, `a1` from the
-// previous iteration, and the last two groups read those of the next tile.
-// With one wave per SIMD the MFMA pipe idles whenever the wave stalls on other
-// issue, so the remaining work is spread one item between consecutive MFMAs
-// in a fixed order (sched_barrier keeps the compiler from regrouping it): the
-// wait + barrier that make tile i+1 visible (after group 0), the eight copies
-// of tile i + NST - 1, the next tile's B reads and their packing into `bn`.
 #define FPO_SB() __builtin_amdgcn_sched_barrier(0)
+
+// One MFMA group (fragment row f of K step with operands b): the four MFMAs
+// with up to four items of other work placed one after each (sched_barrier
+// keeps the order: with one wave per SIMD the MFMA pipe idles whenever the
+// wave stalls on a burst of other issue).
+template <class X0, class X1, class X2, class X3>
+__device__ __forceinline__ void mfma_group(f32x16 (&acc)[4][4], int f, u32x4 a, const u32x4 (&b)[4],
+                                           X0 x0, X1 x1, X2 x2, X3 x3) {
+  acc[f][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                      __builtin_bit_cast(bf16x8, b[0]), acc[f][0], 0, 0, 0);
+  FPO_SB(); x0(); FPO_SB();
+  acc[f][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                      __builtin_bit_cast(bf16x8, b[1]), acc[f][1], 0, 0, 0);
+  FPO_SB(); x1(); FPO_SB();
+  acc[f][2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                      __builtin_bit_cast(bf16x8, b[2]), acc[f][2], 0, 0, 0);
+  FPO_SB(); x2(); FPO_SB();
+  acc[f][3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                      __builtin_bit_cast(bf16x8, b[3]), acc[f][3], 0, 0, 0);
+  FPO_SB(); x3(); FPO_SB();
+}
+
+// One K tile j (stage j % 2): 16 MFMA groups g = 4h + f. On entry `bc` holds
+// the B operands of K step 0 and a[0], a[1] the A fragments of groups 0, 1.
+// Tile j+1's copies 4..15 go out in groups 0..5 (0..3 went out at the end of
+// the previous tile); the B operands of step h+1 are read in groups 4h, 4h+1
+// and packed in 4h+2, 4h+3; A fragments are read two groups ahead (groups
+// 14, 15 four ahead, so that all reads of the stage are complete at the
+// barrier). After group 13: wait for tile j+1's copies, barrier. Groups 14, 15
+// read tile j+1's first operands and issue tile j+2's copies 0..3 into the
+// stage just released.
 template <bool BNC>
 __device__ __forceinline__ void gemm2_iter(const Pipe2<BNC>& p, G2Smem& sm, f32x16 (&acc)[4][4],
-                                           const u32x4 (&bc)[8], u32x4 (&bn)[8], u32x2 (&raw)[16],
-                                           u32x4 (&bq)[8], u32x4& a0, u32x4& a1, int i, int kt0) {
-  using P = Pipe2<BNC>;
-  constexpr int NST = G2::NST;
-  const u32x4* cur = sm.s + (i % NST) * G2::STAGE_CHUNKS;
-  const u32x4* nxt = sm.s + ((i + 1) % NST) * G2::STAGE_CHUNKS;
-  const int st = (i + NST - 1) % NST, kt = kt0 + i + NST - 1;
-  // group 0: f0 h0
-  P::mfma1(a0, bc, acc, 0, 0, 0); FPO_SB();
-  u32x4 a2 = P::read_a(cur, 2, 0); FPO_SB();
-  P::mfma1(a0, bc, acc, 0, 0, 1); FPO_SB();
-  P::mfma1(a0, bc, acc, 0, 0, 2); FPO_SB();
-  P::mfma1(a0, bc, acc, 0, 0, 3); FPO_SB();
-  wait_vmcnt<(NST - 3) * G2::LOADS_PER_STAGE>();
-  stage_barrier(); FPO_SB();
-  // group 1: f1 h0
-  P::mfma1(a1, bc, acc, 1, 0, 0); FPO_SB();
-  u32x4 a3 = P::read_a(cur, 3, 0); FPO_SB();
-  P::mfma1(a1, bc, acc, 1, 0, 1); FPO_SB();
-  p.issue_one(st, kt, 0); FPO_SB();
-  P::mfma1(a1, bc, acc, 1, 0, 2); FPO_SB();
-  P::read_b(nxt, raw, bq, 0); FPO_SB();
-  P::mfma1(a1, bc, acc, 1, 0, 3); FPO_SB();
-  p.issue_one(st, kt, 1); FPO_SB();
-  // group 2: f2 h0
-  P::mfma1(a2, bc, acc, 2, 0, 0); FPO_SB();
-  u32x4 a4 = P::read_a(cur, 0, 1); FPO_SB();
-  P::mfma1(a2, bc, acc, 2, 0, 1); FPO_SB();
-  p.issue_one(st, kt, 2); FPO_SB();
-  P::mfma1(a2, bc, acc, 2, 0, 2); FPO_SB();
-  P::read_b(nxt, raw, bq, 1); FPO_SB();
-  P::mfma1(a2, bc, acc, 2, 0, 3); FPO_SB();
-  p.issue_one(st, kt, 3); FPO_SB();
-  // group 3: f3 h0
-  P::mfma1(a3, bc, acc, 3, 0, 0); FPO_SB();
-  u32x4 a5 = P::read_a(cur, 1, 1); FPO_SB();
-  P::mfma1(a3, bc, acc, 3, 0, 1); FPO_SB();
-  p.issue_one(st, kt, 4); FPO_SB();
-  P::mfma1(a3, bc, acc, 3, 0, 2); FPO_SB();
-  P::mfma1(a3, bc, acc, 3, 0, 3); FPO_SB();
-  p.issue_one(st, kt, 5); FPO_SB();
-  // group 4: f0 h1
-  P::mfma1(a4, bc, acc, 0, 1, 0); FPO_SB();
-  u32x4 a6 = P::read_a(cur, 2, 1); FPO_SB();
-  P::mfma1(a4, bc, acc, 0, 1, 1); FPO_SB();
-  P::pack_b(raw, bq, bn, 0); FPO_SB();
-  P::mfma1(a4, bc, acc, 0, 1, 2); FPO_SB();
-  p.issue_one(st, kt, 6); FPO_SB();
-  P::mfma1(a4, bc, acc, 0, 1, 3); FPO_SB();
-  // group 5: f1 h1
-  P::mfma1(a5, bc, acc, 1, 1, 0); FPO_SB();
-  u32x4 a7 = P::read_a(cur, 3, 1); FPO_SB();
-  P::mfma1(a5, bc, acc, 1, 1, 1); FPO_SB();
-  P::pack_b(raw, bq, bn, 2); FPO_SB();
-  P::mfma1(a5, bc, acc, 1, 1, 2); FPO_SB();
-  p.issue_one(st, kt, 7); FPO_SB();
-  P::mfma1(a5, bc, acc, 1, 1, 3); FPO_SB();
-  // group 6: f2 h1
-  P::mfma1(a6, bc, acc, 2, 1, 0); FPO_SB();
-  a0 = P::read_a(nxt, 0, 0); FPO_SB();
-  P::mfma1(a6, bc, acc, 2, 1, 1); FPO_SB();
-  P::mfma1(a6, bc, acc, 2, 1, 2); FPO_SB();
-  P::mfma1(a6, bc, acc, 2, 1, 3); FPO_SB();
-  // group 7: f3 h1
-  P::mfma1(a7, bc, acc, 3, 1, 0); FPO_SB();
-  a1 = P::read_a(nxt, 1, 0); FPO_SB();
-  P::mfma1(a7, bc, acc, 3, 1, 1); FPO_SB();
-  P::mfma1(a7, bc, acc, 3, 1, 2); FPO_SB();
-  P::mfma1(a7, bc, acc, 3, 1, 3); FPO_SB();
+                                           u32x4 (&bc)[4], u32x4 (&a)[2], int j, int kt0) {
+  const u32x4* cur = sm.s + (j & 1) * G2::STAGE_CHUNKS;
+  const u32x4* nxt = sm.s + ((j + 1) & 1) * G2::STAGE_CHUNKS;
+  const int s1 = (j + 1) & 1, t1 = kt0 + j + 1;  // tile j+1: copies 4..15 now
+  const int s2 = j & 1, t2 = kt0 + j + 2;        // tile j+2: copies 0..3 after the barrier
+  auto nop = [] {};
+  u32x2 raw[8];
+  u32x4 bq[4], bn[4];
+  u32x4 a2, a3, a4, a5, a6, a7, a8, a9, a10, a11, a12, a13, a14, a15;
+  // ---- K step 0
+  mfma_group(acc, 0, a[0], bc, [&] { a2 = p.read_a(cur, 2, 0); }, [&] { p.issue_one(s1, t1, 4); },
+             [&] { p.read_b(cur, 1, 0, raw, bq); }, [&] { p.issue_one(s1, t1, 5); });
+  mfma_group(acc, 1, a[1], bc, [&] { a3 = p.read_a(cur, 3, 0); }, [&] { p.issue_one(s1, t1, 6); },
+             [&] { p.read_b(cur, 1, 1, raw, bq); }, [&] { p.issue_one(s1, t1, 7); });
+  mfma_group(acc, 2, a2, bc, [&] { a4 = p.read_a(cur, 0, 1); }, [&] { p.issue_one(s1, t1, 8); },
+             [&] { Pipe2<BNC>::pack_b(raw, bq, bn, 0); }, [&] { p.issue_one(s1, t1, 9); });
+  mfma_group(acc, 3, a3, bc, [&] { a5 = p.read_a(cur, 1, 1); }, [&] { p.issue_one(s1, t1, 10); },
+             [&] { Pipe2<BNC>::pack_b(raw, bq, bn, 1); }, [&] { p.issue_one(s1, t1, 11); });
+  // ---- K step 1
+  mfma_group(acc, 0, a4, bn, [&] { a6 = p.read_a(cur, 2, 1); }, [&] { p.issue_one(s1, t1, 12); },
+             [&] { p.read_b(cur, 2, 0, raw, bq); }, [&] { p.issue_one(s1, t1, 13); });
+  mfma_group(acc, 1, a5, bn, [&] { a7 = p.read_a(cur, 3, 1); }, [&] { p.issue_one(s1, t1, 14); },
+             [&] { p.read_b(cur, 2, 1, raw, bq); }, [&] { p.issue_one(s1, t1, 15); });
+  mfma_group(acc, 2, a6, bn, [&] { a8 = p.read_a(cur, 0, 2); }, nop,
+             [&] { Pipe2<BNC>::pack_b(raw, bq, bc, 0); }, nop);
+  mfma_group(acc, 3, a7, bn, [&] { a9 = p.read_a(cur, 1, 2); }, nop,
+             [&] { Pipe2<BNC>::pack_b(raw, bq, bc, 1); }, nop);
+  // ---- K step 2 (operands in bc)
+  mfma_group(acc, 0, a8, bc, [&] { a10 = p.read_a(cur, 2, 2); }, nop,
+             [&] { p.read_b(cur, 3, 0, raw, bq); }, nop);
+  mfma_group(acc, 1, a9, bc, [&] { a11 = p.read_a(cur, 3, 2); }, nop,
+             [&] { p.read_b(cur, 3, 1, raw, bq); }, nop);
+  mfma_group(acc, 2, a10, bc, [&] { a12 = p.read_a(cur, 0, 3); }, [&] { a14 = p.read_a(cur, 2, 3); },
+             [&] { Pipe2<BNC>::pack_b(raw, bq, bn, 0); }, nop);
+  mfma_group(acc, 3, a11, bc, [&] { a13 = p.read_a(cur, 1, 3); }, [&] { a15 = p.read_a(cur, 3, 3); },
+             [&] { Pipe2<BNC>::pack_b(raw, bq, bn, 1); }, nop);
+  // ---- K step 3 (operands in bn)
+  mfma_group(acc, 0, a12, bn, nop, nop, nop, nop);
+  mfma_group(acc, 1, a13, bn, nop, nop, nop, [&] {
+    // every read of this stage is complete and tile j+1 has landed
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+    wait_vmcnt<0>();
+    stage_barrier();
+  });
+  mfma_group(acc, 2, a14, bn, [&] { p.read_b(nxt, 0, 0, raw, bq); }, [&] { a[0] = p.read_a(nxt, 0, 0); },
+             [&] { p.read_b(nxt, 0, 1, raw, bq); }, [&] { p.issue_one(s2, t2, 0); });
+  mfma_group(acc, 3, a15, bn, [&] { a[1] = p.read_a(nxt, 1, 0); }, [&] { p.issue_one(s2, t2, 1); },
+             [&] { p.issue_one(s2, t2, 2); }, [&] { p.issue_one(s2, t2, 3); });
+  Pipe2<BNC>::pack_b(raw, bq, bc, 0);
+  Pipe2<BNC>::pack_b(raw, bq, bc, 1);
 }
 #undef FPO_SB
 
 // C tile accumulated over K tiles [kt0, kt1). A and B point at the band of the
 // tile (A: row m0; B: column n0 (N-contiguous) or row n0 (K-contiguous)).
-//
-// Software pipeline over an NST-stage ring: while tile i is multiplied, tile
-// i+1's operands are read (B packed) and tile i+NST-1's copies are issued.
-// Copies are issued every iteration (beyond the last tile they read zeros into
-// a stage no longer needed), so the wait before each barrier is a constant
-// count: only tiles i+2 .. i+NST-2 may still be in flight. A stage is
-// overwritten only after every wave has passed the barrier that follows its
-// last read (its reads feed MFMAs issued before that barrier).
+// Copies are issued for every iteration (beyond the last tile they read
+// zeros, or the next split's data, into a stage no longer needed), so every
+// wait is the same: vmcnt(0) at the barrier of each tile.
 template <bool BNC>
 __device__ __forceinline__ void gemm2_mainloop(G2Smem& sm, f32x16 (&acc)[4][4], const Operand& A,
                                                const Operand& B, int M_rem, int N_rem, int K,
                                                int kt0, int kt1) {
-  constexpr int NST = G2::NST;
   const int n = kt1 - kt0;
   if (n <= 0) return;
   Pipe2<BNC> p;
   p.setup(sm.s, A, B, M_rem, N_rem, K);
 #pragma unroll
-  for (int s = 0; s < NST - 1; ++s) p.issue(s, kt0 + s);
-  wait_vmcnt<(NST - 2) * G2::LOADS_PER_STAGE>();
+  for (int q = 0; q < 16; ++q) p.issue_one(0, kt0, q);
+  wait_vmcnt<0>();
   stage_barrier();
-  u32x4 bc[8], bn[8], bq[8];
-  u32x2 raw[16];
-  Pipe2<BNC>::read_b(sm.s, raw, bq, 0);
-  Pipe2<BNC>::read_b(sm.s, raw, bq, 1);
-  u32x4 a0 = Pipe2<BNC>::read_a(sm.s, 0, 0), a1 = Pipe2<BNC>::read_a(sm.s, 1, 0);
-  Pipe2<BNC>::pack_b(raw, bq, bc, 0);
-  Pipe2<BNC>::pack_b(raw, bq, bc, 2);
-  for (int i = 0; i < n; ++i) {
-    gemm2_iter<BNC>(p, sm, acc, bc, bn, raw, bq, a0, a1, i, kt0);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) bc[j] = bn[j];
-  }
+  for (int q = 0; q < 4; ++q) p.issue_one(1, kt0 + 1, q);
+  u32x2 raw[8];
+  u32x4 bq[4], bc[4], a[2];
+  p.read_b(sm.s, 0, 0, raw, bq);
+  p.read_b(sm.s, 0, 1, raw, bq);
+  a[0] = p.read_a(sm.s, 0, 0);
+  a[1] = p.read_a(sm.s, 1, 0);
+  Pipe2<BNC>::pack_b(raw, bq, bc, 0);
+  Pipe2<BNC>::pack_b(raw, bq, bc, 1);
+  for (int j = 0; j < n; ++j) gemm2_iter<BNC>(p, sm, acc, bc, a, j, kt0);
   wait_vmcnt<0>();
   __syncthreads();
 }

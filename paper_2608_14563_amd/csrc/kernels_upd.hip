@@ -61,50 +61,69 @@ __global__ __launch_bounds__(256) void update_kernel(UpdArgs a, int n, OptScalar
   float* s1 = a.s1[m];
   float* s2 = a.s2[m];
   void* lp = a.W_lp[m];
+  // Every operand is streamed once: all of a thread's loads are issued before
+  // any store (they overlap instead of serialising per step), and loads and
+  // stores are non-temporal so the stream does not evict cached data.
+  constexpr int U = kElemsPerBlock / 1024;
+  const bool sgd = o.kind == 0;
+  f32x4 gv[U], w[U], v1[U], v2[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t i = base + threadIdx.x * 4 + u * 1024;
+    gv[u] = w[u] = v1[u] = v2[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (i < end) {
+      gv[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g + i));
+      w[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(W + i));
+      if (!(sgd && o.first)) v1[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s1 + i));
+      if (!sgd) v2[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s2 + i));
+    }
+  }
   float ss = 0.f;
-  for (int64_t i = base + threadIdx.x * 4; i < end; i += 1024) {
-    f32x4 gv = *reinterpret_cast<const f32x4*>(g + i) * s;
-    f32x4 w = *reinterpret_cast<const f32x4*>(W + i);
-    if (o.kind == 0) {  // SGD with momentum
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t i = base + threadIdx.x * 4 + u * 1024;
+    if (i >= end) continue;
+    const f32x4 gs = gv[u] * s;
+    f32x4 wv = w[u];
+    if (sgd) {  // SGD with momentum
       f32x4 bv;
       if (o.first) {
-        bv = gv;
+        bv = gs;
       } else {
-        f32x4 old = *reinterpret_cast<const f32x4*>(s1 + i);
-        bv.x = fmaf(o.momentum, old.x, gv.x);
-        bv.y = fmaf(o.momentum, old.y, gv.y);
-        bv.z = fmaf(o.momentum, old.z, gv.z);
-        bv.w = fmaf(o.momentum, old.w, gv.w);
+        bv.x = fmaf(o.momentum, v1[u].x, gs.x);
+        bv.y = fmaf(o.momentum, v1[u].y, gs.y);
+        bv.z = fmaf(o.momentum, v1[u].z, gs.z);
+        bv.w = fmaf(o.momentum, v1[u].w, gs.w);
       }
-      *reinterpret_cast<f32x4*>(s1 + i) = bv;
-      w.x = fmaf(-o.lr, bv.x, w.x);
-      w.y = fmaf(-o.lr, bv.y, w.y);
-      w.z = fmaf(-o.lr, bv.z, w.z);
-      w.w = fmaf(-o.lr, bv.w, w.w);
+      __builtin_nontemporal_store(bv, reinterpret_cast<f32x4*>(s1 + i));
+      wv.x = fmaf(-o.lr, bv.x, wv.x);
+      wv.y = fmaf(-o.lr, bv.y, wv.y);
+      wv.z = fmaf(-o.lr, bv.z, wv.z);
+      wv.w = fmaf(-o.lr, bv.w, wv.w);
     } else {  // AdamW, decoupled weight decay, bias corrected
-      f32x4 mv = *reinterpret_cast<const f32x4*>(s1 + i);
-      f32x4 vv = *reinterpret_cast<const f32x4*>(s2 + i);
+      f32x4 mv = v1[u], vv = v2[u];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float ge = gv[e];
+        const float ge = gs[e];
         const float me = o.beta1 * mv[e] + o.one_m_beta1 * ge;
         const float ve = o.beta2 * vv[e] + o.one_m_beta2 * ge * ge;
         mv[e] = me;
         vv[e] = ve;
         const float denom = sqrtf(ve) * o.inv_sqrt_bc2 + o.adam_eps;
-        w[e] = w[e] * o.decay - o.lr * (me * o.inv_bc1) / denom;
+        wv[e] = wv[e] * o.decay - o.lr * (me * o.inv_bc1) / denom;
       }
-      *reinterpret_cast<f32x4*>(s1 + i) = mv;
-      *reinterpret_cast<f32x4*>(s2 + i) = vv;
+      __builtin_nontemporal_store(mv, reinterpret_cast<f32x4*>(s1 + i));
+      __builtin_nontemporal_store(vv, reinterpret_cast<f32x4*>(s2 + i));
     }
-    *reinterpret_cast<f32x4*>(W + i) = w;
+    __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>(W + i));
     if (lp) {
       if (o.lp_bf16)
-        st4((uint16_t*)lp, i, w);
+        __builtin_nontemporal_store(u32x2{pack_bf16x2(wv.x, wv.y), pack_bf16x2(wv.z, wv.w)},
+                                    reinterpret_cast<u32x2*>((uint16_t*)lp + i));
       else
-        st4((float*)lp, i, w);
+        __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>((float*)lp + i));
     }
-    ss += w.x * w.x + w.y * w.y + w.z * w.z + w.w * w.w;
+    ss += wv.x * wv.x + wv.y * wv.y + wv.z * wv.z + wv.w * wv.w;
   }
   const double t = block_sum_d((double)ss, red);
   if (threadIdx.x == 0) part[b] = t;
@@ -200,15 +219,31 @@ __global__ __launch_bounds__(256) void cosine_kernel(CosArgs a, int n, int b_bf1
   const int64_t end = (a.numel[m] < base + kElemsPerBlock) ? a.numel[m] : base + kElemsPerBlock;
   const float* A = a.A[m];
   const void* B = a.B[m];
-  float dt = 0.f, sa = 0.f, sb = 0.f;
-  for (int64_t i = base + threadIdx.x * 4; i < end; i += 1024) {
-    f32x4 x = *reinterpret_cast<const f32x4*>(A + i);
-    sa += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
-    if (B) {
-      f32x4 y = b_bf16 ? ld4((const uint16_t*)B, i) : ld4((const float*)B, i);
-      dt += x.x * y.x + x.y * y.y + x.z * y.z + x.w * y.w;
-      sb += y.x * y.x + y.y * y.y + y.z * y.z + y.w * y.w;
+  constexpr int U = kElemsPerBlock / 1024;
+  f32x4 xs[U], ys[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t i = base + threadIdx.x * 4 + u * 1024;
+    xs[u] = ys[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (i < end) {
+      xs[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(A + i));
+      if (B) {
+        if (b_bf16) {
+          const u32x2 h = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>((const uint16_t*)B + i));
+          ys[u] = f32x4{bf16_lo(h.x), bf16_hi(h.x), bf16_lo(h.y), bf16_hi(h.y)};
+        } else {
+          ys[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>((const float*)B + i));
+        }
+      }
     }
+  }
+  float dt = 0.f, sa = 0.f, sb = 0.f;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const f32x4 x = xs[u], y = ys[u];  // zero outside the matrix
+    sa += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+    dt += x.x * y.x + x.y * y.y + x.z * y.z + x.w * y.w;
+    sb += y.x * y.x + y.y * y.y + y.z * y.z + y.w * y.w;
   }
   const double d0 = block_sum_d((double)dt, red);
   const double d1 = block_sum_d((double)sa, red);
