@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=1, help="workload id (paper_2608_14563_amd.inputs.CONFIGS)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--vocab-chunk", type=int, default=0,
+                    help="vocabulary chunk width (0: the library's planner)")
     ap.add_argument("--cpu-tokens", type=int, default=16, help="tokens in the oracle's timed sample")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration)")
@@ -212,7 +214,7 @@ def main():
     bad = torch.empty(1, dtype=torch.int32, device=dev)
     dW = [torch.empty(d, c.d_ff, dtype=torch.float32, device=dev) for _ in range(c.L)]
     ss = torch.empty(c.L, dtype=torch.float64, device=dev)
-    ws_oe = api.workspace(api.fpo_output_error_workspace(T, d, c.V, torch.bfloat16), dev)
+    ws_oe = api.workspace(api.fpo_output_error_workspace(T, d, c.V, torch.bfloat16, args.vocab_chunk), dev)
     ws_pg = api.workspace(api.fpo_pseudograd_workspace(T, d, c.d_ff, c.L, torch.bfloat16), dev)
     torch.cuda.synchronize()
     step_no = [0]
@@ -220,7 +222,8 @@ def main():
     def step():
         step_no[0] += 1
         api.fpo_output_error(tx, tgam, tW, ty, g_t, g_tilde_lp=g_lp, lse=lse, loss=loss, argmax=amax,
-                             bad_targets=bad, ws=ws_oe, eps=c.eps, min_rms=c.min_rms)
+                             bad_targets=bad, ws=ws_oe, eps=c.eps, min_rms=c.min_rms,
+                             vocab_chunk=args.vocab_chunk)
         api.fpo_pseudograd(g_lp, tacts, dW3=dW, sumsq=ss,
                            opt=api.OptConfig(lr=c.lr, clip_frac=c.clip_frac, step=step_no[0]),
                            W_master=Wm, W_lp=Wlp, state1=s1, W_sumsq=Wsq, ws=ws_pg)

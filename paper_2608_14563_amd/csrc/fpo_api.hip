@@ -54,19 +54,25 @@ struct OePlan {
   int nsplit = 1;
 };
 
+// Workgroups one wave of the MI355X grid holds (one 256 x 256 tile per CU).
+constexpr int64_t kWaveSlots = 256;
+
 OePlan plan_oe(const fpo_oe_desc& d) {
   const bool bf16 = d.dtype == FPO_BF16;
   const int64_t BM = bf16 ? 256 : 128, BN = BM, WTN = bf16 ? 128 : 64;
-  // staged p~ budget: 32M elements per chunk
+  // staged p~ budget: 32M elements per chunk; chunks of equal width. (Widths
+  // that minimise partly idle tile waves but leave a small last chunk measure
+  // slower at the power limit: the extra chunk's launches and merge cost more
+  // than a partly idle wave.)
   int64_t vmax = d.vocab_chunk > 0 ? round_up(d.vocab_chunk, 256)
                                    : std::max<int64_t>(256, ((int64_t)32 * 1024 * 1024 / d.T) / 256 * 256);
   vmax = std::min(vmax, round_up(d.V, 256));
-  const int64_t nchunk = ceil_div(d.V, vmax);
   OePlan p;
-  p.Vc = round_up(ceil_div(d.V, nchunk), 256);
+  p.Vc = round_up(ceil_div(d.V, ceil_div(d.V, vmax)), 256);
   p.nb = p.Vc / WTN;
+  // split the projection's K range so that its launch fills one wave
   const int64_t tiles = ceil_div(d.T, BM) * ceil_div(d.d, BN);
-  int64_t ns = ceil_div(512, tiles);
+  int64_t ns = ceil_div(kWaveSlots, tiles);
   ns = std::min<int64_t>(ns, 8);
   ns = std::min<int64_t>(ns, std::max<int64_t>(1, p.nb / 2));
   p.nsplit = (int)std::max<int64_t>(1, ns);
