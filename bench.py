@@ -42,7 +42,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--vocab-chunk", type=int, default=0,
                     help="vocabulary chunk width (0: the library's planner)")
-    ap.add_argument("--cpu-tokens", type=int, default=16, help="tokens in the oracle's timed sample")
+    ap.add_argument("--cpu-tokens", type=int, default=128, help="tokens in the oracle's timed sample")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration)")
     return ap.parse_args()
