@@ -60,12 +60,14 @@ constexpr int64_t kWaveSlots = 256;
 OePlan plan_oe(const fpo_oe_desc& d) {
   const bool bf16 = d.dtype == FPO_BF16;
   const int64_t BM = bf16 ? 256 : 128, BN = BM, WTN = bf16 ? 128 : 64;
-  // staged p~ budget: 32M elements per chunk; chunks of equal width. (Widths
-  // that minimise partly idle tile waves but leave a small last chunk measure
-  // slower at the power limit: the extra chunk's launches and merge cost more
-  // than a partly idle wave.)
+  // staged p~ budget: 2^30 elements (2 GiB bf16), so the vocabulary of the
+  // 7-8B shapes at T <= 4096 is one chunk: one logits launch, one projection
+  // launch accumulating over the whole vocabulary (one merge of the partials),
+  // one statistics pass. Chunks have equal width. (Measured at T = 2048,
+  // V = 100352: one chunk 2.4% faster per step than seven; widths that
+  // minimise partly idle tile waves but leave a small last chunk are slower.)
   int64_t vmax = d.vocab_chunk > 0 ? round_up(d.vocab_chunk, 256)
-                                   : std::max<int64_t>(256, ((int64_t)32 * 1024 * 1024 / d.T) / 256 * 256);
+                                   : std::max<int64_t>(256, ((int64_t)1 << 30) / d.T / 256 * 256);
   vmax = std::min(vmax, round_up(d.V, 256));
   OePlan p;
   p.Vc = round_up(ceil_div(d.V, ceil_div(d.V, vmax)), 256);
@@ -89,6 +91,7 @@ size_t carve_oe(const fpo_oe_desc& d, const OePlan& p, void* ws, fpo::OeLaunch* 
   int32_t* blk_i = c.take<int32_t>(d.T * p.nb);
   float* fout = c.take<float>(d.T * p.nsplit);
   float* alpha = c.take<float>(d.T);
+  float* refs = c.take<float>(d.T * p.nsplit);
   float* runM = c.take<float>(d.T);
   float* runS = c.take<float>(d.T);
   int32_t* runA = c.take<int32_t>(d.T);
@@ -101,6 +104,7 @@ size_t carve_oe(const fpo_oe_desc& d, const OePlan& p, void* ws, fpo::OeLaunch* 
     L->blk_i = blk_i;
     L->fout = fout;
     L->alpha = alpha;
+    L->refs = refs;
     L->runM = runM;
     L->runS = runS;
     L->runA = runA;

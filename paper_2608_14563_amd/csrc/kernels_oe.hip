@@ -220,8 +220,8 @@ __global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
 // ------------------------------------------------------------------ stats
 // One wave per token. Folds the chunk's block statistics (block max m_b, sum
 // of exp(z - m_b), first arg-max) into the running max M, partition S and
-// argmax, and brings the staged p~ of every block to one reference per split
-// of the chunk: ref_s = max of the split's block maxima, p~ <- p~ exp(m_b - ref_s).
+// argmax, and picks one reference per split of the chunk: ref_s = max of the
+// split's block maxima (rescale_p then brings p~ to it: p~ <- p~ exp(m_b - ref_s)).
 // The projection accumulates split s in scale ref_s and stores
 //   G_s <- acc * exp(ref_s - M_new) + G_s * exp(M_old - M_new),
 // so every factor is <= 1 and nothing can overflow.
@@ -233,7 +233,7 @@ __global__ __launch_bounds__(256) void chunk_stats_kernel(
     const float* __restrict__ blk_m, const float* __restrict__ blk_s,
     const int32_t* __restrict__ blk_i, float* __restrict__ runM, float* __restrict__ runS,
     int32_t* __restrict__ runA, float* __restrict__ fout, float* __restrict__ alpha,
-    PT* __restrict__ P, int64_t ldp) {
+    float* __restrict__ refs) {
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + w;
   if (row >= T) return;  // whole wave exits together; no barrier below
@@ -264,37 +264,16 @@ __global__ __launch_bounds__(256) void chunk_stats_kernel(
   float s = 0.f;
   for (int b = l; b < nb; b += 64) s += bs[b] * __expf(bm[b] - Mnew);
   s = wave_sum(s);
-  // rescale staged p~ to its split's reference (16-byte chunks)
-  constexpr int EPC = 16 / sizeof(PT);
-  PT* pr = P + (int64_t)row * ldp;
-  const int ncv = (vc_valid + EPC - 1) / EPC;
-  for (int c = l; c < ncv; c += 64) {
-    const int b = (c * EPC) / blkw;
-    const int sp = b / bps;
-    float rs = ref[0];
-#pragma unroll
-    for (int k = 1; k < kMaxSplit; ++k)
-      if (k == sp) rs = ref[k];
-    const float m = bm[b];
-    if (m == rs) continue;
-    const float f = __expf(m - rs);
-    u32x4* q = reinterpret_cast<u32x4*>(pr) + c;
-    if constexpr (sizeof(PT) == 2) {
-      u32x4 v = *q;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = pack_bf16x2(bf16_lo(v[e]) * f, bf16_hi(v[e]) * f);
-      *q = v;
-    } else {
-      f32x4 v = __builtin_bit_cast(f32x4, *q) * f;
-      *q = __builtin_bit_cast(u32x4, v);
-    }
-  }
   if (l < nsplit) {
-    float fo = 0.f;
+    float fo = 0.f, rf = 0.f;
 #pragma unroll
     for (int sp = 0; sp < kMaxSplit; ++sp)
-      if (sp == l) fo = __expf(ref[sp] - Mnew);  // 0 for a split without blocks
+      if (sp == l) {
+        fo = __expf(ref[sp] - Mnew);  // 0 for a split without blocks
+        rf = ref[sp];
+      }
     fout[(int64_t)row * nsplit + l] = fo;
+    refs[(int64_t)row * nsplit + l] = rf;
   }
   if (l == 0) {
     const float a = first ? 0.f : __expf(Mold - Mnew);
@@ -302,6 +281,52 @@ __global__ __launch_bounds__(256) void chunk_stats_kernel(
     runM[row] = Mnew;
     alpha[row] = a;
     if (first || mc > Mold) runA[row] = ai;
+  }
+}
+
+// Staged p~ of block b (split s = b / bps) times exp(m_b - ref_s) <= 1, in
+// place. Streams the chunk once: 16-byte runs, four per thread, all loads
+// before stores, non-temporal; grid (run groups, tokens).
+constexpr int kRescaleU = 4;
+
+template <typename PT>
+__global__ __launch_bounds__(256) void rescale_p_kernel(int vc_valid, int nb, int bps, int nsplit,
+                                                        int blkw, const float* __restrict__ blk_m,
+                                                        const float* __restrict__ refs,
+                                                        PT* __restrict__ P, int64_t ldp) {
+  constexpr int EPC = 16 / sizeof(PT);
+  const int64_t row = blockIdx.y;
+  const int ncv = (vc_valid + EPC - 1) / EPC;
+  u32x4* pr = reinterpret_cast<u32x4*>(P + row * ldp);
+  const float* bm = blk_m + row * nb;
+  const float* rf = refs + row * nsplit;
+  const int c0 = blockIdx.x * 256 * kRescaleU + threadIdx.x;
+  u32x4 v[kRescaleU];
+  float fct[kRescaleU];
+#pragma unroll
+  for (int u = 0; u < kRescaleU; ++u) {
+    const int c = c0 + u * 256;
+    fct[u] = 1.f;
+    if (c < ncv) {
+      v[u] = __builtin_nontemporal_load(pr + c);
+      const int b = (c * EPC) / blkw;
+      const float m = bm[b], r = rf[b / bps];
+      fct[u] = m == r ? 1.f : __expf(m - r);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < kRescaleU; ++u) {
+    const int c = c0 + u * 256;
+    if (c >= ncv || fct[u] == 1.f) continue;
+    const float f = fct[u];
+    u32x4 w = v[u];
+    if constexpr (sizeof(PT) == 2) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(bf16_lo(w[e]) * f, bf16_hi(w[e]) * f);
+    } else {
+      w = __builtin_bit_cast(u32x4, __builtin_bit_cast(f32x4, w) * f);
+    }
+    __builtin_nontemporal_store(w, pr + c);
   }
 }
 
@@ -515,8 +540,16 @@ static hipError_t run_output_error(const OeLaunch& a) {
     FPO_LAUNCH("chunk_stats", st,
                chunk_stats_kernel<T><<<dim3((unsigned)((a.T + 3) / 4)), dim3(256), 0, st>>>(
         (int)a.T, nbv, bps, a.nsplit, c == 0, TT::WTN, vc_valid, a.blk_m, a.blk_s, a.blk_i,
-        a.runM, a.runS, a.runA, a.fout, a.alpha, P, a.Vc));
+        a.runM, a.runS, a.runA, a.fout, a.alpha, a.refs));
     FPO_CHECK_LAUNCH();
+    {
+      constexpr int EPC = 16 / sizeof(T);
+      const int ncv = (vc_valid + EPC - 1) / EPC;
+      FPO_LAUNCH("rescale_p", st,
+                 rescale_p_kernel<T><<<dim3((unsigned)((ncv + 256 * kRescaleU - 1) / (256 * kRescaleU)), (unsigned)a.T),
+                                       dim3(256), 0, st>>>(vc_valid, nbv, bps, a.nsplit, TT::WTN, a.blk_m, a.refs, P, a.Vc));
+      FPO_CHECK_LAUNCH();
+    }
     FPO_LAUNCH("proj_chunk", st,
                proj_chunk_kernel<E><<<dim3(gm * (unsigned)((a.d + TT::BN - 1) / TT::BN) * a.nsplit), dim3(256), 0, st>>>(
         P, a.Vc, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, nbv, bps, TT::WTN, c == 0, a.nsplit,

@@ -36,6 +36,7 @@ struct OeLaunch {
   int32_t* blk_i;
   float* fout;
   float* alpha;
+  float* refs;  // [T, nsplit] split references of the current chunk
   float* runM;
   float* runS;
   int32_t* runA;
