@@ -396,7 +396,14 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
     U.part = upart;
     U.stream = stream;
   }
-  hipError_t e = fpo::launch_pseudograd(P);
+  hipError_t e;
+  if (opt && P.bf16 && !full) {
+    // W3 only, bf16: layer l's update overlaps layer l+1's outer products
+    e = fpo::launch_pseudograd_update(P, U);
+    if (e != hipSuccess) return hip_fail(e, "fpo_pseudograd overlapped launch");
+    return FPO_OK;
+  }
+  e = fpo::launch_pseudograd(P);
   if (e != hipSuccess) return hip_fail(e, "fpo_pseudograd launch");
   if (opt) {
     e = fpo::launch_update(U);

@@ -13,6 +13,8 @@
 #include "launch.hpp"
 #include "prof.hpp"
 
+#include <mutex>
+
 namespace fpo {
 
 template <typename T>
@@ -382,6 +384,79 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
     }
   }
   return hipSuccess;
+}
+
+// Side stream and events of one device for the overlapped pseudogradient +
+// update (created on first use, kept until the process ends; one call's
+// enqueue sequence holds the device's lock).
+struct PgOverlap {
+  std::mutex mu;
+  bool ready = false;
+  hipStream_t side = nullptr;
+  hipEvent_t ready_l = nullptr, done = nullptr;
+};
+constexpr int kMaxDevices = 64;
+static PgOverlap g_pgo[kMaxDevices];
+
+static hipError_t pg_overlap_init(PgOverlap& p) {
+  if (p.ready) return hipSuccess;
+  hipError_t e;
+  // default priority: both streams at the same priority
+  if ((e = hipStreamCreateWithFlags(&p.side, hipStreamNonBlocking)) != hipSuccess) return e;
+  if ((e = hipEventCreateWithFlags(&p.ready_l, hipEventDisableTiming)) != hipSuccess) return e;
+  if ((e = hipEventCreateWithFlags(&p.done, hipEventDisableTiming)) != hipSuccess) return e;
+  p.ready = true;
+  return hipSuccess;
+}
+
+// W3-only bf16 pseudogradient with the optimizer step overlapped: the outer
+// products run one layer per launch on the caller's stream; once layer l's
+// tiles and norm are done, its update (the standalone update kernel, which
+// needs few registers and no LDS, so its workgroups sit beside the GEMM's on
+// the same CUs) streams on a side stream while layer l+1's MFMAs run. Same
+// kernels and reduction order as the separate calls, so results are
+// bit-identical to them.
+hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u) {
+  hipStream_t st = (hipStream_t)a.stream;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  PgOverlap& po = g_pgo[dev];
+  std::lock_guard<std::mutex> lock(po.mu);
+  if ((e = pg_overlap_init(po)) != hipSuccess) return e;
+  FPO_LAUNCH("transpose_pad", st,
+             transpose_pad_kernel<uint16_t><<<dim3((unsigned)(a.Tp / 64), (unsigned)((a.d + 63) / 64)), dim3(256), 0, st>>>(
+      (const uint16_t*)a.g_lp, a.T, a.d, (uint16_t*)a.gT, a.Tp, a.Tp));
+  FPO_CHECK_LAUNCH();
+  const int ntiles = (int)pseudograd_tiles(true, a.d, a.d_ff);
+  int64_t blk_base = 0;
+  for (int l = 0; l < a.L; ++l) {
+    OuterArgs oa{};
+    oa.A[0] = a.gT;
+    oa.B[0] = a.a[l];
+    oa.C[0] = a.dW3[l];
+    oa.R[0] = a.ref[l];
+    double* tpart = a.part + (int64_t)l * ntiles * 3;
+    FPO_LAUNCH("outer", st,
+               outer_kernel<TileBF16><<<dim3(ntiles), dim3(256), 0, st>>>(oa, (int)a.d, (int)a.d_ff, (int)a.T,
+                                                                 a.Tp, a.d_ff, a.scale, tpart));
+    FPO_CHECK_LAUNCH();
+    FPO_LAUNCH("reduce_parts", st,
+               reduce_parts_kernel<<<dim3(1), dim3(256), 0, st>>>(
+        tpart, ntiles, l, a.sumsq, a.ref_dot ? a.ref_dot + l : nullptr,
+        a.ref_sumsq ? a.ref_sumsq + l : nullptr));
+    FPO_CHECK_LAUNCH();
+    // layer l's dW and ||dW||^2 are complete: update it on the side stream
+    if ((e = hipEventRecord(po.ready_l, st)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(po.side, po.ready_l, 0)) != hipSuccess) return e;
+    if ((e = launch_update_blocks(u, l, blk_base, po.side)) != hipSuccess) return e;
+    blk_base += update_blocks(u.numel[l]);
+  }
+  if ((e = hipEventRecord(po.done, po.side)) != hipSuccess) return e;
+  if ((e = hipStreamWaitEvent(st, po.done, 0)) != hipSuccess) return e;
+  // ||W'||^2 and the clip factors of every matrix
+  return launch_update(u, false);
 }
 
 hipError_t launch_pseudograd(const PgLaunch& a) {

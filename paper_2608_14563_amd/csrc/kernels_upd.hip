@@ -6,11 +6,11 @@
 #include "common.hpp"
 #include "launch.hpp"
 #include "prof.hpp"
+#include "upd.hpp"
 
 namespace fpo {
 
 constexpr int kUpdBatch = 32;        // matrices per launch (kernel-argument budget)
-constexpr int kElemsPerBlock = 4096;  // 256 threads x 4 x float4
 
 int64_t update_blocks(int64_t numel) { return (numel + kElemsPerBlock - 1) / kElemsPerBlock; }
 int64_t cosine_blocks(int64_t numel) { return (numel + kElemsPerBlock - 1) / kElemsPerBlock; }
@@ -25,25 +25,10 @@ struct UpdArgs {
   int64_t blk0[kUpdBatch + 1];
 };
 
-// Device copies of the hyperparameters: each derived factor is formed in double
-// on the host and rounded once to float.
-struct OptScalars {
-  int kind, first, lp_bf16;
-  float lr, momentum, beta1, one_m_beta1, beta2, one_m_beta2, adam_eps, decay;
-  float inv_bc1, inv_sqrt_bc2;  // 1/(1-beta1^t), 1/sqrt(1-beta2^t)
-  double clip_frac;
-};
-
 __device__ __forceinline__ int find_mat(const int64_t* blk0, int n, int64_t b) {
   int m = 0;
   while (m + 1 < n && blk0[m + 1] <= b) ++m;
   return m;
-}
-
-__device__ __forceinline__ float clip_factor(double gs, double ws, double frac) {
-  if (frac <= 0.0 || gs == 0.0) return 1.0f;
-  const double s = frac * sqrt(ws) / sqrt(gs);
-  return (float)(s < 1.0 ? s : 1.0);
 }
 
 __global__ __launch_bounds__(256) void update_kernel(UpdArgs a, int n, OptScalars o,
@@ -54,79 +39,8 @@ __global__ __launch_bounds__(256) void update_kernel(UpdArgs a, int n, OptScalar
   const int64_t b = blockIdx.x;
   const int m = find_mat(a.blk0, n, b);
   const float s = clip_factor(grad_sumsq[m], W_sumsq[m], o.clip_frac);
-  const int64_t base = (b - a.blk0[m]) * kElemsPerBlock;
-  const int64_t end = (a.numel[m] < base + kElemsPerBlock) ? a.numel[m] : base + kElemsPerBlock;
-  const float* g = a.grad[m];
-  float* W = a.W[m];
-  float* s1 = a.s1[m];
-  float* s2 = a.s2[m];
-  void* lp = a.W_lp[m];
-  // Every operand is streamed once: all of a thread's loads are issued before
-  // any store (they overlap instead of serialising per step), and loads and
-  // stores are non-temporal so the stream does not evict cached data.
-  constexpr int U = kElemsPerBlock / 1024;
-  const bool sgd = o.kind == 0;
-  f32x4 gv[U], w[U], v1[U], v2[U];
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int64_t i = base + threadIdx.x * 4 + u * 1024;
-    gv[u] = w[u] = v1[u] = v2[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (i < end) {
-      gv[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g + i));
-      w[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(W + i));
-      if (!(sgd && o.first)) v1[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s1 + i));
-      if (!sgd) v2[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s2 + i));
-    }
-  }
-  float ss = 0.f;
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int64_t i = base + threadIdx.x * 4 + u * 1024;
-    if (i >= end) continue;
-    const f32x4 gs = gv[u] * s;
-    f32x4 wv = w[u];
-    if (sgd) {  // SGD with momentum
-      f32x4 bv;
-      if (o.first) {
-        bv = gs;
-      } else {
-        bv.x = fmaf(o.momentum, v1[u].x, gs.x);
-        bv.y = fmaf(o.momentum, v1[u].y, gs.y);
-        bv.z = fmaf(o.momentum, v1[u].z, gs.z);
-        bv.w = fmaf(o.momentum, v1[u].w, gs.w);
-      }
-      __builtin_nontemporal_store(bv, reinterpret_cast<f32x4*>(s1 + i));
-      wv.x = fmaf(-o.lr, bv.x, wv.x);
-      wv.y = fmaf(-o.lr, bv.y, wv.y);
-      wv.z = fmaf(-o.lr, bv.z, wv.z);
-      wv.w = fmaf(-o.lr, bv.w, wv.w);
-    } else {  // AdamW, decoupled weight decay, bias corrected
-      f32x4 mv = v1[u], vv = v2[u];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float ge = gs[e];
-        const float me = o.beta1 * mv[e] + o.one_m_beta1 * ge;
-        const float ve = o.beta2 * vv[e] + o.one_m_beta2 * ge * ge;
-        mv[e] = me;
-        vv[e] = ve;
-        const float denom = sqrtf(ve) * o.inv_sqrt_bc2 + o.adam_eps;
-        wv[e] = wv[e] * o.decay - o.lr * (me * o.inv_bc1) / denom;
-      }
-      __builtin_nontemporal_store(mv, reinterpret_cast<f32x4*>(s1 + i));
-      __builtin_nontemporal_store(vv, reinterpret_cast<f32x4*>(s2 + i));
-    }
-    __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>(W + i));
-    if (lp) {
-      if (o.lp_bf16)
-        __builtin_nontemporal_store(u32x2{pack_bf16x2(wv.x, wv.y), pack_bf16x2(wv.z, wv.w)},
-                                    reinterpret_cast<u32x2*>((uint16_t*)lp + i));
-      else
-        __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>((float*)lp + i));
-    }
-    ss += wv.x * wv.x + wv.y * wv.y + wv.z * wv.z + wv.w * wv.w;
-  }
-  const double t = block_sum_d((double)ss, red);
-  if (threadIdx.x == 0) part[b] = t;
+  update_block(a.grad[m], a.W[m], a.W_lp[m], a.s1[m], a.s2[m], a.numel[m], b - a.blk0[m], s, o, red,
+               part + b);
 }
 
 __global__ __launch_bounds__(256) void update_reduce_kernel(UpdArgs a, OptScalars o,
@@ -152,25 +66,30 @@ __global__ __launch_bounds__(256) void update_reduce_kernel(UpdArgs a, OptScalar
     if (e_ != hipSuccess) return e_;   \
   } while (0)
 
-hipError_t launch_update(const UpdLaunch& a) {
+// The update blocks of matrix m alone (no reduction), on stream st; its
+// partials start at part + blk_base, as in launch_update.
+hipError_t launch_update_blocks(const UpdLaunch& a, int m, int64_t blk_base, void* stream) {
+  hipStream_t st = (hipStream_t)stream;
+  const OptScalars o = make_opt_scalars(a);
+  UpdArgs ua{};
+  ua.grad[0] = a.grad[m];
+  ua.W[0] = a.W[m];
+  ua.W_lp[0] = a.W_lp[m];
+  ua.s1[0] = a.s1[m];
+  ua.s2[0] = a.s2[m];
+  ua.numel[0] = a.numel[m];
+  ua.blk0[0] = 0;
+  ua.blk0[1] = update_blocks(a.numel[m]);
+  FPO_LAUNCH("update", st,
+             update_kernel<<<dim3((unsigned)ua.blk0[1]), dim3(256), 0, st>>>(ua, 1, o, a.grad_sumsq + m,
+                                                                a.W_sumsq + m, a.part + blk_base));
+  FPO_CHECK_LAUNCH();
+  return hipSuccess;
+}
+
+hipError_t launch_update(const UpdLaunch& a, bool blocks) {
   hipStream_t st = (hipStream_t)a.stream;
-  OptScalars o{};
-  o.kind = a.kind;
-  o.first = a.step <= 1;
-  o.lp_bf16 = a.lp_bf16;
-  o.lr = (float)a.lr;
-  o.momentum = (float)a.momentum;
-  o.beta1 = (float)a.beta1;
-  o.one_m_beta1 = (float)(1.0 - a.beta1);
-  o.beta2 = (float)a.beta2;
-  o.one_m_beta2 = (float)(1.0 - a.beta2);
-  o.adam_eps = (float)a.adam_eps;
-  o.decay = (float)(1.0 - a.lr * a.weight_decay);
-  o.clip_frac = a.clip_frac;
-  const double bc1 = 1.0 - pow(a.beta1, (double)a.step);
-  const double bc2 = 1.0 - pow(a.beta2, (double)a.step);
-  o.inv_bc1 = (float)(1.0 / bc1);
-  o.inv_sqrt_bc2 = (float)(1.0 / sqrt(bc2));
+  const OptScalars o = make_opt_scalars(a);
   int64_t part_off = 0;
   for (int m0 = 0; m0 < a.n; m0 += kUpdBatch) {
     const int n = std::min(kUpdBatch, a.n - m0);
@@ -188,10 +107,12 @@ hipError_t launch_update(const UpdLaunch& a) {
       nb += update_blocks(a.numel[m]);
     }
     ua.blk0[n] = nb;
-    FPO_LAUNCH("update", st,
-               update_kernel<<<dim3((unsigned)nb), dim3(256), 0, st>>>(ua, n, o, a.grad_sumsq + m0,
-                                                          a.W_sumsq + m0, a.part + part_off));
-    FPO_CHECK_LAUNCH();
+    if (blocks) {
+      FPO_LAUNCH("update", st,
+                 update_kernel<<<dim3((unsigned)nb), dim3(256), 0, st>>>(ua, n, o, a.grad_sumsq + m0,
+                                                            a.W_sumsq + m0, a.part + part_off));
+      FPO_CHECK_LAUNCH();
+    }
     FPO_LAUNCH("update_reduce", st,
                update_reduce_kernel<<<dim3(n), dim3(256), 0, st>>>(ua, o, a.part + part_off,
                                                         a.grad_sumsq + m0, a.W_sumsq + m0,

@@ -92,7 +92,14 @@ struct UpdLaunch {
   double* part;
   void* stream;
 };
-hipError_t launch_update(const UpdLaunch& a);
+// blocks = false: only the per-matrix reductions (||W'||^2, clip factors) of
+// blocks already applied (by the fused pseudogradient launch).
+hipError_t launch_update(const UpdLaunch& a, bool blocks = true);
+// The update blocks of matrix m of `a` on `stream` (partials at part + blk_base).
+hipError_t launch_update_blocks(const UpdLaunch& a, int m, int64_t blk_base, void* stream);
+// W3-only bf16 pseudogradients with the optimizer step overlapped (u: the
+// update of the same matrices, grad = the dW3 outputs, grad_sumsq = a.sumsq).
+hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u);
 int64_t update_blocks(int64_t numel);
 
 struct CosLaunch {

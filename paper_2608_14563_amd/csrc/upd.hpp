@@ -1,0 +1,133 @@
+// Relative clip + optimizer step on fp32 masters (App. A; Sec. 3.1
+// optimizers): the per-block device routine shared by the standalone update
+// kernel and the fused outer-product + update kernel, and the host-side
+// derivation of its scalars.
+#pragma once
+
+#include "common.hpp"
+#include "launch.hpp"
+
+#include <math.h>
+
+namespace fpo {
+
+constexpr int kElemsPerBlock = 4096;  // 256 threads x 4 x float4
+
+// Device copies of the hyperparameters: each derived factor is formed in double
+// on the host and rounded once to float.
+struct OptScalars {
+  int kind, first, lp_bf16;
+  float lr, momentum, beta1, one_m_beta1, beta2, one_m_beta2, adam_eps, decay;
+  float inv_bc1, inv_sqrt_bc2;  // 1/(1-beta1^t), 1/sqrt(1-beta2^t)
+  double clip_frac;
+};
+
+// Scalars of one optimizer step, each derived factor formed in double and
+// rounded once to float.
+inline OptScalars make_opt_scalars(const UpdLaunch& a) {
+  OptScalars o{};
+  o.kind = a.kind;
+  o.first = a.step <= 1;
+  o.lp_bf16 = a.lp_bf16;
+  o.lr = (float)a.lr;
+  o.momentum = (float)a.momentum;
+  o.beta1 = (float)a.beta1;
+  o.one_m_beta1 = (float)(1.0 - a.beta1);
+  o.beta2 = (float)a.beta2;
+  o.one_m_beta2 = (float)(1.0 - a.beta2);
+  o.adam_eps = (float)a.adam_eps;
+  o.decay = (float)(1.0 - a.lr * a.weight_decay);
+  o.clip_frac = a.clip_frac;
+  const double bc1 = 1.0 - pow(a.beta1, (double)a.step);
+  const double bc2 = 1.0 - pow(a.beta2, (double)a.step);
+  o.inv_bc1 = (float)(1.0 / bc1);
+  o.inv_sqrt_bc2 = (float)(1.0 / sqrt(bc2));
+  return o;
+}
+
+__device__ __forceinline__ float clip_factor(double gs, double ws, double frac) {
+  if (frac <= 0.0 || gs == 0.0) return 1.0f;
+  const double s = frac * sqrt(ws) / sqrt(gs);
+  return (float)(s < 1.0 ? s : 1.0);
+}
+
+// Update of block b (kElemsPerBlock elements from b * kElemsPerBlock) of one
+// matrix with clip factor s; writes the block's ||W'||^2 to *part_b. Every
+// thread of the 256-thread workgroup must call it (it reduces through `red`,
+// 16 doubles of LDS).
+__device__ __forceinline__ void update_block(const float* __restrict__ g, float* __restrict__ W,
+                                             void* lp, float* __restrict__ s1,
+                                             float* __restrict__ s2, int64_t numel, int64_t b,
+                                             float s, const OptScalars& o, double* red,
+                                             double* part_b) {
+  const int64_t base = b * kElemsPerBlock;
+  const int64_t end = (numel < base + kElemsPerBlock) ? numel : base + kElemsPerBlock;
+  // Every operand is streamed once: all of a thread's loads are issued before
+  // any store (they overlap instead of serialising per step), and loads and
+  // stores are non-temporal so the stream does not evict cached data.
+  constexpr int U = kElemsPerBlock / 1024;
+  const bool sgd = o.kind == 0;
+  f32x4 gv[U], w[U], v1[U], v2[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t i = base + threadIdx.x * 4 + u * 1024;
+    gv[u] = w[u] = v1[u] = v2[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (i < end) {
+      gv[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g + i));
+      w[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(W + i));
+      if (!(sgd && o.first)) v1[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s1 + i));
+      if (!sgd) v2[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s2 + i));
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t i = base + threadIdx.x * 4 + u * 1024;
+    if (i >= end) continue;
+    const f32x4 gs = gv[u] * s;
+    f32x4 wv = w[u];
+    if (sgd) {  // SGD with momentum
+      f32x4 bv;
+      if (o.first) {
+        bv = gs;
+      } else {
+        bv.x = fmaf(o.momentum, v1[u].x, gs.x);
+        bv.y = fmaf(o.momentum, v1[u].y, gs.y);
+        bv.z = fmaf(o.momentum, v1[u].z, gs.z);
+        bv.w = fmaf(o.momentum, v1[u].w, gs.w);
+      }
+      __builtin_nontemporal_store(bv, reinterpret_cast<f32x4*>(s1 + i));
+      wv.x = fmaf(-o.lr, bv.x, wv.x);
+      wv.y = fmaf(-o.lr, bv.y, wv.y);
+      wv.z = fmaf(-o.lr, bv.z, wv.z);
+      wv.w = fmaf(-o.lr, bv.w, wv.w);
+    } else {  // AdamW, decoupled weight decay, bias corrected
+      f32x4 mv = v1[u], vv = v2[u];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float ge = gs[e];
+        const float me = o.beta1 * mv[e] + o.one_m_beta1 * ge;
+        const float ve = o.beta2 * vv[e] + o.one_m_beta2 * ge * ge;
+        mv[e] = me;
+        vv[e] = ve;
+        const float denom = sqrtf(ve) * o.inv_sqrt_bc2 + o.adam_eps;
+        wv[e] = wv[e] * o.decay - o.lr * (me * o.inv_bc1) / denom;
+      }
+      __builtin_nontemporal_store(mv, reinterpret_cast<f32x4*>(s1 + i));
+      __builtin_nontemporal_store(vv, reinterpret_cast<f32x4*>(s2 + i));
+    }
+    __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>(W + i));
+    if (lp) {
+      if (o.lp_bf16)
+        __builtin_nontemporal_store(u32x2{pack_bf16x2(wv.x, wv.y), pack_bf16x2(wv.z, wv.w)},
+                                    reinterpret_cast<u32x2*>((uint16_t*)lp + i));
+      else
+        __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>((float*)lp + i));
+    }
+    ss += wv.x * wv.x + wv.y * wv.y + wv.z * wv.z + wv.w * wv.w;
+  }
+  const double t = block_sum_d((double)ss, red);
+  if (threadIdx.x == 0) *part_b = t;
+}
+
+}  // namespace fpo

@@ -5,6 +5,7 @@ import pytest
 import torch
 
 import oracle as O
+from paper_2608_14563_amd import _lib as L_
 from paper_2608_14563_amd import api
 from paper_2608_14563_amd import inputs as I
 from tests._util import assert_close, bf16_rne_bits, dev_tensor, ulp_diff_f32
@@ -126,30 +127,44 @@ def test_cosine(dev, bdtype):
     assert_close("sa", float(sa[0]), O.cosine(A[0], A[0])[1], "f32")
 
 
-def test_fused_update_matches_separate_calls(dev):
-    c = I.CONFIGS[1].shrink(T=256, d=256, d_ff=512, L=2)
+@pytest.mark.parametrize("kind", ["sgd", "adamw"])
+@pytest.mark.parametrize("T,d,d_ff,L,clip", [(256, 256, 512, 2, 0.01), (300, 264, 1000, 3, 0.01),
+                                             (200, 512, 768, 3, 1e-5)])
+def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip):
+    """The W3 pseudogradient with the optimizer fused (bf16: one launch per
+    layer carrying that layer's outer products and the previous layer's update)
+    is bit-identical to the pseudogradient followed by fpo_apply_update, over two
+    steps (momentum / moments carried), including a ragged shape and an active
+    clip (clip_frac 1e-5)."""
+    c = I.CONFIGS[1].shrink(T=T, d=d, d_ff=d_ff, L=L)
     g = dev_tensor(I.synthetic_signal(c), dev)
-    acts = [dev_tensor(I.activation(c, l), dev) for l in range(2)]
-    W0 = [torch.from_numpy(I.master_weight(c, l)).to(dev) for l in range(2)]
+    acts = [dev_tensor(I.activation(c, l), dev) for l in range(L)]
+    W0 = [torch.from_numpy(I.master_weight(c, l)).to(dev) for l in range(L)]
+    adam = kind == "adamw"
 
     def fresh():
         W = [w.clone() for w in W0]
-        return W, [torch.zeros_like(w) for w in W], [torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in W], \
-            torch.tensor([float((w.double() ** 2).sum()) for w in W], dtype=torch.float64, device=dev)
+        return dict(W=W, s1=[torch.zeros_like(w) for w in W],
+                    s2=[torch.zeros_like(w) for w in W] if adam else None,
+                    lp=[torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in W],
+                    Wsq=torch.tensor([float((w.double() ** 2).sum()) for w in W], dtype=torch.float64, device=dev),
+                    dW=[torch.empty(d, d_ff, dtype=torch.float32, device=dev) for _ in range(L)],
+                    ss=torch.empty(L, dtype=torch.float64, device=dev),
+                    cs=torch.empty(L, dtype=torch.float32, device=dev))
 
-    opt = api.OptConfig(lr=1e-2, clip_frac=0.01, step=1)
-    # separate
-    W, s1, lp, Wsq = fresh()
-    dW = [torch.empty(256, 512, dtype=torch.float32, device=dev) for _ in range(2)]
-    ss = torch.empty(2, dtype=torch.float64, device=dev)
-    api.fpo_pseudograd(g, acts, dW3=dW, sumsq=ss)
-    api.fpo_apply_update(opt, dW, ss, W, s1, Wsq, W_lp=lp)
-    # fused
-    Wf, s1f, lpf, Wsqf = fresh()
-    dWf = [torch.empty(256, 512, dtype=torch.float32, device=dev) for _ in range(2)]
-    ssf = torch.empty(2, dtype=torch.float64, device=dev)
-    api.fpo_pseudograd(g, acts, dW3=dWf, sumsq=ssf, opt=opt, W_master=Wf, W_lp=lpf, state1=s1f, W_sumsq=Wsqf)
-    torch.cuda.synchronize()
-    for a, b in zip(W + s1 + dW, Wf + s1f + dWf):
-        assert torch.equal(a, b)
-    assert torch.equal(Wsq, Wsqf)
+    sep, fus = fresh(), fresh()
+    for step in (1, 2):
+        opt = api.OptConfig(kind=L_.FPO_OPT_ADAMW if adam else L_.FPO_OPT_SGD, lr=1e-2, clip_frac=clip, step=step)
+        api.fpo_pseudograd(g, acts, dW3=sep["dW"], sumsq=sep["ss"])
+        api.fpo_apply_update(opt, sep["dW"], sep["ss"], sep["W"], sep["s1"], sep["Wsq"], W_lp=sep["lp"],
+                             state2=sep["s2"], clip_scale=sep["cs"])
+        api.fpo_pseudograd(g, acts, dW3=fus["dW"], sumsq=fus["ss"], opt=opt, W_master=fus["W"], W_lp=fus["lp"],
+                           state1=fus["s1"], state2=fus["s2"], W_sumsq=fus["Wsq"], clip_scale=fus["cs"])
+        torch.cuda.synchronize()
+        for key in ("W", "s1", "lp", "dW") + (("s2",) if adam else ()):
+            for a, b in zip(sep[key], fus[key]):
+                assert torch.equal(a, b), (key, step)
+        for key in ("Wsq", "ss", "cs"):
+            assert torch.equal(sep[key], fus[key]), (key, step)
+    if clip < 1e-4:
+        assert float(fus["cs"].max()) < 1.0  # the clip was active
