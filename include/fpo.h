@@ -194,6 +194,13 @@ int fpo_output_error(const fpo_oe_desc* desc, const void* h_final, const void* g
  *   opt, upd   both NULL, or both given: the call then also applies
  *              fpo_apply_update to the matrices in `sumsq` order, with the
  *              same result bit for bit as calling it separately
+ *   stream     the work is ordered on this stream. With opt given on the
+ *              FPO_BF16 / FPO_MODE_W3 path, each layer's update runs on a
+ *              second, library-owned stream of the current device (default
+ *              priority), overlapping the next layer's outer products, and is
+ *              joined back to `stream` with an event before the call's last
+ *              kernel; calls on one device from several host threads are
+ *              serialized while they enqueue.
  * Returns FPO_OK or an fpo_status. */
 size_t fpo_pseudograd_workspace(const fpo_pg_desc* desc);
 int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* const* a,
