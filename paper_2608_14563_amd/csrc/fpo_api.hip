@@ -48,6 +48,10 @@ struct Carver {
   }
 };
 
+// A rows x cols band of 2-byte elements addressable through 32-bit buffer
+// offsets with 2^31 reserved as the out-of-range offset.
+bool band_fits(int64_t rows, int64_t cols) { return rows * cols <= ((int64_t)1 << 30); }
+
 // ------------------------------------------------------------------ plans
 struct OePlan {
   int64_t Vc = 0, nb = 0;
@@ -69,6 +73,8 @@ OePlan plan_oe(const fpo_oe_desc& d) {
   int64_t vmax = d.vocab_chunk > 0 ? round_up(d.vocab_chunk, 256)
                                    : std::max<int64_t>(256, ((int64_t)1 << 30) / d.T / 256 * 256);
   vmax = std::min(vmax, round_up(d.V, 256));
+  // a chunk of W_U and the staged p~ are copied through 32-bit offsets
+  if (bf16) vmax = std::min(vmax, std::max<int64_t>(256, (((int64_t)1 << 30) / std::max(d.d, d.T)) / 256 * 256));
   OePlan p;
   p.Vc = round_up(ceil_div(d.V, ceil_div(d.V, vmax)), 256);
   p.nb = p.Vc / WTN;
@@ -128,6 +134,13 @@ int check_oe_desc(const fpo_oe_desc* d) {
   if (!(d->min_rms >= 0.f) || !std::isfinite(d->min_rms))
     return fail(FPO_ERR_ARG, "fpo_output_error: min_rms must be finite and >= 0");
   if (d->vocab_chunk < 0) return fail(FPO_ERR_ARG, "fpo_output_error: vocab_chunk must be >= 0");
+  // bf16 operands are copied through 32-bit buffer offsets: every operand band
+  // (y, a W_U chunk of at least 256 rows, the staged p~) must fit in 2^31 bytes
+  if (d->dtype == FPO_BF16 && (!band_fits(d->T, d->d) || !band_fits(256, d->d) || !band_fits(d->T, 256)))
+    return fail(FPO_ERR_UNSUPPORTED,
+                "fpo_output_error: bf16 operand bands must stay below 2^31 bytes (T*d, 256*d and 256*T "
+                "elements <= 2^30; T=%lld d=%lld)",
+                (long long)d->T, (long long)d->d);
   return FPO_OK;
 }
 
@@ -183,6 +196,17 @@ int check_pg_desc(const fpo_pg_desc* d) {
   if (d->d % 8 || d->d_ff % 8)
     return fail(FPO_ERR_SHAPE, "fpo_pseudograd: d and d_ff must be multiples of 8");
   if (!std::isfinite(d->scale)) return fail(FPO_ERR_ARG, "fpo_pseudograd: scale must be finite");
+  if (d->dtype == FPO_BF16) {
+    // operand bands copied through 32-bit buffer offsets must fit in 2^31 bytes
+    const int64_t Tp = round_up(d->T, 64);
+    bool ok = band_fits(d->d, Tp) && band_fits(d->T, d->d_ff);
+    if (d->mode == FPO_MODE_FULL_MLP)
+      ok = ok && band_fits(d->T, d->d) && band_fits(d->d, d->d_ff) && band_fits(d->d_ff, Tp);
+    if (!ok)
+      return fail(FPO_ERR_UNSUPPORTED,
+                  "fpo_pseudograd: bf16 operand bands must stay below 2^31 bytes (T=%lld d=%lld d_ff=%lld)",
+                  (long long)d->T, (long long)d->d, (long long)d->d_ff);
+  }
   return FPO_OK;
 }
 

@@ -39,7 +39,7 @@ ENTROPY = 260814563
 BLOCK = 1 << 20
 
 # tensor ids inside the spawn key
-T_X, T_GAMMA, T_WU, T_TARGETS, T_Q, T_U, T_W, T_OUTLIER, T_REFNOISE, T_XIN, T_W1, T_W2, T_G, T_STATE, T_MISC = range(15)
+T_X, T_GAMMA, T_WU, T_TARGETS, T_Q, T_U, T_W, T_OUTLIER, T_REFNOISE, T_XIN, T_W1, T_W2, T_G, T_STATE, T_MISC, T_REF1 = range(16)
 
 
 @dataclass(frozen=True)
@@ -221,6 +221,14 @@ def ref_noise(cfg: Config, layer: int) -> np.ndarray:
     """N(0,1) [d, d_ff] float32 for the diagnostic's reference gradient
     R = D + sigma * N, sigma = sqrt(3) * ||D||_F / sqrt(d * d_ff)."""
     return normal(cfg.cid, T_REFNOISE, layer, cfg.d * cfg.d_ff).reshape(cfg.d, cfg.d_ff)
+
+
+def rank1_reference(cfg: Config, layer: int = 0):
+    """u [d], v [d_ff] float32 N(0,1): factors of a rank-1 reference gradient
+    R = u v^T, whose inner product with any outer product has a closed form."""
+    u = normal(cfg.cid, T_REF1, 2 * layer, cfg.d)
+    v = normal(cfg.cid, T_REF1, 2 * layer + 1, cfg.d_ff)
+    return u, v
 
 
 def synthetic_signal(cfg: Config, std: float = 0.02, tensor: int = T_G) -> np.ndarray:

@@ -106,6 +106,22 @@ def test_output_error_validation(lib):
     assert call_oe(lib, oe(), ws_bytes=100) == L.FPO_ERR_WORKSPACE
     msg = lib.fpo_last_error().decode()
     assert "workspace" in msg and "needed" in msg
+    # bf16 operand bands are addressed through 32-bit buffer offsets
+    assert call_oe(lib, oe(T=1 << 19, d=4096)) == L.FPO_ERR_UNSUPPORTED
+    assert "2^31" in lib.fpo_last_error().decode()
+    assert lib.fpo_output_error_workspace(C.byref(oe(T=1 << 19, d=4096, dtype=L.FPO_F32))) > 0  # fp32 unaffected
+    assert lib.fpo_output_error_workspace(C.byref(oe(T=1 << 19, d=4096))) == 0
+
+
+def test_chunk_width_respects_operand_bands(lib):
+    """The planner keeps a W_U chunk (Vc x d) and the staged p~ (T x Vc)
+    within 2^30 elements: for d = 8192 the whole 128K vocabulary would not fit
+    one chunk, so the workspace (dominated by T x Vc p~) is bounded."""
+    T, d, V = 2048, 8192, 131072
+    ws = lib.fpo_output_error_workspace(C.byref(oe(T=T, d=d, V=V)))
+    vc_max = (1 << 30) // d
+    assert 0 < ws
+    assert ws <= T * vc_max * 2 + (T * d * 2) + 64 * T * d * 4 + (64 << 20)
 
 
 def arr(vals):
@@ -139,6 +155,8 @@ def test_pseudograd_validation(lib):
     assert call(good, ws_bytes=16) == L.FPO_ERR_WORKSPACE
     b, kb = arr([FAKE, None])
     assert call(good, A=b) == L.FPO_ERR_NULL
+    # bf16 operand bands (T x d_ff activations) above 2^31 bytes are refused
+    assert call(L.PgDesc(1 << 17, 256, 16384, 2, L.FPO_BF16, L.FPO_MODE_W3, 1.0)) == L.FPO_ERR_UNSUPPORTED
 
 
 def test_apply_update_validation(lib):
