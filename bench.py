@@ -42,7 +42,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--vocab-chunk", type=int, default=0,
                     help="vocabulary chunk width (0: the library's planner)")
-    ap.add_argument("--cpu-tokens", type=int, default=128, help="tokens in the oracle's timed sample")
+    ap.add_argument("--cpu-tokens", type=int, default=1024, help="tokens in the oracle's timed sample")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration)")
     return ap.parse_args()
@@ -123,7 +123,14 @@ def kernel_work(name, c, steps, nchunk):
         # SGD momentum, step > 1: dW r, buf r/w, W r/w (fp32) + bf16 copy w
         return 22.0 * L * d * dff * steps, "byte", "hbm"
     if name == "chunk_stats":
+        # per-(token, 128-entry block) max / sum / argmax read; per-token state written
+        return (12.0 * T * ((V + 127) // 128) + 32.0 * T) * steps, "byte", "hbm"
+    if name == "rescale_p":
         return 4.0 * T * V * steps, "byte", "hbm"  # staged p~ read + write (bf16)
+    if name == "rms_forward":
+        return (4.0 * T * d) * steps, "byte", "hbm"  # x read, y written (bf16)
+    if name == "transpose_pad":
+        return (4.0 * T * d) * steps, "byte", "hbm"  # g~ read, g~^T written (bf16)
     if name == "finalize_vjp":
         return (T * d * (4 + 2 + 2 + 4 + 2)) * steps, "byte", "hbm"
     return None
