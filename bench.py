@@ -27,6 +27,10 @@ METRIC = "FPO update tokens/sec at 8B shapes; % bf16 MFMA peak; HBM GB/s on VJP/
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+# optimizer HBM bytes per parameter at step > 1: dW read 4, master r/w 8, bf16 copy
+# write 2, plus state r/w (momentum 8; AdamW moments 16; plain SGD none)
+OPT_BYTES = {"sgd-momentum": 22.0, "sgd": 14.0, "adamw": 30.0}
+OPT_NAME = {"sgd-momentum": "SGD-momentum", "sgd": "plain SGD (no state)", "adamw": "AdamW"}
 
 
 def log(*a):
@@ -43,6 +47,9 @@ def parse():
     ap.add_argument("--vocab-chunk", type=int, default=0,
                     help="vocabulary chunk width (0: the library's planner)")
     ap.add_argument("--cpu-tokens", type=int, default=1024, help="tokens in the oracle's timed sample")
+    ap.add_argument("--optimizer", choices=sorted(OPT_BYTES), default="sgd-momentum",
+                    help="optimizer on the fp32 masters (HBM bytes per parameter: " +
+                         ", ".join(f"{k} {v}" for k, v in sorted(OPT_BYTES.items())) + ")")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration)")
     return ap.parse_args()
@@ -81,15 +88,21 @@ def prof_read(lib):
 
 
 def source_hash() -> str:
-    """Hash of the kernel sources; a profile's traffic figure applies only while
-    the sources it was measured on are unchanged."""
+    """Hash of the library sources with comments and blank lines removed; a
+    profile's traffic figure applies only while the code it was measured on
+    is unchanged (comment edits do not invalidate it)."""
     import hashlib
+    import re
     h = hashlib.sha256()
     d = os.path.join(ROOT, "paper_2608_14563_amd", "csrc")
     for f in sorted(os.listdir(d)):
         if f.endswith((".hip", ".hpp")):
+            txt = open(os.path.join(d, f), encoding="utf-8").read()
+            txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+            txt = re.sub(r"//[^\n]*", "", txt)
+            code = "\n".join(ln.rstrip() for ln in txt.splitlines() if ln.strip())
             h.update(f.encode())
-            h.update(open(os.path.join(d, f), "rb").read())
+            h.update(code.encode())
     return h.hexdigest()[:16]
 
 
@@ -111,7 +124,7 @@ def profiled_traffic(workload: str, kernel: str):
     return None
 
 
-def kernel_work(name, c, steps, nchunk):
+def kernel_work(name, c, steps, nchunk, opt="sgd-momentum"):
     """Algorithmic work of one kernel over `steps` steps: (amount, unit, bound).
     Flops count only the method's contractions; bytes count each operand once."""
     T, d, V, dff, L = c.T, c.d, c.V, c.d_ff, c.L
@@ -120,8 +133,7 @@ def kernel_work(name, c, steps, nchunk):
     if name == "outer":
         return 2.0 * T * d * dff * L * steps, "flop", "mfma"
     if name == "update":
-        # SGD momentum, step > 1: dW r, buf r/w, W r/w (fp32) + bf16 copy w
-        return 22.0 * L * d * dff * steps, "byte", "hbm"
+        return OPT_BYTES[opt] * L * d * dff * steps, "byte", "hbm"
     if name == "chunk_stats":
         # per-(token, 128-entry block) max / sum / argmax read; per-token state written
         return (12.0 * T * ((V + 127) // 128) + 32.0 * T) * steps, "byte", "hbm"
@@ -143,11 +155,22 @@ def cpu_baseline(c, tokens, x, gam, W_U, y, acts, W0):
     import numpy as np
 
     import oracle as O
+    blas = None
     try:
         from threadpoolctl import threadpool_info
-        thr = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        info = threadpool_info()
+        thr = max([i.get("num_threads", 1) for i in info] or [1])
+        blas = ", ".join(sorted({f"{i.get('internal_api')} ({i.get('num_threads')} threads)" for i in info}))
     except Exception:  # pragma: no cover
         thr = len(os.sched_getaffinity(0))
+    cpu_model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:  # pragma: no cover
+        pass
     ts = min(tokens, c.T)
     t0 = time.perf_counter()
     out = O.output_error(x[:ts], gam, W_U, y[:ts], eps=c.eps, min_rms=c.min_rms, vocab_chunk=8192)
@@ -167,7 +190,8 @@ def cpu_baseline(c, tokens, x, gam, W_U, y, acts, W0):
                        f"layer outer products ({t2 - t0:.1f} s) plus one layer's clipped SGD-momentum step "
                        f"({upd_one:.1f} s); full step estimated as per-token time x T + per-layer update x L "
                        f"= {est:.1f} s"),
-            "seconds": round(t3 - t0, 2)}
+            "seconds": round(t3 - t0, 2), "affinity_cpus": len(os.sched_getaffinity(0)),
+            "cpu_model": cpu_model, "blas": blas}
 
 
 def main():
@@ -209,7 +233,10 @@ def main():
     tx, tgam, tW, ty = t(x), t(gam), t(W_U), t(y)
     tacts = [t(a) for a in acts]
     Wm = [t(w) for w in Wm_host]
-    s1 = [torch.zeros_like(w) for w in Wm]
+    plain = args.optimizer == "sgd"
+    adam = args.optimizer == "adamw"
+    s1 = None if plain else [torch.zeros_like(w) for w in Wm]
+    s2 = [torch.zeros_like(w) for w in Wm] if adam else None
     Wlp = [w.to(torch.bfloat16) for w in Wm]
     Wsq = torch.tensor([float((w.astype(np.float64) ** 2).sum()) for w in Wm_host], dtype=torch.float64, device=dev)
     T, d = c.T, c.d
@@ -226,14 +253,17 @@ def main():
     torch.cuda.synchronize()
     step_no = [0]
 
-    def step():
+    def step(mid=None):
         step_no[0] += 1
         api.fpo_output_error(tx, tgam, tW, ty, g_t, g_tilde_lp=g_lp, lse=lse, loss=loss, argmax=amax,
                              bad_targets=bad, ws=ws_oe, eps=c.eps, min_rms=c.min_rms,
                              vocab_chunk=args.vocab_chunk)
+        if mid is not None:
+            mid.record()
         api.fpo_pseudograd(g_lp, tacts, dW3=dW, sumsq=ss,
-                           opt=api.OptConfig(lr=c.lr, clip_frac=c.clip_frac, step=step_no[0]),
-                           W_master=Wm, W_lp=Wlp, state1=s1, W_sumsq=Wsq, ws=ws_pg)
+                           opt=api.OptConfig(kind=1 if adam else 0, lr=c.lr, momentum=0.0 if plain else 0.9,
+                                             clip_frac=c.clip_frac, step=step_no[0]),
+                           W_master=Wm, W_lp=Wlp, state1=s1, state2=s2, W_sumsq=Wsq, ws=ws_pg)
 
     lib = prof_lib()
     for _ in range(args.warmup):
@@ -254,13 +284,20 @@ def main():
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
+    # per-step events: [start, output error done, pseudograd + update done]
+    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     e0.record()
-    for _ in range(args.steps):
-        step()
+    for k in range(args.steps):
+        marks[k][0].record()
+        step(marks[k][1])
+        marks[k][2].record()
     e1.record()
     torch.cuda.synchronize()
     lib.fpo_prof_disable()
     ms_total = e0.elapsed_time(e1)
+    per_step = sorted(m[0].elapsed_time(m[2]) for m in marks)
+    per_oe = sorted(m[0].elapsed_time(m[1]) for m in marks)
+    per_pg = sorted(m[1].elapsed_time(m[2]) for m in marks)
     dom_stats = prof_read(lib)[dom]
     lib.fpo_prof_reset()
     ms_step = ms_total / args.steps
@@ -268,7 +305,7 @@ def main():
     log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step, {tok_s:.0f} tokens/s; dominant kernel {dom}: "
         f"{dom_stats[0] / dom_stats[1]:.3f} ms avg over {dom_stats[1]} launches")
     nchunk = None
-    w = kernel_work(dom, c, args.steps, nchunk)
+    w = kernel_work(dom, c, args.steps, nchunk, args.optimizer)
     roof = None
     traffic = profiled_traffic(c.name, dom)
     if w is not None:
@@ -286,7 +323,7 @@ def main():
                     "avg_launch_ms": round(dom_stats[0] / dom_stats[1], 4), "launches": dom_stats[1]}
     kernels = {}
     for k, (ms, n) in per_kernel.items():
-        wk = kernel_work(k, c, 1, nchunk)
+        wk = kernel_work(k, c, 1, nchunk, args.optimizer)
         e = {"ms_per_step": round(ms, 4), "launches": n}
         if wk is not None:
             amount, unit, bound = wk
@@ -297,15 +334,34 @@ def main():
                 e["gbs"] = round(amount / (ms / 1e3) / 1e9, 1)
                 e["hbm_frac"] = round(amount / (ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)
         kernels[k] = e
-    flops_step = 4.0 * c.T * c.V * c.d + 2.0 * c.T * c.d * c.d_ff * c.L
+    flops_oe = 4.0 * c.T * c.V * c.d
+    flops_pg = 2.0 * c.T * c.d * c.d_ff * c.L
+    flops_step = flops_oe + flops_pg
+    med = lambda v: v[len(v) // 2]  # noqa: E731
+    props = torch.cuda.get_device_properties(0)
+    clk_khz = getattr(props, "clock_rate", None)
+    peak_clk = (props.multi_processor_count * clk_khz * 1e3 * 4096 / 1e12) if clk_khz else None
+    substeps = {
+        "step_ms_median": round(med(per_step), 4), "step_ms_min": round(per_step[0], 4),
+        "output_error_ms_median": round(med(per_oe), 4),
+        "pseudograd_update_ms_median": round(med(per_pg), 4),
+        "output_error_mfma_frac": round(flops_oe / (med(per_oe) / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "pseudograd_update_mfma_frac": round(flops_pg / (med(per_pg) / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "mfma_peak_tflops_nominal": PEAK_BF16_TFLOPS,
+        "mfma_peak_tflops_at_max_clock": round(peak_clk, 1) if peak_clk else None,
+    }
+    log(f"[bench] median step {substeps['step_ms_median']:.3f} ms (min {substeps['step_ms_min']:.3f}): output error "
+        f"{substeps['output_error_ms_median']:.3f} ms, pseudograd + update {substeps['pseudograd_update_ms_median']:.3f} ms")
     res = {
         "metric": METRIC, "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{c.name}-shaped FPO step: T={c.T} tokens, d={c.d}, d_ff={c.d_ff}, V={c.V}, "
-                               f"{c.L} target layers (W3), bf16 operands / fp32 accumulate, SGD-momentum on fp32 "
-                               f"masters, 1% relative clip", "T": c.T, "d": c.d, "d_ff": c.d_ff, "V": c.V, "L": c.L},
+                               f"{c.L} target layers (W3), bf16 operands / fp32 accumulate, {OPT_NAME[args.optimizer]} "
+                               f"on fp32 masters, 1% relative clip", "T": c.T, "d": c.d, "d_ff": c.d_ff, "V": c.V, "L": c.L,
+                   "optimizer": args.optimizer},
         "step_mfma_frac": round(flops_step / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "substeps": substeps,
         "roofline": roof,
         "kernels": kernels,
     }

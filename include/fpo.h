@@ -118,7 +118,10 @@ typedef struct {
  *   W_lp      low-precision copy written after the step (bf16 RNE of the new
  *             master; fp32 copy when the call's dtype is FPO_F32); the array
  *             or any entry may be NULL to skip it
- *   state1    SGD momentum buffer | AdamW first moment, in/out
+ *   state1    SGD momentum buffer | AdamW first moment, in/out. May be NULL
+ *             (the array or an entry) for SGD with momentum 0: plain SGD
+ *             keeps no state (b = s * dW each step; 14 bytes per parameter
+ *             of HBM traffic instead of 22)
  *   state2    AdamW second moment, in/out (NULL for SGD)
  *   W_sumsq   device double[n_mats]: in ||W||_F^2 of the current masters
  *             (the clip's reference), out ||W'||_F^2 of the new masters

@@ -243,8 +243,12 @@ int fill_update(const fpo_opt* opt, int64_t n, const int64_t* numel, const float
   if (int e = check_opt(opt)) return e;
   if (!upd) return fail(FPO_ERR_NULL, "update buffers are NULL");
   if (n <= 0 || n > fpo::kMaxMats) return fail(FPO_ERR_SHAPE, "n_mats must be in [1, %d]", fpo::kMaxMats);
-  if (!numel || !grad || !grad_sumsq || !upd->W_master || !upd->state1 || !upd->W_sumsq)
-    return fail(FPO_ERR_NULL, "update: numel, grad, grad_sumsq, W_master, state1 and W_sumsq are required");
+  // state1 may be absent only for plain SGD (momentum 0): no state is kept
+  const bool stateless_ok = opt->kind == FPO_OPT_SGD && opt->momentum == 0.0;
+  if (!numel || !grad || !grad_sumsq || !upd->W_master || !upd->W_sumsq || (!upd->state1 && !stateless_ok))
+    return fail(FPO_ERR_NULL,
+                "update: numel, grad, grad_sumsq, W_master, W_sumsq and state1 (unless SGD with momentum 0) "
+                "are required");
   if (opt->kind == FPO_OPT_ADAMW && !upd->state2)
     return fail(FPO_ERR_NULL, "update: AdamW needs state2");
   if (lp_dtype != FPO_F32 && lp_dtype != FPO_BF16)
@@ -264,16 +268,17 @@ int fill_update(const fpo_opt* opt, int64_t n, const int64_t* numel, const float
     if (numel[m] <= 0 || numel[m] % 4)
       return fail(FPO_ERR_SHAPE, "update: numel[%lld]=%lld must be a positive multiple of 4",
                   (long long)m, (long long)numel[m]);
-    if (!grad[m] || !upd->W_master[m] || !upd->state1[m] ||
+    float* s1m = upd->state1 ? upd->state1[m] : nullptr;
+    if (!grad[m] || !upd->W_master[m] || (!s1m && !stateless_ok) ||
         (opt->kind == FPO_OPT_ADAMW && !upd->state2[m]))
       return fail(FPO_ERR_NULL, "update: NULL buffer for matrix %lld", (long long)m);
-    if (!aligned(grad[m], 16) || !aligned(upd->W_master[m], 16) || !aligned(upd->state1[m], 16))
+    if (!aligned(grad[m], 16) || !aligned(upd->W_master[m], 16) || (s1m && !aligned(s1m, 16)))
       return fail(FPO_ERR_ARG, "update: buffers of matrix %lld must be 16-byte aligned", (long long)m);
     U->numel[m] = numel[m];
     U->grad[m] = grad[m];
     U->W[m] = upd->W_master[m];
     U->W_lp[m] = upd->W_lp ? upd->W_lp[m] : nullptr;
-    U->s1[m] = upd->state1[m];
+    U->s1[m] = s1m;
     U->s2[m] = upd->state2 ? upd->state2[m] : nullptr;
   }
   U->grad_sumsq = grad_sumsq;

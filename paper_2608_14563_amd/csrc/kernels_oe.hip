@@ -2,11 +2,14 @@
 //   rms_forward  : rho_t and y_t = gamma * x_t / rho_t            (HBM bound)
 //   logits_chunk : z = y W_c^T for one vocabulary chunk (MFMA), per-block
 //                  row statistics, p~ = exp(z - block max) staged  (MFMA bound)
-//   chunk_stats  : running max / partition function / argmax per token;
-//                  staged p~ brought to one reference per split
+//   chunk_stats  : running max / partition function / argmax per token and
+//                  one reference per split of the chunk
+//   rescale_p    : staged p~ brought to its split's reference      (HBM bound)
 //   proj_chunk   : G_s <- rescale(G_s) + p~ W_c (MFMA), one partial per split
-//   finalize_vjp : g = sum_s G_s / S - W_U[y]; clamped RMSNorm VJP  (HBM bound)
-// The T x V logits never reach HBM; only one chunk of p~ is staged.
+//   finalize_vjp : g = sum_s G_s / S - W_U[y], the target logit, the clamped
+//                  RMSNorm VJP                                     (HBM bound)
+// The T x V logits never reach HBM as logits: p~ (bf16) of one chunk is staged
+// (with the default budget, the whole vocabulary at the 7-8B shapes).
 #include "gemm.hpp"
 #include "gemm2.hpp"
 #include "launch.hpp"

@@ -8,6 +8,9 @@
 //   errh_kernel   : E = g~ W3_init (MFMA); du = E*SiLU(q), dq = E*u*SiLU'(q),
 //                   stored token-contiguous for the W1/W2 outer products
 //   reduce_parts  : fixed-order float64 sums of the tile partials
+// With the optimizer fused (bf16, W3 only), launch_pseudograd_update runs the
+// outer products one layer per launch and each layer's update on a side stream,
+// overlapping the next layer's outer products.
 #include "gemm.hpp"
 #include "gemm2.hpp"
 #include "launch.hpp"

@@ -67,6 +67,8 @@ __device__ __forceinline__ void update_block(const float* __restrict__ g, float*
   // stores are non-temporal so the stream does not evict cached data.
   constexpr int U = kElemsPerBlock / 1024;
   const bool sgd = o.kind == 0;
+  // plain SGD (momentum 0, no state buffer): b = s * dW each step
+  const bool fresh = sgd && (o.first || s1 == nullptr);
   f32x4 gv[U], w[U], v1[U], v2[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
@@ -75,7 +77,7 @@ __device__ __forceinline__ void update_block(const float* __restrict__ g, float*
     if (i < end) {
       gv[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g + i));
       w[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(W + i));
-      if (!(sgd && o.first)) v1[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s1 + i));
+      if (!fresh) v1[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s1 + i));
       if (!sgd) v2[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s2 + i));
     }
   }
@@ -88,7 +90,7 @@ __device__ __forceinline__ void update_block(const float* __restrict__ g, float*
     f32x4 wv = w[u];
     if (sgd) {  // SGD with momentum
       f32x4 bv;
-      if (o.first) {
+      if (fresh) {
         bv = gs;
       } else {
         bv.x = fmaf(o.momentum, v1[u].x, gs.x);
@@ -96,7 +98,7 @@ __device__ __forceinline__ void update_block(const float* __restrict__ g, float*
         bv.z = fmaf(o.momentum, v1[u].z, gs.z);
         bv.w = fmaf(o.momentum, v1[u].w, gs.w);
       }
-      __builtin_nontemporal_store(bv, reinterpret_cast<f32x4*>(s1 + i));
+      if (s1) __builtin_nontemporal_store(bv, reinterpret_cast<f32x4*>(s1 + i));
       wv.x = fmaf(-o.lr, bv.x, wv.x);
       wv.y = fmaf(-o.lr, bv.y, wv.y);
       wv.z = fmaf(-o.lr, bv.z, wv.z);

@@ -182,6 +182,12 @@ def test_apply_update_validation(lib):
     assert call(sgd, numel=(C.c_int64 * 1)(1022)) == L.FPO_ERR_SHAPE
     assert call(sgd, lp=9) == L.FPO_ERR_DTYPE
     assert call(sgd, ws_bytes=8) == L.FPO_ERR_WORKSPACE
+    # no state buffer: allowed only for SGD with momentum 0 (plain SGD)
+    nostate = L.UpdateBufs(W, None, None, None, FAKE, None)
+    assert call(sgd, upd=nostate) == L.FPO_ERR_NULL
+    assert "momentum 0" in lib.fpo_last_error().decode()
+    plain = L.Opt(0, 1e-4, 0.0, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)
+    assert call(plain, upd=nostate, ws_bytes=8) == L.FPO_ERR_WORKSPACE  # passes the state check
 
 
 def test_cosine_validation(lib):

@@ -20,14 +20,17 @@ def make(shapes, seed, gscale):
     return W, G
 
 
-@pytest.mark.parametrize("kind", ["sgd", "adamw"])
+@pytest.mark.parametrize("kind", ["sgd", "adamw", "sgd-plain"])
 @pytest.mark.parametrize("clip,gscale", [(0.01, 1e-2), (0.01, 1e-5), (0.0, 1e-3), (1.0, 1e-3)])
 def test_three_steps(dev, kind, clip, gscale):
+    """Three optimizer steps against the oracle. sgd-plain: momentum 0 with
+    no state buffer (the oracle's SGD-momentum with beta = 0)."""
     shapes = [(256, 688), (64, 100), (8, 4)]
     W, Gs = make(shapes, 7, gscale)
     n = len(shapes)
     tW = [torch.from_numpy(w.copy()).to(dev) for w in W]
-    s1 = [torch.zeros_like(w) for w in tW]
+    plain = kind == "sgd-plain"
+    s1 = None if plain else [torch.zeros_like(w) for w in tW]
     s2 = [torch.zeros_like(w) for w in tW] if kind == "adamw" else None
     lp = [torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in tW]
     Wsq = torch.tensor([float((w.astype(np.float64) ** 2).sum()) for w in W], dtype=torch.float64, device=dev)
@@ -38,12 +41,13 @@ def test_three_steps(dev, kind, clip, gscale):
     om = [np.zeros(s) for s in shapes]
     ov = [np.zeros(s) for s in shapes]
     lr = 1e-3 if kind == "adamw" else 1e-2
+    mom = 0.0 if plain else 0.9
     for step in range(1, 4):
         G = Gs[step - 1]
         tg = [torch.from_numpy(g).to(dev) for g in G]
         gsq = torch.tensor([float((g.astype(np.float64) ** 2).sum()) for g in G], dtype=torch.float64, device=dev)
         Wprev = [w.cpu().numpy().copy() for w in tW]
-        opt = api.OptConfig(kind=0 if kind == "sgd" else 1, lr=lr, clip_frac=clip, step=step)
+        opt = api.OptConfig(kind=1 if kind == "adamw" else 0, lr=lr, momentum=mom, clip_frac=clip, step=step)
         api.fpo_apply_update(opt, tg, gsq, tW, s1, Wsq, W_lp=lp, state2=s2, clip_scale=clipv)
         torch.cuda.synchronize()
         for m in range(n):
@@ -51,10 +55,14 @@ def test_three_steps(dev, kind, clip, gscale):
             s = O.clip_scale(float(gsq[m]), wsq_in, clip)
             assert abs(float(clipv[m]) - s) <= 1e-5 * s
             Gh = s * G[m].astype(np.float64)
-            if kind == "sgd":
-                oW[m], ob[m] = O.sgd_momentum(oW[m], ob[m], Gh, lr, 0.9, step)
-                assert_close("momentum", s1[m].cpu().numpy(), ob[m], "f32")
-                b = s1[m].cpu().numpy().astype(np.float64)
+            if kind != "adamw":
+                oW[m], ob[m] = O.sgd_momentum(oW[m], ob[m], Gh, lr, mom, step)
+                if plain:  # the step used b = fp32(s) * G, no state
+                    b = (np.float32(clipv[m].item()) * G[m]).astype(np.float32).astype(np.float64)
+                    assert_close("step", b, ob[m], "f32")
+                else:
+                    assert_close("momentum", s1[m].cpu().numpy(), ob[m], "f32")
+                    b = s1[m].cpu().numpy().astype(np.float64)
                 expect = (Wprev[m].astype(np.float64) - np.float64(np.float32(lr)) * b).astype(np.float32)
             else:
                 oW[m], om[m], ov[m] = O.adamw(oW[m], om[m], ov[m], Gh, lr, step)
@@ -69,7 +77,7 @@ def test_three_steps(dev, kind, clip, gscale):
                 expect = (Wprev[m].astype(np.float64) * decay
                           - f32(lr) * (mg * ib1) / (np.sqrt(vg) * isb2 + f32(1e-8))).astype(np.float32)
             Wg = tW[m].cpu().numpy()
-            if kind == "sgd":
+            if kind != "adamw":
                 assert ulp_diff_f32(Wg, expect).max() <= 1
             else:
                 # the AdamW step is ~lr per element, not small against W: allow
@@ -127,7 +135,7 @@ def test_cosine(dev, bdtype):
     assert_close("sa", float(sa[0]), O.cosine(A[0], A[0])[1], "f32")
 
 
-@pytest.mark.parametrize("kind", ["sgd", "adamw"])
+@pytest.mark.parametrize("kind", ["sgd", "adamw", "sgd-plain"])
 @pytest.mark.parametrize("T,d,d_ff,L,clip", [(256, 256, 512, 2, 0.01), (300, 264, 1000, 3, 0.01),
                                              (200, 512, 768, 3, 1e-5)])
 def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip):
@@ -141,10 +149,11 @@ def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip):
     acts = [dev_tensor(I.activation(c, l), dev) for l in range(L)]
     W0 = [torch.from_numpy(I.master_weight(c, l)).to(dev) for l in range(L)]
     adam = kind == "adamw"
+    plain = kind == "sgd-plain"
 
     def fresh():
         W = [w.clone() for w in W0]
-        return dict(W=W, s1=[torch.zeros_like(w) for w in W],
+        return dict(W=W, s1=None if plain else [torch.zeros_like(w) for w in W],
                     s2=[torch.zeros_like(w) for w in W] if adam else None,
                     lp=[torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in W],
                     Wsq=torch.tensor([float((w.double() ** 2).sum()) for w in W], dtype=torch.float64, device=dev),
@@ -154,14 +163,15 @@ def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip):
 
     sep, fus = fresh(), fresh()
     for step in (1, 2):
-        opt = api.OptConfig(kind=L_.FPO_OPT_ADAMW if adam else L_.FPO_OPT_SGD, lr=1e-2, clip_frac=clip, step=step)
+        opt = api.OptConfig(kind=L_.FPO_OPT_ADAMW if adam else L_.FPO_OPT_SGD, lr=1e-2, clip_frac=clip, step=step,
+                            momentum=0.0 if plain else 0.9)
         api.fpo_pseudograd(g, acts, dW3=sep["dW"], sumsq=sep["ss"])
         api.fpo_apply_update(opt, sep["dW"], sep["ss"], sep["W"], sep["s1"], sep["Wsq"], W_lp=sep["lp"],
                              state2=sep["s2"], clip_scale=sep["cs"])
         api.fpo_pseudograd(g, acts, dW3=fus["dW"], sumsq=fus["ss"], opt=opt, W_master=fus["W"], W_lp=fus["lp"],
                            state1=fus["s1"], state2=fus["s2"], W_sumsq=fus["Wsq"], clip_scale=fus["cs"])
         torch.cuda.synchronize()
-        for key in ("W", "s1", "lp", "dW") + (("s2",) if adam else ()):
+        for key in ("W", "lp", "dW") + (("s2",) if adam else ()) + (() if plain else ("s1",)):
             for a, b in zip(sep[key], fus[key]):
                 assert torch.equal(a, b), (key, step)
         for key in ("Wsq", "ss", "cs"):
