@@ -31,10 +31,13 @@ Readings of points the paper leaves open (each listed in the design notes):
     gradient); AdamW uses betas (0.9, 0.999), eps 1e-8, decoupled weight decay
     0.01 and bias correction;
   * a cosine with a zero-norm side is 0; the model summary averages the last
-    round(N/4) layers.
+    round(N/4) layers;
+  * the post-FFN composition uses the fp32 g~ (before any bf16 rounding) and
+    the same eps and min-RMS clamp as the final norm.
 Parity status: every function below is pinned by tests/test_oracle_pins.py
 except the clamp branch of rmsnorm_vjp (rho < min_rms), which has no
-external definition beyond its own formula: parity unpinned for that branch.
+external definition beyond its own formula: parity unpinned for that branch
+(it is shared by post_ffn_signal).
 """
 from __future__ import annotations
 
@@ -166,6 +169,19 @@ def pseudograd(g_tilde, a, scale=None):
     af = _f64(a)
     s = 1.0 / g.shape[0] if scale is None else scale
     return s * (g.T @ af)
+
+
+# --------------------------------------------------------------------------
+# Post-feedforward RMSNorm composition (Sec. 3.2 "Post-feedforward RMSNorm";
+# the App. A pseudocode's per-layer rmsnorm_vjp on the cached MLP output;
+# the per-architecture composition appendix): architectures that normalize
+# the MLP output before the residual add (OLMo-2, Gemma 3) pass g~ through
+# that norm's closed-form VJP, with the same min-RMS clamp, before the
+# layer's outer product.
+def post_ffn_signal(g_tilde, mlp_out, gamma_pffn, eps=1e-6, min_rms=0.5):
+    """g_l = rmsnorm_vjp(g~, mlp_out_l, gamma_pffn_l) [T, d]: the layer's left
+    operand (for the W3 outer product and, in full-MLP mode, E = g_l W3_init)."""
+    return rmsnorm_vjp(g_tilde, mlp_out, gamma_pffn, eps, min_rms)
 
 
 # --------------------------------------------------------------------------

@@ -39,7 +39,8 @@ ENTROPY = 260814563
 BLOCK = 1 << 20
 
 # tensor ids inside the spawn key
-T_X, T_GAMMA, T_WU, T_TARGETS, T_Q, T_U, T_W, T_OUTLIER, T_REFNOISE, T_XIN, T_W1, T_W2, T_G, T_STATE, T_MISC, T_REF1 = range(16)
+T_X, T_GAMMA, T_WU, T_TARGETS, T_Q, T_U, T_W, T_OUTLIER, T_REFNOISE, T_XIN, T_W1, T_W2, T_G, T_STATE, T_MISC, T_REF1, \
+    T_PFFN = range(17)
 
 
 @dataclass(frozen=True)
@@ -221,6 +222,26 @@ def ref_noise(cfg: Config, layer: int) -> np.ndarray:
     """N(0,1) [d, d_ff] float32 for the diagnostic's reference gradient
     R = D + sigma * N, sigma = sqrt(3) * ||D||_F / sqrt(d * d_ff)."""
     return normal(cfg.cid, T_REFNOISE, layer, cfg.d * cfg.d_ff).reshape(cfg.d, cfg.d_ff)
+
+
+def post_ffn(cfg: Config, layer: int):
+    """Cached MLP output (the post-FFN norm's input) [T, d] and the layer's
+    post-FFN gain [d], both in the storage dtype, shaped after the paper's
+    OLMo-2 measurements (App. on norm statistics): per-token RMS around a layer
+    mean rising from 0.9 (first target layer) to 2.7 (last), log-normal spread
+    (sigma 0.3), with 1% of tokens (token 0 included, BOS-like) at RMS 0.09 so
+    the min-RMS clamp is active; gain mean rising from 0.25 to 0.39 with a 10%
+    per-channel spread."""
+    frac = layer / max(1, cfg.L - 1)
+    mean_rms = 0.9 + 1.8 * frac
+    r = mean_rms * np.exp(0.3 * normal(cfg.cid, T_PFFN, 4 * layer, cfg.T))
+    k = max(1, int(round(0.01 * cfg.T)))
+    idx = np.unique(np.concatenate([[0], _rng(cfg.cid, T_PFFN, 4 * layer + 1, 0).choice(cfg.T, k, replace=False)]))
+    r[idx] = 0.09
+    z = normal(cfg.cid, T_PFFN, 4 * layer + 2, cfg.T * cfg.d).reshape(cfg.T, cfg.d)
+    out = (z * r[:, None].astype(np.float32)).astype(np.float32)
+    gam = ((0.25 + 0.14 * frac) * (1.0 + 0.1 * normal(cfg.cid, T_PFFN, 4 * layer + 3, cfg.d))).astype(np.float32)
+    return to_storage(out, cfg.dtype), to_storage(gam, cfg.dtype)
 
 
 def rank1_reference(cfg: Config, layer: int = 0):

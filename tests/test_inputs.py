@@ -67,3 +67,22 @@ def test_bf16_rounding_matches_torch_rne():
     assert np.array_equal(ours, ref)
     back = I.bf16_to_f32(ours)
     assert np.array_equal(back, torch.from_numpy(x).to(torch.bfloat16).float().numpy())
+
+
+def test_post_ffn_inputs_follow_the_recipe():
+    c = I.CONFIGS[1].shrink(T=1000, d=256, L=4)
+    for l in (0, c.L - 1):
+        x, g = I.post_ffn(c, l)
+        assert x.shape == (c.T, c.d) and g.shape == (c.d,) and x.dtype == np.uint16
+        xf, gf = I.storage_to_f64(x), I.storage_to_f64(g)
+        rms = np.sqrt((xf ** 2).mean(1))
+        low = rms < 0.2
+        assert low[0] and low.sum() >= 10              # 1% BOS-like outliers, token 0 among them
+        assert np.all(np.abs(rms[low] - 0.09) < 0.02)
+        mean_target = 0.9 + 1.8 * l / (c.L - 1)
+        assert abs(np.median(rms[~low]) / mean_target - 1) < 0.1
+        assert abs(gf.mean() - (0.25 + 0.14 * l / (c.L - 1))) < 0.02
+    a, b = I.post_ffn(c, 1)
+    a2, b2 = I.post_ffn(c, 1)
+    assert np.array_equal(a, a2) and np.array_equal(b, b2)
+

@@ -298,6 +298,51 @@ def test_identity_layer_toy_directional_finite_difference():
     assert abs(float(np.sum(D * dirn)) - fd) < 1e-7 * max(1.0, abs(fd))
 
 
+@pytest.mark.parametrize("seed", [3, 4])
+def test_post_ffn_toy_composed_signal_is_true_gradient(seed):
+    """Sec. 3.2 post-feedforward RMSNorm (App. A pseudocode): each target layer
+    adds postnorm_l(a_l W_l^T) to the residual; with identity layers after the
+    targets, the gradient of the mean cross-entropy w.r.t. W_l is
+    (1/T) [VJP of postnorm_l at the MLP output applied to g~]^T a_l, i.e. the
+    oracle's post_ffn_signal followed by pseudograd (clamp inactive)."""
+    t = toy(seed, T=5, d=6, V=16, d_ff=10, L=2)
+    r = np.random.default_rng(100 + seed)
+    gp = [0.3 * (1 + 0.1 * r.standard_normal(6)) for _ in range(2)]
+    Ws = [torch.tensor(3.0 * W, requires_grad=True) for W in t["W"]]  # MLP-output RMS well above 0.5
+    As = [torch.tensor(a) for a in t["a"]]
+    h = torch.tensor(t["x"])
+    mlp_out = []
+    for a, W, g in zip(As, Ws, gp):
+        m = a @ W.T
+        mlp_out.append(m.detach().numpy())
+        h = h + torch_rmsnorm(m, torch.tensor(g), 1e-6)
+    U = torch_rmsnorm(h, torch.tensor(t["gamma"]), 1e-6)
+    loss = torch.nn.functional.cross_entropy(U @ torch.tensor(t["W_U"]).T, torch.tensor(t["y"]).long(),
+                                             reduction="mean")
+    grads = torch.autograd.grad(loss, Ws)
+    hf = h.detach().numpy()
+    for m in mlp_out:
+        assert np.all(np.sqrt((m ** 2).mean(1)) > 0.5)  # clamp inactive: the composition is exact
+    out = O.output_error(hf, t["gamma"], t["W_U"], t["y"], eps=1e-6, min_rms=0.5)
+    for l in range(2):
+        gl = O.post_ffn_signal(out["g_tilde"], mlp_out[l], gp[l], eps=1e-6, min_rms=0.5)
+        np.testing.assert_allclose(O.pseudograd(gl, t["a"][l]), grads[l].numpy(), rtol=1e-10, atol=1e-13)
+        # and the composition differs from skipping the post-FFN VJP
+        assert not np.allclose(O.pseudograd(out["g_tilde"], t["a"][l]), grads[l].numpy(), rtol=1e-3)
+
+
+def test_post_ffn_signal_scale_and_gain_properties():
+    """Scaling the MLP output by k (RMS stays above the clamp) divides the
+    composed signal by k; the signal is linear in the gain."""
+    r = np.random.default_rng(41)
+    g = r.standard_normal((4, 8))
+    x = 2.0 * r.standard_normal((4, 8))
+    gam = 0.3 + 0.05 * r.standard_normal(8)
+    base = O.post_ffn_signal(g, x, gam, eps=0.0, min_rms=0.5)
+    np.testing.assert_allclose(O.post_ffn_signal(g, 3.0 * x, gam, eps=0.0, min_rms=0.5), base / 3.0, rtol=1e-12)
+    np.testing.assert_allclose(O.post_ffn_signal(g, x, 2.0 * gam, eps=0.0, min_rms=0.5), 2.0 * base, rtol=1e-12)
+
+
 def test_full_mlp_step0_feedback_is_exact_gradient():
     """eq. errh: at step 0 (W3 = W3_init) the W1/W2 signals are the exact gradients."""
     r = np.random.default_rng(31)
