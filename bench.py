@@ -47,6 +47,8 @@ def parse():
     ap.add_argument("--vocab-chunk", type=int, default=0,
                     help="vocabulary chunk width (0: the library's planner)")
     ap.add_argument("--cpu-tokens", type=int, default=1024, help="tokens in the oracle's timed sample")
+    ap.add_argument("--post-ffn", action="store_true",
+                    help="compose each target layer's post-FFN RMSNorm VJP (OLMo-2 / Gemma 3 layout)")
     ap.add_argument("--optimizer", choices=sorted(OPT_BYTES), default="sgd-momentum",
                     help="optimizer on the fp32 masters (HBM bytes per parameter: " +
                          ", ".join(f"{k} {v}" for k, v in sorted(OPT_BYTES.items())) + ")")
@@ -124,7 +126,7 @@ def profiled_traffic(workload: str, kernel: str):
     return None
 
 
-def kernel_work(name, c, steps, nchunk, opt="sgd-momentum"):
+def kernel_work(name, c, steps, nchunk, opt="sgd-momentum", pffn=False):
     """Algorithmic work of one kernel over `steps` steps: (amount, unit, bound).
     Flops count only the method's contractions; bytes count each operand once."""
     T, d, V, dff, L = c.T, c.d, c.V, c.d_ff, c.L
@@ -141,8 +143,11 @@ def kernel_work(name, c, steps, nchunk, opt="sgd-momentum"):
         return 4.0 * T * V * steps, "byte", "hbm"  # staged p~ read + write (bf16)
     if name == "rms_forward":
         return (4.0 * T * d) * steps, "byte", "hbm"  # x read, y written (bf16)
-    if name == "transpose_pad":
-        return (4.0 * T * d) * steps, "byte", "hbm"  # g~ read, g~^T written (bf16)
+    if name == "pffn_vjp":
+        # per layer: g~ fp32 read, MLP output read, composed signal written (bf16)
+        return (8.0 * T * d * L) * steps, "byte", "hbm"
+    if name == "transpose_pad":  # signal read, token-contiguous copy written (bf16); per layer with post-FFN
+        return (4.0 * T * d * (L if pffn else 1)) * steps, "byte", "hbm"
     if name == "finalize_vjp":
         return (T * d * (4 + 2 + 2 + 4 + 2)) * steps, "byte", "hbm"
     return None
@@ -233,6 +238,12 @@ def main():
     tx, tgam, tW, ty = t(x), t(gam), t(W_U), t(y)
     tacts = [t(a) for a in acts]
     Wm = [t(w) for w in Wm_host]
+    pffn = None
+    if args.post_ffn:
+        pf_host = [I.post_ffn(c, l) for l in range(c.L)]
+        pffn_mo = [t(m) for m, _ in pf_host]
+        pffn_g = [t(g) for _, g in pf_host]
+        del pf_host
     plain = args.optimizer == "sgd"
     adam = args.optimizer == "adamw"
     s1 = None if plain else [torch.zeros_like(w) for w in Wm]
@@ -250,6 +261,8 @@ def main():
     ss = torch.empty(c.L, dtype=torch.float64, device=dev)
     ws_oe = api.workspace(api.fpo_output_error_workspace(T, d, c.V, torch.bfloat16, args.vocab_chunk), dev)
     ws_pg = api.workspace(api.fpo_pseudograd_workspace(T, d, c.d_ff, c.L, torch.bfloat16), dev)
+    if args.post_ffn:
+        pffn = api.PostFfn(g_t, pffn_mo, pffn_g, c.eps, c.min_rms)
     torch.cuda.synchronize()
     step_no = [0]
 
@@ -263,7 +276,7 @@ def main():
         api.fpo_pseudograd(g_lp, tacts, dW3=dW, sumsq=ss,
                            opt=api.OptConfig(kind=1 if adam else 0, lr=c.lr, momentum=0.0 if plain else 0.9,
                                              clip_frac=c.clip_frac, step=step_no[0]),
-                           W_master=Wm, W_lp=Wlp, state1=s1, state2=s2, W_sumsq=Wsq, ws=ws_pg)
+                           W_master=Wm, W_lp=Wlp, state1=s1, state2=s2, W_sumsq=Wsq, ws=ws_pg, post_ffn=pffn)
 
     lib = prof_lib()
     for _ in range(args.warmup):
@@ -305,7 +318,7 @@ def main():
     log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step, {tok_s:.0f} tokens/s; dominant kernel {dom}: "
         f"{dom_stats[0] / dom_stats[1]:.3f} ms avg over {dom_stats[1]} launches")
     nchunk = None
-    w = kernel_work(dom, c, args.steps, nchunk, args.optimizer)
+    w = kernel_work(dom, c, args.steps, nchunk, args.optimizer, args.post_ffn)
     roof = None
     traffic = profiled_traffic(c.name, dom)
     if w is not None:
@@ -323,7 +336,7 @@ def main():
                     "avg_launch_ms": round(dom_stats[0] / dom_stats[1], 4), "launches": dom_stats[1]}
     kernels = {}
     for k, (ms, n) in per_kernel.items():
-        wk = kernel_work(k, c, 1, nchunk, args.optimizer)
+        wk = kernel_work(k, c, 1, nchunk, args.optimizer, args.post_ffn)
         e = {"ms_per_step": round(ms, 4), "launches": n}
         if wk is not None:
             amount, unit, bound = wk
@@ -357,9 +370,10 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{c.name}-shaped FPO step: T={c.T} tokens, d={c.d}, d_ff={c.d_ff}, V={c.V}, "
-                               f"{c.L} target layers (W3), bf16 operands / fp32 accumulate, {OPT_NAME[args.optimizer]} "
+                               f"{c.L} target layers (W3{', post-FFN norm VJP per layer' if args.post_ffn else ''}), bf16 operands / fp32 "
+                               f"accumulate, {OPT_NAME[args.optimizer]} "
                                f"on fp32 masters, 1% relative clip", "T": c.T, "d": c.d, "d_ff": c.d_ff, "V": c.V, "L": c.L,
-                   "optimizer": args.optimizer},
+                   "optimizer": args.optimizer, "post_ffn_norm": bool(args.post_ffn)},
         "step_mfma_frac": round(flops_step / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "substeps": substeps,
         "roofline": roof,

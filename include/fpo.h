@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define FPO_ABI_VERSION 1
+#define FPO_ABI_VERSION 2
 
 typedef enum {
   FPO_OK = 0,
@@ -170,6 +170,26 @@ int fpo_output_error(const fpo_oe_desc* desc, const void* h_final, const void* g
                      float* g_pre, float* lse, float* loss, int32_t* argmax,
                      int32_t* bad_targets, void* ws, size_t ws_bytes, void* stream);
 
+/* Post-feedforward RMSNorm composition (Sec. 3.2 "Post-feedforward RMSNorm";
+ * App. A pseudocode; OLMo-2 and Gemma 3 layouts): each target layer's left
+ * operand becomes g_l = the clamped RMSNorm VJP of that layer's post-FFN norm
+ * (input: the cached MLP output, gain: the layer's post-FFN gain) applied to
+ * the fp32 g~:
+ *   rho~ = max(sqrt(mean mlp_out_t^2 + eps), min_rms); x^ = mlp_out_t / rho~;
+ *   c = (1/d) <x^, gamma * g~_t>;  g_l,t = (gamma * g~_t - c x^) / rho~
+ * rounded to the operand dtype, then used for dW3_l and (full-MLP mode) E_l.
+ *   g_tilde   float [T, d]: fpo_output_error's g_tilde
+ *   mlp_out   [host] L pointers to [T, d] (dtype): cached MLP outputs
+ *   gamma     [host] L pointers to [d] (dtype): post-FFN norm gains
+ *   eps, min_rms  as in fpo_oe_desc (the paper uses min_rms 0.5) */
+typedef struct {
+  const float* g_tilde;
+  const void* const* mlp_out;
+  const void* const* gamma;
+  float eps;
+  float min_rms;
+} fpo_post_ffn;
+
 /* ---------------------------------------------------------------------------
  * fpo_pseudograd - per-layer token-summed outer products (eq. w3update, with
  * the App. A divisor supplied as desc->scale) and, in full-MLP mode, the
@@ -194,6 +214,8 @@ int fpo_output_error(const fpo_oe_desc* desc, const void* h_final, const void* g
  *              nullable (layer-viability diagnostic, eq. cosine)
  *   ref_dot, ref_sumsq  double [L] out (required when ref is given):
  *              <dW3_l, R_l> and ||R_l||_F^2
+ *   post_ffn   nullable: compose each layer's post-FFN norm VJP (see
+ *              fpo_post_ffn); g_tilde_lp is then unused and may be NULL
  *   opt, upd   both NULL, or both given: the call then also applies
  *              fpo_apply_update to the matrices in `sumsq` order, with the
  *              same result bit for bit as calling it separately
@@ -210,8 +232,8 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
                    const void* const* W3_init, const void* const* gate, const void* const* up,
                    const void* const* x_in, float* const* dW3, float* const* dW1,
                    float* const* dW2, double* sumsq, const float* const* ref, double* ref_dot,
-                   double* ref_sumsq, const fpo_opt* opt, const fpo_update_bufs* upd, void* ws,
-                   size_t ws_bytes, void* stream);
+                   double* ref_sumsq, const fpo_post_ffn* post_ffn, const fpo_opt* opt,
+                   const fpo_update_bufs* upd, void* ws, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
  * fpo_apply_update - relative clip and optimizer step on fp32 masters

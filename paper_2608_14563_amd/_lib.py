@@ -48,6 +48,12 @@ class UpdateBufs(C.Structure):
                 ("W_sumsq", C.c_void_p), ("clip_scale", C.c_void_p)]
 
 
+class PostFfn(C.Structure):
+    _fields_ = [("g_tilde", C.c_void_p), ("mlp_out", C.POINTER(C.c_void_p)), ("gamma", C.POINTER(C.c_void_p)),
+                ("eps", C.c_float), ("min_rms", C.c_float)]
+
+
+ABI_VERSION = 2
 PP = C.POINTER(C.c_void_p)
 VP = C.c_void_p
 _lib = None
@@ -70,6 +76,9 @@ def load() -> C.CDLL:
     lib = C.CDLL(LIB_PATH)
     lib.fpo_abi_version.restype = C.c_int
     lib.fpo_abi_version.argtypes = []
+    if lib.fpo_abi_version() != ABI_VERSION:
+        raise RuntimeError(f"{LIB_PATH} has ABI version {lib.fpo_abi_version()}, this binding expects "
+                           f"{ABI_VERSION}: rebuild the library")
     lib.fpo_last_error.restype = C.c_char_p
     lib.fpo_last_error.argtypes = []
     lib.fpo_output_error_workspace.restype = C.c_size_t
@@ -81,7 +90,8 @@ def load() -> C.CDLL:
     lib.fpo_pseudograd_workspace.argtypes = [C.POINTER(PgDesc)]
     lib.fpo_pseudograd.restype = C.c_int
     lib.fpo_pseudograd.argtypes = [C.POINTER(PgDesc), VP, PP, PP, PP, PP, PP, PP, PP, PP, VP, PP, VP,
-                                   VP, C.POINTER(Opt), C.POINTER(UpdateBufs), VP, C.c_size_t, VP]
+                                   VP, C.POINTER(PostFfn), C.POINTER(Opt), C.POINTER(UpdateBufs), VP,
+                                   C.c_size_t, VP]
     lib.fpo_apply_update_workspace.restype = C.c_size_t
     lib.fpo_apply_update_workspace.argtypes = [C.c_int64, C.POINTER(C.c_int64)]
     lib.fpo_apply_update.restype = C.c_int

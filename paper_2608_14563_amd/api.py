@@ -17,7 +17,7 @@ import torch
 from . import _lib as L
 
 __all__ = [
-    "fpo_abi_version", "fpo_output_error", "fpo_output_error_workspace", "fpo_pseudograd",
+    "fpo_abi_version", "fpo_output_error", "fpo_output_error_workspace", "fpo_pseudograd", "PostFfn",
     "fpo_pseudograd_workspace", "fpo_apply_update", "fpo_apply_update_workspace", "fpo_cosine",
     "fpo_cosine_workspace", "OptConfig", "workspace", "dtype_code",
 ]
@@ -135,29 +135,50 @@ def fpo_pseudograd_workspace(T, d, d_ff, Lyr, dtype: torch.dtype, full_mlp=False
     return L.load().fpo_pseudograd_workspace(C.byref(desc))
 
 
+@dataclass
+class PostFfn:
+    """Per-layer post-feedforward RMSNorm composition (fpo_post_ffn): the fp32
+    g~ [T, d], each target layer's cached MLP output [T, d] and post-FFN gain
+    [d] (operand dtype)."""
+    g_tilde: torch.Tensor
+    mlp_out: Sequence[torch.Tensor]
+    gamma: Sequence[torch.Tensor]
+    eps: float = 1e-6
+    min_rms: float = 0.5
+
+
 def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, ref_sumsq=None,
                    W3_init=None, gate=None, up=None, x_in=None, dW1=None, dW2=None, scale=None,
                    opt: Optional[OptConfig] = None, W_master=None, W_lp=None, state1=None,
-                   state2=None, W_sumsq=None, clip_scale=None, ws=None):
-    T, d = g_tilde_lp.shape
+                   state2=None, W_sumsq=None, clip_scale=None, ws=None, post_ffn: Optional[PostFfn] = None):
+    """g_tilde_lp may be None when post_ffn is given (its left operands are
+    then formed per layer from post_ffn.g_tilde)."""
+    op = a[0].dtype
+    dev = a[0].device
+    T = a[0].shape[0]
+    d = (g_tilde_lp if g_tilde_lp is not None else post_ffn.g_tilde).shape[1]
     Lyr = len(a)
     d_ff = a[0].shape[1]
     full = W3_init is not None
-    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(g_tilde_lp.dtype),
+    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(op),
                     L.FPO_MODE_FULL_MLP if full else L.FPO_MODE_W3,
                     (1.0 / T) if scale is None else scale)
     lib = L.load()
     if ws is None:
-        ws = workspace(lib.fpo_pseudograd_workspace(C.byref(desc)), g_tilde_lp.device)
+        ws = workspace(lib.fpo_pseudograd_workspace(C.byref(desc)), dev)
     k = _Keep()
-    op = g_tilde_lp.dtype
     o = opt.c() if opt is not None else None
     ub = _upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale, op) if opt is not None else None
+    pf = None
+    if post_ffn is not None:
+        pf = L.PostFfn(_p(post_ffn.g_tilde, F32), k.arr(post_ffn.mlp_out, op), k.arr(post_ffn.gamma, op),
+                       post_ffn.eps, post_ffn.min_rms)
     L.check(lib.fpo_pseudograd(
-        C.byref(desc), _p(g_tilde_lp), k.arr(a, op), k.arr(W3_init, op), k.arr(gate, op), k.arr(up, op),
+        C.byref(desc), _p(g_tilde_lp, op), k.arr(a, op), k.arr(W3_init, op), k.arr(gate, op), k.arr(up, op),
         k.arr(x_in, op), k.arr(dW3, F32), k.arr(dW1, F32), k.arr(dW2, F32), _p(sumsq, F64),
-        k.arr(ref, F32), _p(ref_dot, F64), _p(ref_sumsq, F64), C.byref(o) if o is not None else None, C.byref(ub) if ub is not None else None,
-        _p(ws), ws.numel(), _stream(g_tilde_lp.device)))
+        k.arr(ref, F32), _p(ref_dot, F64), _p(ref_sumsq, F64), C.byref(pf) if pf is not None else None,
+        C.byref(o) if o is not None else None, C.byref(ub) if ub is not None else None,
+        _p(ws), ws.numel(), _stream(dev)))
     return ws
 
 

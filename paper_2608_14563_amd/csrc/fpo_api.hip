@@ -166,12 +166,14 @@ size_t carve_pg(const fpo_pg_desc& d, const PgPlan& p, void* ws, fpo::PgLaunch* 
   const bool full = d.mode == FPO_MODE_FULL_MLP;
   Carver c(ws);
   void* gT = c.take<char>(d.d * p.Tp * esz);
+  void* grow = c.take<char>(d.T * d.d * esz);  // per-layer signal (post-FFN composition)
   void* dq = full ? c.take<char>(d.d_ff * p.Tp * esz) : nullptr;
   void* du = full ? c.take<char>(d.d_ff * p.Tp * esz) : nullptr;
   double* part = c.take<double>(std::max<int64_t>(d.L, 2) * p.ntiles * 3);
   double* up = c.take<double>(p.upd_blocks);
   if (L) {
     L->gT = gT;
+    L->g_row = grow;
     L->dq_T = dq;
     L->du_T = du;
     L->part = part;
@@ -355,12 +357,28 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
                    const void* const* W3_init, const void* const* gate, const void* const* up,
                    const void* const* x_in, float* const* dW3, float* const* dW1, float* const* dW2,
                    double* sumsq, const float* const* ref, double* ref_dot, double* ref_sumsq,
-                   const fpo_opt* opt, const fpo_update_bufs* upd, void* ws, size_t ws_bytes,
-                   void* stream) {
+                   const fpo_post_ffn* post_ffn, const fpo_opt* opt, const fpo_update_bufs* upd,
+                   void* ws, size_t ws_bytes, void* stream) {
   if (int e = check_pg_desc(desc)) return e;
   const bool full = desc->mode == FPO_MODE_FULL_MLP;
   const int L = (int)desc->L;
-  if (!g_tilde_lp || !a) return fail(FPO_ERR_NULL, "fpo_pseudograd: g_tilde_lp and a are required");
+  if (!a) return fail(FPO_ERR_NULL, "fpo_pseudograd: a is required");
+  if (!g_tilde_lp && !post_ffn)
+    return fail(FPO_ERR_NULL, "fpo_pseudograd: g_tilde_lp is required (unless post_ffn is given)");
+  if (post_ffn) {
+    if (!post_ffn->g_tilde || !post_ffn->mlp_out || !post_ffn->gamma)
+      return fail(FPO_ERR_NULL, "fpo_pseudograd: post_ffn needs g_tilde, mlp_out and gamma");
+    if (!aligned(post_ffn->g_tilde, 16)) return fail(FPO_ERR_ARG, "fpo_pseudograd: post_ffn->g_tilde not aligned");
+    if (!(post_ffn->eps >= 0.f) || !std::isfinite(post_ffn->eps) || !(post_ffn->min_rms >= 0.f) ||
+        !std::isfinite(post_ffn->min_rms))
+      return fail(FPO_ERR_ARG, "fpo_pseudograd: post_ffn eps and min_rms must be finite and >= 0");
+    for (int l = 0; l < L; ++l) {
+      if (!post_ffn->mlp_out[l] || !post_ffn->gamma[l])
+        return fail(FPO_ERR_NULL, "fpo_pseudograd: post_ffn buffers of layer %d are NULL", l);
+      if (!aligned(post_ffn->mlp_out[l], 16) || !aligned(post_ffn->gamma[l], 16))
+        return fail(FPO_ERR_ARG, "fpo_pseudograd: post_ffn buffers of layer %d not 16-byte aligned", l);
+    }
+  }
   if (!dW3 && !ref) return fail(FPO_ERR_NULL, "fpo_pseudograd: dW3 may be NULL only with ref");
   if (ref && (!ref_dot || !ref_sumsq))
     return fail(FPO_ERR_NULL, "fpo_pseudograd: ref needs ref_dot and ref_sumsq");
@@ -370,7 +388,8 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
     return fail(FPO_ERR_ARG, "fpo_pseudograd: opt and upd must both be given or both be NULL");
   if (opt && (!dW3 || !sumsq))
     return fail(FPO_ERR_NULL, "fpo_pseudograd: the fused update needs dW3 and sumsq");
-  if (!aligned(g_tilde_lp, 16)) return fail(FPO_ERR_ARG, "fpo_pseudograd: g_tilde_lp must be 16-byte aligned");
+  if (g_tilde_lp && !aligned(g_tilde_lp, 16))
+    return fail(FPO_ERR_ARG, "fpo_pseudograd: g_tilde_lp must be 16-byte aligned");
   fpo::PgLaunch P{};
   P.bf16 = desc->dtype == FPO_BF16;
   P.full_mlp = full;
@@ -398,6 +417,16 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
       P.x_in[l] = x_in[l];
       P.dW1[l] = dW1[l];
       P.dW2[l] = dW2[l];
+    }
+  }
+  if (post_ffn) {
+    P.pffn = true;
+    P.g_f32 = post_ffn->g_tilde;
+    P.pffn_eps = post_ffn->eps;
+    P.pffn_min_rms = post_ffn->min_rms;
+    for (int l = 0; l < L; ++l) {
+      P.mlp_out[l] = post_ffn->mlp_out[l];
+      P.gamma_pffn[l] = post_ffn->gamma[l];
     }
   }
   P.sumsq = sumsq;

@@ -40,6 +40,42 @@ __global__ __launch_bounds__(256) void transpose_pad_kernel(const T* __restrict_
   }
 }
 
+// Post-FFN norm composition: one workgroup per token,
+//   rho~ = max(sqrt(mean x^2 + eps), min_rms); x^ = x / rho~;
+//   c = (1/d) <x^, gamma * g>;  out = (gamma * g - c x^) / rho~
+// with x the cached MLP output, gamma the layer's post-FFN gain and g the fp32
+// signal g~; out in the operand dtype (the layer's left operand).
+template <typename T>
+__global__ __launch_bounds__(256) void pffn_vjp_kernel(int d, const float* __restrict__ g,
+                                                       const T* __restrict__ x,
+                                                       const T* __restrict__ gamma, float eps,
+                                                       float min_rms, T* __restrict__ out) {
+  __shared__ float red[16];
+  const int64_t row = blockIdx.x;
+  const float* gr = g + row * d;
+  const T* xr = x + row * d;
+  float ss = 0.f, cd = 0.f;
+  for (int k = threadIdx.x * 4; k < d; k += 1024) {
+    const f32x4 xv = ld4(xr, k), gm = ld4(gamma, k), gv = *reinterpret_cast<const f32x4*>(gr + k);
+    ss += xv.x * xv.x + xv.y * xv.y + xv.z * xv.z + xv.w * xv.w;
+    cd += xv.x * gm.x * gv.x + xv.y * gm.y * gv.y + xv.z * gm.z * gv.z + xv.w * gm.w * gv.w;
+  }
+  ss = block_sum(ss, red);
+  cd = block_sum(cd, red);
+  const float rt = fmaxf(sqrtf(ss / (float)d + eps), min_rms);
+  const float irt = 1.0f / rt;
+  const float c = cd * irt / (float)d;  // (1/d) <x / rho~, gamma * g>
+  for (int k = threadIdx.x * 4; k < d; k += 1024) {
+    const f32x4 xv = ld4(xr, k), gm = ld4(gamma, k), gv = *reinterpret_cast<const f32x4*>(gr + k);
+    f32x4 o;
+    o.x = (gm.x * gv.x - c * xv.x * irt) * irt;
+    o.y = (gm.y * gv.y - c * xv.y * irt) * irt;
+    o.z = (gm.z * gv.z - c * xv.z * irt) * irt;
+    o.w = (gm.w * gv.w - c * xv.w * irt) * irt;
+    st4(out + row * d, k, o);
+  }
+}
+
 struct OuterArgs {
   const void* A[kMaxMats];
   const void* B[kMaxMats];
@@ -325,17 +361,94 @@ int64_t pseudograd_tiles(bool bf16, int64_t M, int64_t N) {
     if (e_ != hipSuccess) return e_;   \
   } while (0)
 
+// The left operand of layer l: the shared signal, or (post-FFN composition)
+// layer l's VJP of g~ into a.g_row. Leaves its token-contiguous copy in a.gT
+// and returns the row-major one (the full-MLP error GEMM's left operand).
+template <typename T>
+static hipError_t layer_signal(const PgLaunch& a, int l, hipStream_t st, const T** g_rowmajor) {
+  const T* g = (const T*)a.g_lp;
+  if (a.pffn) {
+    FPO_LAUNCH("pffn_vjp", st,
+               pffn_vjp_kernel<T><<<dim3((unsigned)a.T), dim3(256), 0, st>>>(
+        (int)a.d, a.g_f32, (const T*)a.mlp_out[l], (const T*)a.gamma_pffn[l], a.pffn_eps, a.pffn_min_rms,
+        (T*)a.g_row));
+    FPO_CHECK_LAUNCH();
+    g = (const T*)a.g_row;
+  }
+  FPO_LAUNCH("transpose_pad", st,
+             transpose_pad_kernel<T><<<dim3((unsigned)(a.Tp / 64), (unsigned)((a.d + 63) / 64)), dim3(256), 0, st>>>(
+      g, a.T, a.d, (T*)a.gT, a.Tp, a.Tp));
+  FPO_CHECK_LAUNCH();
+  *g_rowmajor = g;
+  return hipSuccess;
+}
+
 template <class E>
 static hipError_t run_pseudograd(const PgLaunch& a) {
   using T = typename E::T;
   using TT = Tile<E>;
   hipStream_t st = (hipStream_t)a.stream;
-  // token-contiguous copy of the signal
-  FPO_LAUNCH("transpose_pad", st,
-             transpose_pad_kernel<T><<<dim3((unsigned)(a.Tp / 64), (unsigned)((a.d + 63) / 64)), dim3(256), 0, st>>>(
-      (const T*)a.g_lp, a.T, a.d, (T*)a.gT, a.Tp, a.Tp));
-  FPO_CHECK_LAUNCH();
-  // W3 outer products: M = d, N = d_ff, K = T
+  const int ntiles = (int)pseudograd_tiles(a.bf16, a.d, a.d_ff);
+  const int ntiles2 = (int)pseudograd_tiles(a.bf16, a.d_ff, a.d);
+  hipError_t e;
+  const T* g = nullptr;
+  // one layer's W1/W2 signals through W3_init (eq. errh) from the row-major signal g
+  auto full_mlp_layer = [&](int l, const T* gl) -> hipError_t {
+    FPO_LAUNCH("errh", st,
+               errh_kernel<E><<<dim3((unsigned)(((a.Tp + TT::BM - 1) / TT::BM) * ((a.d_ff + TT::BN - 1) / TT::BN))), dim3(256), 0, st>>>(
+        gl, (const T*)a.W3i[l], (const T*)a.q[l], (const T*)a.u[l], (int)a.T, (int)a.Tp, (int)a.d,
+        (int)a.d_ff, (T*)a.dq_T, (T*)a.du_T));
+    FPO_CHECK_LAUNCH();
+    OuterArgs oa{};
+    oa.A[0] = a.dq_T;
+    oa.B[0] = a.x_in[l];
+    oa.C[0] = a.dW1[l];
+    oa.A[1] = a.du_T;
+    oa.B[1] = a.x_in[l];
+    oa.C[1] = a.dW2[l];
+    FPO_LAUNCH("outer", st,
+               outer_kernel<E><<<dim3(ntiles2 * 2), dim3(256), 0, st>>>(oa, (int)a.d_ff, (int)a.d, (int)a.T,
+                                                         a.Tp, a.d, a.scale, a.part));
+    FPO_CHECK_LAUNCH();
+    // matrices W1(l) and W2(l) sit at a.L + l and 2 a.L + l of sumsq
+    if (a.sumsq) {
+      FPO_LAUNCH("reduce_parts", st,
+                 reduce_parts_kernel<<<dim3(1), dim3(256), 0, st>>>(a.part, ntiles2, a.L + l, a.sumsq,
+                                                         nullptr, nullptr));
+      FPO_CHECK_LAUNCH();
+      FPO_LAUNCH("reduce_parts", st,
+                 reduce_parts_kernel<<<dim3(1), dim3(256), 0, st>>>(a.part + (int64_t)ntiles2 * 3, ntiles2,
+                                                         2 * a.L + l, a.sumsq, nullptr, nullptr));
+      FPO_CHECK_LAUNCH();
+    }
+    return hipSuccess;
+  };
+  if (a.pffn) {
+    // post-FFN composition: every layer has its own left operand
+    for (int l = 0; l < a.L; ++l) {
+      if ((e = layer_signal<T>(a, l, st, &g)) != hipSuccess) return e;
+      OuterArgs oa{};
+      oa.A[0] = a.gT;
+      oa.B[0] = a.a[l];
+      oa.C[0] = a.dW3[l];
+      oa.R[0] = a.ref[l];
+      double* tpart = a.part + (int64_t)l * ntiles * 3;
+      FPO_LAUNCH("outer", st,
+                 outer_kernel<E><<<dim3(ntiles), dim3(256), 0, st>>>(oa, (int)a.d, (int)a.d_ff, (int)a.T,
+                                                       a.Tp, a.d_ff, a.scale, tpart));
+      FPO_CHECK_LAUNCH();
+      FPO_LAUNCH("reduce_parts", st,
+                 reduce_parts_kernel<<<dim3(1), dim3(256), 0, st>>>(
+          tpart, ntiles, l, a.sumsq, a.ref_dot ? a.ref_dot + l : nullptr,
+          a.ref_sumsq ? a.ref_sumsq + l : nullptr));
+      FPO_CHECK_LAUNCH();
+      if (a.full_mlp && (e = full_mlp_layer(l, g)) != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
+  // shared signal: token-contiguous copy once, all layers' W3 outer products
+  // (M = d, N = d_ff, K = T) in one launch
+  if ((e = layer_signal<T>(a, 0, st, &g)) != hipSuccess) return e;
   {
     OuterArgs oa{};
     for (int l = 0; l < a.L; ++l) {
@@ -344,7 +457,6 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
       oa.C[l] = a.dW3[l];
       oa.R[l] = a.ref[l];
     }
-    const int ntiles = (int)pseudograd_tiles(a.bf16, a.d, a.d_ff);
     FPO_LAUNCH("outer", st,
                outer_kernel<E><<<dim3(ntiles * a.L), dim3(256), 0, st>>>(oa, (int)a.d, (int)a.d_ff, (int)a.T,
                                                            a.Tp, a.d_ff, a.scale, a.part));
@@ -354,38 +466,9 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
                                                          a.ref_sumsq));
     FPO_CHECK_LAUNCH();
   }
-  if (a.full_mlp) {
-    const int ntiles = (int)pseudograd_tiles(a.bf16, a.d_ff, a.d);
-    for (int l = 0; l < a.L; ++l) {
-      FPO_LAUNCH("errh", st,
-                 errh_kernel<E><<<dim3((unsigned)(((a.Tp + TT::BM - 1) / TT::BM) * ((a.d_ff + TT::BN - 1) / TT::BN))), dim3(256), 0, st>>>(
-          (const T*)a.g_lp, (const T*)a.W3i[l], (const T*)a.q[l], (const T*)a.u[l], (int)a.T,
-          (int)a.Tp, (int)a.d, (int)a.d_ff, (T*)a.dq_T, (T*)a.du_T));
-      FPO_CHECK_LAUNCH();
-      OuterArgs oa{};
-      oa.A[0] = a.dq_T;
-      oa.B[0] = a.x_in[l];
-      oa.C[0] = a.dW1[l];
-      oa.A[1] = a.du_T;
-      oa.B[1] = a.x_in[l];
-      oa.C[1] = a.dW2[l];
-      FPO_LAUNCH("outer", st,
-                 outer_kernel<E><<<dim3(ntiles * 2), dim3(256), 0, st>>>(oa, (int)a.d_ff, (int)a.d, (int)a.T,
-                                                           a.Tp, a.d, a.scale, a.part));
-      FPO_CHECK_LAUNCH();
-      // matrices W1(l) and W2(l) sit at a.L + l and 2 a.L + l of sumsq
-      if (a.sumsq) {
-        FPO_LAUNCH("reduce_parts", st,
-                   reduce_parts_kernel<<<dim3(1), dim3(256), 0, st>>>(a.part, ntiles, a.L + l, a.sumsq,
-                                                           nullptr, nullptr));
-        FPO_CHECK_LAUNCH();
-        FPO_LAUNCH("reduce_parts", st,
-                   reduce_parts_kernel<<<dim3(1), dim3(256), 0, st>>>(a.part + (int64_t)ntiles * 3, ntiles,
-                                                           2 * a.L + l, a.sumsq, nullptr, nullptr));
-        FPO_CHECK_LAUNCH();
-      }
-    }
-  }
+  if (a.full_mlp)
+    for (int l = 0; l < a.L; ++l)
+      if ((e = full_mlp_layer(l, g)) != hipSuccess) return e;
   return hipSuccess;
 }
 
@@ -428,13 +511,12 @@ hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u) {
   PgOverlap& po = g_pgo[dev];
   std::lock_guard<std::mutex> lock(po.mu);
   if ((e = pg_overlap_init(po)) != hipSuccess) return e;
-  FPO_LAUNCH("transpose_pad", st,
-             transpose_pad_kernel<uint16_t><<<dim3((unsigned)(a.Tp / 64), (unsigned)((a.d + 63) / 64)), dim3(256), 0, st>>>(
-      (const uint16_t*)a.g_lp, a.T, a.d, (uint16_t*)a.gT, a.Tp, a.Tp));
-  FPO_CHECK_LAUNCH();
+  const uint16_t* g = nullptr;
   const int ntiles = (int)pseudograd_tiles(true, a.d, a.d_ff);
   int64_t blk_base = 0;
   for (int l = 0; l < a.L; ++l) {
+    // the shared signal is transposed once; a post-FFN signal per layer
+    if ((l == 0 || a.pffn) && (e = layer_signal<uint16_t>(a, l, st, &g)) != hipSuccess) return e;
     OuterArgs oa{};
     oa.A[0] = a.gT;
     oa.B[0] = a.a[l];

@@ -61,11 +61,18 @@ struct PgLaunch {
   float* dW1[kMaxMats];
   float* dW2[kMaxMats];
   const float* ref[kMaxMats];
+  // post-FFN composition: per layer, g_l = VJP(g~ fp32; mlp_out_l, gamma_l)
+  bool pffn;
+  const float* g_f32;               // [T, d]
+  const void* mlp_out[kMaxMats];    // [T, d]
+  const void* gamma_pffn[kMaxMats]; // [d]
+  float pffn_eps, pffn_min_rms;
   double* sumsq;                    // [n_mats] or null
   double* ref_dot;
   double* ref_sumsq;
   // workspace
   void* gT;                         // [d, Tp] transposed signal
+  void* g_row;                      // [T, d] per-layer signal (post-FFN composition)
   void* dq_T;                       // [d_ff, Tp] full-MLP gate error (transposed)
   void* du_T;                       // [d_ff, Tp] full-MLP up error (transposed)
   double* part;                     // per-tile partials

@@ -54,7 +54,7 @@ def test_library_exports_every_header_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert lib.fpo_abi_version() == 1
+    assert lib.fpo_abi_version() == 2 == L.ABI_VERSION
 
 
 def oe(T=128, d=256, V=4096, dtype=L.FPO_BF16, eps=1e-6, min_rms=0.5, chunk=0):
@@ -133,9 +133,9 @@ def test_pseudograd_validation(lib):
     a, ka = arr([FAKE, FAKE])
     dw, kd = arr([FAKE, FAKE])
 
-    def call(desc, A=a, dW3=dw, ref=None, ref_dot=None, opt=None, upd=None, ws_bytes=1 << 40, g=FAKE):
+    def call(desc, A=a, dW3=dw, ref=None, ref_dot=None, opt=None, upd=None, ws_bytes=1 << 40, g=FAKE, pf=None):
         return lib.fpo_pseudograd(C.byref(desc) if desc is not None else None, g, A, None, None, None, None,
-                                  dW3, None, None, None, ref, ref_dot, None, opt, upd, FAKE, ws_bytes, None)
+                                  dW3, None, None, None, ref, ref_dot, None, pf, opt, upd, FAKE, ws_bytes, None)
 
     good = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_W3, 1 / 128)
     assert call(None) == L.FPO_ERR_NULL
@@ -155,6 +155,17 @@ def test_pseudograd_validation(lib):
     assert call(good, ws_bytes=16) == L.FPO_ERR_WORKSPACE
     b, kb = arr([FAKE, None])
     assert call(good, A=b) == L.FPO_ERR_NULL
+    # post-FFN composition: g_tilde_lp may then be NULL; the composition's own buffers are required
+    mo, kmo = arr([FAKE, FAKE])
+    gm, kgm = arr([FAKE, FAKE])
+    assert call(good, g=None, pf=C.byref(L.PostFfn(FAKE, mo, gm, 1e-6, 0.5)), ws_bytes=16) == L.FPO_ERR_WORKSPACE
+    assert call(good, g=None, pf=C.byref(L.PostFfn(None, mo, gm, 1e-6, 0.5))) == L.FPO_ERR_NULL
+    assert call(good, g=None, pf=C.byref(L.PostFfn(FAKE, None, gm, 1e-6, 0.5))) == L.FPO_ERR_NULL
+    m1, km1 = arr([FAKE, None])
+    assert call(good, g=None, pf=C.byref(L.PostFfn(FAKE, mo, m1, 1e-6, 0.5))) == L.FPO_ERR_NULL
+    assert call(good, g=None, pf=C.byref(L.PostFfn(FAKE, mo, gm, -1.0, 0.5))) == L.FPO_ERR_ARG
+    assert call(good, g=None, pf=C.byref(L.PostFfn(FAKE, mo, gm, 1e-6, float("nan")))) == L.FPO_ERR_ARG
+    assert call(good, g=None, pf=C.byref(L.PostFfn(FAKE + 4, mo, gm, 1e-6, 0.5))) == L.FPO_ERR_ARG
     # bf16 operand bands (T x d_ff activations) above 2^31 bytes are refused
     assert call(L.PgDesc(1 << 17, 256, 16384, 2, L.FPO_BF16, L.FPO_MODE_W3, 1.0)) == L.FPO_ERR_UNSUPPORTED
 

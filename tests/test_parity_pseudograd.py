@@ -237,3 +237,99 @@ def test_full_size_diagnostic_rank1_reference(dev):
             assert float(ss[l]) == float(ss[k])
         del af
 
+
+def pffn_case(c, L):
+    """fp32 g~ [T, d] and each layer's (mlp_out, gamma_pffn) storage arrays."""
+    g32 = I.normal(c.cid, I.T_G, 7, c.T * c.d, std=0.02).reshape(c.T, c.d)
+    return g32, [I.post_ffn(c, l) for l in range(L)]
+
+
+def run_pffn(c, g32, pf, acts, dev, extra=None, **kw):
+    tg = torch.from_numpy(g32).to(dev)
+    mo = [dev_tensor(m, dev) for m, _ in pf]
+    gm = [dev_tensor(g, dev) for _, g in pf]
+    ta = [dev_tensor(a, dev) for a in acts]
+    dW = [torch.empty(c.d, c.d_ff, dtype=torch.float32, device=dev) for _ in acts]
+    ss = torch.empty(len(acts) * (3 if extra else 1), dtype=torch.float64, device=dev)
+    args = dict(dW3=dW, sumsq=ss, post_ffn=api.PostFfn(tg, mo, gm, c.eps, c.min_rms), **kw)
+    if extra is not None:
+        args.update(extra(dev))
+    api.fpo_pseudograd(None, ta, **args)
+    torch.cuda.synchronize()
+    return dW, ss, args
+
+
+@pytest.mark.parametrize("cid,T,d,d_ff,L", [(0, 128, 256, 688, 2), (0, 300, 264, 520, 3), (1, 300, 264, 520, 2),
+                                            (1, 1000, 512, 1032, 2)])
+def test_post_ffn_w3(dev, cid, T, d, d_ff, L):
+    """Post-feedforward RMSNorm composition (per-layer left operands, 1% of
+    tokens below the min-RMS floor) against the oracle."""
+    c = I.CONFIGS[cid].shrink(T=T, d=d, d_ff=d_ff, L=L)
+    g32, pf = pffn_case(c, L)
+    acts = [I.activation(c, l) for l in range(L)]
+    dW, ss, _ = run_pffn(c, g32, pf, acts, dev)
+    for l in range(L):
+        gl = O.post_ffn_signal(g32, pf[l][0], pf[l][1], eps=c.eps, min_rms=c.min_rms)
+        D = O.pseudograd(gl, acts[l])
+        assert_close(f"dW[{l}] (post-FFN)", host64(dW[l]), D, c.dtype)
+        assert_close(f"sumsq[{l}]", float(ss[l]), float((D * D).sum()), c.dtype)
+        # the composition matters here: skipping it is far outside the tolerance
+        assert np.linalg.norm(O.pseudograd(g32, acts[l]) - D) > 0.2 * np.linalg.norm(D)
+
+
+@pytest.mark.parametrize("cid,T,d,d_ff,L", [(0, 128, 256, 688, 2), (1, 200, 256, 520, 2)])
+def test_post_ffn_full_mlp(dev, cid, T, d, d_ff, L):
+    c = I.CONFIGS[cid].shrink(T=T, d=d, d_ff=d_ff, L=L)
+    g32, pf = pffn_case(c, L)
+    caches = [I.mlp_cache(c, l) for l in range(L)]
+    extras = [I.full_mlp_extra(c, l) for l in range(L)]
+    W3i = [I.master_weight(c, l) for l in range(L)]
+    store = {}
+
+    def extra(dev):
+        op = dev_tensor(caches[0][2], dev).dtype
+        store["dW1"] = [torch.empty(c.d_ff, c.d, dtype=torch.float32, device=dev) for _ in range(L)]
+        store["dW2"] = [torch.empty(c.d_ff, c.d, dtype=torch.float32, device=dev) for _ in range(L)]
+        return dict(W3_init=[dev_tensor(I.to_storage(w, c.dtype), dev) for w in W3i],
+                    gate=[dev_tensor(q, dev) for q, _, _ in caches], up=[dev_tensor(u, dev) for _, u, _ in caches],
+                    x_in=[dev_tensor(e[0], dev) for e in extras], dW1=store["dW1"], dW2=store["dW2"])
+
+    dW3, ss, _ = run_pffn(c, g32, pf, [a for _, _, a in caches], dev, extra=extra)
+    for l in range(L):
+        gl = O.post_ffn_signal(g32, pf[l][0], pf[l][1], eps=c.eps, min_rms=c.min_rms)
+        q, u, a = caches[l]
+        D1, D2 = O.full_mlp_grads(gl, I.to_storage(W3i[l], c.dtype), q, u, extras[l][0])
+        assert_close("dW3", host64(dW3[l]), O.pseudograd(gl, a), c.dtype)
+        assert_close("dW1", host64(store["dW1"][l]), D1, c.dtype)
+        assert_close("dW2", host64(store["dW2"][l]), D2, c.dtype)
+        assert_close("sumsq W1", float(ss[L + l]), float((D1 ** 2).sum()), c.dtype)
+
+
+@pytest.mark.slow
+def test_full_size_post_ffn_fused_update(dev):
+    """OLMo-2 shapes (the layout with a post-FFN norm) at full size, in the
+    benchmark's launch configuration with --post-ffn: the composed signal, the
+    outer products and the overlapped SGD-momentum step; sampled entries."""
+    c = I.CONFIGS[1]
+    g32, pf = pffn_case(c, c.L)
+    acts = [I.activation(c, l) for l in range(c.L)]
+    Wh = [I.master_weight(c, l) for l in range(c.L)]
+    W = [torch.from_numpy(w).to(dev) for w in Wh]
+    wsq = np.array([float((w.astype(np.float64) ** 2).sum()) for w in Wh])
+    s1 = [torch.zeros_like(w) for w in W]
+    cs = torch.empty(c.L, dtype=torch.float32, device=dev)
+    dW, ss, _ = run_pffn(c, g32, pf, acts, dev,
+                         opt=api.OptConfig(lr=c.lr, clip_frac=c.clip_frac, step=1), W_master=W,
+                         W_lp=[torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in W], state1=s1,
+                         W_sumsq=torch.tensor(wsq, dtype=torch.float64, device=dev), clip_scale=cs)
+    r = np.random.default_rng(7)
+    for l in range(c.L):
+        gl = O.post_ffn_signal(g32, pf[l][0], pf[l][1], eps=c.eps, min_rms=c.min_rms)
+        ii = np.concatenate([r.integers(0, c.d, 64), [0, c.d - 1]])
+        jj = np.concatenate([r.integers(0, c.d_ff, 64), [c.d_ff - 1, 0]])
+        D = np.einsum("ti,ti->i", gl[:, ii], I.storage_to_f64(acts[l][:, jj])) / c.T
+        assert_close(f"dW[{l}] samples", dW[l][ii, jj].cpu().numpy().astype(np.float64), D, "bf16")
+        s = min(1.0, c.clip_frac * np.sqrt(wsq[l]) / np.sqrt(float(ss[l])))
+        assert abs(float(cs[l]) - s) <= 1e-6 * s
+        assert_close(f"momentum[{l}] samples", s1[l][ii, jj].cpu().numpy().astype(np.float64), s * D, "bf16")
+

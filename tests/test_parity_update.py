@@ -136,9 +136,9 @@ def test_cosine(dev, bdtype):
 
 
 @pytest.mark.parametrize("kind", ["sgd", "adamw", "sgd-plain"])
-@pytest.mark.parametrize("T,d,d_ff,L,clip", [(256, 256, 512, 2, 0.01), (300, 264, 1000, 3, 0.01),
-                                             (200, 512, 768, 3, 1e-5)])
-def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip):
+@pytest.mark.parametrize("T,d,d_ff,L,clip,pffn", [(256, 256, 512, 2, 0.01, False), (300, 264, 1000, 3, 0.01, False),
+                                                  (200, 512, 768, 3, 1e-5, False), (300, 264, 1000, 3, 0.01, True)])
+def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip, pffn):
     """The W3 pseudogradient with the optimizer fused (bf16: one launch per
     layer carrying that layer's outer products and the previous layer's update)
     is bit-identical to the pseudogradient followed by fpo_apply_update, over two
@@ -146,6 +146,11 @@ def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip):
     clip (clip_frac 1e-5)."""
     c = I.CONFIGS[1].shrink(T=T, d=d, d_ff=d_ff, L=L)
     g = dev_tensor(I.synthetic_signal(c), dev)
+    kw = {}
+    if pffn:  # per-layer post-FFN composition on both paths
+        g32 = torch.from_numpy(I.normal(c.cid, I.T_G, 7, T * d, std=0.02).reshape(T, d)).to(dev)
+        pfs = [I.post_ffn(c, l) for l in range(L)]
+        kw = dict(post_ffn=api.PostFfn(g32, [dev_tensor(m, dev) for m, _ in pfs], [dev_tensor(x, dev) for _, x in pfs]))
     acts = [dev_tensor(I.activation(c, l), dev) for l in range(L)]
     W0 = [torch.from_numpy(I.master_weight(c, l)).to(dev) for l in range(L)]
     adam = kind == "adamw"
@@ -165,11 +170,11 @@ def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip):
     for step in (1, 2):
         opt = api.OptConfig(kind=L_.FPO_OPT_ADAMW if adam else L_.FPO_OPT_SGD, lr=1e-2, clip_frac=clip, step=step,
                             momentum=0.0 if plain else 0.9)
-        api.fpo_pseudograd(g, acts, dW3=sep["dW"], sumsq=sep["ss"])
+        api.fpo_pseudograd(g, acts, dW3=sep["dW"], sumsq=sep["ss"], **kw)
         api.fpo_apply_update(opt, sep["dW"], sep["ss"], sep["W"], sep["s1"], sep["Wsq"], W_lp=sep["lp"],
                              state2=sep["s2"], clip_scale=sep["cs"])
         api.fpo_pseudograd(g, acts, dW3=fus["dW"], sumsq=fus["ss"], opt=opt, W_master=fus["W"], W_lp=fus["lp"],
-                           state1=fus["s1"], state2=fus["s2"], W_sumsq=fus["Wsq"], clip_scale=fus["cs"])
+                           state1=fus["s1"], state2=fus["s2"], W_sumsq=fus["Wsq"], clip_scale=fus["cs"], **kw)
         torch.cuda.synchronize()
         for key in ("W", "lp", "dW") + (("s2",) if adam else ()) + (() if plain else ("s1",)):
             for a, b in zip(sep[key], fus[key]):
