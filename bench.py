@@ -143,11 +143,12 @@ def kernel_work(name, c, steps, nchunk, opt="sgd-momentum", pffn=False):
         return 4.0 * T * V * steps, "byte", "hbm"  # staged p~ read + write (bf16)
     if name == "rms_forward":
         return (4.0 * T * d) * steps, "byte", "hbm"  # x read, y written (bf16)
-    if name == "pffn_vjp":
-        # per layer: g~ fp32 read, MLP output read, composed signal written (bf16)
-        return (8.0 * T * d * L) * steps, "byte", "hbm"
-    if name == "transpose_pad":  # signal read, token-contiguous copy written (bf16); per layer with post-FFN
-        return (4.0 * T * d * (L if pffn else 1)) * steps, "byte", "hbm"
+    if name == "pffn_stats":  # per layer: g~ fp32 and MLP output read
+        return (6.0 * T * d * L) * steps, "byte", "hbm"
+    if name == "signal_transpose":
+        # shared signal: read + token-contiguous copy written (bf16); post-FFN, per layer:
+        # g~ fp32 and MLP output read, composed signal written
+        return ((8.0 * T * d * L) if pffn else (4.0 * T * d)) * steps, "byte", "hbm"
     if name == "finalize_vjp":
         return (T * d * (4 + 2 + 2 + 4 + 2)) * steps, "byte", "hbm"
     return None
@@ -260,7 +261,8 @@ def main():
     dW = [torch.empty(d, c.d_ff, dtype=torch.float32, device=dev) for _ in range(c.L)]
     ss = torch.empty(c.L, dtype=torch.float64, device=dev)
     ws_oe = api.workspace(api.fpo_output_error_workspace(T, d, c.V, torch.bfloat16, args.vocab_chunk), dev)
-    ws_pg = api.workspace(api.fpo_pseudograd_workspace(T, d, c.d_ff, c.L, torch.bfloat16), dev)
+    ws_pg = api.workspace(api.fpo_pseudograd_workspace(T, d, c.d_ff, c.L, torch.bfloat16,
+                                                       post_ffn=args.post_ffn), dev)
     if args.post_ffn:
         pffn = api.PostFfn(g_t, pffn_mo, pffn_g, c.eps, c.min_rms)
     torch.cuda.synchronize()

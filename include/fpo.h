@@ -64,7 +64,7 @@ typedef enum {
 } fpo_status;
 
 typedef enum { FPO_F32 = 0, FPO_BF16 = 1 } fpo_dtype;
-typedef enum { FPO_MODE_W3 = 0, FPO_MODE_FULL_MLP = 1 } fpo_mode;
+typedef enum { FPO_MODE_W3 = 0, FPO_MODE_FULL_MLP = 1, FPO_MODE_POST_FFN = 2 } fpo_mode; /* bit flags */
 typedef enum { FPO_OPT_SGD = 0, FPO_OPT_ADAMW = 1 } fpo_opt_kind;
 
 /* Output-error call description.
@@ -83,9 +83,11 @@ typedef struct {
 
 /* Pseudogradient call description.
  *   L      number of target layers in this call (<= 64)
- *   mode   FPO_MODE_W3: down projection only; FPO_MODE_FULL_MLP: also the
- *          gate (W1) and up (W2) signals through the fixed feedback W3_init
- *          (eq. errh)
+ *   mode   FPO_MODE_W3 (0): down projection only; FPO_MODE_FULL_MLP (bit 0):
+ *          also the gate (W1) and up (W2) signals through the fixed feedback
+ *          W3_init (eq. errh); FPO_MODE_POST_FFN (bit 1): compose each layer's
+ *          post-FFN RMSNorm VJP (the call's post_ffn argument is then
+ *          required; the workspace holds every layer's composed signal)
  *   scale  multiplier of the token sum; the paper divides by the token count
  *          (App. A pseudocode), so callers pass 1/T */
 typedef struct {
@@ -214,8 +216,9 @@ typedef struct {
  *              nullable (layer-viability diagnostic, eq. cosine)
  *   ref_dot, ref_sumsq  double [L] out (required when ref is given):
  *              <dW3_l, R_l> and ||R_l||_F^2
- *   post_ffn   nullable: compose each layer's post-FFN norm VJP (see
- *              fpo_post_ffn); g_tilde_lp is then unused and may be NULL
+ *   post_ffn   required iff desc->mode has FPO_MODE_POST_FFN: compose each
+ *              layer's post-FFN norm VJP (see fpo_post_ffn); g_tilde_lp is
+ *              then unused and may be NULL
  *   opt, upd   both NULL, or both given: the call then also applies
  *              fpo_apply_update to the matrices in `sumsq` order, with the
  *              same result bit for bit as calling it separately

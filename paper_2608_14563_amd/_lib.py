@@ -13,7 +13,7 @@ LIB_PATH = os.path.join(_HERE, "libfpo.so")
 
 FPO_OK, FPO_ERR_NULL, FPO_ERR_SHAPE, FPO_ERR_DTYPE, FPO_ERR_ARG, FPO_ERR_WORKSPACE, FPO_ERR_UNSUPPORTED, FPO_ERR_HIP = range(8)
 FPO_F32, FPO_BF16 = 0, 1
-FPO_MODE_W3, FPO_MODE_FULL_MLP = 0, 1
+FPO_MODE_W3, FPO_MODE_FULL_MLP, FPO_MODE_POST_FFN = 0, 1, 2  # bit flags
 FPO_OPT_SGD, FPO_OPT_ADAMW = 0, 1
 
 STATUS_NAMES = {0: "FPO_OK", 1: "FPO_ERR_NULL", 2: "FPO_ERR_SHAPE", 3: "FPO_ERR_DTYPE", 4: "FPO_ERR_ARG",

@@ -130,8 +130,12 @@ def _upd_bufs(keep: _Keep, W_master, W_lp, state1, state2, W_sumsq, clip_scale, 
 
 
 # --------------------------------------------------------------------- pseudograd
-def fpo_pseudograd_workspace(T, d, d_ff, Lyr, dtype: torch.dtype, full_mlp=False) -> int:
-    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(dtype), L.FPO_MODE_FULL_MLP if full_mlp else L.FPO_MODE_W3, 1.0)
+def _mode(full_mlp: bool, post_ffn: bool) -> int:
+    return (L.FPO_MODE_FULL_MLP if full_mlp else L.FPO_MODE_W3) | (L.FPO_MODE_POST_FFN if post_ffn else 0)
+
+
+def fpo_pseudograd_workspace(T, d, d_ff, Lyr, dtype: torch.dtype, full_mlp=False, post_ffn=False) -> int:
+    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(dtype), _mode(full_mlp, post_ffn), 1.0)
     return L.load().fpo_pseudograd_workspace(C.byref(desc))
 
 
@@ -160,8 +164,7 @@ def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, 
     Lyr = len(a)
     d_ff = a[0].shape[1]
     full = W3_init is not None
-    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(op),
-                    L.FPO_MODE_FULL_MLP if full else L.FPO_MODE_W3,
+    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(op), _mode(full, post_ffn is not None),
                     (1.0 / T) if scale is None else scale)
     lib = L.load()
     if ws is None:

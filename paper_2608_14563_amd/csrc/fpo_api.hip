@@ -154,7 +154,7 @@ PgPlan plan_pg(const fpo_pg_desc& d) {
   const bool bf16 = d.dtype == FPO_BF16;
   p.Tp = round_up(d.T, 64);
   p.ntiles = fpo::pseudograd_tiles(bf16, d.d, d.d_ff);
-  const bool full = d.mode == FPO_MODE_FULL_MLP;
+  const bool full = (d.mode & FPO_MODE_FULL_MLP) != 0;
   p.nmats = (int)(full ? 3 * d.L : d.L);
   p.upd_blocks = p.nmats * fpo::update_blocks(d.d * d.d_ff);
   return p;
@@ -163,10 +163,14 @@ PgPlan plan_pg(const fpo_pg_desc& d) {
 size_t carve_pg(const fpo_pg_desc& d, const PgPlan& p, void* ws, fpo::PgLaunch* L,
                 double** upd_part) {
   const int64_t esz = d.dtype == FPO_BF16 ? 2 : 4;
-  const bool full = d.mode == FPO_MODE_FULL_MLP;
+  const bool full = (d.mode & FPO_MODE_FULL_MLP) != 0;
+  const bool pffn = (d.mode & FPO_MODE_POST_FFN) != 0;
   Carver c(ws);
-  void* gT = c.take<char>(d.d * p.Tp * esz);
-  void* grow = c.take<char>(d.T * d.d * esz);  // per-layer signal (post-FFN composition)
+  // token-contiguous left operand(s): shared, or one per layer (post-FFN)
+  void* gT = c.take<char>((pffn ? d.L : 1) * d.d * p.Tp * esz);
+  // post-FFN + full-MLP: each layer's signal row-major too (error GEMM operand)
+  void* grow = (pffn && full) ? c.take<char>(d.L * d.T * d.d * esz) : nullptr;
+  float* pstats = pffn ? c.take<float>(2 * d.T) : nullptr;  // per-token norm statistics
   void* dq = full ? c.take<char>(d.d_ff * p.Tp * esz) : nullptr;
   void* du = full ? c.take<char>(d.d_ff * p.Tp * esz) : nullptr;
   double* part = c.take<double>(std::max<int64_t>(d.L, 2) * p.ntiles * 3);
@@ -174,6 +178,7 @@ size_t carve_pg(const fpo_pg_desc& d, const PgPlan& p, void* ws, fpo::PgLaunch* 
   if (L) {
     L->gT = gT;
     L->g_row = grow;
+    L->pffn_stats = pstats;
     L->dq_T = dq;
     L->du_T = du;
     L->part = part;
@@ -186,7 +191,7 @@ int check_pg_desc(const fpo_pg_desc* d) {
   if (!d) return fail(FPO_ERR_NULL, "fpo_pseudograd: desc is NULL");
   if (d->dtype != FPO_F32 && d->dtype != FPO_BF16)
     return fail(FPO_ERR_DTYPE, "fpo_pseudograd: unknown dtype %d", (int)d->dtype);
-  if (d->mode != FPO_MODE_W3 && d->mode != FPO_MODE_FULL_MLP)
+  if (d->mode < 0 || d->mode > (FPO_MODE_FULL_MLP | FPO_MODE_POST_FFN))
     return fail(FPO_ERR_ARG, "fpo_pseudograd: unknown mode %d", (int)d->mode);
   if (d->T <= 0 || d->d <= 0 || d->d_ff <= 0 || d->L <= 0 || d->T > kIntMax || d->d > kIntMax ||
       d->d_ff > kIntMax)
@@ -202,7 +207,7 @@ int check_pg_desc(const fpo_pg_desc* d) {
     // operand bands copied through 32-bit buffer offsets must fit in 2^31 bytes
     const int64_t Tp = round_up(d->T, 64);
     bool ok = band_fits(d->d, Tp) && band_fits(d->T, d->d_ff);
-    if (d->mode == FPO_MODE_FULL_MLP)
+    if (d->mode & FPO_MODE_FULL_MLP)
       ok = ok && band_fits(d->T, d->d) && band_fits(d->d, d->d_ff) && band_fits(d->d_ff, Tp);
     if (!ok)
       return fail(FPO_ERR_UNSUPPORTED,
@@ -360,9 +365,12 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
                    const fpo_post_ffn* post_ffn, const fpo_opt* opt, const fpo_update_bufs* upd,
                    void* ws, size_t ws_bytes, void* stream) {
   if (int e = check_pg_desc(desc)) return e;
-  const bool full = desc->mode == FPO_MODE_FULL_MLP;
+  const bool full = (desc->mode & FPO_MODE_FULL_MLP) != 0;
+  const bool pffn = (desc->mode & FPO_MODE_POST_FFN) != 0;
   const int L = (int)desc->L;
   if (!a) return fail(FPO_ERR_NULL, "fpo_pseudograd: a is required");
+  if (pffn != (post_ffn != nullptr))
+    return fail(FPO_ERR_ARG, "fpo_pseudograd: post_ffn must be given exactly when mode has FPO_MODE_POST_FFN");
   if (!g_tilde_lp && !post_ffn)
     return fail(FPO_ERR_NULL, "fpo_pseudograd: g_tilde_lp is required (unless post_ffn is given)");
   if (post_ffn) {

@@ -1,7 +1,9 @@
 // Per-layer outer products (eq. w3update; App. A divisor) and the full-MLP
 // feedback path (eq. errh):
-//   transpose_pad : g~ [T, d] -> g~^T [d, Tp] (zero columns t >= T) so that the
-//                   token axis, the contraction axis, is contiguous
+//   signal_transpose : g~ [T, d] -> g~^T [d, Tp] (zero columns t >= T) so that
+//                   the token axis, the contraction axis, is contiguous; with
+//                   the post-FFN composition it forms each layer's signal
+//                   (pffn_stats: its per-token norm statistics) on the way
 //   outer_kernel  : C_m = scale * A_m B_m for a list of matrices (MFMA),
 //                   A_m [M, Tp] token-contiguous, B_m [T, N] row-major; epilogue
 //                   writes C and per-tile ||C||^2 (and <C, R>, ||R||^2)
@@ -20,36 +22,15 @@
 
 namespace fpo {
 
+// Per-token statistics of the post-FFN norm composition (one workgroup per
+// token): irt = 1 / max(sqrt(mean x^2 + eps), min_rms) and
+// c = (1/d) <x * irt, gamma * g>, with x the cached MLP output, gamma the
+// layer's post-FFN gain and g the fp32 signal g~.
 template <typename T>
-__global__ __launch_bounds__(256) void transpose_pad_kernel(const T* __restrict__ src, int64_t R,
-                                                            int64_t C, T* __restrict__ dst,
-                                                            int64_t ldd, int64_t Rp) {
-  // src [R, C] -> dst [C, ldd] with dst[c, r] = src[r, c] for r < R, 0 for R <= r < Rp
-  __shared__ float tile[64][65];
-  const int64_t r0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64;
-  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-    const int rr = e / 64, cc = e % 64;
-    const int64_t r = r0 + rr, c = c0 + cc;
-    tile[rr][cc] = (r < R && c < C) ? ld_as_f32(src, r * C + c) : 0.f;
-  }
-  __syncthreads();
-  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-    const int cc = e / 64, rr = e % 64;
-    const int64_t r = r0 + rr, c = c0 + cc;
-    if (c < C && r < Rp) st_from_f32(dst, c * ldd + r, tile[rr][cc]);
-  }
-}
-
-// Post-FFN norm composition: one workgroup per token,
-//   rho~ = max(sqrt(mean x^2 + eps), min_rms); x^ = x / rho~;
-//   c = (1/d) <x^, gamma * g>;  out = (gamma * g - c x^) / rho~
-// with x the cached MLP output, gamma the layer's post-FFN gain and g the fp32
-// signal g~; out in the operand dtype (the layer's left operand).
-template <typename T>
-__global__ __launch_bounds__(256) void pffn_vjp_kernel(int d, const float* __restrict__ g,
-                                                       const T* __restrict__ x,
-                                                       const T* __restrict__ gamma, float eps,
-                                                       float min_rms, T* __restrict__ out) {
+__global__ __launch_bounds__(256) void pffn_stats_kernel(int d, const float* __restrict__ g,
+                                                         const T* __restrict__ x,
+                                                         const T* __restrict__ gamma, float eps,
+                                                         float min_rms, float2* __restrict__ stats) {
   __shared__ float red[16];
   const int64_t row = blockIdx.x;
   const float* gr = g + row * d;
@@ -62,17 +43,58 @@ __global__ __launch_bounds__(256) void pffn_vjp_kernel(int d, const float* __res
   }
   ss = block_sum(ss, red);
   cd = block_sum(cd, red);
-  const float rt = fmaxf(sqrtf(ss / (float)d + eps), min_rms);
-  const float irt = 1.0f / rt;
-  const float c = cd * irt / (float)d;  // (1/d) <x / rho~, gamma * g>
-  for (int k = threadIdx.x * 4; k < d; k += 1024) {
-    const f32x4 xv = ld4(xr, k), gm = ld4(gamma, k), gv = *reinterpret_cast<const f32x4*>(gr + k);
-    f32x4 o;
-    o.x = (gm.x * gv.x - c * xv.x * irt) * irt;
-    o.y = (gm.y * gv.y - c * xv.y * irt) * irt;
-    o.z = (gm.z * gv.z - c * xv.z * irt) * irt;
-    o.w = (gm.w * gv.w - c * xv.w * irt) * irt;
-    st4(out + row * d, k, o);
+  if (threadIdx.x == 0) {
+    const float irt = 1.0f / fmaxf(sqrtf(ss / (float)d + eps), min_rms);
+    stats[row] = float2{irt, cd * irt / (float)d};
+  }
+}
+
+// The token-contiguous copy of a layer's left operand: dst [C, ldd] with
+// dst[c, r] = v(r, c) for r < R and 0 for R <= r < Rp, where v is src[r, c]
+// (shared signal) or, for the post-FFN composition, the clamped VJP
+//   v = (gamma_c g[r, c] - c_r x[r, c] irt_r) irt_r
+// in the operand dtype (also stored row-major to row_out when given). 64 x 64
+// tiles through LDS, 16-byte loads and 8- / 16-byte stores.
+template <typename T, bool PFFN>
+__global__ __launch_bounds__(256) void signal_transpose_kernel(
+    const void* __restrict__ src, const T* __restrict__ x, const T* __restrict__ gamma,
+    const float2* __restrict__ stats, int64_t R, int64_t C, T* __restrict__ dst, int64_t ldd,
+    int64_t Rp, T* __restrict__ row_out) {
+  __shared__ float tile[64][65];
+  const int64_t r0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64;
+  // 64 rows x 16 column quads
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int q = threadIdx.x + 256 * k, rr = q >> 4, cq = (q & 15) * 4;
+    const int64_t r = r0 + rr, c = c0 + cq;
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    if (r < R && c < C) {  // C % 8 == 0: a quad is all in or all out
+      if constexpr (PFFN) {
+        const f32x4 gv = *reinterpret_cast<const f32x4*>((const float*)src + r * C + c);
+        const f32x4 xv = ld4(x, r * C + c), gm = ld4(gamma, c);
+        const float2 st = stats[r];
+        v.x = (gm.x * gv.x - st.y * xv.x * st.x) * st.x;
+        v.y = (gm.y * gv.y - st.y * xv.y * st.x) * st.x;
+        v.z = (gm.z * gv.z - st.y * xv.z * st.x) * st.x;
+        v.w = (gm.w * gv.w - st.y * xv.w * st.x) * st.x;
+        if (row_out) st4(row_out, r * C + c, v);
+      } else {
+        v = ld4((const T*)src, r * C + c);
+      }
+    }
+    tile[rr][cq] = v.x;
+    tile[rr][cq + 1] = v.y;
+    tile[rr][cq + 2] = v.z;
+    tile[rr][cq + 3] = v.w;
+  }
+  __syncthreads();
+  // 64 columns x 16 row quads
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int q = threadIdx.x + 256 * k, cc = q >> 4, rq = (q & 15) * 4;
+    const int64_t r = r0 + rq, c = c0 + cc;
+    if (c < C && r < Rp)  // Rp % 64 == 0
+      st4(dst, c * ldd + r, f32x4{tile[rq][cc], tile[rq + 1][cc], tile[rq + 2][cc], tile[rq + 3][cc]});
   }
 }
 
@@ -361,26 +383,44 @@ int64_t pseudograd_tiles(bool bf16, int64_t M, int64_t N) {
     if (e_ != hipSuccess) return e_;   \
   } while (0)
 
-// The left operand of layer l: the shared signal, or (post-FFN composition)
-// layer l's VJP of g~ into a.g_row. Leaves its token-contiguous copy in a.gT
-// and returns the row-major one (the full-MLP error GEMM's left operand).
+// Left operands of every layer, formed before any outer product (while HBM is
+// otherwise idle): the shared signal's token-contiguous copy in a.gT, or, with
+// the post-FFN composition, each layer's composed signal in a.gT + l * d * Tp
+// (and row-major in a.g_row + l * T * d for the full-MLP error GEMM).
 template <typename T>
-static hipError_t layer_signal(const PgLaunch& a, int l, hipStream_t st, const T** g_rowmajor) {
-  const T* g = (const T*)a.g_lp;
-  if (a.pffn) {
-    FPO_LAUNCH("pffn_vjp", st,
-               pffn_vjp_kernel<T><<<dim3((unsigned)a.T), dim3(256), 0, st>>>(
-        (int)a.d, a.g_f32, (const T*)a.mlp_out[l], (const T*)a.gamma_pffn[l], a.pffn_eps, a.pffn_min_rms,
-        (T*)a.g_row));
+static hipError_t prepare_signals(const PgLaunch& a, hipStream_t st) {
+  const dim3 grid((unsigned)(a.Tp / 64), (unsigned)((a.d + 63) / 64));
+  if (!a.pffn) {
+    FPO_LAUNCH("signal_transpose", st,
+               signal_transpose_kernel<T, false><<<grid, dim3(256), 0, st>>>(
+        a.g_lp, nullptr, nullptr, nullptr, a.T, a.d, (T*)a.gT, a.Tp, a.Tp, nullptr));
     FPO_CHECK_LAUNCH();
-    g = (const T*)a.g_row;
+    return hipSuccess;
   }
-  FPO_LAUNCH("transpose_pad", st,
-             transpose_pad_kernel<T><<<dim3((unsigned)(a.Tp / 64), (unsigned)((a.d + 63) / 64)), dim3(256), 0, st>>>(
-      g, a.T, a.d, (T*)a.gT, a.Tp, a.Tp));
-  FPO_CHECK_LAUNCH();
-  *g_rowmajor = g;
+  for (int l = 0; l < a.L; ++l) {
+    FPO_LAUNCH("pffn_stats", st,
+               pffn_stats_kernel<T><<<dim3((unsigned)a.T), dim3(256), 0, st>>>(
+        (int)a.d, a.g_f32, (const T*)a.mlp_out[l], (const T*)a.gamma_pffn[l], a.pffn_eps, a.pffn_min_rms,
+        (float2*)a.pffn_stats));
+    FPO_CHECK_LAUNCH();
+    T* row = a.full_mlp ? (T*)a.g_row + (int64_t)l * a.T * a.d : nullptr;
+    FPO_LAUNCH("signal_transpose", st,
+               signal_transpose_kernel<T, true><<<grid, dim3(256), 0, st>>>(
+        a.g_f32, (const T*)a.mlp_out[l], (const T*)a.gamma_pffn[l], (const float2*)a.pffn_stats, a.T, a.d,
+        (T*)a.gT + (int64_t)l * a.d * a.Tp, a.Tp, a.Tp, row));
+    FPO_CHECK_LAUNCH();
+  }
   return hipSuccess;
+}
+
+// Layer l's token-contiguous left operand [d, Tp] and its row-major form [T, d].
+template <typename T>
+static const T* signal_T(const PgLaunch& a, int l) {
+  return (const T*)a.gT + (a.pffn ? (int64_t)l * a.d * a.Tp : 0);
+}
+template <typename T>
+static const T* signal_rows(const PgLaunch& a, int l) {
+  return a.pffn ? (const T*)a.g_row + (int64_t)l * a.T * a.d : (const T*)a.g_lp;
 }
 
 template <class E>
@@ -391,13 +431,32 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
   const int ntiles = (int)pseudograd_tiles(a.bf16, a.d, a.d_ff);
   const int ntiles2 = (int)pseudograd_tiles(a.bf16, a.d_ff, a.d);
   hipError_t e;
-  const T* g = nullptr;
-  // one layer's W1/W2 signals through W3_init (eq. errh) from the row-major signal g
-  auto full_mlp_layer = [&](int l, const T* gl) -> hipError_t {
+  if ((e = prepare_signals<T>(a, st)) != hipSuccess) return e;
+  // W3 outer products of every layer (M = d, N = d_ff, K = T) in one launch
+  {
+    OuterArgs oa{};
+    for (int l = 0; l < a.L; ++l) {
+      oa.A[l] = signal_T<T>(a, l);
+      oa.B[l] = a.a[l];
+      oa.C[l] = a.dW3[l];
+      oa.R[l] = a.ref[l];
+    }
+    FPO_LAUNCH("outer", st,
+               outer_kernel<E><<<dim3(ntiles * a.L), dim3(256), 0, st>>>(oa, (int)a.d, (int)a.d_ff, (int)a.T,
+                                                           a.Tp, a.d_ff, a.scale, a.part));
+    FPO_CHECK_LAUNCH();
+    FPO_LAUNCH("reduce_parts", st,
+               reduce_parts_kernel<<<dim3(a.L), dim3(256), 0, st>>>(a.part, ntiles, 0, a.sumsq, a.ref_dot,
+                                                         a.ref_sumsq));
+    FPO_CHECK_LAUNCH();
+  }
+  if (!a.full_mlp) return hipSuccess;
+  // W1/W2 signals through W3_init (eq. errh), one layer at a time
+  for (int l = 0; l < a.L; ++l) {
     FPO_LAUNCH("errh", st,
                errh_kernel<E><<<dim3((unsigned)(((a.Tp + TT::BM - 1) / TT::BM) * ((a.d_ff + TT::BN - 1) / TT::BN))), dim3(256), 0, st>>>(
-        gl, (const T*)a.W3i[l], (const T*)a.q[l], (const T*)a.u[l], (int)a.T, (int)a.Tp, (int)a.d,
-        (int)a.d_ff, (T*)a.dq_T, (T*)a.du_T));
+        signal_rows<T>(a, l), (const T*)a.W3i[l], (const T*)a.q[l], (const T*)a.u[l], (int)a.T, (int)a.Tp,
+        (int)a.d, (int)a.d_ff, (T*)a.dq_T, (T*)a.du_T));
     FPO_CHECK_LAUNCH();
     OuterArgs oa{};
     oa.A[0] = a.dq_T;
@@ -421,54 +480,7 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
                                                          2 * a.L + l, a.sumsq, nullptr, nullptr));
       FPO_CHECK_LAUNCH();
     }
-    return hipSuccess;
-  };
-  if (a.pffn) {
-    // post-FFN composition: every layer has its own left operand
-    for (int l = 0; l < a.L; ++l) {
-      if ((e = layer_signal<T>(a, l, st, &g)) != hipSuccess) return e;
-      OuterArgs oa{};
-      oa.A[0] = a.gT;
-      oa.B[0] = a.a[l];
-      oa.C[0] = a.dW3[l];
-      oa.R[0] = a.ref[l];
-      double* tpart = a.part + (int64_t)l * ntiles * 3;
-      FPO_LAUNCH("outer", st,
-                 outer_kernel<E><<<dim3(ntiles), dim3(256), 0, st>>>(oa, (int)a.d, (int)a.d_ff, (int)a.T,
-                                                       a.Tp, a.d_ff, a.scale, tpart));
-      FPO_CHECK_LAUNCH();
-      FPO_LAUNCH("reduce_parts", st,
-                 reduce_parts_kernel<<<dim3(1), dim3(256), 0, st>>>(
-          tpart, ntiles, l, a.sumsq, a.ref_dot ? a.ref_dot + l : nullptr,
-          a.ref_sumsq ? a.ref_sumsq + l : nullptr));
-      FPO_CHECK_LAUNCH();
-      if (a.full_mlp && (e = full_mlp_layer(l, g)) != hipSuccess) return e;
-    }
-    return hipSuccess;
   }
-  // shared signal: token-contiguous copy once, all layers' W3 outer products
-  // (M = d, N = d_ff, K = T) in one launch
-  if ((e = layer_signal<T>(a, 0, st, &g)) != hipSuccess) return e;
-  {
-    OuterArgs oa{};
-    for (int l = 0; l < a.L; ++l) {
-      oa.A[l] = a.gT;
-      oa.B[l] = a.a[l];
-      oa.C[l] = a.dW3[l];
-      oa.R[l] = a.ref[l];
-    }
-    FPO_LAUNCH("outer", st,
-               outer_kernel<E><<<dim3(ntiles * a.L), dim3(256), 0, st>>>(oa, (int)a.d, (int)a.d_ff, (int)a.T,
-                                                           a.Tp, a.d_ff, a.scale, a.part));
-    FPO_CHECK_LAUNCH();
-    FPO_LAUNCH("reduce_parts", st,
-               reduce_parts_kernel<<<dim3(a.L), dim3(256), 0, st>>>(a.part, ntiles, 0, a.sumsq, a.ref_dot,
-                                                         a.ref_sumsq));
-    FPO_CHECK_LAUNCH();
-  }
-  if (a.full_mlp)
-    for (int l = 0; l < a.L; ++l)
-      if ((e = full_mlp_layer(l, g)) != hipSuccess) return e;
   return hipSuccess;
 }
 
@@ -511,14 +523,12 @@ hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u) {
   PgOverlap& po = g_pgo[dev];
   std::lock_guard<std::mutex> lock(po.mu);
   if ((e = pg_overlap_init(po)) != hipSuccess) return e;
-  const uint16_t* g = nullptr;
+  if ((e = prepare_signals<uint16_t>(a, st)) != hipSuccess) return e;
   const int ntiles = (int)pseudograd_tiles(true, a.d, a.d_ff);
   int64_t blk_base = 0;
   for (int l = 0; l < a.L; ++l) {
-    // the shared signal is transposed once; a post-FFN signal per layer
-    if ((l == 0 || a.pffn) && (e = layer_signal<uint16_t>(a, l, st, &g)) != hipSuccess) return e;
     OuterArgs oa{};
-    oa.A[0] = a.gT;
+    oa.A[0] = signal_T<uint16_t>(a, l);
     oa.B[0] = a.a[l];
     oa.C[0] = a.dW3[l];
     oa.R[0] = a.ref[l];

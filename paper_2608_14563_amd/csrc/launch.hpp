@@ -72,7 +72,8 @@ struct PgLaunch {
   double* ref_sumsq;
   // workspace
   void* gT;                         // [d, Tp] transposed signal
-  void* g_row;                      // [T, d] per-layer signal (post-FFN composition)
+  void* g_row;                      // [T, d] per-layer signal (post-FFN composition, full-MLP)
+  float* pffn_stats;                // [T, 2] its per-token norm statistics
   void* dq_T;                       // [d_ff, Tp] full-MLP gate error (transposed)
   void* du_T;                       // [d_ff, Tp] full-MLP up error (transposed)
   double* part;                     // per-tile partials

@@ -155,17 +155,26 @@ def test_pseudograd_validation(lib):
     assert call(good, ws_bytes=16) == L.FPO_ERR_WORKSPACE
     b, kb = arr([FAKE, None])
     assert call(good, A=b) == L.FPO_ERR_NULL
-    # post-FFN composition: g_tilde_lp may then be NULL; the composition's own buffers are required
+    # post-FFN composition (mode flag + argument): g_tilde_lp may then be NULL
     mo, kmo = arr([FAKE, FAKE])
     gm, kgm = arr([FAKE, FAKE])
-    assert call(good, g=None, pf=C.byref(L.PostFfn(FAKE, mo, gm, 1e-6, 0.5)), ws_bytes=16) == L.FPO_ERR_WORKSPACE
-    assert call(good, g=None, pf=C.byref(L.PostFfn(None, mo, gm, 1e-6, 0.5))) == L.FPO_ERR_NULL
-    assert call(good, g=None, pf=C.byref(L.PostFfn(FAKE, None, gm, 1e-6, 0.5))) == L.FPO_ERR_NULL
+    pmode = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_POST_FFN, 1 / 128)
+    pf = C.byref(L.PostFfn(FAKE, mo, gm, 1e-6, 0.5))
+    assert call(pmode, g=None, pf=pf, ws_bytes=16) == L.FPO_ERR_WORKSPACE
+    assert call(pmode, g=None) == L.FPO_ERR_ARG          # mode without the argument
+    assert call(good, pf=pf) == L.FPO_ERR_ARG            # argument without the mode
+    assert call(L.PgDesc(128, 256, 688, 2, 1, 4, 1.0)) == L.FPO_ERR_ARG  # unknown mode bit
+    assert call(pmode, g=None, pf=C.byref(L.PostFfn(None, mo, gm, 1e-6, 0.5))) == L.FPO_ERR_NULL
+    assert call(pmode, g=None, pf=C.byref(L.PostFfn(FAKE, None, gm, 1e-6, 0.5))) == L.FPO_ERR_NULL
     m1, km1 = arr([FAKE, None])
-    assert call(good, g=None, pf=C.byref(L.PostFfn(FAKE, mo, m1, 1e-6, 0.5))) == L.FPO_ERR_NULL
-    assert call(good, g=None, pf=C.byref(L.PostFfn(FAKE, mo, gm, -1.0, 0.5))) == L.FPO_ERR_ARG
-    assert call(good, g=None, pf=C.byref(L.PostFfn(FAKE, mo, gm, 1e-6, float("nan")))) == L.FPO_ERR_ARG
-    assert call(good, g=None, pf=C.byref(L.PostFfn(FAKE + 4, mo, gm, 1e-6, 0.5))) == L.FPO_ERR_ARG
+    assert call(pmode, g=None, pf=C.byref(L.PostFfn(FAKE, mo, m1, 1e-6, 0.5))) == L.FPO_ERR_NULL
+    assert call(pmode, g=None, pf=C.byref(L.PostFfn(FAKE, mo, gm, -1.0, 0.5))) == L.FPO_ERR_ARG
+    assert call(pmode, g=None, pf=C.byref(L.PostFfn(FAKE, mo, gm, 1e-6, float("nan")))) == L.FPO_ERR_ARG
+    assert call(pmode, g=None, pf=C.byref(L.PostFfn(FAKE + 4, mo, gm, 1e-6, 0.5))) == L.FPO_ERR_ARG
+    # the workspace holds every layer's composed signal
+    w0 = lib.fpo_pseudograd_workspace(C.byref(good))
+    w1 = lib.fpo_pseudograd_workspace(C.byref(pmode))
+    assert w1 >= w0 + (2 - 1) * 256 * 128 * 2
     # bf16 operand bands (T x d_ff activations) above 2^31 bytes are refused
     assert call(L.PgDesc(1 << 17, 256, 16384, 2, L.FPO_BF16, L.FPO_MODE_W3, 1.0)) == L.FPO_ERR_UNSUPPORTED
 
