@@ -46,7 +46,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--vocab-chunk", type=int, default=0,
                     help="vocabulary chunk width (0: the library's planner)")
-    ap.add_argument("--cpu-tokens", type=int, default=1024, help="tokens in the oracle's timed sample")
+    ap.add_argument("--cpu-tokens", type=int, default=0,
+                    help="tokens in the oracle's timed sample (0: the whole step)")
     ap.add_argument("--post-ffn", action="store_true",
                     help="compose each target layer's post-FFN RMSNorm VJP (OLMo-2 / Gemma 3 layout)")
     ap.add_argument("--optimizer", choices=sorted(OPT_BYTES), default="sgd-momentum",
@@ -154,10 +155,11 @@ def kernel_work(name, c, steps, nchunk, opt="sgd-momentum", pffn=False):
     return None
 
 
-def cpu_baseline(c, tokens, x, gam, W_U, y, acts, W0):
-    """The oracle, timed on a bounded sample of the same workload: the first
-    `tokens` tokens through the output error and every layer's outer product,
-    plus the optimizer step of one layer; scaled to the full step."""
+def cpu_baseline(c, tokens, x, gam, W_U, y, acts, Wm):
+    """The oracle, timed on the host cores: the first `tokens` tokens (all T
+    by default) through the output error and every layer's outer product, then
+    every layer's clipped SGD-momentum step. With fewer than T tokens the full
+    step is estimated as per-token time x T + the measured updates."""
     import numpy as np
 
     import oracle as O
@@ -177,26 +179,25 @@ def cpu_baseline(c, tokens, x, gam, W_U, y, acts, W0):
                 break
     except OSError:  # pragma: no cover
         pass
-    ts = min(tokens, c.T)
+    ts = c.T if tokens <= 0 else min(tokens, c.T)
     t0 = time.perf_counter()
     out = O.output_error(x[:ts], gam, W_U, y[:ts], eps=c.eps, min_rms=c.min_rms, vocab_chunk=8192)
+    Ds = [O.pseudograd(out["g_tilde"], a[:ts], scale=1.0 / c.T) for a in acts]
     t1 = time.perf_counter()
-    for a in acts:
-        D = O.pseudograd(out["g_tilde"], a[:ts], scale=1.0 / c.T)
+    for D, W in zip(Ds, Wm):
+        s = O.clip_scale(float((D * D).sum()), float((W.astype(np.float64) ** 2).sum()), c.clip_frac)
+        O.sgd_momentum(W, np.zeros_like(D), s * D, c.lr, 0.9, step=2)
     t2 = time.perf_counter()
-    D = O.pseudograd(out["g_tilde"], acts[0][:ts], scale=1.0 / c.T)
-    s = O.clip_scale(float((D * D).sum()), float((W0.astype(np.float64) ** 2).sum()), c.clip_frac)
-    O.sgd_momentum(W0, np.zeros_like(D), s * D, c.lr, 0.9, step=2)
-    t3 = time.perf_counter()
-    upd_one = t3 - t2
-    per_tok = (t2 - t0) / ts
-    est = per_tok * c.T + upd_one * c.L
-    return {"value": c.T / est, "unit": "tokens/s", "cores": int(thr), "kind": "oracle",
-            "sample": (f"first {ts} of {c.T} tokens through output error (full V={c.V}) and all {c.L} "
-                       f"layer outer products ({t2 - t0:.1f} s) plus one layer's clipped SGD-momentum step "
-                       f"({upd_one:.1f} s); full step estimated as per-token time x T + per-layer update x L "
-                       f"= {est:.1f} s"),
-            "seconds": round(t3 - t0, 2), "affinity_cpus": len(os.sched_getaffinity(0)),
+    est = (t1 - t0) / ts * c.T + (t2 - t1)
+    if ts == c.T:
+        sample = (f"the whole step: {c.T} tokens through output error (full V={c.V}) and all {c.L} layer "
+                  f"outer products ({t1 - t0:.1f} s), then all {c.L} clipped SGD-momentum steps ({t2 - t1:.1f} s)")
+    else:
+        sample = (f"first {ts} of {c.T} tokens through output error (full V={c.V}) and all {c.L} layer outer "
+                  f"products ({t1 - t0:.1f} s), then all {c.L} clipped SGD-momentum steps ({t2 - t1:.1f} s); "
+                  f"full step estimated as per-token time x T + updates = {est:.1f} s")
+    return {"value": c.T / est, "unit": "tokens/s", "cores": int(thr), "kind": "oracle", "sample": sample,
+            "seconds": round(t2 - t0, 2), "affinity_cpus": len(os.sched_getaffinity(0)),
             "cpu_model": cpu_model, "blas": blas}
 
 
@@ -382,8 +383,8 @@ def main():
         "kernels": kernels,
     }
     if not args.no_cpu_baseline:
-        log(f"[bench] timing the CPU oracle on a {args.cpu_tokens}-token sample")
-        res["cpu_baseline"] = cpu_baseline(c, args.cpu_tokens, x, gam, W_U, y, acts, Wm_host[0])
+        log("[bench] timing the CPU oracle")
+        res["cpu_baseline"] = cpu_baseline(c, args.cpu_tokens, x, gam, W_U, y, acts, Wm_host)
     else:
         res["cpu_baseline"] = None
     print(json.dumps(res), flush=True)
