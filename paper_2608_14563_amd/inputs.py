@@ -40,7 +40,7 @@ BLOCK = 1 << 20
 
 # tensor ids inside the spawn key
 T_X, T_GAMMA, T_WU, T_TARGETS, T_Q, T_U, T_W, T_OUTLIER, T_REFNOISE, T_XIN, T_W1, T_W2, T_G, T_STATE, T_MISC, T_REF1, \
-    T_PFFN = range(17)
+    T_PFFN, T_MODEL = range(18)
 
 
 @dataclass(frozen=True)
@@ -256,3 +256,87 @@ def synthetic_signal(cfg: Config, std: float = 0.02, tensor: int = T_G) -> np.nd
     """A seeded stand-in for the pseudogradient signal g~ [T, d] (storage
     dtype), used to exercise the outer-product call on its own at full size."""
     return to_storage(normal(cfg.cid, tensor, 0, cfg.T * cfg.d, std=std).reshape(cfg.T, cfg.d), cfg.dtype)
+
+
+# ---------------------------------------------------------------- transformer
+# A decoder-only SwiGLU transformer with random weights: the model whose
+# forward pass with cache and autograd gradient feed the end-to-end
+# layer-viability diagnostic (Sec. 2.1-2.2). Only its weights and token ids are
+# drawn here; each side of the comparison runs the model itself.
+@dataclass(frozen=True)
+class ModelConfig:
+    mid: int            # first element of the spawn key (disjoint from Config ids)
+    name: str
+    V: int
+    d: int
+    d_ff: int
+    n_layers: int
+    n_heads: int
+    n_kv_heads: int     # grouped key/value heads; n_heads % n_kv_heads == 0
+    batch: int          # sequences
+    seq: int            # tokens per sequence (T = batch * seq)
+    layout: str         # "pre": norms on the block inputs (Llama, Qwen3, Falcon3)
+                        # "post": norms on the block outputs (OLMo-2)
+    eps: float = 1e-6
+    min_rms: float = 0.5
+    emb_std: float = 1.0
+
+    @property
+    def T(self) -> int:
+        return self.batch * self.seq
+
+    @property
+    def head_dim(self) -> int:
+        return self.d // self.n_heads
+
+    def shrink(self, **kw) -> "ModelConfig":
+        return replace(self, **kw)
+
+
+MODELS = {
+    "tiny": ModelConfig(200, "tiny", 512, 128, 344, 4, 4, 2, 2, 48, "pre"),
+    "tiny-post": ModelConfig(201, "tiny-post", 512, 128, 344, 4, 4, 2, 2, 48, "post"),
+    "qwen3-8b": ModelConfig(202, "qwen3-8b", 151936, 4096, 12288, 36, 32, 8, 16, 512, "pre"),
+    "olmo2-7b": ModelConfig(203, "olmo2-7b", 100352, 4096, 11008, 32, 32, 32, 16, 512, "post"),
+}
+
+# per-layer weight names, shapes (row-major [out, in]) and fan-in; weights are
+# N(0, 1/fan_in), norm gains 1 + N(0, 0.1^2)
+_LAYER_SHAPES = ("wq", "wk", "wv", "wo", "w1", "w2", "w3")
+
+
+def layer_shapes(m: ModelConfig) -> dict:
+    hq, hkv = m.n_heads * m.head_dim, m.n_kv_heads * m.head_dim
+    return {"wq": (hq, m.d), "wk": (hkv, m.d), "wv": (hkv, m.d), "wo": (m.d, hq),
+            "w1": (m.d_ff, m.d), "w2": (m.d_ff, m.d), "w3": (m.d, m.d_ff)}
+
+
+def model_layer(m: ModelConfig, layer: int) -> dict:
+    """float32 weights of one block: wq, wk, wv, wo (attention), w1 (gate),
+    w2 (up), w3 (down) and the gains n1, n2 of its two norms (before attention
+    and the MLP in the "pre" layout, after them in the "post" layout)."""
+    out = {}
+    for k, name in enumerate(_LAYER_SHAPES):
+        shp = layer_shapes(m)[name]
+        out[name] = normal(m.mid, T_MODEL, 16 * (layer + 1) + k, shp[0] * shp[1],
+                           std=1.0 / np.sqrt(shp[1])).reshape(shp)
+    for k, name in enumerate(("n1", "n2")):
+        out[name] = normal(m.mid, T_MODEL, 16 * (layer + 1) + 8 + k, m.d, std=0.1, mean=1.0)
+    return out
+
+
+def model_head(m: ModelConfig) -> dict:
+    """float32 embedding E [V, d] (N(0, emb_std^2)), final-norm gain [d] and
+    unembedding W_U [V, d] (N(0, 1/d))."""
+    return {"embed": normal(m.mid, T_MODEL, 0, m.V * m.d, std=m.emb_std).reshape(m.V, m.d),
+            "final_norm": normal(m.mid, T_MODEL, 1, m.d, std=0.1, mean=1.0),
+            "W_U": normal(m.mid, T_MODEL, 2, m.V * m.d, std=1.0 / np.sqrt(m.d)).reshape(m.V, m.d)}
+
+
+def model_tokens(m: ModelConfig) -> np.ndarray:
+    """int32 token ids [batch, seq + 1], Zipf(1.1) over the vocabulary; inputs
+    are ids[:, :-1] and next-token targets ids[:, 1:]."""
+    n = m.batch * (m.seq + 1)
+    u = uniform01(m.mid, T_MODEL, 3, n)
+    t = np.minimum(np.searchsorted(zipf_cdf(m.V), u, side="right"), m.V - 1)
+    return t.astype(np.int32).reshape(m.batch, m.seq + 1)
