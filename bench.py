@@ -53,6 +53,9 @@ def parse():
     ap.add_argument("--optimizer", choices=sorted(OPT_BYTES), default="sgd-momentum",
                     help="optimizer on the fp32 masters (HBM bytes per parameter: " +
                          ", ".join(f"{k} {v}" for k, v in sorted(OPT_BYTES.items())) + ")")
+    ap.add_argument("--e2e-diagnostic", default=None, metavar="MODEL",
+                    help="instead of the training step, time the end-to-end layer-viability diagnostic on a "
+                         "random-init transformer (paper_2608_14563_amd.inputs.MODELS, e.g. qwen3-8b)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (HBM counter calibration)")
     return ap.parse_args()
@@ -201,6 +204,148 @@ def cpu_baseline(c, tokens, x, gam, W_U, y, acts, Wm):
             "cpu_model": cpu_model, "blas": blas}
 
 
+def cpu_baseline_e2e(m, model, ids, tokens=512):
+    """The oracle's end-to-end diagnostic (float64 model, autograd, FPO
+    oracle) timed on the host cores on a bounded sample: the first `tokens`
+    tokens of one sequence through the full-vocabulary head and one, then two,
+    of the model's blocks (its last ones, weights copied from the device).
+    The difference prices one block; the full job is estimated as
+    (head + L blocks) x T / tokens (per-token cost; attention's length-dependent
+    share is about 2% of a block at 512 tokens)."""
+    import numpy as np
+    import torch
+
+    from oracle import transformer as OT
+    h = lambda t: t.detach().float().cpu().numpy()  # noqa: E731
+    head = {k: h(v) for k, v in model.head.items()}
+    L = m.n_layers
+    lay = [{k: h(v) for k, v in model.layers[l].items()} for l in (L - 2, L - 1)]
+    sid = ids[:1, :tokens + 1].cpu().numpy()
+    OT.diagnostic(m.shrink(n_layers=1, batch=1, seq=8), head, lay[1:], sid[:, :9])  # warm-up, untimed
+    times = []
+    for k in (1, 2):
+        mk = m.shrink(n_layers=k, batch=1, seq=tokens)
+        t0 = time.perf_counter()
+        OT.diagnostic(mk, head, lay[2 - k:], sid)
+        times.append(time.perf_counter() - t0)
+    per_block = max(times[1] - times[0], 0.0)
+    head_s = max(times[0] - per_block, 0.0)
+    est = (head_s + L * per_block) * m.T / tokens
+    return {"value": m.T / est, "unit": "tokens/s", "cores": torch.get_num_threads(), "kind": "oracle",
+            "sample": (f"first {tokens} tokens of one sequence through the head (V={m.V}) and 1, then 2, of the "
+                       f"{L} blocks: {times[0]:.1f} s and {times[1]:.1f} s, so head {head_s:.1f} s + "
+                       f"{per_block:.1f} s per block; full job estimated as (head + {L} blocks) x {m.T}/{tokens} "
+                       f"= {est:.0f} s"),
+            "seconds": round(sum(times), 2)}
+
+
+def bench_e2e(args):
+    """End-to-end layer-viability diagnostic (Sec. 2.2): one step = the
+    model's float32 forward with cache, its autograd gradient, and the FPO
+    side in libfpo (output error, every layer's W3 pseudogradient reduced
+    against the true gradient, output cosines) over one calibration batch."""
+    import numpy as np
+    import torch
+
+    from paper_2608_14563_amd import diagnostic as D
+    from paper_2608_14563_amd import inputs as I
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.backends.cuda.matmul.allow_tf32 = False
+    dev = torch.device("cuda:0")
+    m = I.MODELS[args.e2e_diagnostic]
+    op = torch.bfloat16
+    log(f"[bench] e2e diagnostic {m.name}: V={m.V} d={m.d} d_ff={m.d_ff} layers={m.n_layers} heads={m.n_heads}/"
+        f"{m.n_kv_heads} T={m.batch}x{m.seq}={m.T} layout={m.layout}")
+    model = D.Transformer.seeded_on_device(m, dev)
+    ids = torch.from_numpy(I.model_tokens(m).astype(np.int64)).to(dev)
+    lib = prof_lib()
+
+    def once(ev=None):
+        if ev:
+            ev[0].record()
+        c = D.forward_with_cache(model, ids, op)
+        if ev:
+            ev[1].record()
+        tg = D.true_gradients(c)
+        if ev:
+            ev[2].record()
+        out = D.fpo_launch(model, c, tg, op)
+        if ev:
+            ev[3].record()
+        return out
+
+    for _ in range(args.warmup):
+        D.fpo_finish(once())
+    torch.cuda.synchronize()
+    lib.fpo_prof_reset()
+    lib.fpo_prof_enable(b"")
+    res = D.fpo_finish(once())
+    torch.cuda.synchronize()
+    lib.fpo_prof_disable()
+    per_kernel = prof_read(lib)
+    lib.fpo_prof_reset()
+    dom = max(per_kernel, key=lambda k: per_kernel[k][0])
+    log("[bench] libfpo ms per diagnostic: " + ", ".join(f"{k}={v[0]:.3f}/{v[1]}" for k, v in sorted(per_kernel.items(), key=lambda kv: -kv[1][0])))
+    lib.fpo_prof_enable(dom.encode())
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for k in range(args.steps):
+        out = once(evs[k])
+        del out
+    e1.record()
+    torch.cuda.synchronize()
+    lib.fpo_prof_disable()
+    dom_stats = prof_read(lib)[dom]
+    lib.fpo_prof_reset()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    med = lambda v: sorted(v)[len(v) // 2]  # noqa: E731
+    fwd = med([e[0].elapsed_time(e[1]) for e in evs])
+    bwd = med([e[1].elapsed_time(e[2]) for e in evs])
+    fpo = med([e[2].elapsed_time(e[3]) for e in evs])
+    c = I.Config(-1, m.name, "bf16", m.d, m.d_ff, m.V, m.T, m.n_layers, zipf=True, outliers=False, diag=True)
+    roof = None
+    w = kernel_work(dom, c, args.steps, None)
+    if w is not None:
+        amount, unit, bound = w
+        secs = dom_stats[0] / 1000.0
+        ach = amount / secs / (1e12 if unit == "flop" else 1e9)
+        peak = PEAK_BF16_TFLOPS if unit == "flop" else PEAK_HBM_GBS
+        roof = {"bound": bound, "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s" if unit == "flop" else "GB/s",
+                "frac": round(ach / peak, 4), "traffic": profiled_traffic(m.name + "-e2e", dom), "kernel": dom,
+                "avg_launch_ms": round(dom_stats[0] / dom_stats[1], 4), "launches": dom_stats[1]}
+    flops_fpo = 4.0 * m.T * m.V * m.d + 2.0 * m.T * m.d * m.d_ff * m.n_layers
+    tok_s = m.T / (ms_step / 1e3)
+    log(f"[bench] {args.steps} diagnostics: {ms_step:.1f} ms each ({tok_s:.0f} tokens/s); forward {fwd:.1f} ms, "
+        f"autograd {bwd:.1f} ms, libfpo {fpo:.2f} ms; W3 cos last quarter {D.summary(res['cos_w3']):.3f}")
+    out = {
+        "metric": "end-to-end layer-viability diagnostic tokens/sec (forward with cache + autograd true gradient + "
+                  "FPO pseudogradient cosines, every layer)",
+        "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32 model / bf16 FPO operands", "data": "synthetic (random-init weights, Zipf tokens)",
+        "config": {"workload": f"{m.name}-shaped random-init transformer, diagnostic over {m.batch} sequences x "
+                               f"{m.seq} tokens, all {m.n_layers} layers scored", "V": m.V, "d": m.d, "d_ff": m.d_ff,
+                   "layers": m.n_layers, "heads": m.n_heads, "kv_heads": m.n_kv_heads, "T": m.T, "layout": m.layout},
+        "substeps": {"forward_ms_median": round(fwd, 2), "autograd_ms_median": round(bwd, 2),
+                     "libfpo_ms_median": round(fpo, 3),
+                     "libfpo_mfma_frac": round(flops_fpo / (fpo / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)},
+        "roofline": roof,
+        "kernels": {k: {"ms": round(v[0], 4), "launches": v[1]} for k, v in per_kernel.items()},
+        "cos_w3": [round(float(x), 4) for x in res["cos_w3"]],
+        "cos_out": [round(float(x), 4) for x in res["cos_out"]],
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a sample")
+        out["cpu_baseline"] = cpu_baseline_e2e(m, model, ids)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.calibrate_copy:
@@ -210,6 +355,9 @@ def main():
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build has no "
               "multi-GPU path: run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.e2e_diagnostic:
+        bench_e2e(args)
+        return
     import numpy as np
     import torch
 

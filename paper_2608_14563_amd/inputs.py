@@ -296,6 +296,9 @@ class ModelConfig:
 MODELS = {
     "tiny": ModelConfig(200, "tiny", 512, 128, 344, 4, 4, 2, 2, 48, "pre"),
     "tiny-post": ModelConfig(201, "tiny-post", 512, 128, 344, 4, 4, 2, 2, 48, "post"),
+    # several 256-wide tiles with ragged tails in T, d, d_ff and V
+    "small": ModelConfig(204, "small", 2000, 384, 1032, 3, 6, 2, 3, 100, "pre"),
+    "small-post": ModelConfig(205, "small-post", 2000, 384, 1032, 3, 6, 6, 3, 100, "post"),
     "qwen3-8b": ModelConfig(202, "qwen3-8b", 151936, 4096, 12288, 36, 32, 8, 16, 512, "pre"),
     "olmo2-7b": ModelConfig(203, "olmo2-7b", 100352, 4096, 11008, 32, 32, 32, 16, 512, "post"),
 }
@@ -340,3 +343,31 @@ def model_tokens(m: ModelConfig) -> np.ndarray:
     u = uniform01(m.mid, T_MODEL, 3, n)
     t = np.minimum(np.searchsorted(zipf_cdf(m.V), u, side="right"), m.V - 1)
     return t.astype(np.int32).reshape(m.batch, m.seq + 1)
+
+
+def model_weights_device(m: ModelConfig, device, seed: int = 0):
+    """The distributions of model_head / model_layer drawn directly on a GPU
+    with torch's seeded Philox generator (a different stream from the host
+    draws): for 7-8B shapes, whose host draws would take minutes. Returns
+    (head, layers) dicts of float32 device tensors."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(ENTROPY * 1000 + m.mid * 10 + seed)
+
+    def nrm(shape, std, mean=0.0):
+        t = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+        if std != 1.0:
+            t.mul_(std)
+        if mean != 0.0:
+            t.add_(mean)
+        return t
+
+    head = {"embed": nrm((m.V, m.d), m.emb_std), "final_norm": nrm((m.d,), 0.1, 1.0),
+            "W_U": nrm((m.V, m.d), 1.0 / np.sqrt(m.d))}
+    layers = []
+    for _ in range(m.n_layers):
+        w = {name: nrm(shp, 1.0 / np.sqrt(shp[1])) for name, shp in layer_shapes(m).items()}
+        w["n1"] = nrm((m.d,), 0.1, 1.0)
+        w["n2"] = nrm((m.d,), 0.1, 1.0)
+        layers.append(w)
+    return head, layers
