@@ -492,13 +492,15 @@ struct PgOverlap {
   bool ready = false;
   hipStream_t side = nullptr;
   hipEvent_t ready_l = nullptr, done = nullptr;
+  int cus = 0;  // compute units: workgroups of an update that runs beside the outer products
 };
 constexpr int kMaxDevices = 64;
 static PgOverlap g_pgo[kMaxDevices];
 
-static hipError_t pg_overlap_init(PgOverlap& p) {
+static hipError_t pg_overlap_init(PgOverlap& p, int dev) {
   if (p.ready) return hipSuccess;
   hipError_t e;
+  if ((e = hipDeviceGetAttribute(&p.cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
   // default priority: both streams at the same priority
   if ((e = hipStreamCreateWithFlags(&p.side, hipStreamNonBlocking)) != hipSuccess) return e;
   if ((e = hipEventCreateWithFlags(&p.ready_l, hipEventDisableTiming)) != hipSuccess) return e;
@@ -511,9 +513,10 @@ static hipError_t pg_overlap_init(PgOverlap& p) {
 // products run one layer per launch on the caller's stream; once layer l's
 // tiles and norm are done, its update (the standalone update kernel, which
 // needs few registers and no LDS, so its workgroups sit beside the GEMM's on
-// the same CUs) streams on a side stream while layer l+1's MFMAs run. Same
-// kernels and reduction order as the separate calls, so results are
-// bit-identical to them.
+// the same CUs) streams on a side stream while layer l+1's MFMAs run, with one
+// workgroup per CU so that each CU holds one outer-product workgroup and one
+// update workgroup. Same per-block arithmetic and reduction order as the
+// separate calls, so results are bit-identical to them.
 hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u) {
   hipStream_t st = (hipStream_t)a.stream;
   int dev = 0;
@@ -522,7 +525,7 @@ hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u) {
   if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
   PgOverlap& po = g_pgo[dev];
   std::lock_guard<std::mutex> lock(po.mu);
-  if ((e = pg_overlap_init(po)) != hipSuccess) return e;
+  if ((e = pg_overlap_init(po, dev)) != hipSuccess) return e;
   if ((e = prepare_signals<uint16_t>(a, st)) != hipSuccess) return e;
   const int ntiles = (int)pseudograd_tiles(true, a.d, a.d_ff);
   int64_t blk_base = 0;
@@ -545,7 +548,9 @@ hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u) {
     // layer l's dW and ||dW||^2 are complete: update it on the side stream
     if ((e = hipEventRecord(po.ready_l, st)) != hipSuccess) return e;
     if ((e = hipStreamWaitEvent(po.side, po.ready_l, 0)) != hipSuccess) return e;
-    if ((e = launch_update_blocks(u, l, blk_base, po.side)) != hipSuccess) return e;
+    // one workgroup per CU while the next layer's outer products run; the last
+    // update runs alone and takes the whole machine
+    if ((e = launch_update_blocks(u, l, blk_base, po.side, l + 1 < a.L ? po.cus : 0)) != hipSuccess) return e;
     blk_base += update_blocks(u.numel[l]);
   }
   if ((e = hipEventRecord(po.done, po.side)) != hipSuccess) return e;

@@ -43,6 +43,25 @@ __global__ __launch_bounds__(256) void update_kernel(UpdArgs a, int n, OptScalar
                part + b);
 }
 
+// The same blocks as update_kernel, visited grid-stride by a fixed number of
+// workgroups: run beside the outer products, one workgroup per CU fits next to
+// an outer-product workgroup (registers and LDS), so neither kernel waits for
+// the other's waves to drain. Each block's partial goes to the same slot as in
+// update_kernel, so every result is bit-identical.
+__global__ __launch_bounds__(256) void update_loop_kernel(UpdArgs a, int n, OptScalars o,
+                                                          const double* __restrict__ grad_sumsq,
+                                                          const double* __restrict__ W_sumsq,
+                                                          double* __restrict__ part) {
+  __shared__ double red[16];
+  const int64_t nb = a.blk0[n];
+  for (int64_t b = blockIdx.x; b < nb; b += gridDim.x) {
+    const int m = find_mat(a.blk0, n, b);
+    const float s = clip_factor(grad_sumsq[m], W_sumsq[m], o.clip_frac);
+    update_block(a.grad[m], a.W[m], a.W_lp[m], a.s1[m], a.s2[m], a.numel[m], b - a.blk0[m], s, o, red,
+                 part + b);
+  }
+}
+
 __global__ __launch_bounds__(256) void update_reduce_kernel(UpdArgs a, OptScalars o,
                                                             const double* __restrict__ part,
                                                             const double* __restrict__ grad_sumsq,
@@ -67,8 +86,9 @@ __global__ __launch_bounds__(256) void update_reduce_kernel(UpdArgs a, OptScalar
   } while (0)
 
 // The update blocks of matrix m alone (no reduction), on stream st; its
-// partials start at part + blk_base, as in launch_update.
-hipError_t launch_update_blocks(const UpdLaunch& a, int m, int64_t blk_base, void* stream) {
+// partials start at part + blk_base, as in launch_update. grid > 0: that many
+// workgroups visit the blocks grid-stride (update_loop_kernel).
+hipError_t launch_update_blocks(const UpdLaunch& a, int m, int64_t blk_base, void* stream, int grid) {
   hipStream_t st = (hipStream_t)stream;
   const OptScalars o = make_opt_scalars(a);
   UpdArgs ua{};
@@ -80,9 +100,15 @@ hipError_t launch_update_blocks(const UpdLaunch& a, int m, int64_t blk_base, voi
   ua.numel[0] = a.numel[m];
   ua.blk0[0] = 0;
   ua.blk0[1] = update_blocks(a.numel[m]);
-  FPO_LAUNCH("update", st,
-             update_kernel<<<dim3((unsigned)ua.blk0[1]), dim3(256), 0, st>>>(ua, 1, o, a.grad_sumsq + m,
-                                                                a.W_sumsq + m, a.part + blk_base));
+  if (grid > 0 && grid < ua.blk0[1]) {
+    FPO_LAUNCH("update", st,
+               update_loop_kernel<<<dim3((unsigned)grid), dim3(256), 0, st>>>(ua, 1, o, a.grad_sumsq + m,
+                                                                 a.W_sumsq + m, a.part + blk_base));
+  } else {
+    FPO_LAUNCH("update", st,
+               update_kernel<<<dim3((unsigned)ua.blk0[1]), dim3(256), 0, st>>>(ua, 1, o, a.grad_sumsq + m,
+                                                                  a.W_sumsq + m, a.part + blk_base));
+  }
   FPO_CHECK_LAUNCH();
   return hipSuccess;
 }

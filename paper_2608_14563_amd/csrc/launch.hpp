@@ -103,8 +103,9 @@ struct UpdLaunch {
 // blocks = false: only the per-matrix reductions (||W'||^2, clip factors) of
 // blocks already applied (by the fused pseudogradient launch).
 hipError_t launch_update(const UpdLaunch& a, bool blocks = true);
-// The update blocks of matrix m of `a` on `stream` (partials at part + blk_base).
-hipError_t launch_update_blocks(const UpdLaunch& a, int m, int64_t blk_base, void* stream);
+// The update blocks of matrix m of `a` on `stream` (partials at part + blk_base);
+// grid > 0: that many workgroups visit the blocks grid-stride.
+hipError_t launch_update_blocks(const UpdLaunch& a, int m, int64_t blk_base, void* stream, int grid = 0);
 // W3-only bf16 pseudogradients with the optimizer step overlapped (u: the
 // update of the same matrices, grad = the dW3 outputs, grad_sumsq = a.sumsq).
 hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u);

@@ -137,13 +137,15 @@ def test_cosine(dev, bdtype):
 
 @pytest.mark.parametrize("kind", ["sgd", "adamw", "sgd-plain"])
 @pytest.mark.parametrize("T,d,d_ff,L,clip,pffn", [(256, 256, 512, 2, 0.01, False), (300, 264, 1000, 3, 0.01, False),
-                                                  (200, 512, 768, 3, 1e-5, False), (300, 264, 1000, 3, 0.01, True)])
+                                                  (200, 512, 768, 3, 1e-5, False), (300, 264, 1000, 3, 0.01, True),
+                                                  (200, 1032, 1288, 3, 0.01, False)])
 def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip, pffn):
     """The W3 pseudogradient with the optimizer fused (bf16: one launch per
     layer carrying that layer's outer products and the previous layer's update)
     is bit-identical to the pseudogradient followed by fpo_apply_update, over two
-    steps (momentum / moments carried), including a ragged shape and an active
-    clip (clip_frac 1e-5)."""
+    steps (momentum / moments carried), including a ragged shape, an active
+    clip (clip_frac 1e-5), and matrices of more update blocks than the GPU has
+    compute units (the overlapped update then visits its blocks grid-stride)."""
     c = I.CONFIGS[1].shrink(T=T, d=d, d_ff=d_ff, L=L)
     g = dev_tensor(I.synthetic_signal(c), dev)
     kw = {}
