@@ -5,7 +5,8 @@ One step = one pass of the whole hot path over one batch of T tokens:
 fpo_output_error (final-norm recompute, vocabulary-chunked logits + online
 softmax + error, projection through W_U, clamped RMSNorm VJP) followed by
 fpo_pseudograd with the fused update (per-layer outer products for every
-target layer, relative 1% clip, SGD-momentum on fp32 masters, bf16 copy).
+target layer staged in bf16 as the paper's bf16 einsum produces them,
+relative 1% clip, SGD-momentum on fp32 masters, bf16 copy).
 Inputs are seeded synthetic tensors of the workload's shapes, resident in HBM
 before timing starts. Prints one JSON line on stdout; progress goes to stderr.
 
@@ -50,6 +51,9 @@ def parse():
                     help="tokens in the oracle's timed sample (0: the whole step)")
     ap.add_argument("--post-ffn", action="store_true",
                     help="compose each target layer's post-FFN RMSNorm VJP (OLMo-2 / Gemma 3 layout)")
+    ap.add_argument("--grad-f32", action="store_true",
+                    help="hand the fused update an fp32 pseudogradient instead of the bf16-staged one "
+                         "(FPO_MODE_GRAD_BF16, the precision of the paper's bf16 einsum)")
     ap.add_argument("--optimizer", choices=sorted(OPT_BYTES), default="sgd-momentum",
                     help="optimizer on the fp32 masters (HBM bytes per parameter: " +
                          ", ".join(f"{k} {v}" for k, v in sorted(OPT_BYTES.items())) + ")")
@@ -130,7 +134,7 @@ def profiled_traffic(workload: str, kernel: str):
     return None
 
 
-def kernel_work(name, c, steps, nchunk, opt="sgd-momentum", pffn=False):
+def kernel_work(name, c, steps, nchunk, opt="sgd-momentum", pffn=False, grad_bf16=False):
     """Algorithmic work of one kernel over `steps` steps: (amount, unit, bound).
     Flops count only the method's contractions; bytes count each operand once."""
     T, d, V, dff, L = c.T, c.d, c.V, c.d_ff, c.L
@@ -138,8 +142,8 @@ def kernel_work(name, c, steps, nchunk, opt="sgd-momentum", pffn=False):
         return 2.0 * T * V * d * steps, "flop", "mfma"
     if name == "outer":
         return 2.0 * T * d * dff * L * steps, "flop", "mfma"
-    if name == "update":
-        return OPT_BYTES[opt] * L * d * dff * steps, "byte", "hbm"
+    if name == "update":  # a staged bf16 pseudogradient reads 2 bytes instead of 4
+        return (OPT_BYTES[opt] - (2.0 if grad_bf16 else 0.0)) * L * d * dff * steps, "byte", "hbm"
     if name == "chunk_stats":
         # per-(token, 128-entry block) max / sum / argmax read; per-token state written
         return (12.0 * T * ((V + 127) // 128) + 32.0 * T) * steps, "byte", "hbm"
@@ -410,8 +414,9 @@ def main():
     dW = [torch.empty(d, c.d_ff, dtype=torch.float32, device=dev) for _ in range(c.L)]
     ss = torch.empty(c.L, dtype=torch.float64, device=dev)
     ws_oe = api.workspace(api.fpo_output_error_workspace(T, d, c.V, torch.bfloat16, args.vocab_chunk), dev)
+    stage = not args.grad_f32
     ws_pg = api.workspace(api.fpo_pseudograd_workspace(T, d, c.d_ff, c.L, torch.bfloat16,
-                                                       post_ffn=args.post_ffn), dev)
+                                                       post_ffn=args.post_ffn, grad_bf16=stage), dev)
     if args.post_ffn:
         pffn = api.PostFfn(g_t, pffn_mo, pffn_g, c.eps, c.min_rms)
     torch.cuda.synchronize()
@@ -424,7 +429,7 @@ def main():
                              vocab_chunk=args.vocab_chunk)
         if mid is not None:
             mid.record()
-        api.fpo_pseudograd(g_lp, tacts, dW3=dW, sumsq=ss,
+        api.fpo_pseudograd(g_lp, tacts, dW3=None if stage else dW, sumsq=ss, grad_bf16=stage,
                            opt=api.OptConfig(kind=1 if adam else 0, lr=c.lr, momentum=0.0 if plain else 0.9,
                                              clip_frac=c.clip_frac, step=step_no[0]),
                            W_master=Wm, W_lp=Wlp, state1=s1, state2=s2, W_sumsq=Wsq, ws=ws_pg, post_ffn=pffn)
@@ -469,7 +474,7 @@ def main():
     log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step, {tok_s:.0f} tokens/s; dominant kernel {dom}: "
         f"{dom_stats[0] / dom_stats[1]:.3f} ms avg over {dom_stats[1]} launches")
     nchunk = None
-    w = kernel_work(dom, c, args.steps, nchunk, args.optimizer, args.post_ffn)
+    w = kernel_work(dom, c, args.steps, nchunk, args.optimizer, args.post_ffn, stage)
     roof = None
     traffic = profiled_traffic(c.name, dom)
     if w is not None:
@@ -487,7 +492,7 @@ def main():
                     "avg_launch_ms": round(dom_stats[0] / dom_stats[1], 4), "launches": dom_stats[1]}
     kernels = {}
     for k, (ms, n) in per_kernel.items():
-        wk = kernel_work(k, c, 1, nchunk, args.optimizer, args.post_ffn)
+        wk = kernel_work(k, c, 1, nchunk, args.optimizer, args.post_ffn, stage)
         e = {"ms_per_step": round(ms, 4), "launches": n}
         if wk is not None:
             amount, unit, bound = wk
@@ -522,9 +527,11 @@ def main():
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": f"{c.name}-shaped FPO step: T={c.T} tokens, d={c.d}, d_ff={c.d_ff}, V={c.V}, "
                                f"{c.L} target layers (W3{', post-FFN norm VJP per layer' if args.post_ffn else ''}), bf16 operands / fp32 "
-                               f"accumulate, {OPT_NAME[args.optimizer]} "
+                               f"accumulate, pseudogradient handed to the update in {'fp32' if args.grad_f32 else 'bf16'}, "
+                               f"{OPT_NAME[args.optimizer]} "
                                f"on fp32 masters, 1% relative clip", "T": c.T, "d": c.d, "d_ff": c.d_ff, "V": c.V, "L": c.L,
-                   "optimizer": args.optimizer, "post_ffn_norm": bool(args.post_ffn)},
+                   "optimizer": args.optimizer, "post_ffn_norm": bool(args.post_ffn),
+                   "pseudogradient_staging": "f32" if args.grad_f32 else "bf16"},
         "step_mfma_frac": round(flops_step / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "substeps": substeps,
         "roofline": roof,

@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define FPO_ABI_VERSION 2
+#define FPO_ABI_VERSION 3
 
 typedef enum {
   FPO_OK = 0,
@@ -64,7 +64,12 @@ typedef enum {
 } fpo_status;
 
 typedef enum { FPO_F32 = 0, FPO_BF16 = 1 } fpo_dtype;
-typedef enum { FPO_MODE_W3 = 0, FPO_MODE_FULL_MLP = 1, FPO_MODE_POST_FFN = 2 } fpo_mode; /* bit flags */
+typedef enum {
+  FPO_MODE_W3 = 0,
+  FPO_MODE_FULL_MLP = 1,
+  FPO_MODE_POST_FFN = 2,
+  FPO_MODE_GRAD_BF16 = 4
+} fpo_mode; /* bit flags */
 typedef enum { FPO_OPT_SGD = 0, FPO_OPT_ADAMW = 1 } fpo_opt_kind;
 
 /* Output-error call description.
@@ -208,7 +213,8 @@ typedef struct {
  *              (NULL otherwise): W3_init [d, d_ff], q and u [T, d_ff],
  *              x_in [T, d], all dtype
  *   dW3        [host] L pointers to float [d, d_ff] out. May be NULL only
- *              when `ref` is given (fused diagnostic: no dW3 is stored)
+ *              when `ref` is given (fused diagnostic: no dW3 is stored), and
+ *              must be NULL in FPO_MODE_GRAD_BF16
  *   dW1, dW2   [host] L pointers to float [d_ff, d] out (FULL_MLP only)
  *   sumsq      double out, nullable: ||dW||_F^2 per matrix, in the order
  *              W3(0..L-1) then, in FULL_MLP mode, W1(0..L-1), W2(0..L-1)

@@ -13,7 +13,7 @@ LIB_PATH = os.path.join(_HERE, "libfpo.so")
 
 FPO_OK, FPO_ERR_NULL, FPO_ERR_SHAPE, FPO_ERR_DTYPE, FPO_ERR_ARG, FPO_ERR_WORKSPACE, FPO_ERR_UNSUPPORTED, FPO_ERR_HIP = range(8)
 FPO_F32, FPO_BF16 = 0, 1
-FPO_MODE_W3, FPO_MODE_FULL_MLP, FPO_MODE_POST_FFN = 0, 1, 2  # bit flags
+FPO_MODE_W3, FPO_MODE_FULL_MLP, FPO_MODE_POST_FFN, FPO_MODE_GRAD_BF16 = 0, 1, 2, 4  # bit flags
 FPO_OPT_SGD, FPO_OPT_ADAMW = 0, 1
 
 STATUS_NAMES = {0: "FPO_OK", 1: "FPO_ERR_NULL", 2: "FPO_ERR_SHAPE", 3: "FPO_ERR_DTYPE", 4: "FPO_ERR_ARG",
@@ -53,7 +53,7 @@ class PostFfn(C.Structure):
                 ("eps", C.c_float), ("min_rms", C.c_float)]
 
 
-ABI_VERSION = 2
+ABI_VERSION = 3
 PP = C.POINTER(C.c_void_p)
 VP = C.c_void_p
 _lib = None

@@ -130,12 +130,14 @@ def _upd_bufs(keep: _Keep, W_master, W_lp, state1, state2, W_sumsq, clip_scale, 
 
 
 # --------------------------------------------------------------------- pseudograd
-def _mode(full_mlp: bool, post_ffn: bool) -> int:
-    return (L.FPO_MODE_FULL_MLP if full_mlp else L.FPO_MODE_W3) | (L.FPO_MODE_POST_FFN if post_ffn else 0)
+def _mode(full_mlp: bool, post_ffn: bool, grad_bf16: bool = False) -> int:
+    return ((L.FPO_MODE_FULL_MLP if full_mlp else L.FPO_MODE_W3) | (L.FPO_MODE_POST_FFN if post_ffn else 0)
+            | (L.FPO_MODE_GRAD_BF16 if grad_bf16 else 0))
 
 
-def fpo_pseudograd_workspace(T, d, d_ff, Lyr, dtype: torch.dtype, full_mlp=False, post_ffn=False) -> int:
-    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(dtype), _mode(full_mlp, post_ffn), 1.0)
+def fpo_pseudograd_workspace(T, d, d_ff, Lyr, dtype: torch.dtype, full_mlp=False, post_ffn=False,
+                             grad_bf16=False) -> int:
+    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(dtype), _mode(full_mlp, post_ffn, grad_bf16), 1.0)
     return L.load().fpo_pseudograd_workspace(C.byref(desc))
 
 
@@ -154,9 +156,12 @@ class PostFfn:
 def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, ref_sumsq=None,
                    W3_init=None, gate=None, up=None, x_in=None, dW1=None, dW2=None, scale=None,
                    opt: Optional[OptConfig] = None, W_master=None, W_lp=None, state1=None,
-                   state2=None, W_sumsq=None, clip_scale=None, ws=None, post_ffn: Optional[PostFfn] = None):
+                   state2=None, W_sumsq=None, clip_scale=None, ws=None, post_ffn: Optional[PostFfn] = None,
+                   grad_bf16: bool = False):
     """g_tilde_lp may be None when post_ffn is given (its left operands are
-    then formed per layer from post_ffn.g_tilde)."""
+    then formed per layer from post_ffn.g_tilde). grad_bf16 (FPO_MODE_GRAD_BF16,
+    fused update only, dW3 None): the pseudogradient is staged in bf16 in the
+    workspace instead of being returned."""
     op = a[0].dtype
     dev = a[0].device
     T = a[0].shape[0]
@@ -164,7 +169,7 @@ def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, 
     Lyr = len(a)
     d_ff = a[0].shape[1]
     full = W3_init is not None
-    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(op), _mode(full, post_ffn is not None),
+    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(op), _mode(full, post_ffn is not None, grad_bf16),
                     (1.0 / T) if scale is None else scale)
     lib = L.load()
     if ws is None:

@@ -175,6 +175,12 @@ size_t carve_pg(const fpo_pg_desc& d, const PgPlan& p, void* ws, fpo::PgLaunch* 
   void* du = full ? c.take<char>(d.d_ff * p.Tp * esz) : nullptr;
   double* part = c.take<double>(std::max<int64_t>(d.L, 2) * p.ntiles * 3);
   double* up = c.take<double>(p.upd_blocks);
+  // staged bf16 pseudogradients (FPO_MODE_GRAD_BF16), one 256-aligned matrix per layer
+  const bool stage = (d.mode & FPO_MODE_GRAD_BF16) != 0;
+  for (int64_t l = 0; l < (stage ? d.L : 0); ++l) {
+    uint16_t* sl = c.take<uint16_t>(d.d * d.d_ff);
+    if (L) L->dW3_bf16[l] = sl;
+  }
   if (L) {
     L->gT = gT;
     L->g_row = grow;
@@ -191,8 +197,11 @@ int check_pg_desc(const fpo_pg_desc* d) {
   if (!d) return fail(FPO_ERR_NULL, "fpo_pseudograd: desc is NULL");
   if (d->dtype != FPO_F32 && d->dtype != FPO_BF16)
     return fail(FPO_ERR_DTYPE, "fpo_pseudograd: unknown dtype %d", (int)d->dtype);
-  if (d->mode < 0 || d->mode > (FPO_MODE_FULL_MLP | FPO_MODE_POST_FFN))
+  if (d->mode < 0 || d->mode > (FPO_MODE_FULL_MLP | FPO_MODE_POST_FFN | FPO_MODE_GRAD_BF16))
     return fail(FPO_ERR_ARG, "fpo_pseudograd: unknown mode %d", (int)d->mode);
+  if ((d->mode & FPO_MODE_GRAD_BF16) && (d->dtype != FPO_BF16 || (d->mode & FPO_MODE_FULL_MLP)))
+    return fail(FPO_ERR_UNSUPPORTED,
+                "fpo_pseudograd: FPO_MODE_GRAD_BF16 is implemented for the W3-only FPO_BF16 path");
   if (d->T <= 0 || d->d <= 0 || d->d_ff <= 0 || d->L <= 0 || d->T > kIntMax || d->d > kIntMax ||
       d->d_ff > kIntMax)
     return fail(FPO_ERR_SHAPE, "fpo_pseudograd: sizes must be in [1, 2^31): T=%lld d=%lld d_ff=%lld L=%lld",
@@ -244,7 +253,7 @@ int check_ws(void* ws, size_t have, size_t need, const char* who) {
   return FPO_OK;
 }
 
-int fill_update(const fpo_opt* opt, int64_t n, const int64_t* numel, const float* const* grad,
+int fill_update(const fpo_opt* opt, int64_t n, const int64_t* numel, const void* const* grad,
                 const double* grad_sumsq, const fpo_update_bufs* upd, int32_t lp_dtype,
                 fpo::UpdLaunch* U) {
   if (int e = check_opt(opt)) return e;
@@ -387,15 +396,18 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
         return fail(FPO_ERR_ARG, "fpo_pseudograd: post_ffn buffers of layer %d not 16-byte aligned", l);
     }
   }
-  if (!dW3 && !ref) return fail(FPO_ERR_NULL, "fpo_pseudograd: dW3 may be NULL only with ref");
+  const bool stage = (desc->mode & FPO_MODE_GRAD_BF16) != 0;
+  if (stage && (dW3 || !opt))
+    return fail(FPO_ERR_ARG, "fpo_pseudograd: FPO_MODE_GRAD_BF16 needs dW3 == NULL and the fused update");
+  if (!dW3 && !ref && !stage) return fail(FPO_ERR_NULL, "fpo_pseudograd: dW3 may be NULL only with ref");
   if (ref && (!ref_dot || !ref_sumsq))
     return fail(FPO_ERR_NULL, "fpo_pseudograd: ref needs ref_dot and ref_sumsq");
   if (full && (!W3_init || !gate || !up || !x_in || !dW1 || !dW2))
     return fail(FPO_ERR_NULL, "fpo_pseudograd: full-MLP mode needs W3_init, gate, up, x_in, dW1, dW2");
   if ((opt == nullptr) != (upd == nullptr))
     return fail(FPO_ERR_ARG, "fpo_pseudograd: opt and upd must both be given or both be NULL");
-  if (opt && (!dW3 || !sumsq))
-    return fail(FPO_ERR_NULL, "fpo_pseudograd: the fused update needs dW3 and sumsq");
+  if (opt && ((!dW3 && !stage) || !sumsq))
+    return fail(FPO_ERR_NULL, "fpo_pseudograd: the fused update needs dW3 (or FPO_MODE_GRAD_BF16) and sumsq");
   if (g_tilde_lp && !aligned(g_tilde_lp, 16))
     return fail(FPO_ERR_ARG, "fpo_pseudograd: g_tilde_lp must be 16-byte aligned");
   fpo::PgLaunch P{};
@@ -452,13 +464,14 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
     const int n = pl.nmats;
     if (n > fpo::kMaxMats) return fail(FPO_ERR_SHAPE, "fpo_pseudograd: fused update limited to %d matrices", fpo::kMaxMats);
     int64_t numel[fpo::kMaxMats];
-    const float* grads[fpo::kMaxMats];
+    const void* grads[fpo::kMaxMats];
     for (int m = 0; m < n; ++m) {
       const int l = m % L, kind = m / L;
       numel[m] = desc->d * desc->d_ff;
-      grads[m] = kind == 0 ? dW3[l] : (kind == 1 ? dW1[l] : dW2[l]);
+      grads[m] = stage ? (const void*)P.dW3_bf16[l] : kind == 0 ? dW3[l] : (kind == 1 ? dW1[l] : dW2[l]);
     }
     if (int e = fill_update(opt, n, numel, grads, sumsq, upd, desc->dtype, &U)) return e;
+    U.grad_bf16 = stage;
     U.part = upart;
     U.stream = stream;
   }
@@ -488,7 +501,8 @@ int fpo_apply_update(const fpo_opt* opt, int64_t n_mats, const int64_t* numel,
                      const fpo_update_bufs* upd, int32_t lp_dtype, void* ws, size_t ws_bytes,
                      void* stream) {
   fpo::UpdLaunch U{};
-  if (int e = fill_update(opt, n_mats, numel, grad, grad_sumsq, upd, lp_dtype, &U)) return e;
+  if (int e = fill_update(opt, n_mats, numel, (const void* const*)grad, grad_sumsq, upd, lp_dtype, &U))
+    return e;
   if (int e = check_ws(ws, ws_bytes, update_ws(n_mats, numel), "fpo_apply_update")) return e;
   U.part = (double*)ws;
   U.stream = stream;

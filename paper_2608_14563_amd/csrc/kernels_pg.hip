@@ -102,6 +102,7 @@ struct OuterArgs {
   const void* A[kMaxMats];
   const void* B[kMaxMats];
   float* C[kMaxMats];
+  uint16_t* Cb[kMaxMats];  // bf16 output instead of C (bf16 tiles only), or null
   const float* R[kMaxMats];
 };
 
@@ -148,8 +149,11 @@ __device__ __forceinline__ void outer_epilogue(VA (&acc)[FM][FN], const Map& mp,
 
 // bf16 form: 16 rows of a fragment are loaded (reference) before use, so
 // the loads overlap; every lane's 4 columns are consecutive.
+// With Cb the tile is stored rounded to bf16 (RNE) and the partial norms and
+// dot products are of the rounded values.
 __device__ __forceinline__ void outer_epilogue2(const f32x16 (&acc)[4][4], int m0, int n0, int M,
                                                 int N, float scale, float* __restrict__ C,
+                                                uint16_t* __restrict__ Cb,
                                                 const float* __restrict__ R, double* red,
                                                 double* __restrict__ part_out) {
   const AccMap2<true> mp;
@@ -171,7 +175,12 @@ __device__ __forceinline__ void outer_epilogue2(const f32x16 (&acc)[4][4], int m
     for (int r = 0; r < 16; ++r) {
       const int row = m0 + mp.row(f, r);
       if (!cok || row >= M) continue;
-      const f32x4 v = f32x4{acc[f][0][r], acc[f][1][r], acc[f][2][r], acc[f][3][r]} * scale;
+      f32x4 v = f32x4{acc[f][0][r], acc[f][1][r], acc[f][2][r], acc[f][3][r]} * scale;
+      if (Cb) {
+        const u32x2 h = {pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w)};
+        *reinterpret_cast<u32x2*>(Cb + (int64_t)row * N + c) = h;
+        v = f32x4{bf16_lo(h.x), bf16_hi(h.x), bf16_lo(h.y), bf16_hi(h.y)};
+      }
       if (C) *reinterpret_cast<f32x4*>(C + (int64_t)row * N + c) = v;
       ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
       if (R) {
@@ -220,7 +229,7 @@ __global__ __launch_bounds__(256, 1) void outer_kernel(OuterArgs args, int M, in
     const Operand A{Am + (int64_t)m0 * lda, lda, band_bytes(M - m0, lda)};
     const Operand B{Bm + n0, ldb, band_bytes(K, ldb, n0)};
     gemm2_mainloop<true>(sm, acc, A, B, M - m0, N - n0, K, 0, (K + G2::BK - 1) / G2::BK);
-    outer_epilogue2(acc, m0, n0, M, N, scale, args.C[mat], args.R[mat], red, po);
+    outer_epilogue2(acc, m0, n0, M, N, scale, args.C[mat], args.Cb[mat], args.R[mat], red, po);
   } else {
     __shared__ GemmSmem<E> sm;
     f32x4 acc[E::FM][E::FN];
@@ -439,6 +448,7 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
       oa.A[l] = signal_T<T>(a, l);
       oa.B[l] = a.a[l];
       oa.C[l] = a.dW3[l];
+      oa.Cb[l] = a.dW3_bf16[l];
       oa.R[l] = a.ref[l];
     }
     FPO_LAUNCH("outer", st,
@@ -534,6 +544,7 @@ hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u) {
     oa.A[0] = signal_T<uint16_t>(a, l);
     oa.B[0] = a.a[l];
     oa.C[0] = a.dW3[l];
+    oa.Cb[0] = a.dW3_bf16[l];
     oa.R[0] = a.ref[l];
     double* tpart = a.part + (int64_t)l * ntiles * 3;
     FPO_LAUNCH("outer", st,

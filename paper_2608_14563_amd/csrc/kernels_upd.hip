@@ -16,7 +16,7 @@ int64_t update_blocks(int64_t numel) { return (numel + kElemsPerBlock - 1) / kEl
 int64_t cosine_blocks(int64_t numel) { return (numel + kElemsPerBlock - 1) / kElemsPerBlock; }
 
 struct UpdArgs {
-  const float* grad[kUpdBatch];
+  const void* grad[kUpdBatch];  // float32, or bf16 (the kernels' GB16)
   float* W[kUpdBatch];
   void* W_lp[kUpdBatch];
   float* s1[kUpdBatch];
@@ -31,6 +31,7 @@ __device__ __forceinline__ int find_mat(const int64_t* blk0, int n, int64_t b) {
   return m;
 }
 
+template <bool GB16, bool ADAM>
 __global__ __launch_bounds__(256) void update_kernel(UpdArgs a, int n, OptScalars o,
                                                      const double* __restrict__ grad_sumsq,
                                                      const double* __restrict__ W_sumsq,
@@ -39,27 +40,27 @@ __global__ __launch_bounds__(256) void update_kernel(UpdArgs a, int n, OptScalar
   const int64_t b = blockIdx.x;
   const int m = find_mat(a.blk0, n, b);
   const float s = clip_factor(grad_sumsq[m], W_sumsq[m], o.clip_frac);
-  update_block(a.grad[m], a.W[m], a.W_lp[m], a.s1[m], a.s2[m], a.numel[m], b - a.blk0[m], s, o, red,
-               part + b);
+  update_visit<GB16, ADAM, 1>(a.grad[m], a.W[m], a.W_lp[m], a.s1[m], a.s2[m], a.numel[m], b - a.blk0[m], 1,
+                               a.blk0[m + 1] - a.blk0[m], s, o, red, part + a.blk0[m]);
 }
 
-// The same blocks as update_kernel, visited grid-stride by a fixed number of
-// workgroups: run beside the outer products, one workgroup per CU fits next to
-// an outer-product workgroup (registers and LDS), so neither kernel waits for
-// the other's waves to drain. Each block's partial goes to the same slot as in
-// update_kernel, so every result is bit-identical.
-__global__ __launch_bounds__(256) void update_loop_kernel(UpdArgs a, int n, OptScalars o,
+// The blocks of one matrix (a.blk0[1] of them) visited by a fixed number of
+// workgroups, NB blocks per visit (block b and b + gridDim.x, ...): run beside
+// the outer products, one workgroup per CU fits next to an outer-product
+// workgroup (registers and LDS), so neither kernel waits for the other's waves
+// to drain, and NB blocks' loads in flight per workgroup hide memory latency.
+// Each block's result and partial are those of update_kernel, bit for bit.
+template <bool GB16, bool ADAM, int NB>
+__global__ __launch_bounds__(256) void update_loop_kernel(UpdArgs a, OptScalars o,
                                                           const double* __restrict__ grad_sumsq,
                                                           const double* __restrict__ W_sumsq,
                                                           double* __restrict__ part) {
   __shared__ double red[16];
-  const int64_t nb = a.blk0[n];
-  for (int64_t b = blockIdx.x; b < nb; b += gridDim.x) {
-    const int m = find_mat(a.blk0, n, b);
-    const float s = clip_factor(grad_sumsq[m], W_sumsq[m], o.clip_frac);
-    update_block(a.grad[m], a.W[m], a.W_lp[m], a.s1[m], a.s2[m], a.numel[m], b - a.blk0[m], s, o, red,
-                 part + b);
-  }
+  const int64_t nb = a.blk0[1];
+  const float s = clip_factor(grad_sumsq[0], W_sumsq[0], o.clip_frac);
+  for (int64_t b = blockIdx.x; b < nb; b += (int64_t)NB * gridDim.x)
+    update_visit<GB16, ADAM, NB>(a.grad[0], a.W[0], a.W_lp[0], a.s1[0], a.s2[0], a.numel[0], b, gridDim.x, nb,
+                                  s, o, red, part);
 }
 
 __global__ __launch_bounds__(256) void update_reduce_kernel(UpdArgs a, OptScalars o,
@@ -85,6 +86,24 @@ __global__ __launch_bounds__(256) void update_reduce_kernel(UpdArgs a, OptScalar
     if (e_ != hipSuccess) return e_;   \
   } while (0)
 
+// update_kernel over nb blocks of the n matrices of ua, in the variant for the
+// gradient dtype and optimizer.
+static hipError_t launch_update_kernel(const UpdArgs& ua, int n, const OptScalars& o, bool gb16, bool adam,
+                                       const double* gs, const double* ws, double* pt, unsigned nb,
+                                       hipStream_t st) {
+  const dim3 g(nb);
+  if (gb16 && adam)
+    FPO_LAUNCH("update", st, update_kernel<true, true><<<g, dim3(256), 0, st>>>(ua, n, o, gs, ws, pt));
+  else if (gb16)
+    FPO_LAUNCH("update", st, update_kernel<true, false><<<g, dim3(256), 0, st>>>(ua, n, o, gs, ws, pt));
+  else if (adam)
+    FPO_LAUNCH("update", st, update_kernel<false, true><<<g, dim3(256), 0, st>>>(ua, n, o, gs, ws, pt));
+  else
+    FPO_LAUNCH("update", st, update_kernel<false, false><<<g, dim3(256), 0, st>>>(ua, n, o, gs, ws, pt));
+  FPO_CHECK_LAUNCH();
+  return hipSuccess;
+}
+
 // The update blocks of matrix m alone (no reduction), on stream st; its
 // partials start at part + blk_base, as in launch_update. grid > 0: that many
 // workgroups visit the blocks grid-stride (update_loop_kernel).
@@ -100,14 +119,26 @@ hipError_t launch_update_blocks(const UpdLaunch& a, int m, int64_t blk_base, voi
   ua.numel[0] = a.numel[m];
   ua.blk0[0] = 0;
   ua.blk0[1] = update_blocks(a.numel[m]);
-  if (grid > 0 && grid < ua.blk0[1]) {
-    FPO_LAUNCH("update", st,
-               update_loop_kernel<<<dim3((unsigned)grid), dim3(256), 0, st>>>(ua, 1, o, a.grad_sumsq + m,
-                                                                 a.W_sumsq + m, a.part + blk_base));
+  const bool loop = grid > 0 && grid < ua.blk0[1];
+  const double* gs = a.grad_sumsq + m;
+  const double* ws = a.W_sumsq + m;
+  double* pt = a.part + blk_base;
+  const bool adam = a.kind == kOptAdamW;
+  if (loop) {
+    // SGD: two blocks per visit (128 VGPRs, still beside an outer-product
+    // workgroup); AdamW's second moment leaves room for one
+    const dim3 g((unsigned)grid);
+    if (adam && a.grad_bf16)
+      FPO_LAUNCH("update", st, update_loop_kernel<true, true, 1><<<g, dim3(256), 0, st>>>(ua, o, gs, ws, pt));
+    else if (adam)
+      FPO_LAUNCH("update", st, update_loop_kernel<false, true, 1><<<g, dim3(256), 0, st>>>(ua, o, gs, ws, pt));
+    else if (a.grad_bf16)
+      FPO_LAUNCH("update", st, update_loop_kernel<true, false, 2><<<g, dim3(256), 0, st>>>(ua, o, gs, ws, pt));
+    else
+      FPO_LAUNCH("update", st, update_loop_kernel<false, false, 2><<<g, dim3(256), 0, st>>>(ua, o, gs, ws, pt));
   } else {
-    FPO_LAUNCH("update", st,
-               update_kernel<<<dim3((unsigned)ua.blk0[1]), dim3(256), 0, st>>>(ua, 1, o, a.grad_sumsq + m,
-                                                                  a.W_sumsq + m, a.part + blk_base));
+    if (hipError_t e = launch_update_kernel(ua, 1, o, a.grad_bf16, adam, gs, ws, pt, (unsigned)ua.blk0[1], st))
+      return e;
   }
   FPO_CHECK_LAUNCH();
   return hipSuccess;
@@ -134,10 +165,10 @@ hipError_t launch_update(const UpdLaunch& a, bool blocks) {
     }
     ua.blk0[n] = nb;
     if (blocks) {
-      FPO_LAUNCH("update", st,
-                 update_kernel<<<dim3((unsigned)nb), dim3(256), 0, st>>>(ua, n, o, a.grad_sumsq + m0,
-                                                            a.W_sumsq + m0, a.part + part_off));
-      FPO_CHECK_LAUNCH();
+      if (hipError_t e = launch_update_kernel(ua, n, o, a.grad_bf16, a.kind == kOptAdamW,
+                                              a.grad_sumsq + m0, a.W_sumsq + m0, a.part + part_off,
+                                              (unsigned)nb, st))
+        return e;
     }
     FPO_LAUNCH("update_reduce", st,
                update_reduce_kernel<<<dim3(n), dim3(256), 0, st>>>(ua, o, a.part + part_off,

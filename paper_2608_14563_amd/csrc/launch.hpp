@@ -58,6 +58,7 @@ struct PgLaunch {
   const void* u[kMaxMats];
   const void* x_in[kMaxMats];       // [T, d]
   float* dW3[kMaxMats];
+  uint16_t* dW3_bf16[kMaxMats];     // staged bf16 pseudogradient (instead of dW3), or null
   float* dW1[kMaxMats];
   float* dW2[kMaxMats];
   const float* ref[kMaxMats];
@@ -82,13 +83,16 @@ struct PgLaunch {
 hipError_t launch_pseudograd(const PgLaunch& a);
 int64_t pseudograd_tiles(bool bf16, int64_t M, int64_t N);
 
+constexpr int kOptAdamW = 1;  // fpo_opt_kind FPO_OPT_ADAMW
+
 struct UpdLaunch {
   int kind;
   double lr, momentum, beta1, beta2, adam_eps, weight_decay, clip_frac;
   int64_t step;
   int n;
   int64_t numel[kMaxMats];
-  const float* grad[kMaxMats];
+  const void* grad[kMaxMats];       // float32, or bf16 when grad_bf16
+  bool grad_bf16;
   float* W[kMaxMats];
   void* W_lp[kMaxMats];
   bool lp_bf16;

@@ -51,85 +51,106 @@ __device__ __forceinline__ float clip_factor(double gs, double ws, double frac) 
   return (float)(s < 1.0 ? s : 1.0);
 }
 
-// Update of block b (kElemsPerBlock elements from b * kElemsPerBlock) of one
-// matrix with clip factor s; writes the block's ||W'||^2 to *part_b. Every
-// thread of the 256-thread workgroup must call it (it reduces through `red`,
-// 16 doubles of LDS).
-__device__ __forceinline__ void update_block(const float* __restrict__ g, float* __restrict__ W,
-                                             void* lp, float* __restrict__ s1,
-                                             float* __restrict__ s2, int64_t numel, int64_t b,
-                                             float s, const OptScalars& o, double* red,
-                                             double* part_b) {
-  const int64_t base = b * kElemsPerBlock;
-  const int64_t end = (numel < base + kElemsPerBlock) ? numel : base + kElemsPerBlock;
-  // Every operand is streamed once: all of a thread's loads are issued before
-  // any store (they overlap instead of serialising per step), and loads and
-  // stores are non-temporal so the stream does not evict cached data.
+// Update of NB blocks (kElemsPerBlock elements each; block k starts at
+// (b0 + k * bstride) * kElemsPerBlock, blocks at or past nb are skipped) of one
+// matrix with clip factor s; writes each block's ||W'||^2 to part[block].
+// Every thread of the 256-thread workgroup must call it (it reduces through
+// `red`, 16 doubles of LDS). ADAM selects the optimizer at compile time so
+// that SGD keeps no second-moment registers. The gradient is float32, or bf16
+// when GB16 (the staged pseudogradient, widened exactly). A block's result
+// and partial do not depend on NB or on which blocks share the call.
+template <bool GB16, bool ADAM, int NB>
+__device__ __forceinline__ void update_visit(const void* __restrict__ gp, float* __restrict__ W,
+                                              void* lp, float* __restrict__ s1,
+                                              float* __restrict__ s2, int64_t numel, int64_t b0,
+                                              int64_t bstride, int64_t nb, float s,
+                                              const OptScalars& o, double* red,
+                                              double* __restrict__ part) {
+  // Every operand is streamed once: all of a thread's loads (of all NB blocks)
+  // are issued before any store, and loads and stores are non-temporal so the
+  // stream does not evict cached data.
   constexpr int U = kElemsPerBlock / 1024;
-  const bool sgd = o.kind == 0;
   // plain SGD (momentum 0, no state buffer): b = s * dW each step
-  const bool fresh = sgd && (o.first || s1 == nullptr);
-  f32x4 gv[U], w[U], v1[U], v2[U];
+  const bool fresh = !ADAM && (o.first || s1 == nullptr);
+  f32x4 gv[NB][U], w[NB][U], v1[NB][U];
+  f32x4 v2[ADAM ? NB : 1][U];
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int64_t i = base + threadIdx.x * 4 + u * 1024;
-    gv[u] = w[u] = v1[u] = v2[u] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (i < end) {
-      gv[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(g + i));
-      w[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(W + i));
-      if (!fresh) v1[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s1 + i));
-      if (!sgd) v2[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s2 + i));
+  for (int k = 0; k < NB; ++k) {
+    const int64_t base = (b0 + k * bstride) * kElemsPerBlock;
+    const int64_t end = (b0 + k * bstride >= nb) ? 0 : (numel < base + kElemsPerBlock ? numel : base + kElemsPerBlock);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + threadIdx.x * 4 + u * 1024;
+      gv[k][u] = w[k][u] = v1[k][u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if constexpr (ADAM) v2[k][u] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (i < end) {
+        if constexpr (GB16) {
+          const u32x2 h = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>((const uint16_t*)gp + i));
+          gv[k][u] = f32x4{bf16_lo(h.x), bf16_hi(h.x), bf16_lo(h.y), bf16_hi(h.y)};
+        } else {
+          gv[k][u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>((const float*)gp + i));
+        }
+        w[k][u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(W + i));
+        if (!fresh) v1[k][u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s1 + i));
+        if constexpr (ADAM) v2[k][u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s2 + i));
+      }
     }
   }
-  float ss = 0.f;
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int64_t i = base + threadIdx.x * 4 + u * 1024;
-    if (i >= end) continue;
-    const f32x4 gs = gv[u] * s;
-    f32x4 wv = w[u];
-    if (sgd) {  // SGD with momentum
-      f32x4 bv;
-      if (fresh) {
-        bv = gs;
-      } else {
-        bv.x = fmaf(o.momentum, v1[u].x, gs.x);
-        bv.y = fmaf(o.momentum, v1[u].y, gs.y);
-        bv.z = fmaf(o.momentum, v1[u].z, gs.z);
-        bv.w = fmaf(o.momentum, v1[u].w, gs.w);
-      }
-      if (s1) __builtin_nontemporal_store(bv, reinterpret_cast<f32x4*>(s1 + i));
-      wv.x = fmaf(-o.lr, bv.x, wv.x);
-      wv.y = fmaf(-o.lr, bv.y, wv.y);
-      wv.z = fmaf(-o.lr, bv.z, wv.z);
-      wv.w = fmaf(-o.lr, bv.w, wv.w);
-    } else {  // AdamW, decoupled weight decay, bias corrected
-      f32x4 mv = v1[u], vv = v2[u];
+  for (int k = 0; k < NB; ++k) {
+    const int64_t blk = b0 + k * bstride;
+    const int64_t base = blk * kElemsPerBlock;
+    const int64_t end = (blk >= nb) ? 0 : (numel < base + kElemsPerBlock ? numel : base + kElemsPerBlock);
+    float ss = 0.f;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float ge = gs[e];
-        const float me = o.beta1 * mv[e] + o.one_m_beta1 * ge;
-        const float ve = o.beta2 * vv[e] + o.one_m_beta2 * ge * ge;
-        mv[e] = me;
-        vv[e] = ve;
-        const float denom = sqrtf(ve) * o.inv_sqrt_bc2 + o.adam_eps;
-        wv[e] = wv[e] * o.decay - o.lr * (me * o.inv_bc1) / denom;
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = base + threadIdx.x * 4 + u * 1024;
+      if (i >= end) continue;
+      const f32x4 gs = gv[k][u] * s;
+      f32x4 wv = w[k][u];
+      if constexpr (!ADAM) {  // SGD with momentum
+        f32x4 bv;
+        if (fresh) {
+          bv = gs;
+        } else {
+          bv.x = fmaf(o.momentum, v1[k][u].x, gs.x);
+          bv.y = fmaf(o.momentum, v1[k][u].y, gs.y);
+          bv.z = fmaf(o.momentum, v1[k][u].z, gs.z);
+          bv.w = fmaf(o.momentum, v1[k][u].w, gs.w);
+        }
+        if (s1) __builtin_nontemporal_store(bv, reinterpret_cast<f32x4*>(s1 + i));
+        wv.x = fmaf(-o.lr, bv.x, wv.x);
+        wv.y = fmaf(-o.lr, bv.y, wv.y);
+        wv.z = fmaf(-o.lr, bv.z, wv.z);
+        wv.w = fmaf(-o.lr, bv.w, wv.w);
+      } else {  // AdamW, decoupled weight decay, bias corrected
+        f32x4 mv = v1[k][u], vv = v2[k][u];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float ge = gs[e];
+          const float me = o.beta1 * mv[e] + o.one_m_beta1 * ge;
+          const float ve = o.beta2 * vv[e] + o.one_m_beta2 * ge * ge;
+          mv[e] = me;
+          vv[e] = ve;
+          const float denom = sqrtf(ve) * o.inv_sqrt_bc2 + o.adam_eps;
+          wv[e] = wv[e] * o.decay - o.lr * (me * o.inv_bc1) / denom;
+        }
+        __builtin_nontemporal_store(mv, reinterpret_cast<f32x4*>(s1 + i));
+        __builtin_nontemporal_store(vv, reinterpret_cast<f32x4*>(s2 + i));
       }
-      __builtin_nontemporal_store(mv, reinterpret_cast<f32x4*>(s1 + i));
-      __builtin_nontemporal_store(vv, reinterpret_cast<f32x4*>(s2 + i));
+      __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>(W + i));
+      if (lp) {
+        if (o.lp_bf16)
+          __builtin_nontemporal_store(u32x2{pack_bf16x2(wv.x, wv.y), pack_bf16x2(wv.z, wv.w)},
+                                      reinterpret_cast<u32x2*>((uint16_t*)lp + i));
+        else
+          __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>((float*)lp + i));
+      }
+      ss += wv.x * wv.x + wv.y * wv.y + wv.z * wv.z + wv.w * wv.w;
     }
-    __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>(W + i));
-    if (lp) {
-      if (o.lp_bf16)
-        __builtin_nontemporal_store(u32x2{pack_bf16x2(wv.x, wv.y), pack_bf16x2(wv.z, wv.w)},
-                                    reinterpret_cast<u32x2*>((uint16_t*)lp + i));
-      else
-        __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>((float*)lp + i));
-    }
-    ss += wv.x * wv.x + wv.y * wv.y + wv.z * wv.z + wv.w * wv.w;
+    const double t = block_sum_d((double)ss, red);
+    if (threadIdx.x == 0 && blk < nb) part[blk] = t;
   }
-  const double t = block_sum_d((double)ss, red);
-  if (threadIdx.x == 0) *part_b = t;
 }
 
 }  // namespace fpo

@@ -54,7 +54,7 @@ def test_library_exports_every_header_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert lib.fpo_abi_version() == 2 == L.ABI_VERSION
+    assert lib.fpo_abi_version() == 3 == L.ABI_VERSION
 
 
 def oe(T=128, d=256, V=4096, dtype=L.FPO_BF16, eps=1e-6, min_rms=0.5, chunk=0):
@@ -163,7 +163,7 @@ def test_pseudograd_validation(lib):
     assert call(pmode, g=None, pf=pf, ws_bytes=16) == L.FPO_ERR_WORKSPACE
     assert call(pmode, g=None) == L.FPO_ERR_ARG          # mode without the argument
     assert call(good, pf=pf) == L.FPO_ERR_ARG            # argument without the mode
-    assert call(L.PgDesc(128, 256, 688, 2, 1, 4, 1.0)) == L.FPO_ERR_ARG  # unknown mode bit
+    assert call(L.PgDesc(128, 256, 688, 2, 1, 8, 1.0)) == L.FPO_ERR_ARG  # unknown mode bit
     assert call(pmode, g=None, pf=C.byref(L.PostFfn(None, mo, gm, 1e-6, 0.5))) == L.FPO_ERR_NULL
     assert call(pmode, g=None, pf=C.byref(L.PostFfn(FAKE, None, gm, 1e-6, 0.5))) == L.FPO_ERR_NULL
     m1, km1 = arr([FAKE, None])
@@ -175,6 +175,17 @@ def test_pseudograd_validation(lib):
     w0 = lib.fpo_pseudograd_workspace(C.byref(good))
     w1 = lib.fpo_pseudograd_workspace(C.byref(pmode))
     assert w1 >= w0 + (2 - 1) * 256 * 128 * 2
+    # bf16 staging of the pseudogradient for the fused update (W3-only bf16 path)
+    stg = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_GRAD_BF16, 1 / 128)
+    assert call(L.PgDesc(128, 256, 688, 2, L.FPO_F32, L.FPO_MODE_GRAD_BF16, 1 / 128)) == L.FPO_ERR_UNSUPPORTED
+    assert call(L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_GRAD_BF16 | L.FPO_MODE_FULL_MLP,
+                         1 / 128)) == L.FPO_ERR_UNSUPPORTED
+    assert lib.fpo_pseudograd_workspace(C.byref(L.PgDesc(128, 256, 688, 2, L.FPO_F32, L.FPO_MODE_GRAD_BF16,
+                                                         1 / 128))) == 0
+    assert call(stg) == L.FPO_ERR_ARG                    # dW3 given
+    assert call(stg, dW3=None) == L.FPO_ERR_ARG          # no fused update
+    w2 = lib.fpo_pseudograd_workspace(C.byref(stg))
+    assert w2 >= w0 + 2 * 256 * 688 * 2                   # one staged bf16 matrix per layer
     # bf16 operand bands (T x d_ff activations) above 2^31 bytes are refused
     assert call(L.PgDesc(1 << 17, 256, 16384, 2, L.FPO_BF16, L.FPO_MODE_W3, 1.0)) == L.FPO_ERR_UNSUPPORTED
 

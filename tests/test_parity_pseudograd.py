@@ -146,10 +146,11 @@ def test_full_size_sampled(dev, cid):
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("cid", [1, 2, 3])
-def test_full_size_fused_update(dev, cid):
+@pytest.mark.parametrize("cid,stage", [(1, False), (2, False), (3, False), (1, True), (3, True)])
+def test_full_size_fused_update(dev, cid, stage):
     """The benchmark's launch configuration at full size: pseudogradient with
-    the SGD-momentum step overlapped (first step). Sampled momentum entries
+    the SGD-momentum step overlapped (first step), its pseudogradient returned
+    in fp32 or staged in bf16 (FPO_MODE_GRAD_BF16). Sampled momentum entries
     against the oracle's clipped pseudogradient s * D (s from the reported
     norms), W' and the bf16 copy exactly as fp32 / RNE from the GPU momentum,
     and the reported clip factor."""
@@ -168,8 +169,8 @@ def test_full_size_fused_update(dev, cid):
     ss = torch.empty(c.L, dtype=torch.float64, device=dev)
     cs = torch.empty(c.L, dtype=torch.float32, device=dev)
     opt = api.OptConfig(lr=c.lr, clip_frac=c.clip_frac, step=1)
-    api.fpo_pseudograd(tg, ta, dW3=dW, sumsq=ss, opt=opt, W_master=W, W_lp=lp, state1=s1, W_sumsq=Wsq,
-                       clip_scale=cs)
+    api.fpo_pseudograd(tg, ta, dW3=None if stage else dW, sumsq=ss, opt=opt, W_master=W, W_lp=lp, state1=s1,
+                       W_sumsq=Wsq, clip_scale=cs, grad_bf16=stage)
     torch.cuda.synchronize()
     ssh = ss.cpu().numpy()
     gf = I.storage_to_f64(g)

@@ -185,3 +185,59 @@ def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip, pff
             assert torch.equal(sep[key], fus[key]), (key, step)
     if clip < 1e-4:
         assert float(fus["cs"].max()) < 1.0  # the clip was active
+
+
+@pytest.mark.parametrize("kind", ["sgd", "adamw", "sgd-plain"])
+@pytest.mark.parametrize("T,d,d_ff,L,clip,pffn", [(300, 264, 1000, 3, 0.01, False), (200, 1032, 1288, 3, 1e-5, False),
+                                                  (300, 264, 1000, 2, 0.01, True)])
+def test_fused_update_with_bf16_staged_pseudogradient(dev, kind, T, d, d_ff, L, clip, pffn):
+    """FPO_MODE_GRAD_BF16: the fused path stages each layer's pseudogradient
+    rounded to bf16 (RNE). Over two steps it is bit-identical to the separate
+    calls fed the same rounded pseudogradient (the fp32 pseudogradient rounded
+    by torch) and the staged call's norms; those norms are the squared norms of
+    the rounded values."""
+    c = I.CONFIGS[1].shrink(T=T, d=d, d_ff=d_ff, L=L)
+    g = dev_tensor(I.synthetic_signal(c), dev)
+    kw = {}
+    if pffn:
+        g32 = torch.from_numpy(I.normal(c.cid, I.T_G, 7, T * d, std=0.02).reshape(T, d)).to(dev)
+        pfs = [I.post_ffn(c, l) for l in range(L)]
+        kw = dict(post_ffn=api.PostFfn(g32, [dev_tensor(m, dev) for m, _ in pfs], [dev_tensor(x, dev) for _, x in pfs]))
+    acts = [dev_tensor(I.activation(c, l), dev) for l in range(L)]
+    W0 = [torch.from_numpy(I.master_weight(c, l)).to(dev) for l in range(L)]
+    adam = kind == "adamw"
+    plain = kind == "sgd-plain"
+
+    def fresh():
+        W = [w.clone() for w in W0]
+        return dict(W=W, s1=None if plain else [torch.zeros_like(w) for w in W],
+                    s2=[torch.zeros_like(w) for w in W] if adam else None,
+                    lp=[torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in W],
+                    Wsq=torch.tensor([float((w.double() ** 2).sum()) for w in W], dtype=torch.float64, device=dev),
+                    ss=torch.empty(L, dtype=torch.float64, device=dev),
+                    cs=torch.empty(L, dtype=torch.float32, device=dev))
+
+    sep, fus = fresh(), fresh()
+    dW = [torch.empty(d, d_ff, dtype=torch.float32, device=dev) for _ in range(L)]
+    for step in (1, 2):
+        opt = api.OptConfig(kind=L_.FPO_OPT_ADAMW if adam else L_.FPO_OPT_SGD, lr=1e-2, clip_frac=clip, step=step,
+                            momentum=0.0 if plain else 0.9)
+        api.fpo_pseudograd(g, acts, dW3=None, sumsq=fus["ss"], opt=opt, W_master=fus["W"], W_lp=fus["lp"],
+                           state1=fus["s1"], state2=fus["s2"], W_sumsq=fus["Wsq"], clip_scale=fus["cs"],
+                           grad_bf16=True, **kw)
+        api.fpo_pseudograd(g, acts, dW3=dW, sumsq=sep["ss"], **kw)
+        dWr = [x.to(torch.bfloat16).float() for x in dW]
+        torch.cuda.synchronize()
+        for l in range(L):
+            n2 = float((dWr[l].double() ** 2).sum())
+            assert abs(float(fus["ss"][l]) - n2) <= 1e-6 * n2, (l, step)
+        api.fpo_apply_update(opt, dWr, fus["ss"], sep["W"], sep["s1"], sep["Wsq"], W_lp=sep["lp"],
+                             state2=sep["s2"], clip_scale=sep["cs"])
+        torch.cuda.synchronize()
+        for key in ("W", "lp") + (("s2",) if adam else ()) + (() if plain else ("s1",)):
+            for a, b in zip(sep[key], fus[key]):
+                assert torch.equal(a, b), (key, step)
+        for key in ("Wsq", "cs"):
+            assert torch.equal(sep[key], fus[key]), (key, step)
+    if clip < 1e-4:
+        assert float(fus["cs"].max()) < 1.0
