@@ -23,7 +23,8 @@ Readings of points the paper leaves open (each listed in the design notes):
   * dW is divided by the token count T; e, g and g~ stay per token;
   * the 1% clip applies to the gradient before the optimizer (App. A
     pseudocode), against the Frobenius norm of the fp32 master;
-    s = 1 when ||dW|| = 0;
+    s = 1 when ||dW|| = 0; the other reading (App. A prose: the weight update
+    itself is clipped) is the *_update_clip pair;
   * a target outside [0, V) zeroes that token's error row, gives loss 0 and
     is counted;
   * argmax takes the lowest index among equal maxima;
@@ -237,6 +238,37 @@ def adamw(W, m, v, G, lr, step, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0
     vh = v2 / (1.0 - beta2 ** step)
     W2 = _f64(W) * (1.0 - lr * weight_decay) - lr * mh / (np.sqrt(vh) + eps)
     return W2, m2, v2
+
+
+# --------------------------------------------------------------------------
+# The other reading of the 1% clip (App. A prose: each step's weight update is
+# clipped, ||W' - W||_F <= frac ||W||_F): the optimizer runs on the unclipped
+# gradient, its state advances unclipped, and only the step applied to W is
+# scaled.
+def sgd_momentum_update_clip(W, buf, G, lr, momentum=0.9, step=1, frac=0.01):
+    """Return (W', buf', s): buf' as in sgd_momentum, delta = -lr * buf',
+    s = clip_scale(||delta||^2, ||W||^2, frac), W' = W + s * delta."""
+    G = _f64(G)
+    b = G.copy() if step == 1 else momentum * _f64(buf) + G
+    W = _f64(W)
+    delta = -lr * b
+    s = clip_scale(float(np.sum(delta * delta)), float(np.sum(W * W)), frac)
+    return W + s * delta, b, s
+
+
+def adamw_update_clip(W, m, v, G, lr, step, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01, frac=0.01):
+    """Return (W', m', v', s): moments as in adamw, delta = -lr * wd * W -
+    lr * m_hat / (sqrt(v_hat) + eps) (the whole AdamW step, decay included),
+    s = clip_scale(||delta||^2, ||W||^2, frac), W' = W + s * delta."""
+    G = _f64(G)
+    m2 = beta1 * _f64(m) + (1.0 - beta1) * G
+    v2 = beta2 * _f64(v) + (1.0 - beta2) * G * G
+    mh = m2 / (1.0 - beta1 ** step)
+    vh = v2 / (1.0 - beta2 ** step)
+    W = _f64(W)
+    delta = -lr * weight_decay * W - lr * mh / (np.sqrt(vh) + eps)
+    s = clip_scale(float(np.sum(delta * delta)), float(np.sum(W * W)), frac)
+    return W + s * delta, m2, v2, s
 
 
 def bf16_rne(x):

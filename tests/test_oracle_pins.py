@@ -426,6 +426,46 @@ def test_adamw_matches_torch_three_steps():
     np.testing.assert_allclose(v, opt.state[P]["exp_avg_sq"].numpy(), rtol=1e-13)
 
 
+@pytest.mark.parametrize("kind", ["sgd", "adamw"])
+@pytest.mark.parametrize("frac", [1e-4, 10.0])
+def test_update_clip_variant_against_torch(kind, frac):
+    """The clip-the-update reading: torch.optim's own step from the current
+    (clipped) weights gives the unclipped update delta; the oracle must apply
+    W + s * delta with s = min(1, frac ||W|| / ||delta||) and keep torch's
+    (unclipped) optimizer state, over three steps. frac 10 leaves the clip
+    idle, so the result is torch's trajectory itself."""
+    r = np.random.default_rng(44)
+    W = r.standard_normal((4, 5))
+    Gs = [r.standard_normal((4, 5)) * (1e-3 if kind == "adamw" else 1.0) for _ in range(3)]
+    P = torch.nn.Parameter(torch.tensor(W))
+    opt = (torch.optim.SGD([P], lr=1e-2, momentum=0.9) if kind == "sgd" else
+           torch.optim.AdamW([P], lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=0.01))
+    Wo, b1, b2 = W.copy(), np.zeros_like(W), np.zeros_like(W)
+    for k, G in enumerate(Gs, start=1):
+        with torch.no_grad():
+            P.copy_(torch.tensor(Wo))
+        P.grad = torch.tensor(G)
+        opt.step()
+        delta = P.detach().numpy() - Wo
+        s_exp = min(1.0, frac * np.linalg.norm(Wo) / np.linalg.norm(delta))
+        if kind == "sgd":
+            W2, b1, s = O.sgd_momentum_update_clip(Wo, b1, G, 1e-2, 0.9, step=k, frac=frac)
+            np.testing.assert_allclose(b1, opt.state[P]["momentum_buffer"].numpy(), rtol=1e-14)
+        else:
+            W2, b1, b2, s = O.adamw_update_clip(Wo, b1, b2, G, 1e-3, k, frac=frac)
+            np.testing.assert_allclose(b1, opt.state[P]["exp_avg"].numpy(), rtol=1e-13)
+            np.testing.assert_allclose(b2, opt.state[P]["exp_avg_sq"].numpy(), rtol=1e-13)
+        assert abs(s - s_exp) <= 1e-12 * s_exp
+        np.testing.assert_allclose(W2 - Wo, s_exp * delta, rtol=1e-9, atol=1e-15)
+        if frac < 1.0:
+            assert s < 1.0
+            assert abs(np.linalg.norm(W2 - Wo) - frac * np.linalg.norm(Wo)) <= 1e-9 * frac * np.linalg.norm(Wo)
+        else:
+            assert s == 1.0
+            np.testing.assert_allclose(W2, P.detach().numpy(), rtol=1e-13, atol=1e-15)
+        Wo = W2
+
+
 # ------------------------------------------------------------ cosine
 def test_cosine_closed_forms():
     r = np.random.default_rng(51)
