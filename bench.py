@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--grad-f32", action="store_true",
                     help="hand the fused update an fp32 pseudogradient instead of the bf16-staged one "
                          "(FPO_MODE_GRAD_BF16, the precision of the paper's bf16 einsum)")
+    ap.add_argument("--clip-target", choices=["gradient", "update"], default="gradient",
+                    help="what the 1%% clip bounds: the gradient before the step (App. A pseudocode) or the "
+                         "step applied to W (two passes, no overlap with the outer products)")
     ap.add_argument("--optimizer", choices=sorted(OPT_BYTES), default="sgd-momentum",
                     help="optimizer on the fp32 masters (HBM bytes per parameter: " +
                          ", ".join(f"{k} {v}" for k, v in sorted(OPT_BYTES.items())) + ")")
@@ -134,7 +137,7 @@ def profiled_traffic(workload: str, kernel: str):
     return None
 
 
-def kernel_work(name, c, steps, nchunk, opt="sgd-momentum", pffn=False, grad_bf16=False):
+def kernel_work(name, c, steps, nchunk, opt="sgd-momentum", pffn=False, grad_bf16=False, clip_update=False):
     """Algorithmic work of one kernel over `steps` steps: (amount, unit, bound).
     Flops count only the method's contractions; bytes count each operand once."""
     T, d, V, dff, L = c.T, c.d, c.V, c.d_ff, c.L
@@ -142,8 +145,15 @@ def kernel_work(name, c, steps, nchunk, opt="sgd-momentum", pffn=False, grad_bf1
         return 2.0 * T * V * d * steps, "flop", "mfma"
     if name == "outer":
         return 2.0 * T * d * dff * L * steps, "flop", "mfma"
-    if name == "update":  # a staged bf16 pseudogradient reads 2 bytes instead of 4
-        return (OPT_BYTES[opt] - (2.0 if grad_bf16 else 0.0)) * L * d * dff * steps, "byte", "hbm"
+    gb = 2.0 if grad_bf16 else 4.0  # a staged bf16 pseudogradient reads 2 bytes instead of 4
+    if name == "update" and clip_update:  # pass 2: W r/w, bf16 copy, the new state (or dW) read
+        per = {"sgd-momentum": 14.0, "sgd": 10.0 + gb, "adamw": 18.0}[opt]
+        return per * L * d * dff * steps, "byte", "hbm"
+    if name == "update_delta":  # pass 1: dW (and state, W for AdamW) read, new state written
+        per = {"sgd-momentum": gb + 8.0, "sgd": gb, "adamw": gb + 20.0}[opt]
+        return per * L * d * dff * steps, "byte", "hbm"
+    if name == "update":
+        return (OPT_BYTES[opt] - (4.0 - gb)) * L * d * dff * steps, "byte", "hbm"
     if name == "chunk_stats":
         # per-(token, 128-entry block) max / sum / argmax read; per-token state written
         return (12.0 * T * ((V + 127) // 128) + 32.0 * T) * steps, "byte", "hbm"
@@ -431,7 +441,8 @@ def main():
             mid.record()
         api.fpo_pseudograd(g_lp, tacts, dW3=None if stage else dW, sumsq=ss, grad_bf16=stage,
                            opt=api.OptConfig(kind=1 if adam else 0, lr=c.lr, momentum=0.0 if plain else 0.9,
-                                             clip_frac=c.clip_frac, step=step_no[0]),
+                                             clip_frac=c.clip_frac, step=step_no[0],
+                                             clip_target=1 if args.clip_target == "update" else 0),
                            W_master=Wm, W_lp=Wlp, state1=s1, state2=s2, W_sumsq=Wsq, ws=ws_pg, post_ffn=pffn)
 
     lib = prof_lib()
@@ -474,7 +485,8 @@ def main():
     log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step, {tok_s:.0f} tokens/s; dominant kernel {dom}: "
         f"{dom_stats[0] / dom_stats[1]:.3f} ms avg over {dom_stats[1]} launches")
     nchunk = None
-    w = kernel_work(dom, c, args.steps, nchunk, args.optimizer, args.post_ffn, stage)
+    cu = args.clip_target == "update"
+    w = kernel_work(dom, c, args.steps, nchunk, args.optimizer, args.post_ffn, stage, cu)
     roof = None
     traffic = profiled_traffic(c.name, dom)
     if w is not None:
@@ -492,7 +504,7 @@ def main():
                     "avg_launch_ms": round(dom_stats[0] / dom_stats[1], 4), "launches": dom_stats[1]}
     kernels = {}
     for k, (ms, n) in per_kernel.items():
-        wk = kernel_work(k, c, 1, nchunk, args.optimizer, args.post_ffn, stage)
+        wk = kernel_work(k, c, 1, nchunk, args.optimizer, args.post_ffn, stage, cu)
         e = {"ms_per_step": round(ms, 4), "launches": n}
         if wk is not None:
             amount, unit, bound = wk
@@ -531,7 +543,7 @@ def main():
                                f"{OPT_NAME[args.optimizer]} "
                                f"on fp32 masters, 1% relative clip", "T": c.T, "d": c.d, "d_ff": c.d_ff, "V": c.V, "L": c.L,
                    "optimizer": args.optimizer, "post_ffn_norm": bool(args.post_ffn),
-                   "pseudogradient_staging": "f32" if args.grad_f32 else "bf16"},
+                   "pseudogradient_staging": "f32" if args.grad_f32 else "bf16", "clip_target": args.clip_target},
         "step_mfma_frac": round(flops_step / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "substeps": substeps,
         "roofline": roof,

@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define FPO_ABI_VERSION 3
+#define FPO_ABI_VERSION 4
 
 typedef enum {
   FPO_OK = 0,
@@ -71,6 +71,7 @@ typedef enum {
   FPO_MODE_GRAD_BF16 = 4
 } fpo_mode; /* bit flags */
 typedef enum { FPO_OPT_SGD = 0, FPO_OPT_ADAMW = 1 } fpo_opt_kind;
+typedef enum { FPO_CLIP_GRADIENT = 0, FPO_CLIP_UPDATE = 1 } fpo_clip_target;
 
 /* Output-error call description.
  *   eps         inside rho = sqrt(mean x^2 + eps), forward and VJP (Sec. 3.2)
@@ -107,8 +108,15 @@ typedef struct {
  *          step (step == 1) stores the clipped gradient as the buffer.
  *   AdamW: beta1, beta2, adam_eps, decoupled weight_decay (0.01 in the
  *          paper), bias correction with the 1-based `step`.
- *   clip_frac  relative clip ||s*dW||_F <= clip_frac * ||W||_F applied to the
- *          gradient before the step (0.01 in the paper); <= 0 disables it.
+ *   clip_frac  relative clip, 0.01 in the paper; <= 0 disables it.
+ *   clip_target  what the clip bounds. FPO_CLIP_GRADIENT (0, the App. A
+ *          pseudocode): ||s*dW||_F <= clip_frac * ||W||_F applied to the
+ *          gradient before the step. FPO_CLIP_UPDATE (1, the App. A prose
+ *          "clip each step's weight update"): the optimizer runs on the
+ *          unclipped gradient and its state advances unclipped; only the
+ *          step applied to W is scaled, ||W' - W||_F <= clip_frac * ||W||_F,
+ *          with delta = -lr * b' (SGD) or -lr*wd*W - lr*m_hat/(sqrt(v_hat)+eps)
+ *          (AdamW). Two streaming passes instead of one.
  * Hyperparameters are double; the derived factors (1 - beta, 1 - lr * wd,
  * bias corrections) are formed in double on the host and rounded once to
  * float32 for the device arithmetic. AdamW moments must be zero before step 1;
@@ -117,6 +125,7 @@ typedef struct {
   int32_t kind; /* fpo_opt_kind */
   double lr, momentum, beta1, beta2, adam_eps, weight_decay, clip_frac;
   int64_t step;
+  int32_t clip_target; /* fpo_clip_target */
 } fpo_opt;
 
 /* Buffers an update writes in place. Every member is a [host] array of
@@ -132,7 +141,8 @@ typedef struct {
  *   state2    AdamW second moment, in/out (NULL for SGD)
  *   W_sumsq   device double[n_mats]: in ||W||_F^2 of the current masters
  *             (the clip's reference), out ||W'||_F^2 of the new masters
- *   clip_scale device float[n_mats], out: the clip factor s used (nullable) */
+ *   clip_scale device float[n_mats], out: the clip factor s used (nullable;
+ *             in FPO_CLIP_UPDATE mode the factor applied to the update) */
 typedef struct {
   float* const* W_master;
   void* const* W_lp;
@@ -251,6 +261,8 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
  * min(1, clip_frac * sqrt(W_sumsq[m]) / sqrt(grad_sumsq[m])); G = s_m * grad;
  * then the SGD-momentum or AdamW step on W_master, the optional low-precision
  * copy, and W_sumsq[m] <- ||W'||_F^2. The scale is computed on the device.
+ * With opt->clip_target == FPO_CLIP_UPDATE the same s formula takes
+ * ||delta||^2 of the unclipped step instead of grad_sumsq (see fpo_opt).
  *
  *   n_mats       number of matrices (<= 64 per call)
  *   numel        [host] int64 [n_mats]: elements per matrix (multiple of 4)

@@ -15,6 +15,7 @@ FPO_OK, FPO_ERR_NULL, FPO_ERR_SHAPE, FPO_ERR_DTYPE, FPO_ERR_ARG, FPO_ERR_WORKSPA
 FPO_F32, FPO_BF16 = 0, 1
 FPO_MODE_W3, FPO_MODE_FULL_MLP, FPO_MODE_POST_FFN, FPO_MODE_GRAD_BF16 = 0, 1, 2, 4  # bit flags
 FPO_OPT_SGD, FPO_OPT_ADAMW = 0, 1
+FPO_CLIP_GRADIENT, FPO_CLIP_UPDATE = 0, 1
 
 STATUS_NAMES = {0: "FPO_OK", 1: "FPO_ERR_NULL", 2: "FPO_ERR_SHAPE", 3: "FPO_ERR_DTYPE", 4: "FPO_ERR_ARG",
                 5: "FPO_ERR_WORKSPACE", 6: "FPO_ERR_UNSUPPORTED", 7: "FPO_ERR_HIP"}
@@ -39,7 +40,7 @@ class PgDesc(C.Structure):
 class Opt(C.Structure):
     _fields_ = [("kind", C.c_int32), ("lr", C.c_double), ("momentum", C.c_double), ("beta1", C.c_double),
                 ("beta2", C.c_double), ("adam_eps", C.c_double), ("weight_decay", C.c_double),
-                ("clip_frac", C.c_double), ("step", C.c_int64)]
+                ("clip_frac", C.c_double), ("step", C.c_int64), ("clip_target", C.c_int32)]
 
 
 class UpdateBufs(C.Structure):
@@ -53,7 +54,7 @@ class PostFfn(C.Structure):
                 ("eps", C.c_float), ("min_rms", C.c_float)]
 
 
-ABI_VERSION = 3
+ABI_VERSION = 4
 PP = C.POINTER(C.c_void_p)
 VP = C.c_void_p
 _lib = None

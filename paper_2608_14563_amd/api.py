@@ -118,10 +118,11 @@ class OptConfig:
     weight_decay: float = 0.01
     clip_frac: float = 0.01
     step: int = 1
+    clip_target: int = L.FPO_CLIP_GRADIENT  # or L.FPO_CLIP_UPDATE: bound ||W' - W|| instead of ||dW||
 
     def c(self) -> L.Opt:
         return L.Opt(self.kind, self.lr, self.momentum, self.beta1, self.beta2, self.adam_eps,
-                     self.weight_decay, self.clip_frac, self.step)
+                     self.weight_decay, self.clip_frac, self.step, self.clip_target)
 
 
 def _upd_bufs(keep: _Keep, W_master, W_lp, state1, state2, W_sumsq, clip_scale, lp_dtype):

@@ -161,7 +161,7 @@ PgPlan plan_pg(const fpo_pg_desc& d) {
 }
 
 size_t carve_pg(const fpo_pg_desc& d, const PgPlan& p, void* ws, fpo::PgLaunch* L,
-                double** upd_part) {
+                double** upd_part, double** upd_dsq = nullptr) {
   const int64_t esz = d.dtype == FPO_BF16 ? 2 : 4;
   const bool full = (d.mode & FPO_MODE_FULL_MLP) != 0;
   const bool pffn = (d.mode & FPO_MODE_POST_FFN) != 0;
@@ -175,6 +175,7 @@ size_t carve_pg(const fpo_pg_desc& d, const PgPlan& p, void* ws, fpo::PgLaunch* 
   void* du = full ? c.take<char>(d.d_ff * p.Tp * esz) : nullptr;
   double* part = c.take<double>(std::max<int64_t>(d.L, 2) * p.ntiles * 3);
   double* up = c.take<double>(p.upd_blocks);
+  double* dsq = c.take<double>(p.nmats);  // ||delta||^2 per matrix (clip-the-update mode)
   // staged bf16 pseudogradients (FPO_MODE_GRAD_BF16), one 256-aligned matrix per layer
   const bool stage = (d.mode & FPO_MODE_GRAD_BF16) != 0;
   for (int64_t l = 0; l < (stage ? d.L : 0); ++l) {
@@ -190,6 +191,7 @@ size_t carve_pg(const fpo_pg_desc& d, const PgPlan& p, void* ws, fpo::PgLaunch* 
     L->part = part;
   }
   if (upd_part) *upd_part = up;
+  if (upd_dsq) *upd_dsq = dsq;
   return c.off;
 }
 
@@ -232,6 +234,8 @@ int check_opt(const fpo_opt* o) {
     return fail(FPO_ERR_ARG, "unknown optimizer kind %d", (int)o->kind);
   if (!(o->lr >= 0.0) || !std::isfinite(o->lr)) return fail(FPO_ERR_ARG, "lr must be finite and >= 0");
   if (o->step < 1) return fail(FPO_ERR_ARG, "step is 1-based (got %lld)", (long long)o->step);
+  if (o->clip_target != FPO_CLIP_GRADIENT && o->clip_target != FPO_CLIP_UPDATE)
+    return fail(FPO_ERR_ARG, "unknown clip_target %d", (int)o->clip_target);
   if (!std::isfinite(o->clip_frac)) return fail(FPO_ERR_ARG, "clip_frac must be finite");
   if (o->kind == FPO_OPT_SGD && !(o->momentum >= 0.0 && o->momentum <= 1.0))
     return fail(FPO_ERR_ARG, "momentum must be in [0, 1]");
@@ -278,6 +282,7 @@ int fill_update(const fpo_opt* opt, int64_t n, const int64_t* numel, const void*
   U->weight_decay = opt->weight_decay;
   U->clip_frac = opt->clip_frac;
   U->step = opt->step;
+  U->clip_update = opt->clip_target == FPO_CLIP_UPDATE;
   U->n = (int)n;
   U->lp_bf16 = lp_dtype == FPO_BF16;
   for (int64_t m = 0; m < n; ++m) {
@@ -303,10 +308,11 @@ int fill_update(const fpo_opt* opt, int64_t n, const int64_t* numel, const void*
   return FPO_OK;
 }
 
+// per-block partials, then n doubles of ||delta||^2 (clip-the-update mode)
 size_t update_ws(int64_t n, const int64_t* numel) {
   int64_t blocks = 0;
   for (int64_t m = 0; m < n; ++m) blocks += fpo::update_blocks(numel[m]);
-  return (size_t)round_up(blocks * 8, kAlign);
+  return (size_t)(round_up(blocks * 8, kAlign) + round_up(n * 8, kAlign));
 }
 
 }  // namespace
@@ -458,7 +464,8 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
   const size_t need = carve_pg(*desc, pl, nullptr, nullptr, nullptr);
   if (int e = check_ws(ws, ws_bytes, need, "fpo_pseudograd")) return e;
   double* upart = nullptr;
-  carve_pg(*desc, pl, ws, &P, &upart);
+  double* udsq = nullptr;
+  carve_pg(*desc, pl, ws, &P, &upart, &udsq);
   fpo::UpdLaunch U{};
   if (opt) {
     const int n = pl.nmats;
@@ -473,11 +480,14 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
     if (int e = fill_update(opt, n, numel, grads, sumsq, upd, desc->dtype, &U)) return e;
     U.grad_bf16 = stage;
     U.part = upart;
+    U.dsq = udsq;
     U.stream = stream;
   }
   hipError_t e;
-  if (opt && P.bf16 && !full) {
-    // W3 only, bf16: layer l's update overlaps layer l+1's outer products
+  if (opt && P.bf16 && !full && !U.clip_update) {
+    // W3 only, bf16, gradient clip: layer l's update overlaps layer l+1's
+    // outer products (clip-the-update needs every step's norm first: two
+    // passes after the pseudogradient)
     e = fpo::launch_pseudograd_update(P, U);
     if (e != hipSuccess) return hip_fail(e, "fpo_pseudograd overlapped launch");
     return FPO_OK;
@@ -505,6 +515,9 @@ int fpo_apply_update(const fpo_opt* opt, int64_t n_mats, const int64_t* numel,
     return e;
   if (int e = check_ws(ws, ws_bytes, update_ws(n_mats, numel), "fpo_apply_update")) return e;
   U.part = (double*)ws;
+  int64_t blocks = 0;
+  for (int64_t m = 0; m < n_mats; ++m) blocks += fpo::update_blocks(numel[m]);
+  U.dsq = (double*)((char*)ws + round_up(blocks * 8, kAlign));
   U.stream = stream;
   hipError_t e = fpo::launch_update(U);
   if (e != hipSuccess) return hip_fail(e, "fpo_apply_update launch");

@@ -63,6 +63,42 @@ __global__ __launch_bounds__(256) void update_loop_kernel(UpdArgs a, OptScalars 
                                   s, o, red, part);
 }
 
+// Clip-the-update mode, pass 1 (one workgroup per block): new optimizer state
+// and per-block ||delta||^2.
+template <bool GB16, bool ADAM>
+__global__ __launch_bounds__(256) void delta_kernel(UpdArgs a, int n, OptScalars o, double* __restrict__ part) {
+  __shared__ double red[16];
+  const int64_t b = blockIdx.x;
+  const int m = find_mat(a.blk0, n, b);
+  delta_block<GB16, ADAM>(a.grad[m], a.W[m], a.s1[m], a.s2[m], a.numel[m], b - a.blk0[m], o, red, part + b);
+}
+
+// Fixed-order sum of each matrix's block partials into out[m].
+__global__ __launch_bounds__(256) void sum_parts_kernel(UpdArgs a, const double* __restrict__ part,
+                                                        double* __restrict__ out) {
+  __shared__ double red[16];
+  const int m = blockIdx.x;
+  double acc = 0.0;
+  for (int64_t b = a.blk0[m] + threadIdx.x; b < a.blk0[m + 1]; b += 256) acc += part[b];
+  acc = block_sum_d(acc, red);
+  if (threadIdx.x == 0) out[m] = acc;
+}
+
+// Clip-the-update mode, pass 2: W' = W + s * delta with
+// s = min(1, clip_frac ||W|| / ||delta||), per-block ||W'||^2.
+template <bool GB16, bool ADAM>
+__global__ __launch_bounds__(256) void apply_kernel(UpdArgs a, int n, OptScalars o,
+                                                    const double* __restrict__ dsq,
+                                                    const double* __restrict__ W_sumsq,
+                                                    double* __restrict__ part) {
+  __shared__ double red[16];
+  const int64_t b = blockIdx.x;
+  const int m = find_mat(a.blk0, n, b);
+  const float s = clip_factor(dsq[m], W_sumsq[m], o.clip_frac);
+  apply_block<GB16, ADAM>(a.grad[m], a.W[m], a.W_lp[m], a.s1[m], a.s2[m], a.numel[m], b - a.blk0[m], s, o, red,
+                          part + b);
+}
+
 __global__ __launch_bounds__(256) void update_reduce_kernel(UpdArgs a, OptScalars o,
                                                             const double* __restrict__ part,
                                                             const double* __restrict__ grad_sumsq,
@@ -74,7 +110,8 @@ __global__ __launch_bounds__(256) void update_reduce_kernel(UpdArgs a, OptScalar
   for (int64_t b = a.blk0[m] + threadIdx.x; b < a.blk0[m + 1]; b += 256) acc += part[b];
   acc = block_sum_d(acc, red);
   if (threadIdx.x == 0) {
-    // the clip factor used by update_kernel, from the W_sumsq it read
+    // the clip factor the update used, from the W_sumsq it read (grad_sumsq:
+    // ||dW||^2, or ||delta||^2 in clip-the-update mode)
     if (clip_scale) clip_scale[m] = clip_factor(grad_sumsq[m], W_sumsq[m], o.clip_frac);
     W_sumsq[m] = acc;
   }
@@ -164,15 +201,35 @@ hipError_t launch_update(const UpdLaunch& a, bool blocks) {
       nb += update_blocks(a.numel[m]);
     }
     ua.blk0[n] = nb;
-    if (blocks) {
+    const double* clip_ref = a.grad_sumsq + m0;
+    if (a.clip_update) {
+      const bool adam = a.kind == kOptAdamW, gb = a.grad_bf16;
+      const dim3 g((unsigned)nb);
+      double* pt = a.part + part_off;
+      if (adam && gb) FPO_LAUNCH("update_delta", st, delta_kernel<true, true><<<g, dim3(256), 0, st>>>(ua, n, o, pt));
+      else if (adam) FPO_LAUNCH("update_delta", st, delta_kernel<false, true><<<g, dim3(256), 0, st>>>(ua, n, o, pt));
+      else if (gb) FPO_LAUNCH("update_delta", st, delta_kernel<true, false><<<g, dim3(256), 0, st>>>(ua, n, o, pt));
+      else FPO_LAUNCH("update_delta", st, delta_kernel<false, false><<<g, dim3(256), 0, st>>>(ua, n, o, pt));
+      FPO_CHECK_LAUNCH();
+      FPO_LAUNCH("update_reduce", st, sum_parts_kernel<<<dim3(n), dim3(256), 0, st>>>(ua, pt, a.dsq + m0));
+      FPO_CHECK_LAUNCH();
+      const double* dq = a.dsq + m0;
+      const double* ws = a.W_sumsq + m0;
+      if (adam && gb) FPO_LAUNCH("update", st, apply_kernel<true, true><<<g, dim3(256), 0, st>>>(ua, n, o, dq, ws, pt));
+      else if (adam) FPO_LAUNCH("update", st, apply_kernel<false, true><<<g, dim3(256), 0, st>>>(ua, n, o, dq, ws, pt));
+      else if (gb) FPO_LAUNCH("update", st, apply_kernel<true, false><<<g, dim3(256), 0, st>>>(ua, n, o, dq, ws, pt));
+      else FPO_LAUNCH("update", st, apply_kernel<false, false><<<g, dim3(256), 0, st>>>(ua, n, o, dq, ws, pt));
+      FPO_CHECK_LAUNCH();
+      clip_ref = a.dsq + m0;
+    } else if (blocks) {
       if (hipError_t e = launch_update_kernel(ua, n, o, a.grad_bf16, a.kind == kOptAdamW,
                                               a.grad_sumsq + m0, a.W_sumsq + m0, a.part + part_off,
                                               (unsigned)nb, st))
         return e;
     }
     FPO_LAUNCH("update_reduce", st,
-               update_reduce_kernel<<<dim3(n), dim3(256), 0, st>>>(ua, o, a.part + part_off,
-                                                        a.grad_sumsq + m0, a.W_sumsq + m0,
+               update_reduce_kernel<<<dim3(n), dim3(256), 0, st>>>(ua, o, a.part + part_off, clip_ref,
+                                                        a.W_sumsq + m0,
                                                         a.clip_scale ? a.clip_scale + m0 : nullptr));
     FPO_CHECK_LAUNCH();
     part_off += nb;

@@ -102,6 +102,10 @@ struct UpdLaunch {
   double* W_sumsq;
   float* clip_scale;
   double* part;
+  // clip-the-update mode: the clip bounds ||W' - W|| instead of ||dW|| (two
+  // passes; dsq: [n] ||delta||^2 scratch)
+  bool clip_update;
+  double* dsq;
   void* stream;
 };
 // blocks = false: only the per-matrix reductions (||W'||^2, clip factors) of

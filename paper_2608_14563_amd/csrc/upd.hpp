@@ -18,6 +18,7 @@ constexpr int kElemsPerBlock = 4096;  // 256 threads x 4 x float4
 struct OptScalars {
   int kind, first, lp_bf16;
   float lr, momentum, beta1, one_m_beta1, beta2, one_m_beta2, adam_eps, decay;
+  float lr_wd;  // lr * weight_decay: AdamW's decay term of the update (clip-the-update mode)
   float inv_bc1, inv_sqrt_bc2;  // 1/(1-beta1^t), 1/sqrt(1-beta2^t)
   double clip_frac;
 };
@@ -37,6 +38,7 @@ inline OptScalars make_opt_scalars(const UpdLaunch& a) {
   o.one_m_beta2 = (float)(1.0 - a.beta2);
   o.adam_eps = (float)a.adam_eps;
   o.decay = (float)(1.0 - a.lr * a.weight_decay);
+  o.lr_wd = (float)(a.lr * a.weight_decay);
   o.clip_frac = a.clip_frac;
   const double bc1 = 1.0 - pow(a.beta1, (double)a.step);
   const double bc2 = 1.0 - pow(a.beta2, (double)a.step);
@@ -151,6 +153,126 @@ __device__ __forceinline__ void update_visit(const void* __restrict__ gp, float*
     const double t = block_sum_d((double)ss, red);
     if (threadIdx.x == 0 && blk < nb) part[blk] = t;
   }
+}
+
+// ---- clip-the-update mode (||W' - W|| <= clip_frac ||W||): two passes.
+// The optimizer's update of one element, unclipped: delta = -lr * b' (SGD,
+// b' = momentum * b + g, or g at the first step / without state), or
+// delta = -lr_wd * W - lr * m_hat / (sqrt(v_hat) + eps) (AdamW) from the new
+// moments. Pass 1 writes the new state and the block's ||delta||^2; pass 2
+// recomputes delta from the stored state and applies W' = W + s * delta.
+template <bool ADAM>
+__device__ __forceinline__ float upd_delta(float w, float b_or_m, float v, const OptScalars& o) {
+  if constexpr (ADAM) {
+    const float denom = sqrtf(v) * o.inv_sqrt_bc2 + o.adam_eps;
+    return -o.lr_wd * w - o.lr * (b_or_m * o.inv_bc1) / denom;
+  } else {
+    return -o.lr * b_or_m;
+  }
+}
+
+template <bool GB16>
+__device__ __forceinline__ f32x4 load_grad4(const void* gp, int64_t i) {
+  if constexpr (GB16) {
+    const u32x2 h = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>((const uint16_t*)gp + i));
+    return f32x4{bf16_lo(h.x), bf16_hi(h.x), bf16_lo(h.y), bf16_hi(h.y)};
+  } else {
+    return __builtin_nontemporal_load(reinterpret_cast<const f32x4*>((const float*)gp + i));
+  }
+}
+
+// Pass 1 over block b: new optimizer state (written) and the block's
+// ||delta||^2 (to *part_b).
+template <bool GB16, bool ADAM>
+__device__ __forceinline__ void delta_block(const void* __restrict__ gp, const float* __restrict__ W,
+                                            float* __restrict__ s1, float* __restrict__ s2,
+                                            int64_t numel, int64_t b, const OptScalars& o,
+                                            double* red, double* part_b) {
+  constexpr int U = kElemsPerBlock / 1024;
+  const int64_t base = b * kElemsPerBlock;
+  const int64_t end = numel < base + kElemsPerBlock ? numel : base + kElemsPerBlock;
+  const bool fresh = !ADAM && (o.first || s1 == nullptr);
+  f32x4 gv[U], w[U], v1[U], v2[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t i = base + threadIdx.x * 4 + u * 1024;
+    gv[u] = w[u] = v1[u] = v2[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (i < end) {
+      gv[u] = load_grad4<GB16>(gp, i);
+      if constexpr (ADAM) {
+        w[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(W + i));
+        v2[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s2 + i));
+      }
+      if (!fresh) v1[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s1 + i));
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t i = base + threadIdx.x * 4 + u * 1024;
+    if (i >= end) continue;
+    f32x4 nb, nv = v2[u];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float ge = gv[u][e];
+      if constexpr (ADAM) {
+        nb[e] = o.beta1 * v1[u][e] + o.one_m_beta1 * ge;
+        nv[e] = o.beta2 * v2[u][e] + o.one_m_beta2 * ge * ge;
+      } else {
+        nb[e] = fresh ? ge : fmaf(o.momentum, v1[u][e], ge);
+      }
+      const float dl = upd_delta<ADAM>(w[u][e], nb[e], nv[e], o);
+      ss += dl * dl;
+    }
+    if (s1) __builtin_nontemporal_store(nb, reinterpret_cast<f32x4*>(s1 + i));
+    if constexpr (ADAM) __builtin_nontemporal_store(nv, reinterpret_cast<f32x4*>(s2 + i));
+  }
+  const double t = block_sum_d((double)ss, red);
+  if (threadIdx.x == 0) *part_b = t;
+}
+
+// Pass 2 over block b: W' = W + s * delta (delta from the stored new state, or
+// from the gradient when SGD keeps none), the low-precision copy, and the
+// block's ||W'||^2 (to *part_b).
+template <bool GB16, bool ADAM>
+__device__ __forceinline__ void apply_block(const void* __restrict__ gp, float* __restrict__ W, void* lp,
+                                            const float* __restrict__ s1, const float* __restrict__ s2,
+                                            int64_t numel, int64_t b, float s, const OptScalars& o,
+                                            double* red, double* part_b) {
+  constexpr int U = kElemsPerBlock / 1024;
+  const int64_t base = b * kElemsPerBlock;
+  const int64_t end = numel < base + kElemsPerBlock ? numel : base + kElemsPerBlock;
+  f32x4 w[U], v1[U], v2[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t i = base + threadIdx.x * 4 + u * 1024;
+    w[u] = v1[u] = v2[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (i < end) {
+      w[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(W + i));
+      v1[u] = s1 ? __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s1 + i)) : load_grad4<GB16>(gp, i);
+      if constexpr (ADAM) v2[u] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(s2 + i));
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int64_t i = base + threadIdx.x * 4 + u * 1024;
+    if (i >= end) continue;
+    f32x4 wv;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) wv[e] = fmaf(s, upd_delta<ADAM>(w[u][e], v1[u][e], v2[u][e], o), w[u][e]);
+    __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>(W + i));
+    if (lp) {
+      if (o.lp_bf16)
+        __builtin_nontemporal_store(u32x2{pack_bf16x2(wv.x, wv.y), pack_bf16x2(wv.z, wv.w)},
+                                    reinterpret_cast<u32x2*>((uint16_t*)lp + i));
+      else
+        __builtin_nontemporal_store(wv, reinterpret_cast<f32x4*>((float*)lp + i));
+    }
+    ss += wv.x * wv.x + wv.y * wv.y + wv.z * wv.z + wv.w * wv.w;
+  }
+  const double t = block_sum_d((double)ss, red);
+  if (threadIdx.x == 0) *part_b = t;
 }
 
 }  // namespace fpo

@@ -54,7 +54,7 @@ def test_library_exports_every_header_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert lib.fpo_abi_version() == 3 == L.ABI_VERSION
+    assert lib.fpo_abi_version() == 4 == L.ABI_VERSION
 
 
 def oe(T=128, d=256, V=4096, dtype=L.FPO_BF16, eps=1e-6, min_rms=0.5, chunk=0):
@@ -206,6 +206,7 @@ def test_apply_update_validation(lib):
     assert call(L.Opt(4, 1e-4, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)) == L.FPO_ERR_ARG
     assert call(L.Opt(0, -1.0, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)) == L.FPO_ERR_ARG
     assert call(L.Opt(0, 1e-4, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 0)) == L.FPO_ERR_ARG
+    assert call(L.Opt(0, 1e-4, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 1, 2)) == L.FPO_ERR_ARG  # unknown clip target
     assert call(L.Opt(1, 1e-4, 0.9, 1.0, 0.999, 1e-8, 0.01, 0.01, 1)) == L.FPO_ERR_ARG
     assert call(L.Opt(1, 1e-4, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)) == L.FPO_ERR_NULL  # AdamW needs state2
     assert call(sgd, upd=None) == L.FPO_ERR_NULL

@@ -91,6 +91,79 @@ def test_three_steps(dev, kind, clip, gscale):
             assert abs(float(Wsq[m]) - float((Wg.astype(np.float64) ** 2).sum())) <= 1e-6 * float(Wsq[m])
 
 
+@pytest.mark.parametrize("kind", ["sgd", "adamw", "sgd-plain"])
+@pytest.mark.parametrize("clip,gscale", [(0.01, 1e-1), (0.01, 1e-5), (0.0, 1e-3)])
+def test_three_steps_clip_update(dev, kind, clip, gscale):
+    """Clip-the-update reading (FPO_CLIP_UPDATE), three steps against the
+    oracle's *_update_clip: unclipped optimizer state, the factor applied to
+    the step, W' = W + s * delta within fp32 rounding, ||W' - W|| <= clip ||W||."""
+    shapes = [(256, 688), (64, 100), (8, 4)]
+    W, Gs = make(shapes, 9, gscale)
+    n = len(shapes)
+    tW = [torch.from_numpy(w.copy()).to(dev) for w in W]
+    plain = kind == "sgd-plain"
+    adam = kind == "adamw"
+    s1 = None if plain else [torch.zeros_like(w) for w in tW]
+    s2 = [torch.zeros_like(w) for w in tW] if adam else None
+    lp = [torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in tW]
+    Wsq = torch.tensor([float((w.astype(np.float64) ** 2).sum()) for w in W], dtype=torch.float64, device=dev)
+    clipv = torch.empty(n, dtype=torch.float32, device=dev)
+    oW = [w.astype(np.float64) for w in W]
+    ob = [np.zeros(s) for s in shapes]
+    ov = [np.zeros(s) for s in shapes]
+    lr = 1e-3 if adam else 1e-2
+    mom = 0.0 if plain else 0.9
+    active = False
+    for step in range(1, 4):
+        G = Gs[step - 1]
+        tg = [torch.from_numpy(g).to(dev) for g in G]
+        gsq = torch.tensor([float((g.astype(np.float64) ** 2).sum()) for g in G], dtype=torch.float64, device=dev)
+        Wprev = [w.cpu().numpy().copy() for w in tW]
+        opt = api.OptConfig(kind=1 if adam else 0, lr=lr, momentum=mom, clip_frac=clip, step=step,
+                            clip_target=L_.FPO_CLIP_UPDATE)
+        api.fpo_apply_update(opt, tg, gsq, tW, s1, Wsq, W_lp=lp, state2=s2, clip_scale=clipv)
+        torch.cuda.synchronize()
+        for m in range(n):
+            # the oracle continues from the GPU's weights so that both clip the same step
+            Wp = Wprev[m].astype(np.float64)
+            if adam:
+                oW[m], ob[m], ov[m], s = O.adamw_update_clip(Wp, ob[m], ov[m], G[m], lr, step, frac=clip)
+                assert_close("exp_avg", s1[m].cpu().numpy(), ob[m], "f32")
+                assert_close("exp_avg_sq", s2[m].cpu().numpy(), ov[m], "f32")
+            else:
+                oW[m], ob[m], s = O.sgd_momentum_update_clip(Wp, ob[m], G[m], lr, mom, step, frac=clip)
+                if not plain:
+                    assert_close("momentum", s1[m].cpu().numpy(), ob[m], "f32")
+            assert abs(float(clipv[m]) - s) <= 1e-5 * s, (m, step, float(clipv[m]), s)
+            active = active or s < 1.0
+            Wg = tW[m].cpu().numpy().astype(np.float64)
+            # W' from the GPU's own new state and factor, in float64: the step is
+            # exact up to fp32 rounding of W' and of the step itself
+            f32 = lambda v: np.float64(np.float32(v))  # noqa: E731
+            sg = float(clipv[m])
+            if adam:
+                mg = s1[m].cpu().numpy().astype(np.float64)
+                vg = s2[m].cpu().numpy().astype(np.float64)
+                ib1 = f32(1.0 / (1 - 0.9 ** step))
+                isb2 = f32(1.0 / np.sqrt(1 - 0.999 ** step))
+                delta = -f32(lr * 0.01) * Wp - f32(lr) * (mg * ib1) / (np.sqrt(vg) * isb2 + f32(1e-8))
+            else:
+                bg = G[m].astype(np.float64) if plain else s1[m].cpu().numpy().astype(np.float64)
+                delta = -f32(lr) * bg
+            expect = Wp + sg * delta
+            tol = 2 * np.spacing(np.abs(expect).astype(np.float32)).astype(np.float64) + 4 * 2.0 ** -23 * np.abs(sg * delta)
+            assert np.all(np.abs(Wg - expect) <= tol), (m, step)
+            # and the master moved as the oracle says, to its own precision
+            assert np.max(np.abs(Wg - oW[m])) <= 1e-6 * max(1.0, np.max(np.abs(oW[m])))
+            if clip > 0:
+                assert np.linalg.norm(Wg - Wp) <= clip * np.linalg.norm(Wp) * (1 + 1e-4)
+            assert np.array_equal(lp[m].view(torch.int16).cpu().numpy().view(np.uint16),
+                                  bf16_rne_bits(Wg.astype(np.float32)))
+            assert abs(float(Wsq[m]) - float((Wg ** 2).sum())) <= 1e-6 * float(Wsq[m])
+    # AdamW's step is ~lr per element whatever the gradient's scale
+    assert active == (clip > 0 and (adam or gscale > 1e-2))
+
+
 def test_clip_edge_cases(dev):
     W = torch.full((4, 4), 0.5, dtype=torch.float32, device=dev)
     z = torch.zeros(4, 4, dtype=torch.float32, device=dev)
@@ -135,11 +208,12 @@ def test_cosine(dev, bdtype):
     assert_close("sa", float(sa[0]), O.cosine(A[0], A[0])[1], "f32")
 
 
+@pytest.mark.parametrize("target", [0, 1], ids=["clip-grad", "clip-update"])
 @pytest.mark.parametrize("kind", ["sgd", "adamw", "sgd-plain"])
 @pytest.mark.parametrize("T,d,d_ff,L,clip,pffn", [(256, 256, 512, 2, 0.01, False), (300, 264, 1000, 3, 0.01, False),
                                                   (200, 512, 768, 3, 1e-5, False), (300, 264, 1000, 3, 0.01, True),
                                                   (200, 1032, 1288, 3, 0.01, False)])
-def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip, pffn):
+def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip, pffn, target):
     """The W3 pseudogradient with the optimizer fused (bf16: one launch per
     layer carrying that layer's outer products and the previous layer's update)
     is bit-identical to the pseudogradient followed by fpo_apply_update, over two
@@ -171,7 +245,7 @@ def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip, pff
     sep, fus = fresh(), fresh()
     for step in (1, 2):
         opt = api.OptConfig(kind=L_.FPO_OPT_ADAMW if adam else L_.FPO_OPT_SGD, lr=1e-2, clip_frac=clip, step=step,
-                            momentum=0.0 if plain else 0.9)
+                            momentum=0.0 if plain else 0.9, clip_target=target)
         api.fpo_pseudograd(g, acts, dW3=sep["dW"], sumsq=sep["ss"], **kw)
         api.fpo_apply_update(opt, sep["dW"], sep["ss"], sep["W"], sep["s1"], sep["Wsq"], W_lp=sep["lp"],
                              state2=sep["s2"], clip_scale=sep["cs"])
@@ -187,10 +261,11 @@ def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip, pff
         assert float(fus["cs"].max()) < 1.0  # the clip was active
 
 
+@pytest.mark.parametrize("target", [0, 1], ids=["clip-grad", "clip-update"])
 @pytest.mark.parametrize("kind", ["sgd", "adamw", "sgd-plain"])
 @pytest.mark.parametrize("T,d,d_ff,L,clip,pffn", [(300, 264, 1000, 3, 0.01, False), (200, 1032, 1288, 3, 1e-5, False),
                                                   (300, 264, 1000, 2, 0.01, True)])
-def test_fused_update_with_bf16_staged_pseudogradient(dev, kind, T, d, d_ff, L, clip, pffn):
+def test_fused_update_with_bf16_staged_pseudogradient(dev, kind, T, d, d_ff, L, clip, pffn, target):
     """FPO_MODE_GRAD_BF16: the fused path stages each layer's pseudogradient
     rounded to bf16 (RNE). Over two steps it is bit-identical to the separate
     calls fed the same rounded pseudogradient (the fp32 pseudogradient rounded
@@ -221,7 +296,7 @@ def test_fused_update_with_bf16_staged_pseudogradient(dev, kind, T, d, d_ff, L, 
     dW = [torch.empty(d, d_ff, dtype=torch.float32, device=dev) for _ in range(L)]
     for step in (1, 2):
         opt = api.OptConfig(kind=L_.FPO_OPT_ADAMW if adam else L_.FPO_OPT_SGD, lr=1e-2, clip_frac=clip, step=step,
-                            momentum=0.0 if plain else 0.9)
+                            momentum=0.0 if plain else 0.9, clip_target=target)
         api.fpo_pseudograd(g, acts, dW3=None, sumsq=fus["ss"], opt=opt, W_master=fus["W"], W_lp=fus["lp"],
                            state1=fus["s1"], state2=fus["s2"], W_sumsq=fus["Wsq"], clip_scale=fus["cs"],
                            grad_bf16=True, **kw)
