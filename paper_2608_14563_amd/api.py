@@ -31,13 +31,25 @@ def dtype_code(t: torch.dtype) -> int:
     raise TypeError(f"unsupported dtype {t}")
 
 
-def _p(t: Optional[torch.Tensor], dtype: Optional[torch.dtype] = None) -> Optional[int]:
+def _p(t: Optional[torch.Tensor], dtype: Optional[torch.dtype] = None, shape=None, dev=None,
+       name: str = "tensor") -> Optional[int]:
+    """Device pointer of t after the checks the C ABI cannot make from a bare
+    pointer: a contiguous tensor on the (given) GPU, of the given dtype and
+    shape (a tuple: exact; an int: at least that many elements)."""
     if t is None:
         return None
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise ValueError(f"{name}: libfpo takes GPU tensors")
+    if dev is not None and t.device != dev:
+        raise ValueError(f"{name}: on {t.device}, expected {dev}")
     if not t.is_contiguous():
-        raise ValueError("tensors passed to libfpo must be contiguous")
+        raise ValueError(f"{name}: tensors passed to libfpo must be contiguous")
     if dtype is not None and t.dtype != dtype:
-        raise TypeError(f"expected a {dtype} tensor, got {t.dtype}")
+        raise TypeError(f"{name}: expected a {dtype} tensor, got {t.dtype}")
+    if isinstance(shape, tuple) and tuple(t.shape) != shape:
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {shape}")
+    if isinstance(shape, int) and t.numel() < shape:
+        raise ValueError(f"{name}: {t.numel()} elements, at least {shape} needed")
     return t.data_ptr()
 
 
@@ -54,12 +66,17 @@ class _Keep:
     def __init__(self):
         self.refs = []
 
-    def arr(self, tensors: Optional[Sequence[Optional[torch.Tensor]]], dtype=None):
+    def arr(self, tensors: Optional[Sequence[Optional[torch.Tensor]]], dtype=None, shape=None, dev=None,
+            n: Optional[int] = None, name: str = "tensors"):
+        """[host] array of device pointers; n: required length; shape per
+        entry (a tuple, or a callable of the index)."""
         if tensors is None:
             return None
+        if n is not None and len(tensors) != n:
+            raise ValueError(f"{name}: {len(tensors)} entries, expected {n}")
         a = (C.c_void_p * max(1, len(tensors)))()
         for i, t in enumerate(tensors):
-            a[i] = _p(t, dtype)
+            a[i] = _p(t, dtype, shape(i) if callable(shape) else shape, dev, f"{name}[{i}]")
         self.refs.append(a)
         return C.cast(a, L.PP)
 
@@ -94,15 +111,18 @@ def fpo_output_error(h_final, gamma, W_U, targets, g_tilde, g_tilde_lp=None, g_p
     T, d = h_final.shape
     V = W_U.shape[0]
     op = h_final.dtype
+    dev = h_final.device
     desc = _oe_desc(T, d, V, dtype_code(op), eps, min_rms, vocab_chunk)
     lib = L.load()
     if ws is None:
-        ws = workspace(lib.fpo_output_error_workspace(C.byref(desc)), h_final.device)
+        ws = workspace(lib.fpo_output_error_workspace(C.byref(desc)), dev)
     L.check(lib.fpo_output_error(
-        C.byref(desc), _p(h_final), _p(gamma, op), _p(W_U, op), _p(targets, I32), _p(g_tilde, F32),
-        _p(g_tilde_lp, op), _p(g_pre, F32), _p(lse, F32), _p(loss, F32), _p(argmax, I32),
-        _p(bad_targets, I32), _p(ws), ws.numel(),
-        _stream(h_final.device)))
+        C.byref(desc), _p(h_final, op, (T, d), dev, "h_final"), _p(gamma, op, (d,), dev, "gamma"),
+        _p(W_U, op, (V, d), dev, "W_U"), _p(targets, I32, (T,), dev, "targets"),
+        _p(g_tilde, F32, (T, d), dev, "g_tilde"), _p(g_tilde_lp, op, (T, d), dev, "g_tilde_lp"),
+        _p(g_pre, F32, (T, d), dev, "g_pre"), _p(lse, F32, (T,), dev, "lse"), _p(loss, F32, (T,), dev, "loss"),
+        _p(argmax, I32, (T,), dev, "argmax"), _p(bad_targets, I32, 1, dev, "bad_targets"),
+        _p(ws, None, None, dev, "ws"), ws.numel(), _stream(dev)))
     return ws
 
 
@@ -125,9 +145,24 @@ class OptConfig:
                      self.weight_decay, self.clip_frac, self.step, self.clip_target)
 
 
-def _upd_bufs(keep: _Keep, W_master, W_lp, state1, state2, W_sumsq, clip_scale, lp_dtype):
-    return L.UpdateBufs(keep.arr(W_master, F32), keep.arr(W_lp, lp_dtype), keep.arr(state1, F32),
-                        keep.arr(state2, F32), _p(W_sumsq, F64), _p(clip_scale, F32))
+def _upd_bufs(keep: _Keep, W_master, W_lp, state1, state2, W_sumsq, clip_scale, lp_dtype, numels, dev):
+    """Update buffers of len(numels) matrices, entry m of numels[m] elements."""
+    n = len(numels)
+    if W_master is None:
+        raise ValueError("W_master is required")
+    sh = lambda m: numels[m]  # noqa: E731
+
+    def same(ts, name):
+        if ts is not None:
+            for m, t in enumerate(ts):
+                if t is not None and t.numel() != numels[m]:
+                    raise ValueError(f"{name}[{m}]: {t.numel()} elements, expected {numels[m]}")
+
+    for ts, name in ((W_master, "W_master"), (W_lp, "W_lp"), (state1, "state1"), (state2, "state2")):
+        same(ts, name)
+    return L.UpdateBufs(keep.arr(W_master, F32, sh, dev, n, "W_master"), keep.arr(W_lp, lp_dtype, sh, dev, n, "W_lp"),
+                        keep.arr(state1, F32, sh, dev, n, "state1"), keep.arr(state2, F32, sh, dev, n, "state2"),
+                        _p(W_sumsq, F64, n, dev, "W_sumsq"), _p(clip_scale, F32, n, dev, "clip_scale"))
 
 
 # --------------------------------------------------------------------- pseudograd
@@ -177,17 +212,25 @@ def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, 
         ws = workspace(lib.fpo_pseudograd_workspace(C.byref(desc)), dev)
     k = _Keep()
     o = opt.c() if opt is not None else None
-    ub = _upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale, op) if opt is not None else None
+    nm = 3 * Lyr if full else Lyr
+    numels = [d * d_ff] * nm
+    ub = (_upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale, op, numels, dev)
+          if opt is not None else None)
     pf = None
     if post_ffn is not None:
-        pf = L.PostFfn(_p(post_ffn.g_tilde, F32), k.arr(post_ffn.mlp_out, op), k.arr(post_ffn.gamma, op),
-                       post_ffn.eps, post_ffn.min_rms)
+        pf = L.PostFfn(_p(post_ffn.g_tilde, F32, (T, d), dev, "post_ffn.g_tilde"),
+                       k.arr(post_ffn.mlp_out, op, (T, d), dev, Lyr, "post_ffn.mlp_out"),
+                       k.arr(post_ffn.gamma, op, (d,), dev, Lyr, "post_ffn.gamma"), post_ffn.eps, post_ffn.min_rms)
     L.check(lib.fpo_pseudograd(
-        C.byref(desc), _p(g_tilde_lp, op), k.arr(a, op), k.arr(W3_init, op), k.arr(gate, op), k.arr(up, op),
-        k.arr(x_in, op), k.arr(dW3, F32), k.arr(dW1, F32), k.arr(dW2, F32), _p(sumsq, F64),
-        k.arr(ref, F32), _p(ref_dot, F64), _p(ref_sumsq, F64), C.byref(pf) if pf is not None else None,
+        C.byref(desc), _p(g_tilde_lp, op, (T, d), dev, "g_tilde_lp"), k.arr(a, op, (T, d_ff), dev, Lyr, "a"),
+        k.arr(W3_init, op, (d, d_ff), dev, Lyr, "W3_init"), k.arr(gate, op, (T, d_ff), dev, Lyr, "gate"),
+        k.arr(up, op, (T, d_ff), dev, Lyr, "up"), k.arr(x_in, op, (T, d), dev, Lyr, "x_in"),
+        k.arr(dW3, F32, (d, d_ff), dev, Lyr, "dW3"), k.arr(dW1, F32, (d_ff, d), dev, Lyr, "dW1"),
+        k.arr(dW2, F32, (d_ff, d), dev, Lyr, "dW2"), _p(sumsq, F64, nm, dev, "sumsq"),
+        k.arr(ref, F32, (d, d_ff), dev, Lyr, "ref"), _p(ref_dot, F64, Lyr, dev, "ref_dot"),
+        _p(ref_sumsq, F64, Lyr, dev, "ref_sumsq"), C.byref(pf) if pf is not None else None,
         C.byref(o) if o is not None else None, C.byref(ub) if ub is not None else None,
-        _p(ws), ws.numel(), _stream(dev)))
+        _p(ws, None, None, dev, "ws"), ws.numel(), _stream(dev)))
     return ws
 
 
@@ -201,14 +244,17 @@ def fpo_apply_update(opt: OptConfig, grad, grad_sumsq, W_master, state1, W_sumsq
                      state2=None, clip_scale=None, lp_dtype: torch.dtype = torch.bfloat16, ws=None):
     n = len(grad)
     k = _Keep()
-    numel = k.i64([g.numel() for g in grad])
+    numels = [g.numel() for g in grad]
+    numel = k.i64(numels)
+    dev = grad[0].device
     lib = L.load()
     if ws is None:
-        ws = workspace(lib.fpo_apply_update_workspace(n, numel), grad[0].device)
+        ws = workspace(lib.fpo_apply_update_workspace(n, numel), dev)
     o = opt.c()
-    ub = _upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale, lp_dtype)
-    L.check(lib.fpo_apply_update(C.byref(o), n, numel, k.arr(grad, F32), _p(grad_sumsq, F64), C.byref(ub),
-                                 dtype_code(lp_dtype), _p(ws), ws.numel(), _stream(grad[0].device)))
+    ub = _upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale, lp_dtype, numels, dev)
+    L.check(lib.fpo_apply_update(C.byref(o), n, numel, k.arr(grad, F32, None, dev, n, "grad"),
+                                 _p(grad_sumsq, F64, n, dev, "grad_sumsq"), C.byref(ub), dtype_code(lp_dtype),
+                                 _p(ws, None, None, dev, "ws"), ws.numel(), _stream(dev)))
     return ws
 
 
@@ -227,6 +273,15 @@ def fpo_cosine(A, B=None, dot=None, sumsq_A=None, sumsq_B=None, cos=None, ws=Non
         ws = workspace(lib.fpo_cosine_workspace(n, numel), A[0].device)
     bdt = B[0].dtype if B is not None else F32
     dt = dtype_code(bdt)
-    L.check(lib.fpo_cosine(n, numel, k.arr(A, F32), k.arr(B, bdt), dt, _p(dot, F64), _p(sumsq_A, F64),
-                           _p(sumsq_B, F64), _p(cos, F32), _p(ws), ws.numel(), _stream(A[0].device)))
+    dev = A[0].device
+    if B is not None:
+        if len(B) != n:
+            raise ValueError(f"B: {len(B)} entries, expected {n}")
+        for m in range(n):
+            if B[m].numel() != A[m].numel():
+                raise ValueError(f"B[{m}]: {B[m].numel()} elements, A[{m}] has {A[m].numel()}")
+    L.check(lib.fpo_cosine(n, numel, k.arr(A, F32, None, dev, n, "A"), k.arr(B, bdt, None, dev, n, "B"), dt,
+                           _p(dot, F64, n, dev, "dot"), _p(sumsq_A, F64, n, dev, "sumsq_A"),
+                           _p(sumsq_B, F64, n, dev, "sumsq_B"), _p(cos, F32, n, dev, "cos"),
+                           _p(ws, None, None, dev, "ws"), ws.numel(), _stream(dev)))
     return ws

@@ -230,3 +230,18 @@ def test_cosine_validation(lib):
     assert lib.fpo_cosine(1, n, A, None, 3, None, None, None, None, FAKE, 1 << 20, None) == L.FPO_ERR_DTYPE
     assert lib.fpo_cosine(1, (C.c_int64 * 1)(6), A, None, 0, None, None, None, None, FAKE, 1 << 20, None) == L.FPO_ERR_SHAPE
     assert lib.fpo_cosine(1, n, A, None, 0, None, None, None, None, FAKE, 8, None) == L.FPO_ERR_WORKSPACE
+
+
+def test_binding_rejects_host_tensors():
+    """The binding hands the library device pointers only: host tensors are
+    refused before any call (no GPU needed)."""
+    import torch
+
+    from paper_2608_14563_amd import api
+    T, d, V = 4, 8, 16
+    x = torch.zeros(T, d)
+    with pytest.raises(ValueError, match="GPU tensors"):
+        api.fpo_output_error(x, torch.ones(d), torch.zeros(V, d), torch.zeros(T, dtype=torch.int32),
+                             torch.empty(T, d), ws=torch.empty(1 << 20, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="GPU tensors"):
+        api.fpo_cosine([torch.zeros(8)], [torch.zeros(8)], ws=torch.empty(4096, dtype=torch.uint8))

@@ -125,3 +125,25 @@ def test_cosine_min_size(dev):
         assert abs(float(dot[m]) - d0) <= 1e-6 * abs(d0)
         assert abs(float(cos[m]) - c0) <= 1e-6
     assert abs(float(cos[1]) + 1.0) <= 1e-6
+
+
+def test_binding_checks_shapes(dev):
+    """Mismatched buffer shapes are refused by the binding before the library
+    sees a pointer (the C ABI cannot check a bare pointer's extent)."""
+    T, d, V = 4, 8, 16
+    f = dict(device=dev)
+    x = torch.zeros(T, d, **f)
+    good = dict(gamma=torch.ones(d, **f), W_U=torch.zeros(V, d, **f), targets=torch.zeros(T, dtype=torch.int32, **f))
+    with pytest.raises(ValueError, match="g_tilde"):
+        api.fpo_output_error(x, good["gamma"], good["W_U"], good["targets"], torch.empty(T, d + 8, **f))
+    with pytest.raises(ValueError, match="targets"):
+        api.fpo_output_error(x, good["gamma"], good["W_U"], torch.zeros(T - 1, dtype=torch.int32, **f),
+                             torch.empty(T, d, **f))
+    a = [torch.zeros(T, 16, **f)]
+    with pytest.raises(ValueError, match="dW3"):
+        api.fpo_pseudograd(torch.zeros(T, d, **f), a, dW3=[torch.empty(16, d, **f)])
+    with pytest.raises(ValueError, match="W_master"):
+        api.fpo_apply_update(api.OptConfig(), [torch.zeros(64, **f)], torch.zeros(1, dtype=torch.float64, **f),
+                             [torch.zeros(32, **f)], [torch.zeros(64, **f)], torch.zeros(1, dtype=torch.float64, **f))
+    with pytest.raises(ValueError, match="B\\[0\\]"):
+        api.fpo_cosine([torch.zeros(8, **f)], [torch.zeros(12, **f)])
