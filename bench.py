@@ -42,7 +42,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=1, help="workload id (paper_2608_14563_amd.inputs.CONFIGS)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--vocab-chunk", type=int, default=0,
@@ -98,6 +98,24 @@ def prof_read(lib):
     if k < 0:
         raise RuntimeError("fpo_prof_read failed")
     return {names.raw[32 * i:32 * i + 32].split(b"\0")[0].decode(): (ms[i], cnt[i]) for i in range(k)}
+
+
+def max_engine_clock_mhz():
+    """The GPU's highest engine-clock level (MHz) from the amdgpu driver's
+    sysfs table (pp_dpm_sclk), or None when it is not readable. Read from
+    files only: no child process is started from this (GPU-using) process."""
+    import glob
+    import re
+    best = None
+    for f in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
+        try:
+            txt = open(f).read()
+        except OSError:
+            continue
+        for m in re.finditer(r"(\d+)\s*[Mm][Hh]z", txt):
+            v = int(m.group(1))
+            best = v if best is None else max(best, v)
+    return best
 
 
 def source_hash() -> str:
@@ -369,6 +387,7 @@ def main():
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build has no "
               "multi-GPU path: run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    clk_mhz = max_engine_clock_mhz()
     if args.e2e_diagnostic:
         bench_e2e(args)
         return
@@ -520,8 +539,7 @@ def main():
     flops_step = flops_oe + flops_pg
     med = lambda v: v[len(v) // 2]  # noqa: E731
     props = torch.cuda.get_device_properties(0)
-    clk_khz = getattr(props, "clock_rate", None)
-    peak_clk = (props.multi_processor_count * clk_khz * 1e3 * 4096 / 1e12) if clk_khz else None
+    peak_clk = (props.multi_processor_count * clk_mhz * 1e6 * 4096 / 1e12) if clk_mhz else None
     substeps = {
         "step_ms_median": round(med(per_step), 4), "step_ms_min": round(per_step[0], 4),
         "output_error_ms_median": round(med(per_oe), 4),
@@ -530,6 +548,7 @@ def main():
         "pseudograd_update_mfma_frac": round(flops_pg / (med(per_pg) / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "mfma_peak_tflops_nominal": PEAK_BF16_TFLOPS,
         "mfma_peak_tflops_at_max_clock": round(peak_clk, 1) if peak_clk else None,
+        "max_engine_clock_mhz": clk_mhz,
     }
     log(f"[bench] median step {substeps['step_ms_median']:.3f} ms (min {substeps['step_ms_min']:.3f}): output error "
         f"{substeps['output_error_ms_median']:.3f} ms, pseudograd + update {substeps['pseudograd_update_ms_median']:.3f} ms")
