@@ -18,6 +18,11 @@
  *  - Every call validates its arguments on the host, enqueues work on
  *    `stream` (a hipStream_t; NULL = the default stream) and returns without
  *    synchronising. Results are valid once the stream has reached them.
+ *  - The calls allocate nothing, never synchronise the host and issue no
+ *    memset, so they can be captured into a HIP graph (stream capture); the
+ *    overlapped optimizer path's side stream joins a capture through its
+ *    events. Scalars passed by value (the optimizer step number, hence the
+ *    first-step and AdamW bias-correction terms) are fixed at capture.
  *  - The caller owns every buffer. The library allocates no device memory;
  *    scratch space comes from the caller's workspace, whose size the
  *    matching *_workspace query returns. Workspace pointers must be 256-byte

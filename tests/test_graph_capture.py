@@ -1,0 +1,68 @@
+"""The hot-path calls are capturable into a HIP graph (torch.cuda.CUDAGraph):
+they allocate nothing, never synchronise the host and use no memset; the
+overlapped optimizer path's side stream joins the capture through its events.
+One SGD-momentum step (output error + pseudogradient with the fused update,
+bf16-staged) captured at step 3 is replayed three times, with eager work and
+synchronisations between replays, and every replay is bit-identical to the
+same step run eagerly from the same state. The optimizer scalars (step
+number, hence the first-step and AdamW bias terms) are fixed at capture."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_14563_amd import api
+from paper_2608_14563_amd import inputs as I
+from tests._util import dev_tensor
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("post_ffn", [False, True])
+def test_step_graph_replays_match_eager(dev, post_ffn):
+    c = I.CONFIGS[1].shrink(T=300, d=520, d_ff=1288, V=4104, L=3)
+    x, gam, WU, y = (dev_tensor(a, dev) for a in (I.hidden(c), I.gain(c), I.unembedding(c), I.targets(c)))
+    acts = [dev_tensor(I.activation(c, l), dev) for l in range(c.L)]
+    W0 = [torch.from_numpy(I.master_weight(c, l)).to(dev) for l in range(c.L)]
+    pf = [I.post_ffn(c, l) for l in range(c.L)] if post_ffn else None
+
+    def state():
+        W = [w.clone() for w in W0]
+        s = dict(W=W, s1=[torch.zeros_like(w) for w in W],
+                 lp=[torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in W],
+                 Wsq=torch.tensor([float((w.double() ** 2).sum()) for w in W], dtype=torch.float64, device=dev),
+                 ss=torch.empty(c.L, dtype=torch.float64, device=dev),
+                 g=torch.empty(c.T, c.d, device=dev), glp=torch.empty(c.T, c.d, dtype=torch.bfloat16, device=dev),
+                 ws_oe=api.workspace(api.fpo_output_error_workspace(c.T, c.d, c.V, torch.bfloat16), dev),
+                 ws_pg=api.workspace(api.fpo_pseudograd_workspace(c.T, c.d, c.d_ff, c.L, torch.bfloat16,
+                                                                  post_ffn=post_ffn, grad_bf16=True), dev))
+        if post_ffn:
+            s["pf"] = api.PostFfn(s["g"], [dev_tensor(m, dev) for m, _ in pf], [dev_tensor(gm, dev) for _, gm in pf])
+        return s
+
+    def step(s, k):
+        api.fpo_output_error(x, gam, WU, y, s["g"], s["glp"], ws=s["ws_oe"])
+        api.fpo_pseudograd(None if post_ffn else s["glp"], acts, dW3=None, sumsq=s["ss"], grad_bf16=True,
+                           ws=s["ws_pg"], post_ffn=s.get("pf"),
+                           opt=api.OptConfig(lr=1e-2, clip_frac=0.01, step=k), W_master=s["W"], W_lp=s["lp"],
+                           state1=s["s1"], W_sumsq=s["Wsq"])
+
+    eager, graphed = state(), state()
+    for k in (1, 2):
+        step(eager, k)
+        step(graphed, k)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=torch.cuda.Stream()):
+        step(graphed, 3)  # recorded, not run
+    torch.cuda.synchronize()
+    for k in (3, 4, 5):
+        step(eager, k)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        x.add_(0)  # the program's own eager work between replays
+        for key in ("W", "s1", "lp"):
+            for a, b in zip(eager[key], graphed[key]):
+                assert torch.equal(a, b), (key, k)
+        for key in ("Wsq", "ss", "g", "glp"):
+            assert torch.equal(eager[key], graphed[key]), (key, k)
