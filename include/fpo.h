@@ -21,7 +21,8 @@
  *  - The calls allocate nothing, never synchronise the host and issue no
  *    memset, so they can be captured into a HIP graph (stream capture); the
  *    overlapped optimizer path's side stream joins a capture through its
- *    events. Scalars passed by value (the optimizer step number, hence the
+ *    events (the first such call on a device creates that stream and its
+ *    events: make it before capturing). Scalars passed by value (the optimizer step number, hence the
  *    first-step and AdamW bias-correction terms) are fixed at capture.
  *  - The caller owns every buffer. The library allocates no device memory;
  *    scratch space comes from the caller's workspace, whose size the
