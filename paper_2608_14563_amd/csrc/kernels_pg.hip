@@ -6,7 +6,8 @@
 //                   (pffn_stats: its per-token norm statistics) on the way
 //   outer_kernel  : C_m = scale * A_m B_m for a list of matrices (MFMA),
 //                   A_m [M, Tp] token-contiguous, B_m [T, N] row-major; epilogue
-//                   writes C and per-tile ||C||^2 (and <C, R>, ||R||^2)
+//                   writes C (fp32, or rounded to bf16 for the fused update) and
+//                   per-tile ||C||^2 (and <C, R>, ||R||^2)
 //   errh_kernel   : E = g~ W3_init (MFMA); du = E*SiLU(q), dq = E*u*SiLU'(q),
 //                   stored token-contiguous for the W1/W2 outer products
 //   reduce_parts  : fixed-order float64 sums of the tile partials
@@ -521,11 +522,11 @@ static hipError_t pg_overlap_init(PgOverlap& p, int dev) {
 
 // W3-only bf16 pseudogradient with the optimizer step overlapped: the outer
 // products run one layer per launch on the caller's stream; once layer l's
-// tiles and norm are done, its update (the standalone update kernel, which
-// needs few registers and no LDS, so its workgroups sit beside the GEMM's on
-// the same CUs) streams on a side stream while layer l+1's MFMAs run, with one
-// workgroup per CU so that each CU holds one outer-product workgroup and one
-// update workgroup. Same per-block arithmetic and reduction order as the
+// tiles and norm are done, its update (few registers and no LDS, so its
+// workgroups sit beside the GEMM's on the same CUs) streams on a side stream
+// while layer l+1's MFMAs run, with one workgroup per CU so that each CU holds
+// one outer-product workgroup and one update workgroup; the last layer's update
+// has the machine to itself. Same per-block arithmetic and reduction order as the
 // separate calls, so results are bit-identical to them.
 hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u) {
   hipStream_t st = (hipStream_t)a.stream;
