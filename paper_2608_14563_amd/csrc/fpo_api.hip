@@ -54,16 +54,22 @@ bool band_fits(int64_t rows, int64_t cols) { return rows * cols <= ((int64_t)1 <
 
 // ------------------------------------------------------------------ plans
 struct OePlan {
-  int64_t Vc = 0, nb = 0;
+  int64_t Vc = 0, ldp = 0, nb = 0;
   int nsplit = 1;
 };
 
 // Workgroups one wave of the MI355X grid holds (one 256 x 256 tile per CU).
 constexpr int64_t kWaveSlots = 256;
+// The staged p~ rows are padded by 256 bytes so that the row pitch is an odd
+// multiple of 256 bytes: with a power-of-two pitch (V = 131072: 256 KiB) the
+// 256 rows of one tile share an L2 set and its stores are written back to HBM
+// several times over (measured: 3.3 GB written for a 1.1 GB p~).
+constexpr int64_t kPadBytes = 256;
 
 OePlan plan_oe(const fpo_oe_desc& d) {
   const bool bf16 = d.dtype == FPO_BF16;
   const int64_t BM = bf16 ? 256 : 128, BN = BM, WTN = bf16 ? 128 : 64;
+  const int64_t pad = kPadBytes / (bf16 ? 2 : 4);
   // staged p~ budget: 2^30 elements (2 GiB bf16), so the vocabulary of the
   // 7-8B shapes at T <= 4096 is one chunk: one logits launch, one projection
   // launch accumulating over the whole vocabulary (one merge of the partials),
@@ -73,17 +79,34 @@ OePlan plan_oe(const fpo_oe_desc& d) {
   int64_t vmax = d.vocab_chunk > 0 ? round_up(d.vocab_chunk, 256)
                                    : std::max<int64_t>(256, ((int64_t)1 << 30) / d.T / 256 * 256);
   vmax = std::min(vmax, round_up(d.V, 256));
-  // a chunk of W_U and the staged p~ are copied through 32-bit offsets
-  if (bf16) vmax = std::min(vmax, std::max<int64_t>(256, (((int64_t)1 << 30) / std::max(d.d, d.T)) / 256 * 256));
+  // a chunk of W_U ([Vc, d]) and the staged p~ ([T, Vc + pad]) are copied
+  // through 32-bit offsets
+  if (bf16) {
+    const int64_t lim = std::min(((int64_t)1 << 30) / d.d, ((int64_t)1 << 30) / d.T - pad);
+    vmax = std::min(vmax, std::max<int64_t>(256, lim / 256 * 256));
+  }
   OePlan p;
   p.Vc = round_up(ceil_div(d.V, ceil_div(d.V, vmax)), 256);
+  p.ldp = p.Vc + pad;
   p.nb = p.Vc / WTN;
-  // split the projection's K range so that its launch fills one wave
+  // Split the projection's K range so that its launch fills whole waves: the
+  // smallest split count (at most 8, at least two blocks per split) that gives
+  // at least one wave and the best filled last wave. (T = 4096, d = 3072: 192
+  // tiles, two splits leave the second wave half empty, four fill three.)
   const int64_t tiles = ceil_div(d.T, BM) * ceil_div(d.d, BN);
-  int64_t ns = ceil_div(kWaveSlots, tiles);
-  ns = std::min<int64_t>(ns, 8);
-  ns = std::min<int64_t>(ns, std::max<int64_t>(1, p.nb / 2));
-  p.nsplit = (int)std::max<int64_t>(1, ns);
+  const int64_t nsmax = std::min<int64_t>(8, std::max<int64_t>(1, p.nb / 2));
+  const int64_t ns0 = std::min(nsmax, ceil_div(kWaveSlots, tiles));
+  int64_t best = ns0;
+  double best_fill = 0.0;
+  for (int64_t ns = ns0; ns <= nsmax; ++ns) {
+    const int64_t wg = tiles * ns;
+    const double fill = (double)wg / (double)(ceil_div(wg, kWaveSlots) * kWaveSlots);
+    if (fill > best_fill + 1e-9) {
+      best = ns;
+      best_fill = fill;
+    }
+  }
+  p.nsplit = (int)best;
   return p;
 }
 
@@ -91,7 +114,7 @@ size_t carve_oe(const fpo_oe_desc& d, const OePlan& p, void* ws, fpo::OeLaunch* 
   const int64_t esz = d.dtype == FPO_BF16 ? 2 : 4;
   Carver c(ws);
   void* y = c.take<char>(d.T * d.d * esz);
-  void* P = c.take<char>(d.T * p.Vc * esz);
+  void* P = c.take<char>(d.T * p.ldp * esz);
   float* blk_m = c.take<float>(d.T * p.nb);
   float* blk_s = c.take<float>(d.T * p.nb);
   int32_t* blk_i = c.take<int32_t>(d.T * p.nb);
@@ -136,9 +159,9 @@ int check_oe_desc(const fpo_oe_desc* d) {
   if (d->vocab_chunk < 0) return fail(FPO_ERR_ARG, "fpo_output_error: vocab_chunk must be >= 0");
   // bf16 operands are copied through 32-bit buffer offsets: every operand band
   // (y, a W_U chunk of at least 256 rows, the staged p~) must fit in 2^31 bytes
-  if (d->dtype == FPO_BF16 && (!band_fits(d->T, d->d) || !band_fits(256, d->d) || !band_fits(d->T, 256)))
+  if (d->dtype == FPO_BF16 && (!band_fits(d->T, d->d) || !band_fits(256, d->d) || !band_fits(d->T, 256 + 128)))
     return fail(FPO_ERR_UNSUPPORTED,
-                "fpo_output_error: bf16 operand bands must stay below 2^31 bytes (T*d, 256*d and 256*T "
+                "fpo_output_error: bf16 operand bands must stay below 2^31 bytes (T*d, 256*d and 384*T "
                 "elements <= 2^30; T=%lld d=%lld)",
                 (long long)d->T, (long long)d->d);
   return FPO_OK;
@@ -347,6 +370,7 @@ int fpo_output_error(const fpo_oe_desc* desc, const void* h_final, const void* g
   L.d = desc->d;
   L.V = desc->V;
   L.Vc = p.Vc;
+  L.ldp = p.ldp;
   L.nsplit = p.nsplit;
   L.eps = desc->eps;
   L.min_rms = desc->min_rms;

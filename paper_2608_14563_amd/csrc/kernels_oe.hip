@@ -536,7 +536,7 @@ static hipError_t run_output_error(const OeLaunch& a) {
     const int nbv = (vc_valid + TT::WTN - 1) / TT::WTN;  // blocks holding a valid column
     FPO_LAUNCH("logits_chunk", st,
                logits_chunk_kernel<E><<<dim3(gm * gn), dim3(256), 0, st>>>(
-        y, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, (int)v0, P, a.Vc, nbv, a.blk_m, a.blk_s,
+        y, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, (int)v0, P, a.ldp, nbv, a.blk_m, a.blk_s,
         a.blk_i));
     FPO_CHECK_LAUNCH();
     const int bps = (nbv + a.nsplit - 1) / a.nsplit;
@@ -550,12 +550,12 @@ static hipError_t run_output_error(const OeLaunch& a) {
       const int ncv = (vc_valid + EPC - 1) / EPC;
       FPO_LAUNCH("rescale_p", st,
                  rescale_p_kernel<T><<<dim3((unsigned)((ncv + 256 * kRescaleU - 1) / (256 * kRescaleU)), (unsigned)a.T),
-                                       dim3(256), 0, st>>>(vc_valid, nbv, bps, a.nsplit, TT::WTN, a.blk_m, a.refs, P, a.Vc));
+                                       dim3(256), 0, st>>>(vc_valid, nbv, bps, a.nsplit, TT::WTN, a.blk_m, a.refs, P, a.ldp));
       FPO_CHECK_LAUNCH();
     }
     FPO_LAUNCH("proj_chunk", st,
                proj_chunk_kernel<E><<<dim3(gm * (unsigned)((a.d + TT::BN - 1) / TT::BN) * a.nsplit), dim3(256), 0, st>>>(
-        P, a.Vc, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, nbv, bps, TT::WTN, c == 0, a.nsplit,
+        P, a.ldp, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, nbv, bps, TT::WTN, c == 0, a.nsplit,
         a.fout, a.alpha, a.G, a.T * a.d));
     FPO_CHECK_LAUNCH();
   }

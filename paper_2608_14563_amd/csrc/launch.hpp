@@ -15,6 +15,7 @@ constexpr int kMaxMats = 64;
 struct OeLaunch {
   bool bf16;
   int64_t T, d, V, Vc;
+  int64_t ldp;  // row pitch of the staged p~ (elements, >= Vc)
   int nsplit;
   float eps, min_rms;
   const void* h_final;
