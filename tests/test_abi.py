@@ -123,6 +123,26 @@ def test_chunk_width_respects_operand_bands(lib):
     assert ws <= T * vc_max * 2 + (T * d * 2) + 64 * T * d * 4 + (64 << 20)
 
 
+def test_staged_p_pitch_padding_and_band(lib):
+    """The staged p~ rows are padded by 256 bytes (a power-of-two pitch puts a
+    tile's rows in one L2 set), and the padded band still fits 2^30 elements:
+    at T = 8192, V = 131072 one unpadded chunk would be exactly 2^30 elements,
+    so the planner takes two chunks and the workspace stays below one
+    T x V bf16 p~."""
+    def a256(n):
+        return (n + 255) // 256 * 256
+
+    # one chunk, two projection splits: the documented workspace layout exactly
+    T, d, V, ns = 2048, 4096, 100352, 2
+    nb = V // 128
+    want = (a256(T * d * 2) + a256(T * (V + 128) * 2) + 3 * a256(T * nb * 4) + 2 * a256(T * ns * 4)
+            + 4 * a256(T * 4) + a256(ns * T * d * 4))
+    assert lib.fpo_output_error_workspace(C.byref(oe(T=T, d=d, V=V))) == want
+    T, V = 8192, 131072
+    ws = lib.fpo_output_error_workspace(C.byref(oe(T=T, d=d, V=V)))
+    assert 0 < ws < T * V * 2
+
+
 def arr(vals):
     a = (C.c_void_p * len(vals))(*vals)
     return C.cast(a, L.PP), a
