@@ -27,7 +27,12 @@
  *  - The caller owns every buffer. The library allocates no device memory;
  *    scratch space comes from the caller's workspace, whose size the
  *    matching *_workspace query returns. Workspace pointers must be 256-byte
- *    aligned.
+ *    aligned; every tensor operand (activations, weights, gradients,
+ *    optimizer state, reference gradients) must be 16-byte aligned (the
+ *    kernels move 16 bytes per lane; a bf16 W_lp: 8). Per-token and
+ *    per-matrix outputs
+ *    (lse, loss, argmax, sums of squares, dot products, cosines) need only
+ *    their element alignment.
  *  - Inputs are read only. Outputs are fully overwritten (never accumulated
  *    into) and must not alias inputs, except where a buffer is documented as
  *    in/out.

@@ -91,6 +91,10 @@ def workspace(nbytes: int, device) -> torch.Tensor:
     return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
 
 
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
+
+
 def fpo_abi_version() -> int:
     return L.load().fpo_abi_version()
 
@@ -122,7 +126,7 @@ def fpo_output_error(h_final, gamma, W_U, targets, g_tilde, g_tilde_lp=None, g_p
         _p(g_tilde, F32, (T, d), dev, "g_tilde"), _p(g_tilde_lp, op, (T, d), dev, "g_tilde_lp"),
         _p(g_pre, F32, (T, d), dev, "g_pre"), _p(lse, F32, (T,), dev, "lse"), _p(loss, F32, (T,), dev, "loss"),
         _p(argmax, I32, (T,), dev, "argmax"), _p(bad_targets, I32, 1, dev, "bad_targets"),
-        _p(ws, None, None, dev, "ws"), ws.numel(), _stream(dev)))
+        _p(ws, None, None, dev, "ws"), _nbytes(ws), _stream(dev)))
     return ws
 
 
@@ -230,7 +234,7 @@ def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, 
         k.arr(ref, F32, (d, d_ff), dev, Lyr, "ref"), _p(ref_dot, F64, Lyr, dev, "ref_dot"),
         _p(ref_sumsq, F64, Lyr, dev, "ref_sumsq"), C.byref(pf) if pf is not None else None,
         C.byref(o) if o is not None else None, C.byref(ub) if ub is not None else None,
-        _p(ws, None, None, dev, "ws"), ws.numel(), _stream(dev)))
+        _p(ws, None, None, dev, "ws"), _nbytes(ws), _stream(dev)))
     return ws
 
 
@@ -254,7 +258,7 @@ def fpo_apply_update(opt: OptConfig, grad, grad_sumsq, W_master, state1, W_sumsq
     ub = _upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale, lp_dtype, numels, dev)
     L.check(lib.fpo_apply_update(C.byref(o), n, numel, k.arr(grad, F32, None, dev, n, "grad"),
                                  _p(grad_sumsq, F64, n, dev, "grad_sumsq"), C.byref(ub), dtype_code(lp_dtype),
-                                 _p(ws, None, None, dev, "ws"), ws.numel(), _stream(dev)))
+                                 _p(ws, None, None, dev, "ws"), _nbytes(ws), _stream(dev)))
     return ws
 
 
@@ -283,5 +287,5 @@ def fpo_cosine(A, B=None, dot=None, sumsq_A=None, sumsq_B=None, cos=None, ws=Non
     L.check(lib.fpo_cosine(n, numel, k.arr(A, F32, None, dev, n, "A"), k.arr(B, bdt, None, dev, n, "B"), dt,
                            _p(dot, F64, n, dev, "dot"), _p(sumsq_A, F64, n, dev, "sumsq_A"),
                            _p(sumsq_B, F64, n, dev, "sumsq_B"), _p(cos, F32, n, dev, "cos"),
-                           _p(ws, None, None, dev, "ws"), ws.numel(), _stream(dev)))
+                           _p(ws, None, None, dev, "ws"), _nbytes(ws), _stream(dev)))
     return ws

@@ -316,8 +316,12 @@ int fill_update(const fpo_opt* opt, int64_t n, const int64_t* numel, const void*
     if (!grad[m] || !upd->W_master[m] || (!s1m && !stateless_ok) ||
         (opt->kind == FPO_OPT_ADAMW && !upd->state2[m]))
       return fail(FPO_ERR_NULL, "update: NULL buffer for matrix %lld", (long long)m);
-    if (!aligned(grad[m], 16) || !aligned(upd->W_master[m], 16) || (s1m && !aligned(s1m, 16)))
-      return fail(FPO_ERR_ARG, "update: buffers of matrix %lld must be 16-byte aligned", (long long)m);
+    const void* lpm = upd->W_lp ? upd->W_lp[m] : nullptr;
+    const float* s2m = upd->state2 ? upd->state2[m] : nullptr;
+    if (!aligned(grad[m], 16) || !aligned(upd->W_master[m], 16) || (s1m && !aligned(s1m, 16)) ||
+        (s2m && !aligned(s2m, 16)) || (lpm && !aligned(lpm, U->lp_bf16 ? 8 : 16)))
+      return fail(FPO_ERR_ARG, "update: buffers of matrix %lld must be 16-byte aligned (bf16 W_lp: 8)",
+                  (long long)m);
     U->numel[m] = numel[m];
     U->grad[m] = grad[m];
     U->W[m] = upd->W_master[m];
@@ -458,9 +462,13 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
     if (P.dW3[l] && !aligned(P.dW3[l], 16)) return fail(FPO_ERR_ARG, "fpo_pseudograd: dW3[%d] not aligned", l);
     P.ref[l] = ref ? ref[l] : nullptr;
     if (ref && !ref[l]) return fail(FPO_ERR_NULL, "fpo_pseudograd: ref[%d] is NULL", l);
+    if (ref && !aligned(ref[l], 16)) return fail(FPO_ERR_ARG, "fpo_pseudograd: ref[%d] not 16-byte aligned", l);
     if (full) {
       if (!W3_init[l] || !gate[l] || !up[l] || !x_in[l] || !dW1[l] || !dW2[l])
         return fail(FPO_ERR_NULL, "fpo_pseudograd: full-MLP buffer of layer %d is NULL", l);
+      if (!aligned(W3_init[l], 16) || !aligned(gate[l], 16) || !aligned(up[l], 16) || !aligned(x_in[l], 16) ||
+          !aligned(dW1[l], 16) || !aligned(dW2[l], 16))
+        return fail(FPO_ERR_ARG, "fpo_pseudograd: full-MLP buffers of layer %d must be 16-byte aligned", l);
       P.W3i[l] = W3_init[l];
       P.q[l] = gate[l];
       P.u[l] = up[l];

@@ -209,6 +209,35 @@ def test_pseudograd_validation(lib):
     assert call(L.PgDesc(1 << 17, 256, 16384, 2, L.FPO_BF16, L.FPO_MODE_W3, 1.0)) == L.FPO_ERR_UNSUPPORTED
 
 
+def test_pseudograd_operand_alignment(lib):
+    """Reference gradients and the full-MLP operands are read 16 bytes per
+    lane: a pointer off 16-byte alignment is refused before any launch (the
+    well-aligned call fails only at the workspace check)."""
+    good = [FAKE, FAKE]
+    bad = [FAKE, FAKE + 4]
+
+    def ref_call(ref):
+        r, kr = arr(ref)
+        desc = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_W3, 1 / 128)
+        a, ka = arr(good)
+        return lib.fpo_pseudograd(C.byref(desc), FAKE, a, None, None, None, None, None, None, None, None, r,
+                                  FAKE, FAKE, None, None, None, FAKE, 16, None)
+
+    assert ref_call(good) == L.FPO_ERR_WORKSPACE
+    assert ref_call(bad) == L.FPO_ERR_ARG
+
+    def full_call(which):
+        bufs = [arr(bad if k == which else good) for k in range(7)]
+        p = [b[0] for b in bufs]
+        desc = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_FULL_MLP, 1 / 128)
+        return lib.fpo_pseudograd(C.byref(desc), FAKE, p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[6], None,
+                                  None, None, None, None, None, None, FAKE, 16, None)
+
+    assert full_call(-1) == L.FPO_ERR_WORKSPACE
+    for k in range(1, 7):  # W3_init, gate, up, x_in, dW3 / dW1, dW2
+        assert full_call(k) == L.FPO_ERR_ARG, k
+
+
 def test_apply_update_validation(lib):
     g, kg = arr([FAKE])
     W, kw = arr([FAKE])
@@ -239,6 +268,16 @@ def test_apply_update_validation(lib):
     assert "momentum 0" in lib.fpo_last_error().decode()
     plain = L.Opt(0, 1e-4, 0.0, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)
     assert call(plain, upd=nostate, ws_bytes=8) == L.FPO_ERR_WORKSPACE  # passes the state check
+    # operand alignment: 16 bytes, except a bf16 copy of the weights (8)
+    lp8, k8 = arr([FAKE + 8])
+    with_lp = L.UpdateBufs(W, lp8, s1, None, FAKE, None)
+    assert call(sgd, upd=with_lp, ws_bytes=8) == L.FPO_ERR_WORKSPACE
+    assert call(sgd, upd=with_lp, lp=L.FPO_F32) == L.FPO_ERR_ARG
+    s2b, k2 = arr([FAKE + 4])
+    adam = L.Opt(1, 1e-4, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)
+    assert call(adam, upd=L.UpdateBufs(W, None, s1, s2b, FAKE, None)) == L.FPO_ERR_ARG
+    s1b, k1b = arr([FAKE + 8])
+    assert call(sgd, upd=L.UpdateBufs(W, None, s1b, None, FAKE, None)) == L.FPO_ERR_ARG
 
 
 def test_cosine_validation(lib):
