@@ -43,7 +43,9 @@
  *    and W_lp are bfloat16 (raw 16-bit patterns); everything else is
  *    float32 (g_tilde, dW, masters, optimizer state, reference gradients)
  *    or float64 (sums of squares, dot products).
- *  - d, d_ff and V must be multiples of 8; T, d, d_ff, V, L >= 1.
+ *  - d, d_ff and V must be multiples of 8; T, d, d_ff, V, L >= 1; at most
+ *    2^23 tokens per call, and d <= 2^22 for fpo_pseudograd (launch-grid
+ *    limits).
  *  - Errors: calls return 0 (FPO_OK) or a positive fpo_status. Problems a
  *    host can detect (NULL, non-positive or misaligned sizes, unknown
  *    enum, negative eps / min_rms / lr, small workspace) return before any

@@ -34,6 +34,11 @@ inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 inline bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
 
 constexpr int64_t kIntMax = 0x7fffffff;
+// Launch geometry: the per-token kernels use one workgroup (256 lanes) per
+// token in a 1-D grid, whose lane count must stay below 2^32; the signal
+// transpose tiles d in 64-row steps along a grid dimension capped at 65536.
+constexpr int64_t kMaxTokens = (int64_t)1 << 23;
+constexpr int64_t kMaxHidden = (int64_t)1 << 22;
 constexpr size_t kAlign = 256;
 
 struct Carver {
@@ -152,6 +157,9 @@ int check_oe_desc(const fpo_oe_desc* d) {
   if (d->d % 8 || d->V % 8)
     return fail(FPO_ERR_SHAPE, "fpo_output_error: d and V must be multiples of 8 (d=%lld V=%lld)",
                 (long long)d->d, (long long)d->V);
+  if (d->T > kMaxTokens)
+    return fail(FPO_ERR_SHAPE, "fpo_output_error: at most %lld tokens per call (T=%lld)", (long long)kMaxTokens,
+                (long long)d->T);
   if (!(d->eps >= 0.f) || !std::isfinite(d->eps))
     return fail(FPO_ERR_ARG, "fpo_output_error: eps must be finite and >= 0");
   if (!(d->min_rms >= 0.f) || !std::isfinite(d->min_rms))
@@ -236,6 +244,9 @@ int check_pg_desc(const fpo_pg_desc* d) {
                 (long long)d->L);
   if (d->d % 8 || d->d_ff % 8)
     return fail(FPO_ERR_SHAPE, "fpo_pseudograd: d and d_ff must be multiples of 8");
+  if (d->T > kMaxTokens || d->d > kMaxHidden)
+    return fail(FPO_ERR_SHAPE, "fpo_pseudograd: at most %lld tokens and d <= %lld per call (T=%lld d=%lld)",
+                (long long)kMaxTokens, (long long)kMaxHidden, (long long)d->T, (long long)d->d);
   if (!std::isfinite(d->scale)) return fail(FPO_ERR_ARG, "fpo_pseudograd: scale must be finite");
   if (d->dtype == FPO_BF16) {
     // operand bands copied through 32-bit buffer offsets must fit in 2^31 bytes

@@ -289,21 +289,24 @@ __global__ __launch_bounds__(256) void chunk_stats_kernel(
 
 // Staged p~ of block b (split s = b / bps) times exp(m_b - ref_s) <= 1, in
 // place. Streams the chunk once: 16-byte runs, four per thread, all loads
-// before stores, non-temporal; grid (run groups, tokens).
+// before stores, non-temporal; one flat grid of (token, run group) pairs, the
+// groups of a token adjacent (a 2-D grid would cap the tokens at 65536).
 constexpr int kRescaleU = 4;
 
 template <typename PT>
-__global__ __launch_bounds__(256) void rescale_p_kernel(int vc_valid, int nb, int bps, int nsplit,
-                                                        int blkw, const float* __restrict__ blk_m,
+__global__ __launch_bounds__(256) void rescale_p_kernel(int groups, int vc_valid, int nb, int bps,
+                                                        int nsplit, int blkw,
+                                                        const float* __restrict__ blk_m,
                                                         const float* __restrict__ refs,
                                                         PT* __restrict__ P, int64_t ldp) {
   constexpr int EPC = 16 / sizeof(PT);
-  const int64_t row = blockIdx.y;
+  const int64_t row = blockIdx.x / (unsigned)groups;
+  const int grp = (int)(blockIdx.x - row * groups);
   const int ncv = (vc_valid + EPC - 1) / EPC;
   u32x4* pr = reinterpret_cast<u32x4*>(P + row * ldp);
   const float* bm = blk_m + row * nb;
   const float* rf = refs + row * nsplit;
-  const int c0 = blockIdx.x * 256 * kRescaleU + threadIdx.x;
+  const int c0 = grp * 256 * kRescaleU + threadIdx.x;
   u32x4 v[kRescaleU];
   float fct[kRescaleU];
 #pragma unroll
@@ -548,9 +551,10 @@ static hipError_t run_output_error(const OeLaunch& a) {
     {
       constexpr int EPC = 16 / sizeof(T);
       const int ncv = (vc_valid + EPC - 1) / EPC;
+      const int groups = (ncv + 256 * kRescaleU - 1) / (256 * kRescaleU);
       FPO_LAUNCH("rescale_p", st,
-                 rescale_p_kernel<T><<<dim3((unsigned)((ncv + 256 * kRescaleU - 1) / (256 * kRescaleU)), (unsigned)a.T),
-                                       dim3(256), 0, st>>>(vc_valid, nbv, bps, a.nsplit, TT::WTN, a.blk_m, a.refs, P, a.ldp));
+                 rescale_p_kernel<T><<<dim3((unsigned)(groups * a.T)), dim3(256), 0, st>>>(
+          groups, vc_valid, nbv, bps, a.nsplit, TT::WTN, a.blk_m, a.refs, P, a.ldp));
       FPO_CHECK_LAUNCH();
     }
     FPO_LAUNCH("proj_chunk", st,

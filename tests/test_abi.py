@@ -110,6 +110,9 @@ def test_output_error_validation(lib):
     assert "2^31" in lib.fpo_last_error().decode()
     assert lib.fpo_output_error_workspace(C.byref(oe(T=1 << 19, d=4096, dtype=L.FPO_F32))) > 0  # fp32 unaffected
     assert lib.fpo_output_error_workspace(C.byref(oe(T=1 << 19, d=4096))) == 0
+    # launch geometry: at most 2^23 tokens per call
+    assert call_oe(lib, oe(T=(1 << 23) + 8, d=8, V=256, dtype=L.FPO_F32)) == L.FPO_ERR_SHAPE
+    assert lib.fpo_output_error_workspace(C.byref(oe(T=1 << 23, d=8, V=256, dtype=L.FPO_F32))) > 0
 
 
 def test_chunk_width_respects_operand_bands(lib):
@@ -207,6 +210,10 @@ def test_pseudograd_validation(lib):
     assert w2 >= w0 + 2 * 256 * 688 * 2                   # one staged bf16 matrix per layer
     # bf16 operand bands (T x d_ff activations) above 2^31 bytes are refused
     assert call(L.PgDesc(1 << 17, 256, 16384, 2, L.FPO_BF16, L.FPO_MODE_W3, 1.0)) == L.FPO_ERR_UNSUPPORTED
+    # launch geometry: at most 2^23 tokens and d <= 2^22 per call
+    assert call(L.PgDesc((1 << 23) + 64, 8, 8, 1, L.FPO_F32, L.FPO_MODE_W3, 1.0)) == L.FPO_ERR_SHAPE
+    assert call(L.PgDesc(64, (1 << 22) + 8, 8, 1, L.FPO_F32, L.FPO_MODE_W3, 1.0)) == L.FPO_ERR_SHAPE
+    assert lib.fpo_pseudograd_workspace(C.byref(L.PgDesc(64, 1 << 22, 8, 1, L.FPO_F32, L.FPO_MODE_W3, 1.0))) > 0
 
 
 def test_pseudograd_operand_alignment(lib):

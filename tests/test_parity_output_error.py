@@ -76,6 +76,16 @@ def test_bf16_ragged(dev, T, d, V, chunk):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_more_tokens_than_a_second_grid_dimension_holds(dev, dtype):
+    """T = 65600, above the 65536 cap of a second grid dimension: the
+    per-token kernels and the p~ rescale run on flat grids."""
+    print(f"[oe] T=65600 d=16 V=520 {dtype}", flush=True)
+    c, x, g, W, y = small_case(I.CONFIGS[0] if dtype == "f32" else I.CONFIGS[1], 65600, 16, 520)
+    got = run_gpu(x, g, W, y, dtype, dev)
+    check_against_oracle(x, g, W, y, dtype, got)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_low_rms_rows_activate_clamp(dev, dtype):
     base = I.CONFIGS[0] if dtype == "f32" else I.CONFIGS[1]
     c = base.shrink(T=200, d=256, V=4096)
