@@ -384,8 +384,9 @@ def main():
         calibrate_copy(args.calibrate_copy)
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build has no "
-              "multi-GPU path: run with --gpus 1", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the library has no "
+              "multi-GPU path (the sharding design is documented, not built); run with --gpus 1",
+              file=sys.stderr)
         sys.exit(2)
     clk_mhz = max_engine_clock_mhz()
     if args.e2e_diagnostic:
