@@ -90,7 +90,9 @@ def call_oe(lib, desc, ws=FAKE, ws_bytes=1 << 40, **over):
 def test_output_error_validation(lib):
     assert call_oe(lib, None) == L.FPO_ERR_NULL
     assert call_oe(lib, oe(dtype=3)) == L.FPO_ERR_DTYPE
-    assert call_oe(lib, oe(T=0)) == L.FPO_ERR_SHAPE
+    assert call_oe(lib, oe(T=0)) == L.FPO_ERR_SHAPE     # empty batch: refused, not a no-op
+    assert call_oe(lib, oe(d=0)) == L.FPO_ERR_SHAPE
+    assert call_oe(lib, oe(V=0)) == L.FPO_ERR_SHAPE
     assert call_oe(lib, oe(d=12)) == L.FPO_ERR_SHAPE
     assert call_oe(lib, oe(V=4100)) == L.FPO_ERR_SHAPE
     assert call_oe(lib, oe(V=1 << 31)) == L.FPO_ERR_SHAPE
@@ -165,6 +167,9 @@ def test_pseudograd_validation(lib):
     assert call(L.PgDesc(128, 256, 688, 2, 1, 9, 1.0)) == L.FPO_ERR_ARG
     assert call(L.PgDesc(128, 256, 690, 2, 1, 0, 1.0)) == L.FPO_ERR_SHAPE
     assert call(L.PgDesc(128, 256, 688, 65, 1, 0, 1.0)) == L.FPO_ERR_SHAPE
+    # empty inputs: the pseudogradient is a mean over the batch's tokens
+    for T_, d_, f_, L_ in ((0, 256, 688, 2), (128, 0, 688, 2), (128, 256, 0, 2), (128, 256, 688, 0)):
+        assert call(L.PgDesc(T_, d_, f_, L_, 1, 0, 1.0)) == L.FPO_ERR_SHAPE
     assert call(L.PgDesc(128, 256, 688, 2, 1, 0, float("inf"))) == L.FPO_ERR_ARG
     assert call(good, g=None) == L.FPO_ERR_NULL
     assert call(good, dW3=None) == L.FPO_ERR_NULL
@@ -266,6 +271,7 @@ def test_apply_update_validation(lib):
     assert call(L.Opt(1, 1e-4, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)) == L.FPO_ERR_NULL  # AdamW needs state2
     assert call(sgd, upd=None) == L.FPO_ERR_NULL
     assert call(sgd, n_mats=0) == L.FPO_ERR_SHAPE
+    assert call(sgd, numel=(C.c_int64 * 1)(0)) == L.FPO_ERR_SHAPE  # empty matrix: no relative clip
     assert call(sgd, numel=(C.c_int64 * 1)(1022)) == L.FPO_ERR_SHAPE
     assert call(sgd, lp=9) == L.FPO_ERR_DTYPE
     assert call(sgd, ws_bytes=8) == L.FPO_ERR_WORKSPACE
@@ -291,6 +297,8 @@ def test_cosine_validation(lib):
     A, ka = arr([FAKE])
     n = (C.c_int64 * 1)(1024)
     assert lib.fpo_cosine(0, n, A, None, 0, None, None, None, None, FAKE, 1 << 20, None) == L.FPO_ERR_SHAPE
+    assert lib.fpo_cosine(1, (C.c_int64 * 1)(0), A, None, 0, None, None, None, None, FAKE, 1 << 20,
+                          None) == L.FPO_ERR_SHAPE
     assert lib.fpo_cosine(1, None, A, None, 0, None, None, None, None, FAKE, 1 << 20, None) == L.FPO_ERR_NULL
     assert lib.fpo_cosine(1, n, A, None, 3, None, None, None, None, FAKE, 1 << 20, None) == L.FPO_ERR_DTYPE
     assert lib.fpo_cosine(1, (C.c_int64 * 1)(6), A, None, 0, None, None, None, None, FAKE, 1 << 20, None) == L.FPO_ERR_SHAPE
