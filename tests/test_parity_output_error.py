@@ -102,6 +102,32 @@ def test_low_rms_rows_activate_clamp(dev, dtype):
     check_against_oracle(x, g, W, y, dtype, got)
 
 
+@pytest.mark.parametrize("chunk", [0, 2048])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_argmax_ties_take_the_lowest_index(dev, dtype, chunk):
+    """Identical unembedding rows that dominate every token's logits (as with
+    duplicated or padded vocabulary rows): the kernels compute identical rows
+    identically, so the tie is exact and the argmax is the lowest tied index,
+    across 128-entry blocks, 256-wide tiles and vocabulary chunks. The fp64
+    oracle's matrix product may round the tied entries differently (its edge
+    columns take another summation order), so it only has to pick one of
+    them."""
+    base = I.CONFIGS[0] if dtype == "f32" else I.CONFIGS[1]
+    c = base.shrink(T=300, d=256, V=10000)
+    xf = I.storage_to_f64(I.hidden(c)) + 3.0  # a common direction in every row
+    x = I.to_storage(xf.astype(np.float32), c.dtype)
+    g, y = I.gain(c), I.targets(c)
+    Wf = I.storage_to_f64(I.unembedding(c)).astype(np.float32)
+    tied = [4001, 130, 2500, 2049, 9999]
+    Wf[tied] = 1.0 / 16.0  # logit ~15 against a random-row maximum ~1.3
+    W = I.to_storage(Wf, c.dtype)
+    got = run_gpu(x, g, W, y, dtype, dev, chunk=chunk)
+    ref = O.output_error(x, g, W, y)
+    assert np.all(np.isin(ref["argmax"], tied))
+    assert np.all(got["argmax"] == 130)
+    check_against_oracle(x, g, W, y, dtype, got)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_peaky_logits_and_planted_targets(dev, dtype):
     """W_U x8 makes softmax peaky (online max rescaling across chunks and the

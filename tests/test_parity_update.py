@@ -177,6 +177,30 @@ def test_clip_edge_cases(dev):
     assert not torch.isnan(W).any()
 
 
+@pytest.mark.parametrize("target", [0, 1], ids=["clip-grad", "clip-update"])
+@pytest.mark.parametrize("kind", [L_.FPO_OPT_SGD, L_.FPO_OPT_ADAMW], ids=["sgd", "adamw"])
+def test_clip_at_zero_weights(dev, kind, target):
+    """The relative clip of a zero matrix: 0.01 ||W|| = 0 bounds the step to
+    zero (the oracle's s = 0), so a nonzero gradient moves nothing and leaves
+    no optimizer state behind (both clip targets)."""
+    W = torch.zeros(4, 8, dtype=torch.float32, device=dev)
+    G = torch.linspace(-1.0, 1.0, 32, dtype=torch.float32, device=dev).reshape(4, 8)
+    gsq = torch.tensor([float((G.double() ** 2).sum())], dtype=torch.float64, device=dev)
+    s1 = torch.zeros_like(W)
+    s2 = torch.zeros_like(W) if kind == L_.FPO_OPT_ADAMW else None
+    Wsq = torch.zeros(1, dtype=torch.float64, device=dev)
+    cs = torch.full((1,), -1.0, dtype=torch.float32, device=dev)
+    api.fpo_apply_update(api.OptConfig(kind=kind, lr=1e-2, clip_frac=0.01, clip_target=target), [G], gsq, [W],
+                         [s1], Wsq, state2=[s2] if s2 is not None else None, clip_scale=cs,
+                         lp_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert O.clip_scale(float(gsq[0]), 0.0, 0.01) == 0.0
+    assert float(cs[0]) == 0.0
+    assert torch.all(W == 0) and float(Wsq[0]) == 0.0
+    if target == L_.FPO_CLIP_GRADIENT:  # the clipped gradient (zero) enters the state
+        assert torch.all(s1 == 0)
+
+
 @pytest.mark.parametrize("bdtype", ["f32", "bf16"])
 def test_cosine(dev, bdtype):
     r = np.random.default_rng(3)
