@@ -114,11 +114,15 @@ __device__ __forceinline__ void logits_epilogue(VA (&acc)[FM][FN], const Map& mp
 // per accumulator column block i (vocabulary rows 32f + 8q + 4h + j, h = lane
 // half, j < 4, in increasing order for increasing (f, q, j)); the lane pair
 // (l, l ^ 32) covers the wave's 128 vocabulary entries of that token, so the
-// block statistics need one cross-lane exchange. p~ goes out as 8-byte runs of
-// 4 vocabulary entries.
+// block statistics need one cross-lane exchange. The bf16 p~ tile (256 tokens
+// x 256 entries, 128 KB) is staged in the LDS ring, free after the main loop,
+// as [token][32 chunks of 8 entries] with chunk c of token row r at position
+// c ^ (r & 31) (the 32 token rows of one 8-byte write, and the 32 chunks of
+// one row read back, fall in distinct 16-byte slots), then written out as
+// whole 512-byte token rows: scattered 8-byte runs cost 7% of the kernel.
 template <bool RAGGED>
-__device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], int vt0, int tt0,
-                                                   int T, int vc_valid, int v0,
+__device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], G2Smem& sm, int vt0,
+                                                   int tt0, int T, int vc_valid, int v0,
                                                    uint16_t* __restrict__ P, int64_t ldp, int nb,
                                                    float* __restrict__ blk_m,
                                                    float* __restrict__ blk_s,
@@ -160,7 +164,10 @@ __device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], in
       }
     }
     float s = 0.f;
-    uint16_t* pr = P + (int64_t)t * ldp + vl;
+    // LDS token row of this lane and the tile column of its entries at f = q = 0
+    const int lrow = (w & 1) * G2::WTN + 32 * i + lc;
+    const int col0 = vl - vt0;
+    char* lds_row = reinterpret_cast<char*>(sm.s) + lrow * 512 + (col0 & 7) * 2;
 #pragma unroll
     for (int f = 0; f < 4; ++f)
 #pragma unroll
@@ -172,9 +179,8 @@ __device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], in
           p[j] = (!RAGGED || o < lim) ? __expf(acc[f][i][4 * q + j] - m) : 0.f;
           s += p[j];
         }
-        if (t < T)
-          *reinterpret_cast<u32x2*>(pr + 32 * f + 8 * q) =
-              u32x2{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])};
+        const int chunk = ((col0 + 32 * f + 8 * q) >> 3) ^ lc;  // lrow & 31 == lc
+        *reinterpret_cast<u32x2*>(lds_row + chunk * 16) = u32x2{pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3])};
       }
     s += __shfl_xor(s, 32, 64);
     if (t < T && h == 0 && b < nb) {
@@ -183,6 +189,19 @@ __device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], in
       blk_s[ob] = s;
       blk_i[ob] = (mi == 0x7fffffff) ? mi : v0 + mi;
     }
+  }
+  __syncthreads();
+  // whole token rows out: each half-wave one row, 16 bytes per lane (entries
+  // past vc_valid were staged as zeros; the tile lies inside the chunk's Vc
+  // columns)
+  const int c = threadIdx.x & 31;
+#pragma unroll 4
+  for (int k = 0; k < 32; ++k) {
+    const int r = (int)(threadIdx.x >> 5) + 8 * k;
+    const int t = tt0 + r;
+    if (t >= T) break;  // rows increase with k
+    const u32x4 v = sm.s[r * 32 + (c ^ (r & 31))];
+    *reinterpret_cast<u32x4*>(P + (int64_t)t * ldp + vt0 + 8 * c) = v;
   }
 }
 
@@ -205,9 +224,9 @@ __global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
     const Operand B{y + (int64_t)m0 * d, d, band_bytes(T - m0, d)};
     gemm2_mainloop<false>(sm, acc, A, B, vc_valid - n0, T - m0, d, 0, (d + G2::BK - 1) / G2::BK);
     if (n0 + ((threadIdx.x >> 7) + 1) * G2::WTM <= vc_valid)  // wave-uniform
-      logits_epilogue_vt<false>(acc, n0, m0, T, vc_valid, v0, P, ldp, nb, blk_m, blk_s, blk_i);
+      logits_epilogue_vt<false>(acc, sm, n0, m0, T, vc_valid, v0, P, ldp, nb, blk_m, blk_s, blk_i);
     else
-      logits_epilogue_vt<true>(acc, n0, m0, T, vc_valid, v0, P, ldp, nb, blk_m, blk_s, blk_i);
+      logits_epilogue_vt<true>(acc, sm, n0, m0, T, vc_valid, v0, P, ldp, nb, blk_m, blk_s, blk_i);
   } else {
     __shared__ GemmSmem<E> sm;
     f32x4 acc[E::FM][E::FN];
