@@ -6,6 +6,7 @@ import pytest
 import torch
 
 import oracle as O
+from paper_2608_14563_amd import _lib as L_
 from paper_2608_14563_amd import api
 from paper_2608_14563_amd import inputs as I
 from tests._util import assert_close, bf16_rne_bits, dev_tensor, host64, ulp_diff_f32
@@ -190,6 +191,62 @@ def test_full_size_fused_update(dev, cid, stage):
         lpv = lp[l][ii, jj].view(torch.int16).cpu().numpy().view(np.uint16)
         assert np.array_equal(lpv, bf16_rne_bits(w_new)), l
     # ||W'||^2 reported for the next step's clip
+    for l in (0, c.L - 1):
+        wn = W[l].double()
+        assert abs(float(Wsq[l]) - float((wn * wn).sum())) <= 1e-9 * float(Wsq[l])
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("cid", [1, 3])
+def test_full_size_fused_adamw(dev, cid):
+    """AdamW in the benchmark's launch configuration (--optimizer adamw): the
+    bf16-staged pseudogradient, the step overlapped with the next layer's
+    outer products, first step. Sampled moments against the oracle's AdamW on
+    the clipped pseudogradient s * D (s from the reported norms); W' against
+    the kernel's float32 formula applied to the GPU's own moments (a few ulp:
+    the step ~ lr sign(D) makes the oracle's W' sensitive to near-zero D);
+    the bf16 copy exactly RNE of W'; the reported ||W'||^2."""
+    c = I.CONFIGS[cid]
+    g = signal(c)
+    acts = [I.activation(c, l) for l in range(c.L)]
+    Wh = [I.master_weight(c, l) for l in range(c.L)]
+    W = [torch.from_numpy(w).to(dev) for w in Wh]
+    wsq = np.array([float((w.astype(np.float64) ** 2).sum()) for w in Wh])
+    Wsq = torch.tensor(wsq, dtype=torch.float64, device=dev)
+    m1 = [torch.zeros_like(w) for w in W]
+    m2 = [torch.zeros_like(w) for w in W]
+    lp = [torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in W]
+    ss = torch.empty(c.L, dtype=torch.float64, device=dev)
+    cs = torch.empty(c.L, dtype=torch.float32, device=dev)
+    opt = api.OptConfig(kind=L_.FPO_OPT_ADAMW, lr=c.lr, clip_frac=c.clip_frac, step=1)
+    print(f"[pg] full-size AdamW config {cid}", flush=True)
+    api.fpo_pseudograd(dev_tensor(g, dev), [dev_tensor(a, dev) for a in acts], dW3=None, sumsq=ss, opt=opt,
+                       W_master=W, W_lp=lp, state1=m1, state2=m2, W_sumsq=Wsq, clip_scale=cs, grad_bf16=True)
+    torch.cuda.synchronize()
+    ssh = ss.cpu().numpy()
+    gf = I.storage_to_f64(g)
+    f32 = lambda v: np.float64(np.float32(v))  # noqa: E731
+    r = np.random.default_rng(200 + cid)
+    for l in range(c.L):
+        s = min(1.0, c.clip_frac * np.sqrt(wsq[l]) / np.sqrt(ssh[l]))
+        assert abs(float(cs[l]) - s) <= 1e-6 * s
+        ii = np.concatenate([r.integers(0, c.d, 64), [0, c.d - 1]])
+        jj = np.concatenate([r.integers(0, c.d_ff, 64), [c.d_ff - 1, 0]])
+        D = np.einsum("ti,ti->i", gf[:, ii], I.storage_to_f64(acts[l][:, jj])) / c.T
+        w0 = Wh[l][ii, jj].astype(np.float64)
+        _, om, ov = O.adamw(w0, 0.0, 0.0, s * D, opt.lr, 1, opt.beta1, opt.beta2, opt.adam_eps, opt.weight_decay)
+        mg = m1[l][ii, jj].cpu().numpy().astype(np.float64)
+        vg = m2[l][ii, jj].cpu().numpy().astype(np.float64)
+        assert_close(f"exp_avg[{l}]", mg, om, "bf16")
+        assert_close(f"exp_avg_sq[{l}]", vg, ov, "bf16")
+        step = f32(opt.lr) * (mg * f32(1.0 / (1.0 - opt.beta1))) / (
+            np.sqrt(vg) * f32(1.0 / np.sqrt(1.0 - opt.beta2)) + f32(opt.adam_eps))
+        expect = w0 * f32(1.0 - opt.lr * opt.weight_decay) - step
+        wg = W[l][ii, jj].cpu().numpy()
+        tol = 2 * np.spacing(np.abs(expect).astype(np.float32)).astype(np.float64) + 8 * 2.0 ** -23 * np.abs(step)
+        assert np.all(np.abs(wg.astype(np.float64) - expect) <= tol), l
+        lpv = lp[l][ii, jj].view(torch.int16).cpu().numpy().view(np.uint16)
+        assert np.array_equal(lpv, bf16_rne_bits(wg)), l
     for l in (0, c.L - 1):
         wn = W[l].double()
         assert abs(float(Wsq[l]) - float((wn * wn).sum())) <= 1e-9 * float(Wsq[l])
