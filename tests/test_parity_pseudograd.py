@@ -253,6 +253,60 @@ def test_full_size_fused_adamw(dev, cid):
 
 
 @pytest.mark.slow
+@pytest.mark.parametrize("lr", [None, 2.0], ids=["workload-lr", "lr2-clip-active"])
+def test_full_size_fused_update_clip(dev, lr):
+    """The clip-the-update reading at full size (--clip-target update, OLMo-2
+    shapes, bf16-staged pseudogradient): SGD-momentum state advances on the
+    unclipped pseudogradient (sampled against the oracle's D), the applied
+    step -lr b is scaled by s = min(1, 0.01 ||W|| / ||lr b||) (checked against
+    the oracle's formula on the GPU's own norm), and W' equals W + s (-lr b)
+    from the GPU's state within fp32 rounding. At the workload's lr (1e-4)
+    the bound is idle (s = 1); lr = 2 makes it bite on every layer."""
+    c = I.CONFIGS[1]
+    g = signal(c)
+    acts = [I.activation(c, l) for l in range(c.L)]
+    Wh = [I.master_weight(c, l) for l in range(c.L)]
+    W = [torch.from_numpy(w).to(dev) for w in Wh]
+    wsq = np.array([float((w.astype(np.float64) ** 2).sum()) for w in Wh])
+    Wsq = torch.tensor(wsq, dtype=torch.float64, device=dev)
+    b1 = [torch.zeros_like(w) for w in W]
+    lp = [torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in W]
+    ss = torch.empty(c.L, dtype=torch.float64, device=dev)
+    cs = torch.empty(c.L, dtype=torch.float32, device=dev)
+    lr = c.lr if lr is None else lr
+    opt = api.OptConfig(lr=lr, clip_frac=c.clip_frac, step=1, clip_target=L_.FPO_CLIP_UPDATE)
+    print(f"[pg] full-size clip-the-update lr={lr}", flush=True)
+    api.fpo_pseudograd(dev_tensor(g, dev), [dev_tensor(a, dev) for a in acts], dW3=None, sumsq=ss, opt=opt,
+                       W_master=W, W_lp=lp, state1=b1, W_sumsq=Wsq, clip_scale=cs, grad_bf16=True)
+    torch.cuda.synchronize()
+    gf = I.storage_to_f64(g)
+    f32 = lambda v: np.float64(np.float32(v))  # noqa: E731
+    r = np.random.default_rng(300)
+    for l in range(c.L):
+        bl = b1[l].double()
+        dsq = float(((f32(lr) * bl) ** 2).sum())  # ||delta||^2 of the GPU's step
+        s = O.clip_scale(dsq, wsq[l], c.clip_frac)
+        assert abs(float(cs[l]) - s) <= 1e-5 * s, (l, float(cs[l]), s)
+        assert (s < 1.0) == (lr > 1.0), (l, s)
+        ii = np.concatenate([r.integers(0, c.d, 64), [0, c.d - 1]])
+        jj = np.concatenate([r.integers(0, c.d_ff, 64), [c.d_ff - 1, 0]])
+        D = np.einsum("ti,ti->i", gf[:, ii], I.storage_to_f64(acts[l][:, jj])) / c.T
+        bg = b1[l][ii, jj].cpu().numpy().astype(np.float64)
+        assert_close(f"momentum[{l}] samples", bg, D, "bf16")  # unclipped state
+        w0 = Wh[l][ii, jj].astype(np.float64)
+        delta = -f32(lr) * bg
+        expect = w0 + float(cs[l]) * delta
+        wg = W[l][ii, jj].cpu().numpy()
+        tol = 2 * np.spacing(np.abs(expect).astype(np.float32)).astype(np.float64) + 4 * 2.0 ** -23 * np.abs(delta)
+        assert np.all(np.abs(wg.astype(np.float64) - expect) <= tol), l
+        lpv = lp[l][ii, jj].view(torch.int16).cpu().numpy().view(np.uint16)
+        assert np.array_equal(lpv, bf16_rne_bits(wg)), l
+        # the whole applied step respects the bound
+        dW = W[l].double() - torch.from_numpy(Wh[l]).to(dev).double()
+        assert float(torch.linalg.norm(dW)) <= c.clip_frac * np.sqrt(wsq[l]) * (1 + 1e-4)
+
+
+@pytest.mark.slow
 def test_full_size_diagnostic_rank1_reference(dev):
     """Diagnostic workload at full size (T = 8192, Qwen3-8B shapes, 36 layers):
     the fused cosine terms against a rank-1 reference R = u v^T, for which
