@@ -467,6 +467,8 @@ __global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
 // outside [0, V)), then the clamped VJP
 //   rho~ = max(sqrt(mean x^2 + eps), min_rms); x^ = x / rho~;
 //   c = (1/d) <x^, gamma * g>;  g~ = (gamma * g - c x^) / rho~.
+constexpr int kFinRegIters = 8;  // 1024 entries per iteration of a 256-lane workgroup
+
 template <typename T>
 __global__ __launch_bounds__(256) void finalize_vjp_kernel(
     int d, int V, int nsplit, int64_t split_stride, const float* __restrict__ G,
@@ -485,7 +487,11 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
   const T* xr = x + row * d;
   float* gt = g_tilde + row * d;
   float ss = 0.f, cd = 0.f, zt = 0.f;
-  for (int k = threadIdx.x * 4; k < d; k += 1024) {
+  // pass 1: g = sum_s G_s / S - W_U[y] and the row reductions. Rows of up to
+  // kFinRegIters * 1024 entries keep g and x in registers for pass 2; longer
+  // rows park the rest of g in the g~ row (rewritten in pass 2).
+  f32x4 gk[kFinRegIters], xk[kFinRegIters];
+  auto pass1 = [&](int k) -> f32x4 {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int s = 0; s < nsplit; ++s) acc += *reinterpret_cast<const f32x4*>(G + s * split_stride + row * d + k);
     f32x4 g = {0.f, 0.f, 0.f, 0.f};
@@ -496,10 +502,26 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
       zt += yv.x * wy.x + yv.y * wy.y + yv.z * wy.z + yv.w * wy.w;  // target logit z_y
     }
     if (g_pre) *reinterpret_cast<f32x4*>(g_pre + row * d + k) = g;
-    *reinterpret_cast<f32x4*>(gt + k) = g;
-    f32x4 xv = ld4(xr, k), gm = ld4(gamma, k);
+    return g;
+  };
+  auto reduce = [&](f32x4 g, f32x4 xv, f32x4 gm) {
     ss += xv.x * xv.x + xv.y * xv.y + xv.z * xv.z + xv.w * xv.w;
     cd += xv.x * gm.x * g.x + xv.y * gm.y * g.y + xv.z * gm.z * g.z + xv.w * gm.w * g.w;
+  };
+#pragma unroll
+  for (int it = 0; it < kFinRegIters; ++it) {
+    const int k = threadIdx.x * 4 + it * 1024;
+    gk[it] = xk[it] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (k < d) {
+      gk[it] = pass1(k);
+      xk[it] = ld4(xr, k);
+      reduce(gk[it], xk[it], ld4(gamma, k));
+    }
+  }
+  for (int k = threadIdx.x * 4 + kFinRegIters * 1024; k < d; k += 1024) {
+    const f32x4 g = pass1(k), xv = ld4(xr, k);
+    *reinterpret_cast<f32x4*>(gt + k) = g;
+    reduce(g, xv, ld4(gamma, k));
   }
   ss = block_sum(ss, red);
   cd = block_sum(cd, red);
@@ -508,9 +530,9 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
   const float rt = fmaxf(rho, min_rms);
   const float irt = 1.0f / rt;
   const float c = cd * irt / (float)d;  // (1/d) <x / rho~, gamma * g>
-  for (int k = threadIdx.x * 4; k < d; k += 1024) {
-    f32x4 g = *reinterpret_cast<const f32x4*>(gt + k);
-    f32x4 xv = ld4(xr, k), gm = ld4(gamma, k);
+  // pass 2: g~ = (gamma g - c x^) / rho~
+  auto out = [&](int k, f32x4 g, f32x4 xv) {
+    const f32x4 gm = ld4(gamma, k);
     f32x4 o;
     o.x = (gm.x * g.x - c * xv.x * irt) * irt;
     o.y = (gm.y * g.y - c * xv.y * irt) * irt;
@@ -518,7 +540,14 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
     o.w = (gm.w * g.w - c * xv.w * irt) * irt;
     *reinterpret_cast<f32x4*>(gt + k) = o;
     if (g_tilde_lp) st4(g_tilde_lp + row * d, k, o);
+  };
+#pragma unroll
+  for (int it = 0; it < kFinRegIters; ++it) {
+    const int k = threadIdx.x * 4 + it * 1024;
+    if (k < d) out(k, gk[it], xk[it]);
   }
+  for (int k = threadIdx.x * 4 + kFinRegIters * 1024; k < d; k += 1024)
+    out(k, *reinterpret_cast<const f32x4*>(gt + k), ld4(xr, k));
   if (threadIdx.x == 0) {
     const float l_se = runM[row] + logf(S);
     if (lse) lse[row] = l_se;
