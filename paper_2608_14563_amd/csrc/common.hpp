@@ -93,6 +93,22 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   for (int i = 0; i < nw; ++i) s += red[i];  // fixed order
   return s;
 }
+// One thread's share of sum_b v[b], b in [begin, end), of a 256-lane
+// workgroup: elements begin + tid + 256k in a fixed order, with four
+// independent accumulators so that four loads are in flight.
+__device__ __forceinline__ double strided_sum_d(const double* __restrict__ v, int64_t begin, int64_t end) {
+  double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+  int64_t b = begin + threadIdx.x;
+  for (; b + 768 < end; b += 1024) {
+    a0 += v[b];
+    a1 += v[b + 256];
+    a2 += v[b + 512];
+    a3 += v[b + 768];
+  }
+  for (; b < end; b += 256) a0 += v[b];
+  return (a0 + a1) + (a2 + a3);
+}
+
 __device__ __forceinline__ double block_sum_d(double v, double* red) {
   v = wave_sum_d(v);
   const int w = threadIdx.x / kWave, l = threadIdx.x % kWave, nw = blockDim.x / kWave;

@@ -78,9 +78,7 @@ __global__ __launch_bounds__(256) void sum_parts_kernel(UpdArgs a, const double*
                                                         double* __restrict__ out) {
   __shared__ double red[16];
   const int m = blockIdx.x;
-  double acc = 0.0;
-  for (int64_t b = a.blk0[m] + threadIdx.x; b < a.blk0[m + 1]; b += 256) acc += part[b];
-  acc = block_sum_d(acc, red);
+  const double acc = block_sum_d(strided_sum_d(part, a.blk0[m], a.blk0[m + 1]), red);
   if (threadIdx.x == 0) out[m] = acc;
 }
 
@@ -106,9 +104,7 @@ __global__ __launch_bounds__(256) void update_reduce_kernel(UpdArgs a, OptScalar
                                                             float* __restrict__ clip_scale) {
   __shared__ double red[16];
   const int m = blockIdx.x;
-  double acc = 0.0;
-  for (int64_t b = a.blk0[m] + threadIdx.x; b < a.blk0[m + 1]; b += 256) acc += part[b];
-  acc = block_sum_d(acc, red);
+  const double acc = block_sum_d(strided_sum_d(part, a.blk0[m], a.blk0[m + 1]), red);
   if (threadIdx.x == 0) {
     // the clip factor the update used, from the W_sumsq it read (grad_sumsq:
     // ||dW||^2, or ||delta||^2 in clip-the-update mode)
@@ -297,12 +293,25 @@ __global__ __launch_bounds__(256) void cosine_reduce_kernel(CosArgs a, const dou
                                                             float* __restrict__ cosv) {
   __shared__ double red[16];
   const int m = blockIdx.x;
-  double x = 0.0, y = 0.0, z = 0.0;
-  for (int64_t b = a.blk0[m] + threadIdx.x; b < a.blk0[m + 1]; b += 256) {
+  // two visits per iteration (six independent accumulators) keep loads in flight
+  double x = 0.0, y = 0.0, z = 0.0, x1 = 0.0, y1 = 0.0, z1 = 0.0;
+  int64_t b = a.blk0[m] + threadIdx.x;
+  for (; b + 256 < a.blk0[m + 1]; b += 512) {
+    x += part[3 * b];
+    y += part[3 * b + 1];
+    z += part[3 * b + 2];
+    x1 += part[3 * (b + 256)];
+    y1 += part[3 * (b + 256) + 1];
+    z1 += part[3 * (b + 256) + 2];
+  }
+  for (; b < a.blk0[m + 1]; b += 256) {
     x += part[3 * b];
     y += part[3 * b + 1];
     z += part[3 * b + 2];
   }
+  x += x1;
+  y += y1;
+  z += z1;
   x = block_sum_d(x, red);
   y = block_sum_d(y, red);
   z = block_sum_d(z, red);
