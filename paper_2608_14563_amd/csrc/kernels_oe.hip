@@ -249,6 +249,8 @@ __global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
 // so every factor is <= 1 and nothing can overflow.
 constexpr int kMaxSplit = 8;
 
+constexpr int kStatsRegs = 24;  // blocks per lane held in registers (chunks of up to 1536 blocks)
+
 template <typename PT>
 __global__ __launch_bounds__(256) void chunk_stats_kernel(
     int T, int nb, int bps, int nsplit, int first, int blkw, int vc_valid,
@@ -262,29 +264,68 @@ __global__ __launch_bounds__(256) void chunk_stats_kernel(
   const float* bm = blk_m + (int64_t)row * nb;
   const float* bs = blk_s + (int64_t)row * nb;
   const int32_t* bi = blk_i + (int64_t)row * nb;
-  float mc = -INFINITY;
-  for (int b = l; b < nb; b += 64) mc = fmaxf(mc, bm[b]);
-  mc = wave_max(mc);
+  float mc = -INFINITY, s = 0.f, Mold = -INFINITY, Mnew;
   int ai = 0x7fffffff;
-  for (int b = l; b < nb; b += 64)
-    if (bm[b] == mc) ai = min(ai, bi[b]);
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) ai = min(ai, __shfl_xor(ai, o, 64));
-  const float Mold = first ? -INFINITY : runM[row];
-  const float Mnew = fmaxf(Mold, mc);
   float ref[kMaxSplit];
+  if (nb <= 64 * kStatsRegs) {
+    // each lane's block maxima and sums loaded once (blocks l + 64j), every
+    // pass from registers
+    float vm[kStatsRegs], vs[kStatsRegs];
 #pragma unroll
-  for (int sp = 0; sp < kMaxSplit; ++sp) {
-    float r = -INFINITY;
-    if (sp < nsplit) {
-      for (int b = sp * bps + l; b < min(nb, (sp + 1) * bps); b += 64) r = fmaxf(r, bm[b]);
-      r = wave_max(r);
+    for (int j = 0; j < kStatsRegs; ++j) {
+      const int b = l + 64 * j;
+      vm[j] = b < nb ? bm[b] : -INFINITY;
+      vs[j] = b < nb ? bs[b] : 0.f;
     }
-    ref[sp] = r;
+#pragma unroll
+    for (int j = 0; j < kStatsRegs; ++j) mc = fmaxf(mc, vm[j]);
+    mc = wave_max(mc);
+#pragma unroll
+    for (int j = 0; j < kStatsRegs; ++j) {
+      const int b = l + 64 * j;
+      if (b < nb && vm[j] == mc) ai = min(ai, bi[b]);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) ai = min(ai, __shfl_xor(ai, o, 64));
+    Mold = first ? -INFINITY : runM[row];
+    Mnew = fmaxf(Mold, mc);
+#pragma unroll
+    for (int sp = 0; sp < kMaxSplit; ++sp) {
+      float r = -INFINITY;
+      if (sp < nsplit) {
+#pragma unroll
+        for (int j = 0; j < kStatsRegs; ++j) {
+          const int b = l + 64 * j;
+          if (b >= sp * bps && b < (sp + 1) * bps) r = fmaxf(r, vm[j]);
+        }
+        r = wave_max(r);
+      }
+      ref[sp] = r;
+    }
+    // partition function of the chunk relative to M_new
+#pragma unroll
+    for (int j = 0; j < kStatsRegs; ++j)
+      if (l + 64 * j < nb) s += vs[j] * __expf(vm[j] - Mnew);
+  } else {
+    for (int b = l; b < nb; b += 64) mc = fmaxf(mc, bm[b]);
+    mc = wave_max(mc);
+    for (int b = l; b < nb; b += 64)
+      if (bm[b] == mc) ai = min(ai, bi[b]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) ai = min(ai, __shfl_xor(ai, o, 64));
+    Mold = first ? -INFINITY : runM[row];
+    Mnew = fmaxf(Mold, mc);
+#pragma unroll
+    for (int sp = 0; sp < kMaxSplit; ++sp) {
+      float r = -INFINITY;
+      if (sp < nsplit) {
+        for (int b = sp * bps + l; b < min(nb, (sp + 1) * bps); b += 64) r = fmaxf(r, bm[b]);
+        r = wave_max(r);
+      }
+      ref[sp] = r;
+    }
+    for (int b = l; b < nb; b += 64) s += bs[b] * __expf(bm[b] - Mnew);
   }
-  // partition function of the chunk relative to M_new
-  float s = 0.f;
-  for (int b = l; b < nb; b += 64) s += bs[b] * __expf(bm[b] - Mnew);
   s = wave_sum(s);
   if (l < nsplit) {
     float fo = 0.f, rf = 0.f;

@@ -62,7 +62,7 @@ def test_tiny_fp32_config(dev, chunk):
 
 
 @pytest.mark.parametrize("T,d,V,chunk", [(300, 264, 4104, 1024), (517, 512, 8200, 0), (64, 256, 2048, 256),
-                                         (5, 8200, 264, 0)])
+                                         (5, 8200, 264, 0), (16, 64, 100000, 0)])
 def test_fp32_ragged(dev, T, d, V, chunk):
     c, x, g, W, y = small_case(I.CONFIGS[0], T, d, V)
     got = run_gpu(x, g, W, y, "f32", dev, chunk=chunk)
@@ -70,7 +70,7 @@ def test_fp32_ragged(dev, T, d, V, chunk):
 
 
 @pytest.mark.parametrize("T,d,V,chunk", [(300, 264, 4104, 1024), (600, 512, 10000, 0), (256, 256, 4096, 2048), (1, 128, 1024, 0),
-                                         (5, 8200, 264, 0)])
+                                         (5, 8200, 264, 0), (16, 64, 200000, 0)])
 def test_bf16_ragged(dev, T, d, V, chunk):
     c, x, g, W, y = small_case(I.CONFIGS[1], T, d, V)
     got = run_gpu(x, g, W, y, "bf16", dev, chunk=chunk)
