@@ -18,6 +18,10 @@
 namespace fpo {
 
 // ------------------------------------------------------------------ forward
+// Per-token row kernels (one 256-lane workgroup per token, 1024 entries per
+// sweep) hold rows of up to this many sweeps in registers between passes.
+constexpr int kRowRegIters = 8;
+
 template <typename T>
 __global__ __launch_bounds__(256) void rms_forward_kernel(const T* __restrict__ x,
                                                           const T* __restrict__ gamma, int d,
@@ -26,17 +30,31 @@ __global__ __launch_bounds__(256) void rms_forward_kernel(const T* __restrict__ 
   __shared__ float red[16];
   const int64_t row = blockIdx.x;
   const T* xr = x + row * d;
+  // rows of up to kRowRegIters * 1024 entries are read once (held in registers)
   float ss = 0.f;
-  for (int k = threadIdx.x * 4; k < d; k += 1024) {
-    f32x4 v = ld4(xr, k);
+  f32x4 xk[kRowRegIters];
+#pragma unroll
+  for (int it = 0; it < kRowRegIters; ++it) {
+    const int k = threadIdx.x * 4 + it * 1024;
+    xk[it] = k < d ? ld4(xr, k) : f32x4{0.f, 0.f, 0.f, 0.f};
+    ss += xk[it].x * xk[it].x + xk[it].y * xk[it].y + xk[it].z * xk[it].z + xk[it].w * xk[it].w;
+  }
+  for (int k = threadIdx.x * 4 + kRowRegIters * 1024; k < d; k += 1024) {
+    const f32x4 v = ld4(xr, k);
     ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   ss = block_sum(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
-  for (int k = threadIdx.x * 4; k < d; k += 1024) {
-    f32x4 v = ld4(xr, k), g = ld4(gamma, k);
+  auto out = [&](int k, f32x4 v) {
+    const f32x4 g = ld4(gamma, k);
     st4(y + row * d, k, f32x4{g.x * v.x * inv, g.y * v.y * inv, g.z * v.z * inv, g.w * v.w * inv});
+  };
+#pragma unroll
+  for (int it = 0; it < kRowRegIters; ++it) {
+    const int k = threadIdx.x * 4 + it * 1024;
+    if (k < d) out(k, xk[it]);
   }
+  for (int k = threadIdx.x * 4 + kRowRegIters * 1024; k < d; k += 1024) out(k, ld4(xr, k));
   if (bad && row == 0 && threadIdx.x == 0) *bad = 0;
 }
 
@@ -508,8 +526,6 @@ __global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
 // outside [0, V)), then the clamped VJP
 //   rho~ = max(sqrt(mean x^2 + eps), min_rms); x^ = x / rho~;
 //   c = (1/d) <x^, gamma * g>;  g~ = (gamma * g - c x^) / rho~.
-constexpr int kFinRegIters = 8;  // 1024 entries per iteration of a 256-lane workgroup
-
 template <typename T>
 __global__ __launch_bounds__(256) void finalize_vjp_kernel(
     int d, int V, int nsplit, int64_t split_stride, const float* __restrict__ G,
@@ -529,9 +545,9 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
   float* gt = g_tilde + row * d;
   float ss = 0.f, cd = 0.f, zt = 0.f;
   // pass 1: g = sum_s G_s / S - W_U[y] and the row reductions. Rows of up to
-  // kFinRegIters * 1024 entries keep g and x in registers for pass 2; longer
+  // kRowRegIters * 1024 entries keep g and x in registers for pass 2; longer
   // rows park the rest of g in the g~ row (rewritten in pass 2).
-  f32x4 gk[kFinRegIters], xk[kFinRegIters];
+  f32x4 gk[kRowRegIters], xk[kRowRegIters];
   auto pass1 = [&](int k) -> f32x4 {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int s = 0; s < nsplit; ++s) acc += *reinterpret_cast<const f32x4*>(G + s * split_stride + row * d + k);
@@ -550,7 +566,7 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
     cd += xv.x * gm.x * g.x + xv.y * gm.y * g.y + xv.z * gm.z * g.z + xv.w * gm.w * g.w;
   };
 #pragma unroll
-  for (int it = 0; it < kFinRegIters; ++it) {
+  for (int it = 0; it < kRowRegIters; ++it) {
     const int k = threadIdx.x * 4 + it * 1024;
     gk[it] = xk[it] = f32x4{0.f, 0.f, 0.f, 0.f};
     if (k < d) {
@@ -559,7 +575,7 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
       reduce(gk[it], xk[it], ld4(gamma, k));
     }
   }
-  for (int k = threadIdx.x * 4 + kFinRegIters * 1024; k < d; k += 1024) {
+  for (int k = threadIdx.x * 4 + kRowRegIters * 1024; k < d; k += 1024) {
     const f32x4 g = pass1(k), xv = ld4(xr, k);
     *reinterpret_cast<f32x4*>(gt + k) = g;
     reduce(g, xv, ld4(gamma, k));
@@ -583,11 +599,11 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
     if (g_tilde_lp) st4(g_tilde_lp + row * d, k, o);
   };
 #pragma unroll
-  for (int it = 0; it < kFinRegIters; ++it) {
+  for (int it = 0; it < kRowRegIters; ++it) {
     const int k = threadIdx.x * 4 + it * 1024;
     if (k < d) out(k, gk[it], xk[it]);
   }
-  for (int k = threadIdx.x * 4 + kFinRegIters * 1024; k < d; k += 1024)
+  for (int k = threadIdx.x * 4 + kRowRegIters * 1024; k < d; k += 1024)
     out(k, *reinterpret_cast<const f32x4*>(gt + k), ld4(xr, k));
   if (threadIdx.x == 0) {
     const float l_se = runM[row] + logf(S);
