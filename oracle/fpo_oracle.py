@@ -271,13 +271,6 @@ def adamw_update_clip(W, m, v, G, lr, step, beta1=0.9, beta2=0.999, eps=1e-8, we
     return W + s * delta, m2, v2, s
 
 
-def bf16_rne(x):
-    """bfloat16 bit patterns of float32 values (round to nearest even)."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    r = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    return r.astype(np.uint16)
-
-
 # --------------------------------------------------------------------------
 # Diagnostic cosine (eq. cosine) and the model-level summary (Sec. 2.3).
 def cosine(A, B):

@@ -233,10 +233,6 @@ struct Pipe2 {
       }
     }
   }
-  __device__ __forceinline__ static void mfma1(u32x4 a, u32x4 b, f32x16& acc) {
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                  __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
-  }
 };
 
 #define FPO_SB() __builtin_amdgcn_sched_barrier(0)

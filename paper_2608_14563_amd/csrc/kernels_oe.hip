@@ -271,7 +271,7 @@ constexpr int kStatsRegs = 24;  // blocks per lane held in registers (chunks of 
 
 template <typename PT>
 __global__ __launch_bounds__(256) void chunk_stats_kernel(
-    int T, int nb, int bps, int nsplit, int first, int blkw, int vc_valid,
+    int T, int nb, int bps, int nsplit, int first,
     const float* __restrict__ blk_m, const float* __restrict__ blk_s,
     const int32_t* __restrict__ blk_i, float* __restrict__ runM, float* __restrict__ runS,
     int32_t* __restrict__ runA, float* __restrict__ fout, float* __restrict__ alpha,
@@ -650,7 +650,7 @@ static hipError_t run_output_error(const OeLaunch& a) {
     const int bps = (nbv + a.nsplit - 1) / a.nsplit;
     FPO_LAUNCH("chunk_stats", st,
                chunk_stats_kernel<T><<<dim3((unsigned)((a.T + 3) / 4)), dim3(256), 0, st>>>(
-        (int)a.T, nbv, bps, a.nsplit, c == 0, TT::WTN, vc_valid, a.blk_m, a.blk_s, a.blk_i,
+        (int)a.T, nbv, bps, a.nsplit, c == 0, a.blk_m, a.blk_s, a.blk_i,
         a.runM, a.runS, a.runA, a.fout, a.alpha, a.refs));
     FPO_CHECK_LAUNCH();
     {
