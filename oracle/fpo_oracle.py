@@ -35,10 +35,10 @@ Readings of points the paper leaves open (each listed in the design notes):
     round(N/4) layers;
   * the post-FFN composition uses the fp32 g~ (before any bf16 rounding) and
     the same eps and min-RMS clamp as the final norm.
-Parity status: every function below is pinned by tests/test_oracle_pins.py
-except the clamp branch of rmsnorm_vjp (rho < min_rms), which has no
-external definition beyond its own formula: parity unpinned for that branch
-(it is shared by post_ffn_signal).
+Parity status: every function below is pinned by tests/test_oracle_pins.py,
+the clamp branch of rmsnorm_vjp (rho < min_rms, shared by post_ffn_signal)
+included: it equals the autograd VJP of a plain RMSNorm whose epsilon is
+raised, per row, so that the row's RMS is exactly the floor.
 """
 from __future__ import annotations
 

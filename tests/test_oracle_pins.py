@@ -231,6 +231,29 @@ def test_vjp_clamp_inactive_is_bit_identical_and_active_rows_use_floor():
     np.testing.assert_allclose(a[2], (gam * g[2] - xh * c) / 0.5, rtol=1e-14)
 
 
+def test_vjp_clamp_branch_is_the_vjp_of_an_rmsnorm_lifted_to_the_floor():
+    """Rows whose RMS is below the floor: the clamped VJP equals the exact
+    (autograd) VJP of a plain RMSNorm whose epsilon is raised, for that row, to
+    floor^2 - mean(x^2), so that its RMS is exactly the floor. This definition
+    does not use the VJP formula, so it pins the rho < min_rms branch; the other
+    rows keep the ordinary epsilon and match too."""
+    r = np.random.default_rng(21)
+    x = r.standard_normal((6, 12))
+    x[[1, 4]] *= 0.05  # RMS ~0.05: below the floor
+    gam = 1 + 0.1 * r.standard_normal(12)
+    g = r.standard_normal((6, 12))
+    eps, floor = 1e-6, 0.5
+    ms = (x * x).mean(1)
+    rho = np.sqrt(ms + eps)
+    assert np.all(rho[[1, 4]] < floor) and np.all(rho[[0, 2, 3, 5]] > floor)
+    eps_row = np.where(rho < floor, floor ** 2 - ms, eps)
+    X = torch.tensor(x, requires_grad=True)
+    Y = torch.tensor(gam) * X / torch.sqrt((X * X).mean(1, keepdim=True) + torch.tensor(eps_row)[:, None])
+    (gx,) = torch.autograd.grad((Y * torch.tensor(g)).sum(), X)
+    got = O.rmsnorm_vjp(g, x, gam, eps=eps, min_rms=floor)
+    np.testing.assert_allclose(got, gx.numpy(), rtol=1e-12, atol=1e-14)
+
+
 # ------------------------------------------------------------ pseudograd
 def test_pseudograd_single_token_is_exact_outer_product():
     r = np.random.default_rng(14)
