@@ -68,11 +68,11 @@ extern "C" {
 typedef enum {
   FPO_OK = 0,
   FPO_ERR_NULL = 1,        /* a required pointer is NULL */
-  FPO_ERR_SHAPE = 2,       /* a size is non-positive or breaks the multiple-of-8 rule */
+  FPO_ERR_SHAPE = 2,       /* a size is non-positive, breaks the multiple-of-8 rule or exceeds a limit */
   FPO_ERR_DTYPE = 3,       /* unknown dtype */
   FPO_ERR_ARG = 4,         /* bad scalar argument or enum */
   FPO_ERR_WORKSPACE = 5,   /* workspace NULL, misaligned or smaller than the query */
-  FPO_ERR_UNSUPPORTED = 6, /* valid request this build does not implement */
+  FPO_ERR_UNSUPPORTED = 6, /* valid request the library does not implement */
   FPO_ERR_HIP = 7          /* a HIP runtime call or kernel launch failed */
 } fpo_status;
 
