@@ -17,8 +17,13 @@ from tests._util import dev_tensor
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("post_ffn", [False, True])
-def test_step_graph_replays_match_eager(dev, post_ffn):
+@pytest.mark.parametrize("variant", ["sgd", "sgd-post-ffn", "adamw", "sgd-clip-update", "adamw-clip-update"])
+def test_step_graph_replays_match_eager(dev, variant):
+    """Overlapped path (gradient clip: SGD-momentum, with the post-FFN
+    composition, AdamW) and the two-pass clip-the-update path."""
+    post_ffn = variant == "sgd-post-ffn"
+    adam = variant.startswith("adamw")
+    target = 1 if variant.endswith("clip-update") else 0
     c = I.CONFIGS[1].shrink(T=300, d=520, d_ff=1288, V=4104, L=3)
     x, gam, WU, y = (dev_tensor(a, dev) for a in (I.hidden(c), I.gain(c), I.unembedding(c), I.targets(c)))
     acts = [dev_tensor(I.activation(c, l), dev) for l in range(c.L)]
@@ -27,7 +32,7 @@ def test_step_graph_replays_match_eager(dev, post_ffn):
 
     def state():
         W = [w.clone() for w in W0]
-        s = dict(W=W, s1=[torch.zeros_like(w) for w in W],
+        s = dict(W=W, s1=[torch.zeros_like(w) for w in W], s2=[torch.zeros_like(w) for w in W] if adam else None,
                  lp=[torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in W],
                  Wsq=torch.tensor([float((w.double() ** 2).sum()) for w in W], dtype=torch.float64, device=dev),
                  ss=torch.empty(c.L, dtype=torch.float64, device=dev),
@@ -43,8 +48,9 @@ def test_step_graph_replays_match_eager(dev, post_ffn):
         api.fpo_output_error(x, gam, WU, y, s["g"], s["glp"], ws=s["ws_oe"])
         api.fpo_pseudograd(None if post_ffn else s["glp"], acts, dW3=None, sumsq=s["ss"], grad_bf16=True,
                            ws=s["ws_pg"], post_ffn=s.get("pf"),
-                           opt=api.OptConfig(lr=1e-2, clip_frac=0.01, step=k), W_master=s["W"], W_lp=s["lp"],
-                           state1=s["s1"], W_sumsq=s["Wsq"])
+                           opt=api.OptConfig(kind=1 if adam else 0, lr=1e-3 if adam else 1e-2, clip_frac=0.01,
+                                             step=k, clip_target=target),
+                           W_master=s["W"], W_lp=s["lp"], state1=s["s1"], state2=s["s2"], W_sumsq=s["Wsq"])
 
     eager, graphed = state(), state()
     for k in (1, 2):
@@ -56,12 +62,14 @@ def test_step_graph_replays_match_eager(dev, post_ffn):
         step(graphed, 3)  # recorded, not run
     torch.cuda.synchronize()
     for k in (3, 4, 5):
-        step(eager, k)
+        # the graph keeps step 3's scalars (AdamW's bias correction depends on
+        # the step number; SGD-momentum's only on whether it is the first)
+        step(eager, 3 if adam else k)
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
         x.add_(0)  # the program's own eager work between replays
-        for key in ("W", "s1", "lp"):
+        for key in ("W", "s1", "lp") + (("s2",) if adam else ()):
             for a, b in zip(eager[key], graphed[key]):
                 assert torch.equal(a, b), (key, k)
         for key in ("Wsq", "ss", "g", "glp"):
