@@ -155,6 +155,36 @@ def test_chunking_does_not_change_result():
     assert np.array_equal(a["argmax"], b["argmax"])
 
 
+@pytest.mark.parametrize("eps", [1e-6, 0.3])
+def test_single_logit_matches_torch_forward(eps):
+    """oracle.logit (the argmax tie-margin check of the parity tests) against
+    an independent float64 torch forward z = RMSNorm_gamma(x) W_U^T, on every
+    (token, vocabulary entry) of a toy whose gain is far from 1 and, in the
+    second case, whose eps is large enough that dropping it (or the gain, or
+    taking another token's row) moves every logit by far more than rounding;
+    also from bf16 storage (the bits upcast exactly)."""
+    t = toy(11, T=5, V=13)
+    gam = t["gamma"] * 1.7
+    Z = (torch_rmsnorm(torch.tensor(t["x"]), torch.tensor(gam), eps) @ torch.tensor(t["W_U"]).T).numpy()
+    for r in range(Z.shape[0]):
+        for v in range(Z.shape[1]):
+            assert abs(O.logit(t["x"], gam, t["W_U"], r, v, eps=eps) - Z[r, v]) <= 1e-13 * (1 + abs(Z[r, v]))
+    # bf16 storage arrays: the oracle reads the bit patterns exactly
+    to_bits = lambda a: (np.asarray(a, np.float32).view(np.uint32) >> 16).astype(np.uint16)  # noqa: E731
+    xb, gb, wb = to_bits(t["x"]), to_bits(gam), to_bits(t["W_U"])
+    up = lambda b: torch.tensor((b.astype(np.uint32) << 16).view(np.float32).astype(np.float64))  # noqa: E731
+    Zb = (torch_rmsnorm(up(xb), up(gb), eps) @ up(wb).T).numpy()
+    for r, v in [(0, 0), (2, 7), (4, 12)]:
+        assert abs(O.logit(xb, gb, wb, r, v, eps=eps) - Zb[r, v]) <= 1e-13 * (1 + abs(Zb[r, v]))
+    # the mistakes the pin must catch change the value far beyond the tolerance
+    Z_nogain = (torch_rmsnorm(torch.tensor(t["x"]), torch.ones(len(gam), dtype=torch.float64), eps)
+                @ torch.tensor(t["W_U"]).T).numpy()
+    assert np.min(np.abs(Z_nogain - Z)) > 1e-6
+    if eps > 0.1:
+        Z_noeps = (torch_rmsnorm(torch.tensor(t["x"]), torch.tensor(gam), 0.0) @ torch.tensor(t["W_U"]).T).numpy()
+        assert np.min(np.abs(Z_noeps - Z)) > 1e-6
+
+
 def test_bad_targets_zero_row_and_counted():
     t = toy(8, T=4, V=9)
     y = t["y"].copy()
