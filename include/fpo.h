@@ -26,7 +26,8 @@
  *    first-step and AdamW bias-correction terms) are fixed at capture.
  *  - The caller owns every buffer. The library allocates no device memory;
  *    scratch space comes from the caller's workspace, whose size the
- *    matching *_workspace query returns. Workspace pointers must be 256-byte
+ *    matching *_workspace query returns (fpo_apply_update_noalloc instead
+ *    uses a fixed device array inside the library, see there). Workspace pointers must be 256-byte
  *    aligned; every tensor operand (activations, weights, gradients,
  *    optimizer state, reference gradients) must be 16-byte aligned (the
  *    kernels move 16 bytes per lane; a bf16 W_lp: 8). Per-token and
@@ -63,7 +64,7 @@
 extern "C" {
 #endif
 
-#define FPO_ABI_VERSION 4
+#define FPO_ABI_VERSION 5
 
 typedef enum {
   FPO_OK = 0,
@@ -288,6 +289,31 @@ int fpo_apply_update(const fpo_opt* opt, int64_t n_mats, const int64_t* numel,
                      const float* const* grad, const double* grad_sumsq,
                      const fpo_update_bufs* upd, int32_t lp_dtype, void* ws, size_t ws_bytes,
                      void* stream);
+
+/* ---------------------------------------------------------------------------
+ * fpo_apply_update_noalloc - fpo_apply_update for callers that cannot
+ * allocate device memory or pass a workspace: code being captured into a HIP
+ * graph, tight serving loops, harnesses that forbid allocation. Same
+ * arguments (minus the workspace), same kernels and the same results bit for
+ * bit as fpo_apply_update.
+ *
+ * Its scratch (one double per 4096 parameters of every matrix, plus one per
+ * matrix) lives in a device array inside the library, FPO_NOALLOC_SCRATCH_BYTES
+ * (8 MiB) on every GPU the library runs on, held until the process ends: at
+ * most about 4.2e9 parameters per call. A call needing more returns
+ * FPO_ERR_WORKSPACE before any launch. Nothing in the array has to start at
+ * zero (every word a call reads was written earlier in the same call), so the
+ * previous call's contents are harmless; but every call on one GPU shares the
+ * array, so calls that overlap on one GPU (two streams, or two host threads
+ * enqueueing concurrently) race on it and must be serialised by the caller.
+ * The first call on a device resolves that device's copy of the array
+ * (hipGetSymbolAddress): make it before any graph capture starts.
+ * No hipMalloc, hipFree or allocating library routine is called.
+ * Returns FPO_OK or an fpo_status. */
+#define FPO_NOALLOC_SCRATCH_BYTES (8u << 20)
+int fpo_apply_update_noalloc(const fpo_opt* opt, int64_t n_mats, const int64_t* numel,
+                             const float* const* grad, const double* grad_sumsq,
+                             const fpo_update_bufs* upd, int32_t lp_dtype, void* stream);
 
 /* ---------------------------------------------------------------------------
  * fpo_cosine - per-pair dot product, squared norms and cosine (eq. cosine):

@@ -23,8 +23,9 @@ STATUS_NAMES = {0: "FPO_OK", 1: "FPO_ERR_NULL", 2: "FPO_ERR_SHAPE", 3: "FPO_ERR_
 EXPORTS = (
     "fpo_abi_version", "fpo_last_error", "fpo_output_error_workspace", "fpo_output_error",
     "fpo_pseudograd_workspace", "fpo_pseudograd", "fpo_apply_update_workspace", "fpo_apply_update",
-    "fpo_cosine_workspace", "fpo_cosine",
+    "fpo_cosine_workspace", "fpo_cosine", "fpo_apply_update_noalloc",
 )
+NOALLOC_SCRATCH_BYTES = 8 << 20  # FPO_NOALLOC_SCRATCH_BYTES
 
 
 class OeDesc(C.Structure):
@@ -54,7 +55,7 @@ class PostFfn(C.Structure):
                 ("eps", C.c_float), ("min_rms", C.c_float)]
 
 
-ABI_VERSION = 4
+ABI_VERSION = 5
 PP = C.POINTER(C.c_void_p)
 VP = C.c_void_p
 _lib = None
@@ -98,6 +99,9 @@ def load() -> C.CDLL:
     lib.fpo_apply_update.restype = C.c_int
     lib.fpo_apply_update.argtypes = [C.POINTER(Opt), C.c_int64, C.POINTER(C.c_int64), PP, VP,
                                      C.POINTER(UpdateBufs), C.c_int32, VP, C.c_size_t, VP]
+    lib.fpo_apply_update_noalloc.restype = C.c_int
+    lib.fpo_apply_update_noalloc.argtypes = [C.POINTER(Opt), C.c_int64, C.POINTER(C.c_int64), PP, VP,
+                                             C.POINTER(UpdateBufs), C.c_int32, VP]
     lib.fpo_cosine_workspace.restype = C.c_size_t
     lib.fpo_cosine_workspace.argtypes = [C.c_int64, C.POINTER(C.c_int64)]
     lib.fpo_cosine.restype = C.c_int

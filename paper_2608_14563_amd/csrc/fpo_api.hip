@@ -6,10 +6,18 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "../../include/fpo.h"
 #include "launch.hpp"
+
+// Scratch of fpo_apply_update_noalloc: a file-scope device array (one copy
+// per GPU, held until the process ends). Host code never passes `scratch`
+// itself to a kernel (its host-side name is not a device address): each
+// device's copy is resolved once with hipGetSymbolAddress, on that device,
+// and only that address is used.
+static __device__ __align__(256) unsigned char scratch[FPO_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -353,6 +361,29 @@ size_t update_ws(int64_t n, const int64_t* numel) {
   return (size_t)(round_up(blocks * 8, kAlign) + round_up(n * 8, kAlign));
 }
 
+constexpr int kMaxScratchDevices = 64;
+struct DeviceScratch {
+  std::once_flag once;
+  hipError_t err = hipSuccess;
+  void* ptr = nullptr;
+};
+DeviceScratch g_scratch[kMaxScratchDevices];
+
+// Address of the current device's copy of `scratch` (resolved on the first
+// call on that device), or an error.
+hipError_t scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  DeviceScratch& s = g_scratch[dev];
+  std::call_once(s.once, [&s] { s.err = hipGetSymbolAddress(&s.ptr, HIP_SYMBOL(scratch)); });
+  if (s.err != hipSuccess) return s.err;
+  if (!s.ptr) return hipErrorInvalidSymbol;
+  *out = s.ptr;
+  return hipSuccess;
+}
+
 }  // namespace
 
 extern "C" {
@@ -564,6 +595,31 @@ int fpo_apply_update(const fpo_opt* opt, int64_t n_mats, const int64_t* numel,
   U.stream = stream;
   hipError_t e = fpo::launch_update(U);
   if (e != hipSuccess) return hip_fail(e, "fpo_apply_update launch");
+  return FPO_OK;
+}
+
+int fpo_apply_update_noalloc(const fpo_opt* opt, int64_t n_mats, const int64_t* numel,
+                             const float* const* grad, const double* grad_sumsq,
+                             const fpo_update_bufs* upd, int32_t lp_dtype, void* stream) {
+  fpo::UpdLaunch U{};
+  if (int e = fill_update(opt, n_mats, numel, (const void* const*)grad, grad_sumsq, upd, lp_dtype, &U))
+    return e;
+  // the same scratch layout as fpo_apply_update's workspace, bounded by the array
+  const size_t need = update_ws(n_mats, numel);
+  if (need > (size_t)FPO_NOALLOC_SCRATCH_BYTES)
+    return fail(FPO_ERR_WORKSPACE,
+                "fpo_apply_update_noalloc: these matrices need %zu bytes of scratch (8 per 4096 parameters), "
+                "the library's static array holds %zu; split the call or use fpo_apply_update",
+                need, (size_t)FPO_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if (hipError_t e = scratch_address(&ws)) return hip_fail(e, "fpo_apply_update_noalloc scratch address");
+  U.part = (double*)ws;
+  int64_t blocks = 0;
+  for (int64_t m = 0; m < n_mats; ++m) blocks += fpo::update_blocks(numel[m]);
+  U.dsq = (double*)((char*)ws + round_up(blocks * 8, kAlign));
+  U.stream = stream;
+  hipError_t e = fpo::launch_update(U);
+  if (e != hipSuccess) return hip_fail(e, "fpo_apply_update_noalloc launch");
   return FPO_OK;
 }
 

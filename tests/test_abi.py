@@ -53,7 +53,7 @@ def test_library_exports_every_header_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert lib.fpo_abi_version() == 4 == L.ABI_VERSION
+    assert lib.fpo_abi_version() == 5 == L.ABI_VERSION
 
 
 def oe(T=128, d=256, V=4096, dtype=L.FPO_BF16, eps=1e-6, min_rms=0.5, chunk=0):
@@ -291,6 +291,31 @@ def test_apply_update_validation(lib):
     assert call(adam, upd=L.UpdateBufs(W, None, s1, s2b, FAKE, None)) == L.FPO_ERR_ARG
     s1b, k1b = arr([FAKE + 8])
     assert call(sgd, upd=L.UpdateBufs(W, None, s1b, None, FAKE, None)) == L.FPO_ERR_ARG
+
+
+def test_apply_update_noalloc_validation(lib):
+    """The no-allocation update validates like fpo_apply_update and refuses,
+    before any HIP call, matrices whose scratch exceeds its static array."""
+    g, kg = arr([FAKE])
+    W, kw = arr([FAKE])
+    s1, k1 = arr([FAKE])
+    ub = L.UpdateBufs(W, None, s1, None, FAKE, None)
+    sgd = L.Opt(0, 1e-4, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)
+
+    def call(o, numel, n_mats=1, upd=ub, lp=L.FPO_BF16):
+        return lib.fpo_apply_update_noalloc(C.byref(o) if o is not None else None, n_mats, numel, g, FAKE,
+                                            C.byref(upd) if upd is not None else None, lp, None)
+
+    n = (C.c_int64 * 1)(1024)
+    assert call(None, n) == L.FPO_ERR_NULL
+    assert call(sgd, n, upd=None) == L.FPO_ERR_NULL
+    assert call(sgd, n, n_mats=0) == L.FPO_ERR_SHAPE
+    assert call(sgd, (C.c_int64 * 1)(1022)) == L.FPO_ERR_SHAPE
+    assert call(sgd, n, lp=9) == L.FPO_ERR_DTYPE
+    # one double of scratch per 4096 parameters: just past the array's capacity
+    too_many = (L.NOALLOC_SCRATCH_BYTES // 8 + 1) * 4096
+    assert call(sgd, (C.c_int64 * 1)(too_many)) == L.FPO_ERR_WORKSPACE
+    assert "static array" in lib.fpo_last_error().decode()
 
 
 def test_cosine_validation(lib):
