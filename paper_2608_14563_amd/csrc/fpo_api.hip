@@ -66,8 +66,13 @@ struct Carver {
 bool band_fits(int64_t rows, int64_t cols) { return rows * cols <= ((int64_t)1 << 30); }
 
 // ------------------------------------------------------------------ plans
+// Vocabulary chunks: the first `nwide` chunks are cw + cq wide, the others cw,
+// and the last one takes what remains of V (see fpo::chunk_span). Vc, the
+// widest chunk rounded up to 256, sizes the staged p~.
 struct OePlan {
   int64_t Vc = 0, ldp = 0, nb = 0;
+  int64_t cw = 0, cq = 0;
+  int nchunk = 1, nwide = 0;
   int nsplit = 1;
 };
 
@@ -78,28 +83,67 @@ constexpr int64_t kWaveSlots = 256;
 // 256 rows of one tile share an L2 set and its stores are written back to HBM
 // several times over (measured: 3.3 GB written for a 1.1 GB p~).
 constexpr int64_t kPadBytes = 256;
+// Default bytes of staged p~ per vocabulary chunk (see plan_oe).
+constexpr int64_t kStageBytes = (int64_t)128 << 20;
 
 OePlan plan_oe(const fpo_oe_desc& d) {
   const bool bf16 = d.dtype == FPO_BF16;
   const int64_t BM = bf16 ? 256 : 128, BN = BM, WTN = bf16 ? 128 : 64;
   const int64_t pad = kPadBytes / (bf16 ? 2 : 4);
-  // staged p~ budget: 2^30 elements (2 GiB bf16), so the vocabulary of the
-  // 7-8B shapes at T <= 4096 is one chunk: one logits launch, one projection
-  // launch accumulating over the whole vocabulary (one merge of the partials),
-  // one statistics pass. Chunks have equal width. (Measured at T = 2048,
-  // V = 100352: one chunk 2.4% faster per step than seven; widths that
-  // minimise partly idle tile waves but leave a small last chunk are slower.)
-  int64_t vmax = d.vocab_chunk > 0 ? round_up(d.vocab_chunk, 256)
-                                   : std::max<int64_t>(256, ((int64_t)1 << 30) / d.T / 256 * 256);
-  vmax = std::min(vmax, round_up(d.V, 256));
+  const int64_t esz = bf16 ? 2 : 4;
+  // widest chunk allowed: the caller's width, or by default kStageBytes of
+  // staged p~ (half of the 256 MB Infinity Cache, so that a chunk's p~ is
+  // written by the logits launch and read back by the projection from the
+  // cache rather than HBM; the T x V logits never exist in memory as a whole)
+  int64_t wmax = d.vocab_chunk > 0 ? round_up(d.vocab_chunk, 256)
+                                   : std::max<int64_t>(256, kStageBytes / esz / d.T / 256 * 256);
   // a chunk of W_U ([Vc, d]) and the staged p~ ([T, Vc + pad]) are copied
   // through 32-bit offsets
   if (bf16) {
     const int64_t lim = std::min(((int64_t)1 << 30) / d.d, ((int64_t)1 << 30) / d.T - pad);
-    vmax = std::min(vmax, std::max<int64_t>(256, lim / 256 * 256));
+    wmax = std::min(wmax, std::max<int64_t>(256, lim / 256 * 256));
   }
   OePlan p;
-  p.Vc = round_up(ceil_div(d.V, ceil_div(d.V, vmax)), 256);
+  const int64_t V256 = round_up(d.V, 256);
+  if (V256 <= wmax) {
+    p.cw = V256;
+  } else {
+    const int64_t n0 = ceil_div(d.V, wmax);
+    p.nchunk = (int)n0;
+    p.cw = round_up(ceil_div(d.V, n0), 256);  // equal widths (the caller's choice)
+    // Default plan: widths in whole logits waves. A chunk's logits launch has
+    // ceil(T / BM) token tiles per 256-wide vocabulary tile, so a multiple of
+    // q vocabulary entries fills whole waves of 256 workgroups; the last chunk
+    // alone carries the remainder, and the total number of waves is that of
+    // one launch over the whole vocabulary. (Equal widths left a nearly empty
+    // last wave in every chunk: T = 2048, V = 100352 in four chunks of 25088
+    // ran the logits 19% slower than one launch.)
+    const int64_t q = round_up(std::max<int64_t>(1, kWaveSlots / ceil_div(d.T, BM)) * BN, 256);
+    if (d.vocab_chunk <= 0 && q <= wmax) {
+      for (int64_t n = n0;; ++n) {
+        const int64_t base = d.V / (n * q) * q;
+        if (base == 0) break;                       // keep equal widths
+        const int64_t extra = d.V - n * base;       // < n q
+        const int64_t k = std::min<int64_t>(n - 1, extra / q);
+        const int64_t last = d.V - (n - 1) * base - k * q;
+        const int64_t widest = std::max(k > 0 ? base + q : base, last);
+        if (round_up(widest, 256) > wmax) continue;  // one chunk more
+        p.nchunk = (int)n;
+        p.cw = base;
+        p.cq = q;
+        p.nwide = (int)k;
+        break;
+      }
+    }
+  }
+  // widest chunk
+  int64_t widest = 0;
+  for (int c = 0; c < p.nchunk; ++c) {
+    int64_t v0, w;
+    fpo::chunk_span(d.V, p.nchunk, p.cw, p.cq, p.nwide, c, &v0, &w);
+    widest = std::max(widest, w);
+  }
+  p.Vc = round_up(widest, 256);
   p.ldp = p.Vc + pad;
   p.nb = p.Vc / WTN;
   // Split the projection's K range so that its launch fills whole waves: the
@@ -131,9 +175,9 @@ size_t carve_oe(const fpo_oe_desc& d, const OePlan& p, void* ws, fpo::OeLaunch* 
   float* blk_m = c.take<float>(d.T * p.nb);
   float* blk_s = c.take<float>(d.T * p.nb);
   int32_t* blk_i = c.take<int32_t>(d.T * p.nb);
-  float* fout = c.take<float>(d.T * p.nsplit);
+  float* fout = c.take<float>(d.T);
   float* alpha = c.take<float>(d.T);
-  float* refs = c.take<float>(d.T * p.nsplit);
+  float* ref = c.take<float>(d.T);
   float* runM = c.take<float>(d.T);
   float* runS = c.take<float>(d.T);
   int32_t* runA = c.take<int32_t>(d.T);
@@ -146,7 +190,7 @@ size_t carve_oe(const fpo_oe_desc& d, const OePlan& p, void* ws, fpo::OeLaunch* 
     L->blk_i = blk_i;
     L->fout = fout;
     L->alpha = alpha;
-    L->refs = refs;
+    L->ref = ref;
     L->runM = runM;
     L->runS = runS;
     L->runA = runA;
@@ -417,6 +461,10 @@ int fpo_output_error(const fpo_oe_desc* desc, const void* h_final, const void* g
   L.V = desc->V;
   L.Vc = p.Vc;
   L.ldp = p.ldp;
+  L.nchunk = p.nchunk;
+  L.cw = p.cw;
+  L.cq = p.cq;
+  L.nwide = p.nwide;
   L.nsplit = p.nsplit;
   L.eps = desc->eps;
   L.min_rms = desc->min_rms;

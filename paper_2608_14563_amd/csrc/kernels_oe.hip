@@ -1,15 +1,17 @@
 // Output-error path (Sec. 3.1 steps 2-4; eq. gproj; App. E eq. rmsnorm-vjp):
-//   rms_forward  : rho_t and y_t = gamma * x_t / rho_t            (HBM bound)
+//   rms_forward  : rho_t, y_t = gamma * x_t / rho_t, and the first chunk's
+//                  reference R_t = <y_t, W_U[y_t]> (the target logit)  (HBM bound)
 //   logits_chunk : z = y W_c^T for one vocabulary chunk (MFMA), per-block
-//                  row statistics, p~ = exp(z - block max) staged  (MFMA bound)
-//   chunk_stats  : running max / partition function / argmax per token and
-//                  one reference per split of the chunk
-//   rescale_p    : staged p~ brought to its split's reference      (HBM bound)
+//                  row statistics, p~ = exp(z - R_t) staged            (MFMA bound)
+//   chunk_stats  : running max / partition function / argmax per token; the
+//                  next chunk's reference R_t <- running max; the rare rows
+//                  with a block far above R_t rescaled in place
 //   proj_chunk   : G_s <- rescale(G_s) + p~ W_c (MFMA), one partial per split
 //   finalize_vjp : g = sum_s G_s / S - W_U[y], the target logit, the clamped
-//                  RMSNorm VJP                                     (HBM bound)
-// The T x V logits never reach HBM as logits: p~ (bf16) of one chunk is staged
-// (with the default budget, the whole vocabulary at the 7-8B shapes).
+//                  RMSNorm VJP                                         (HBM bound)
+// The T x V logits are never stored: only one vocabulary chunk of p~ (bf16,
+// at most 2^26 entries by default, so it stays in the 256 MB Infinity Cache)
+// is staged between the logits and projection launches of that chunk.
 #include "gemm.hpp"
 #include "gemm2.hpp"
 #include "launch.hpp"
@@ -22,10 +24,23 @@ namespace fpo {
 // sweep) hold rows of up to this many sweeps in registers between passes.
 constexpr int kRowRegIters = 8;
 
+// The value of f after rounding to the storage type T.
+template <typename T> __device__ __forceinline__ float round_to(float f);
+template <> __device__ __forceinline__ float round_to<float>(float f) { return f; }
+template <> __device__ __forceinline__ float round_to<uint16_t>(float f) { return bf16_to_f32(to_bf16(f)); }
+
+// One workgroup per token: rho and y = gamma * x / rho (stored in the operand
+// dtype), and the reference of the first vocabulary chunk, R = <y, W_U[v]>
+// with v the token's target (entry 0 for a target outside [0, V)) from the
+// stored (rounded) y: any logit is at most the row maximum, which is all the
+// staging of p~ = exp(z - R) needs (see logits_epilogue).
 template <typename T>
 __global__ __launch_bounds__(256) void rms_forward_kernel(const T* __restrict__ x,
                                                           const T* __restrict__ gamma, int d,
                                                           float eps, T* __restrict__ y,
+                                                          const T* __restrict__ W_U,
+                                                          const int32_t* __restrict__ targets, int V,
+                                                          float* __restrict__ ref,
                                                           int32_t* __restrict__ bad) {
   __shared__ float red[16];
   const int64_t row = blockIdx.x;
@@ -45,9 +60,15 @@ __global__ __launch_bounds__(256) void rms_forward_kernel(const T* __restrict__ 
   }
   ss = block_sum(ss, red);
   const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+  const int tg = targets[row];
+  const T* wr = W_U + (int64_t)((tg >= 0 && tg < V) ? tg : 0) * d;
+  float zr = 0.f;
   auto out = [&](int k, f32x4 v) {
     const f32x4 g = ld4(gamma, k);
-    st4(y + row * d, k, f32x4{g.x * v.x * inv, g.y * v.y * inv, g.z * v.z * inv, g.w * v.w * inv});
+    const f32x4 o = {g.x * v.x * inv, g.y * v.y * inv, g.z * v.z * inv, g.w * v.w * inv};
+    st4(y + row * d, k, o);
+    const f32x4 w = ld4(wr, k);
+    zr += round_to<T>(o.x) * w.x + round_to<T>(o.y) * w.y + round_to<T>(o.z) * w.z + round_to<T>(o.w) * w.w;
   };
 #pragma unroll
   for (int it = 0; it < kRowRegIters; ++it) {
@@ -55,17 +76,34 @@ __global__ __launch_bounds__(256) void rms_forward_kernel(const T* __restrict__ 
     if (k < d) out(k, xk[it]);
   }
   for (int k = threadIdx.x * 4 + kRowRegIters * 1024; k < d; k += 1024) out(k, ld4(xr, k));
+  zr = block_sum(zr, red);
+  if (threadIdx.x == 0) ref[row] = zr;
   if (bad && row == 0 && threadIdx.x == 0) *bad = 0;
 }
 
 // ------------------------------------------------------------------ logits
+// Staging reference. A token's p~ entries are exp(z - R) with R its reference
+// for the chunk (a logit of the first chunk, then the running maximum: never
+// above the row maximum), so that every block of the chunk, and every chunk,
+// shares one scale and the projection needs no per-block factor. Entries far
+// below R (z < R - 87) underflow: relative to the sum, which holds an entry of
+// at least exp(0), they weigh below 1e-33. A block whose maximum m exceeds
+// R + kRefMargin would risk overflow in the projection's sums; it is staged as
+// exp(z - m) instead, and the statistics kernel brings that token's row to one
+// scale (base_b below is the scale of block b; both kernels take the same
+// float decision).
+constexpr float kRefMargin = 64.f;
+
+__device__ __forceinline__ float block_base(float m, float R) { return m > R + kRefMargin ? m : R; }
+
 // One workgroup: 256 (bf16) / 128 (fp32) tokens x as many vocabulary columns of
 // the chunk; each wave's 128 / 64 columns form one statistics block b (block
-// max m, sum of exp(z - m), first arg-max). Columns at or beyond `vc_valid`
-// are masked out; p~ = exp(z - m) is staged for the projection.
+// max m, sum of the staged p~, first arg-max). Columns at or beyond `vc_valid`
+// are masked out; p~ = exp(z - base_b) is staged for the projection.
 template <typename PT, bool CONTIG, class Map, class VA, int FM, int FN>
 __device__ __forceinline__ void logits_epilogue(VA (&acc)[FM][FN], const Map& mp, int m0,
                                                 int n0, int b, int T, int vc_valid, int v0,
+                                                const float* __restrict__ ref,
                                                 PT* __restrict__ P, int64_t ldp, int nb,
                                                 float* __restrict__ blk_m,
                                                 float* __restrict__ blk_s,
@@ -98,11 +136,12 @@ __device__ __forceinline__ void logits_epilogue(VA (&acc)[FM][FN], const Map& mp
           mi = i2;
         }
       }
+      const float base = block_base(m, row < T ? ref[row] : 0.f);
       float p[FN];
       float s = 0.f;
 #pragma unroll
       for (int i = 0; i < FN; ++i) {
-        p[i] = (n0 + mp.col(i) < vc_valid) ? __expf(z[i] - m) : 0.f;
+        p[i] = (n0 + mp.col(i) < vc_valid) ? __expf(z[i] - base) : 0.f;
         s += p[i];
       }
       s = wave_sum<Map::LPR>(s);
@@ -141,6 +180,7 @@ __device__ __forceinline__ void logits_epilogue(VA (&acc)[FM][FN], const Map& mp
 template <bool RAGGED>
 __device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], G2Smem& sm, int vt0,
                                                    int tt0, int T, int vc_valid, int v0,
+                                                   const float* __restrict__ ref,
                                                    uint16_t* __restrict__ P, int64_t ldp, int nb,
                                                    float* __restrict__ blk_m,
                                                    float* __restrict__ blk_s,
@@ -151,6 +191,12 @@ __device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], G2
   const int b = vw / G2::WTM;
   const int vl = vw + 4 * h;                // entry of offset 0 in this lane
   const int lim = vc_valid - vl;            // offset o is in range iff o < lim (RAGGED only)
+  float R[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int t = tt0 + (w & 1) * G2::WTN + 32 * i + lc;
+    R[i] = t < T ? ref[t] : 0.f;
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int t = tt0 + (w & 1) * G2::WTN + 32 * i + lc;
@@ -181,6 +227,7 @@ __device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], G2
         mi = i2;
       }
     }
+    const float base = block_base(m, R[i]);
     float s = 0.f;
     // LDS token row of this lane and the tile column of its entries at f = q = 0
     const int lrow = (w & 1) * G2::WTN + 32 * i + lc;
@@ -194,7 +241,7 @@ __device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], G2
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int o = 32 * f + 8 * q + j;
-          p[j] = (!RAGGED || o < lim) ? __expf(acc[f][i][4 * q + j] - m) : 0.f;
+          p[j] = (!RAGGED || o < lim) ? __expf(acc[f][i][4 * q + j] - base) : 0.f;
           s += p[j];
         }
         const int chunk = ((col0 + 32 * f + 8 * q) >> 3) ^ lc;  // lrow & 31 == lc
@@ -226,8 +273,8 @@ __device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], G2
 template <class E>
 __global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
     const typename E::T* __restrict__ y, const typename E::T* __restrict__ Wc, int T, int d,
-    int vc_valid, int v0, typename E::T* __restrict__ P, int64_t ldp, int nb,
-    float* __restrict__ blk_m, float* __restrict__ blk_s, int32_t* __restrict__ blk_i) {
+    int vc_valid, int v0, const float* __restrict__ ref, typename E::T* __restrict__ P, int64_t ldp,
+    int nb, float* __restrict__ blk_m, float* __restrict__ blk_s, int32_t* __restrict__ blk_i) {
   using TT = Tile<E>;
   const int ntm = (T + TT::BM - 1) / TT::BM, ntn = (vc_valid + TT::BN - 1) / TT::BN;
   int tm, tn;
@@ -242,9 +289,9 @@ __global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
     const Operand B{y + (int64_t)m0 * d, d, band_bytes(T - m0, d)};
     gemm2_mainloop<false>(sm, acc, A, B, vc_valid - n0, T - m0, d, 0, (d + G2::BK - 1) / G2::BK);
     if (n0 + ((threadIdx.x >> 7) + 1) * G2::WTM <= vc_valid)  // wave-uniform
-      logits_epilogue_vt<false>(acc, sm, n0, m0, T, vc_valid, v0, P, ldp, nb, blk_m, blk_s, blk_i);
+      logits_epilogue_vt<false>(acc, sm, n0, m0, T, vc_valid, v0, ref, P, ldp, nb, blk_m, blk_s, blk_i);
     else
-      logits_epilogue_vt<true>(acc, sm, n0, m0, T, vc_valid, v0, P, ldp, nb, blk_m, blk_s, blk_i);
+      logits_epilogue_vt<true>(acc, sm, n0, m0, T, vc_valid, v0, ref, P, ldp, nb, blk_m, blk_s, blk_i);
   } else {
     __shared__ GemmSmem<E> sm;
     f32x4 acc[E::FM][E::FN];
@@ -252,42 +299,42 @@ __global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
     const int b = n0 / TT::WTN + ((threadIdx.x >> 6) & 1);  // this wave's block
     gemm_mainloop<E, false>(sm, acc, y, d, T, Wc, d, vc_valid, d, m0, n0, 0,
                             (d + TT::BK - 1) / TT::BK, NoHook{});
-    logits_epilogue<typename E::T, true>(acc, AccMap<E>(), m0, n0, b, T, vc_valid, v0, P, ldp, nb,
+    logits_epilogue<typename E::T, true>(acc, AccMap<E>(), m0, n0, b, T, vc_valid, v0, ref, P, ldp, nb,
                                          blk_m, blk_s, blk_i);
   }
 }
 
 // ------------------------------------------------------------------ stats
 // One wave per token. Folds the chunk's block statistics (block max m_b, sum
-// of exp(z - m_b), first arg-max) into the running max M, partition S and
-// argmax, and picks one reference per split of the chunk: ref_s = max of the
-// split's block maxima (rescale_p then brings p~ to it: p~ <- p~ exp(m_b - ref_s)).
-// The projection accumulates split s in scale ref_s and stores
-//   G_s <- acc * exp(ref_s - M_new) + G_s * exp(M_old - M_new),
-// so every factor is <= 1 and nothing can overflow.
-constexpr int kMaxSplit = 8;
-
+// s_b of the block's staged p~, which is in scale base_b, first arg-max) into
+// the running max M, the partition function S (in scale M) and the argmax:
+//   M_new = max(M_old, max_b m_b);  S <- S exp(M_old - M_new) + sum_b s_b exp(base_b - M_new).
+// The chunk's p~ share the token's reference scale R unless a block was staged
+// in its own (m_b > R + kRefMargin): this wave then brings the token's row to
+// the chunk maximum in place (every factor <= 1). With Ref the row's final
+// scale, the projection stores G_s <- acc exp(Ref - M_new) + G_s exp(M_old - M_new)
+// (fout, alpha), and the next chunk's reference is M_new.
 constexpr int kStatsRegs = 24;  // blocks per lane held in registers (chunks of up to 1536 blocks)
 
 template <typename PT>
 __global__ __launch_bounds__(256) void chunk_stats_kernel(
-    int T, int nb, int bps, int nsplit, int first,
-    const float* __restrict__ blk_m, const float* __restrict__ blk_s,
-    const int32_t* __restrict__ blk_i, float* __restrict__ runM, float* __restrict__ runS,
-    int32_t* __restrict__ runA, float* __restrict__ fout, float* __restrict__ alpha,
-    float* __restrict__ refs) {
+    int T, int nb, int first, const float* __restrict__ blk_m, const float* __restrict__ blk_s,
+    const int32_t* __restrict__ blk_i, float* __restrict__ ref, float* __restrict__ runM,
+    float* __restrict__ runS, int32_t* __restrict__ runA, float* __restrict__ fout,
+    float* __restrict__ alpha, PT* __restrict__ P, int64_t ldp) {
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + w;
   if (row >= T) return;  // whole wave exits together; no barrier below
   const float* bm = blk_m + (int64_t)row * nb;
   const float* bs = blk_s + (int64_t)row * nb;
   const int32_t* bi = blk_i + (int64_t)row * nb;
-  float mc = -INFINITY, s = 0.f, Mold = -INFINITY, Mnew;
+  const float R = ref[row];
+  const float Mold = first ? -INFINITY : runM[row];
+  float mc = -INFINITY, s = 0.f, Mnew;
   int ai = 0x7fffffff;
-  float ref[kMaxSplit];
+  bool own = false;  // a block of this lane was staged in its own scale
   if (nb <= 64 * kStatsRegs) {
-    // each lane's block maxima and sums loaded once (blocks l + 64j), every
-    // pass from registers
+    // each lane's block maxima and sums loaded once (blocks l + 64j)
     float vm[kStatsRegs], vs[kStatsRegs];
 #pragma unroll
     for (int j = 0; j < kStatsRegs; ++j) {
@@ -303,58 +350,49 @@ __global__ __launch_bounds__(256) void chunk_stats_kernel(
       const int b = l + 64 * j;
       if (b < nb && vm[j] == mc) ai = min(ai, bi[b]);
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) ai = min(ai, __shfl_xor(ai, o, 64));
-    Mold = first ? -INFINITY : runM[row];
     Mnew = fmaxf(Mold, mc);
 #pragma unroll
-    for (int sp = 0; sp < kMaxSplit; ++sp) {
-      float r = -INFINITY;
-      if (sp < nsplit) {
-#pragma unroll
-        for (int j = 0; j < kStatsRegs; ++j) {
-          const int b = l + 64 * j;
-          if (b >= sp * bps && b < (sp + 1) * bps) r = fmaxf(r, vm[j]);
-        }
-        r = wave_max(r);
-      }
-      ref[sp] = r;
-    }
-    // partition function of the chunk relative to M_new
-#pragma unroll
     for (int j = 0; j < kStatsRegs; ++j)
-      if (l + 64 * j < nb) s += vs[j] * __expf(vm[j] - Mnew);
+      if (l + 64 * j < nb) {
+        const float bb = block_base(vm[j], R);
+        own |= bb != R;
+        s += vs[j] * __expf(bb - Mnew);
+      }
   } else {
     for (int b = l; b < nb; b += 64) mc = fmaxf(mc, bm[b]);
     mc = wave_max(mc);
     for (int b = l; b < nb; b += 64)
       if (bm[b] == mc) ai = min(ai, bi[b]);
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) ai = min(ai, __shfl_xor(ai, o, 64));
-    Mold = first ? -INFINITY : runM[row];
     Mnew = fmaxf(Mold, mc);
-#pragma unroll
-    for (int sp = 0; sp < kMaxSplit; ++sp) {
-      float r = -INFINITY;
-      if (sp < nsplit) {
-        for (int b = sp * bps + l; b < min(nb, (sp + 1) * bps); b += 64) r = fmaxf(r, bm[b]);
-        r = wave_max(r);
-      }
-      ref[sp] = r;
+    for (int b = l; b < nb; b += 64) {
+      const float bb = block_base(bm[b], R);
+      own |= bb != R;
+      s += bs[b] * __expf(bb - Mnew);
     }
-    for (int b = l; b < nb; b += 64) s += bs[b] * __expf(bm[b] - Mnew);
   }
-  s = wave_sum(s);
-  if (l < nsplit) {
-    float fo = 0.f, rf = 0.f;
 #pragma unroll
-    for (int sp = 0; sp < kMaxSplit; ++sp)
-      if (sp == l) {
-        fo = __expf(ref[sp] - Mnew);  // 0 for a split without blocks
-        rf = ref[sp];
+  for (int o = 32; o > 0; o >>= 1) ai = min(ai, __shfl_xor(ai, o, 64));
+  s = wave_sum(s);
+  const bool any_own = __ballot(own) != 0;  // wave-uniform
+  // a block above R + kRefMargin makes the chunk maximum exceed every base_b
+  const float Ref = any_own ? mc : R;
+  if (any_own) {
+    // the token's staged row, 16-byte runs; 16 runs per block for both
+    // element types (128 bf16 or 64 fp32 entries)
+    u32x4* pr = reinterpret_cast<u32x4*>(P + (int64_t)row * ldp);
+    for (int c = l; c < nb * 16; c += 64) {
+      const float bb = block_base(bm[c >> 4], R);
+      if (bb == Ref) continue;
+      const float f = __expf(bb - Ref);
+      u32x4 v = pr[c];
+      if constexpr (sizeof(PT) == 2) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = pack_bf16x2(bf16_lo(v[e]) * f, bf16_hi(v[e]) * f);
+      } else {
+        v = __builtin_bit_cast(u32x4, __builtin_bit_cast(f32x4, v) * f);
       }
-    fout[(int64_t)row * nsplit + l] = fo;
-    refs[(int64_t)row * nsplit + l] = rf;
+      pr[c] = v;
+    }
   }
   if (l == 0) {
     const float a = first ? 0.f : __expf(Mold - Mnew);
@@ -362,65 +400,19 @@ __global__ __launch_bounds__(256) void chunk_stats_kernel(
     runM[row] = Mnew;
     alpha[row] = a;
     if (first || mc > Mold) runA[row] = ai;
-  }
-}
-
-// Staged p~ of block b (split s = b / bps) times exp(m_b - ref_s) <= 1, in
-// place. Streams the chunk once: 16-byte runs, four per thread, all loads
-// before stores, non-temporal; one flat grid of (token, run group) pairs, the
-// groups of a token adjacent (a 2-D grid would cap the tokens at 65536).
-constexpr int kRescaleU = 4;
-
-template <typename PT>
-__global__ __launch_bounds__(256) void rescale_p_kernel(int groups, int vc_valid, int nb, int bps,
-                                                        int nsplit, int blkw,
-                                                        const float* __restrict__ blk_m,
-                                                        const float* __restrict__ refs,
-                                                        PT* __restrict__ P, int64_t ldp) {
-  constexpr int EPC = 16 / sizeof(PT);
-  const int64_t row = blockIdx.x / (unsigned)groups;
-  const int grp = (int)(blockIdx.x - row * groups);
-  const int ncv = (vc_valid + EPC - 1) / EPC;
-  u32x4* pr = reinterpret_cast<u32x4*>(P + row * ldp);
-  const float* bm = blk_m + row * nb;
-  const float* rf = refs + row * nsplit;
-  const int c0 = grp * 256 * kRescaleU + threadIdx.x;
-  u32x4 v[kRescaleU];
-  float fct[kRescaleU];
-#pragma unroll
-  for (int u = 0; u < kRescaleU; ++u) {
-    const int c = c0 + u * 256;
-    fct[u] = 1.f;
-    if (c < ncv) {
-      v[u] = __builtin_nontemporal_load(pr + c);
-      const int b = (c * EPC) / blkw;
-      const float m = bm[b], r = rf[b / bps];
-      fct[u] = m == r ? 1.f : __expf(m - r);
-    }
-  }
-#pragma unroll
-  for (int u = 0; u < kRescaleU; ++u) {
-    const int c = c0 + u * 256;
-    if (c >= ncv || fct[u] == 1.f) continue;
-    const float f = fct[u];
-    u32x4 w = v[u];
-    if constexpr (sizeof(PT) == 2) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) w[e] = pack_bf16x2(bf16_lo(w[e]) * f, bf16_hi(w[e]) * f);
-    } else {
-      w = __builtin_bit_cast(u32x4, __builtin_bit_cast(f32x4, w) * f);
-    }
-    __builtin_nontemporal_store(w, pr + c);
+    fout[row] = __expf(Ref - Mnew);
+    ref[row] = Mnew;
   }
 }
 
 // ------------------------------------------------------------------ projection
 // G_s[t, :] (one partial per split s of the chunk's blocks) holds
-// sum_v exp(z_tv - M_t) W_U[v, :] over the vocabulary processed so far; the
-// split's products are accumulated in scale ref_s and merged in the epilogue.
+// sum_v exp(z_tv - M_t) W_U[v, :] over its share of the vocabulary processed
+// so far; the chunk's products are accumulated in the row's staging scale and
+// merged in the epilogue with the per-token factors of chunk_stats.
 template <class Map, class VA, int FM, int FN>
 __device__ __forceinline__ void proj_epilogue(VA (&acc)[FM][FN], const Map& mp, int m0, int n0,
-                                              int sp, int nsplit, int T, int d, int first,
+                                              int T, int d, int first,
                                               const float* __restrict__ fout,
                                               const float* __restrict__ alpha,
                                               float* __restrict__ Gs) {
@@ -431,7 +423,7 @@ __device__ __forceinline__ void proj_epilogue(VA (&acc)[FM][FN], const Map& mp, 
       const int row = m0 + mp.row(f, r);
       const int c = n0 + mp.col(0);  // FN consecutive columns
       if (row >= T || c >= d) continue;
-      const float so = fout[(int64_t)row * nsplit + sp];
+      const float so = fout[row];
       const float sa = first ? 0.f : alpha[row];
 #pragma unroll
       for (int i = 0; i < FN; i += 4) {
@@ -444,19 +436,19 @@ __device__ __forceinline__ void proj_epilogue(VA (&acc)[FM][FN], const Map& mp, 
     }
 }
 
-// bf16 form of the merge: the tile's per-row factors exp(ref_s - M_new) and
+// bf16 form of the merge: the tile's per-row factors exp(Ref - M_new) and
 // exp(M_old - M_new) are staged in LDS (the ring is free after the main loop)
 // and each fragment's 16 partial rows are loaded together before use, so the
 // row loads overlap instead of serialising on their latency.
 __device__ __forceinline__ void proj_epilogue2(f32x16 (&acc)[4][4], G2Smem& sm, int m0, int n0,
-                                               int sp, int nsplit, int T, int d, int first,
+                                               int T, int d, int first,
                                                const float* __restrict__ fout,
                                                const float* __restrict__ alpha,
                                                float* __restrict__ Gs) {
   float* sf = reinterpret_cast<float*>(sm.s);
   {
     const int rr = m0 + (int)threadIdx.x;
-    sf[threadIdx.x] = rr < T ? fout[(int64_t)rr * nsplit + sp] : 0.f;
+    sf[threadIdx.x] = rr < T ? fout[rr] : 0.f;
     sf[256 + threadIdx.x] = (!first && rr < T) ? alpha[rr] : 0.f;
   }
   __syncthreads();
@@ -508,7 +500,7 @@ __global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
     const Operand A{P + (int64_t)m0 * ldp, ldp, band_bytes(T - m0, ldp)};
     const Operand B{Wc + n0, d, band_bytes(vc_valid, d, n0)};
     gemm2_mainloop<true>(sm, acc, A, B, T - m0, d - n0, vc_valid, kt0, kt1);
-    proj_epilogue2(acc, sm, m0, n0, sp, nsplit, T, d, first, fout, alpha, Gs);
+    proj_epilogue2(acc, sm, m0, n0, T, d, first, fout, alpha, Gs);
   } else {
     __shared__ GemmSmem<E> sm;
     f32x4 acc[E::FM][E::FN];
@@ -517,7 +509,7 @@ __global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
     const int nkt = (vc_valid + TT::BK - 1) / TT::BK;
     const int kt0 = min(sp * bps * tpb, nkt), kt1 = min(min(nb, (sp + 1) * bps) * tpb, nkt);
     gemm_mainloop<E, true>(sm, acc, P, ldp, T, Wc, d, d, vc_valid, m0, n0, kt0, kt1, NoHook{});
-    proj_epilogue(acc, AccMap<E>(), m0, n0, sp, nsplit, T, d, first, fout, alpha, Gs);
+    proj_epilogue(acc, AccMap<E>(), m0, n0, T, d, first, fout, alpha, Gs);
   }
 }
 
@@ -632,36 +624,27 @@ static hipError_t run_output_error(const OeLaunch& a) {
   T* y = (T*)a.y;
   T* P = (T*)a.P;
   FPO_LAUNCH("rms_forward", st,
-             rms_forward_kernel<T><<<dim3((unsigned)a.T), dim3(256), 0, st>>>(x, gamma, (int)a.d, a.eps, y,
-                                                                   a.bad_targets));
+             rms_forward_kernel<T><<<dim3((unsigned)a.T), dim3(256), 0, st>>>(
+      x, gamma, (int)a.d, a.eps, y, W, a.targets, (int)a.V, a.ref, a.bad_targets));
   FPO_CHECK_LAUNCH();
-  const int nchunk = (int)((a.V + a.Vc - 1) / a.Vc);
   const int gm = (int)((a.T + TT::BM - 1) / TT::BM);
-  for (int c = 0; c < nchunk; ++c) {
-    const int64_t v0 = (int64_t)c * a.Vc;
-    const int vc_valid = (int)std::min<int64_t>(a.Vc, a.V - v0);
+  for (int c = 0; c < a.nchunk; ++c) {
+    int64_t v0, width;
+    chunk_span(a.V, a.nchunk, a.cw, a.cq, a.nwide, c, &v0, &width);
+    const int vc_valid = (int)width;
     const int gn = (vc_valid + TT::BN - 1) / TT::BN;
     const int nbv = (vc_valid + TT::WTN - 1) / TT::WTN;  // blocks holding a valid column
     FPO_LAUNCH("logits_chunk", st,
                logits_chunk_kernel<E><<<dim3(gm * gn), dim3(256), 0, st>>>(
-        y, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, (int)v0, P, a.ldp, nbv, a.blk_m, a.blk_s,
+        y, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, (int)v0, a.ref, P, a.ldp, nbv, a.blk_m, a.blk_s,
         a.blk_i));
     FPO_CHECK_LAUNCH();
-    const int bps = (nbv + a.nsplit - 1) / a.nsplit;
     FPO_LAUNCH("chunk_stats", st,
                chunk_stats_kernel<T><<<dim3((unsigned)((a.T + 3) / 4)), dim3(256), 0, st>>>(
-        (int)a.T, nbv, bps, a.nsplit, c == 0, a.blk_m, a.blk_s, a.blk_i,
-        a.runM, a.runS, a.runA, a.fout, a.alpha, a.refs));
+        (int)a.T, nbv, c == 0, a.blk_m, a.blk_s, a.blk_i, a.ref, a.runM, a.runS, a.runA, a.fout, a.alpha,
+        P, a.ldp));
     FPO_CHECK_LAUNCH();
-    {
-      constexpr int EPC = 16 / sizeof(T);
-      const int ncv = (vc_valid + EPC - 1) / EPC;
-      const int groups = (ncv + 256 * kRescaleU - 1) / (256 * kRescaleU);
-      FPO_LAUNCH("rescale_p", st,
-                 rescale_p_kernel<T><<<dim3((unsigned)(groups * a.T)), dim3(256), 0, st>>>(
-          groups, vc_valid, nbv, bps, a.nsplit, TT::WTN, a.blk_m, a.refs, P, a.ldp));
-      FPO_CHECK_LAUNCH();
-    }
+    const int bps = (nbv + a.nsplit - 1) / a.nsplit;
     FPO_LAUNCH("proj_chunk", st,
                proj_chunk_kernel<E><<<dim3(gm * (unsigned)((a.d + TT::BN - 1) / TT::BN) * a.nsplit), dim3(256), 0, st>>>(
         P, a.ldp, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, nbv, bps, TT::WTN, c == 0, a.nsplit,

@@ -12,10 +12,20 @@ namespace fpo {
 
 constexpr int kMaxMats = 64;
 
+// Vocabulary chunk c of a plan: the first nwide chunks are cw + cq wide, the
+// others cw, and the last one runs to V. Sets its first entry and width.
+inline void chunk_span(int64_t V, int nchunk, int64_t cw, int64_t cq, int nwide, int c, int64_t* v0,
+                       int64_t* w) {
+  *v0 = (int64_t)c * cw + (int64_t)std::min(c, nwide) * cq;
+  *w = c == nchunk - 1 ? V - *v0 : cw + (c < nwide ? cq : 0);
+}
+
 struct OeLaunch {
   bool bf16;
-  int64_t T, d, V, Vc;
-  int64_t ldp;  // row pitch of the staged p~ (elements, >= Vc)
+  int64_t T, d, V, Vc;  // Vc: widest chunk, rounded up to 256
+  int64_t ldp;          // row pitch of the staged p~ (elements, >= Vc)
+  int nchunk, nwide;    // chunk layout (chunk_span)
+  int64_t cw, cq;
   int nsplit;
   float eps, min_rms;
   const void* h_final;
@@ -35,9 +45,9 @@ struct OeLaunch {
   float* blk_m;
   float* blk_s;
   int32_t* blk_i;
-  float* fout;
-  float* alpha;
-  float* refs;  // [T, nsplit] split references of the current chunk
+  float* fout;   // [T] exp(Ref - M_new) of the current chunk
+  float* alpha;  // [T] exp(M_old - M_new)
+  float* ref;    // [T] staging reference of the current chunk
   float* runM;
   float* runS;
   int32_t* runA;

@@ -130,22 +130,43 @@ def test_chunk_width_respects_operand_bands(lib):
 
 def test_staged_p_pitch_padding_and_band(lib):
     """The staged p~ rows are padded by 256 bytes (a power-of-two pitch puts a
-    tile's rows in one L2 set), and the padded band still fits 2^30 elements:
-    at T = 8192, V = 131072 one unpadded chunk would be exactly 2^30 elements,
-    so the planner takes two chunks and the workspace stays below one
-    T x V bf16 p~."""
+    tile's rows in one L2 set), and by default a chunk stages at most 128 MiB
+    of p~ (half the Infinity Cache): the documented workspace layout exactly
+    at T = 2048, V = 100352 (chunks in whole logits waves of 8192 entries:
+    3 x 24576 + 26624, the widest sizing the staged p~; two projection
+    splits)."""
     def a256(n):
         return (n + 255) // 256 * 256
 
-    # one chunk, two projection splits: the documented workspace layout exactly
     T, d, V, ns = 2048, 4096, 100352, 2
-    nb = V // 128
-    want = (a256(T * d * 2) + a256(T * (V + 128) * 2) + 3 * a256(T * nb * 4) + 2 * a256(T * ns * 4)
-            + 4 * a256(T * 4) + a256(ns * T * d * 4))
+    vc = 26624
+    nb = vc // 128
+    want = (a256(T * d * 2) + a256(T * (vc + 128) * 2) + 3 * a256(T * nb * 4) + 6 * a256(T * 4)
+            + a256(ns * T * d * 4))
     assert lib.fpo_output_error_workspace(C.byref(oe(T=T, d=d, V=V))) == want
     T, V = 8192, 131072
     ws = lib.fpo_output_error_workspace(C.byref(oe(T=T, d=d, V=V)))
     assert 0 < ws < T * V * 2
+
+
+def test_default_chunk_keeps_staged_logits_cache_sized(lib):
+    """For every workload the default plan stages at most 128 MiB of p~ per
+    chunk (plus 256 bytes of padding per row), never the whole T x V logits:
+    the workspace is bounded by y, that chunk, its block statistics, the
+    per-token state and at most eight projection partials, and wherever the
+    logits exceed the Infinity Cache it is smaller than the logits alone."""
+    budget = 128 << 20
+    for c in I.CONFIGS.values():
+        dt = L.FPO_BF16 if c.dtype == "bf16" else L.FPO_F32
+        esz = 2 if dt == L.FPO_BF16 else 4
+        blkw = 128 if dt == L.FPO_BF16 else 64
+        ws = lib.fpo_output_error_workspace(C.byref(oe(c.T, c.d, c.V, dt)))
+        vc = min(budget // esz // c.T, c.V + 255)
+        bound = (c.T * c.d * esz + budget + c.T * 256 + 3 * c.T * (vc // blkw + 1) * 4 + 6 * c.T * 4
+                 + 8 * c.T * c.d * 4 + 16 * 256)
+        assert ws <= bound, (c.name, ws, bound)
+        if c.T * c.V * esz > (256 << 20):
+            assert ws < c.T * c.V * esz, c.name
 
 
 def arr(vals):

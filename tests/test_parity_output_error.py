@@ -80,7 +80,7 @@ def test_bf16_ragged(dev, T, d, V, chunk):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_more_tokens_than_a_second_grid_dimension_holds(dev, dtype):
     """T = 65600, above the 65536 cap of a second grid dimension: the
-    per-token kernels and the p~ rescale run on flat grids."""
+    per-token kernels run on flat grids."""
     print(f"[oe] T=65600 d=16 V=520 {dtype}", flush=True)
     c, x, g, W, y = small_case(I.CONFIGS[0] if dtype == "f32" else I.CONFIGS[1], 65600, 16, 520)
     got = run_gpu(x, g, W, y, dtype, dev)
@@ -158,6 +158,39 @@ def test_peaky_logits_and_planted_targets(dev, dtype):
     check_against_oracle(x, g, W2, y2, dtype, got2)
     for t in range(0, 256, 37):
         assert int(got2["argmax"][t]) == 4000 + t
+
+
+@pytest.mark.parametrize("chunk", [0, 1024])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_staging_reference_far_below_the_row_maximum(dev, dtype, chunk):
+    """p~ is staged against a per-token reference (the target logit for the
+    first chunk, then the running maximum); a block more than the margin above
+    it is staged in its own scale and the statistics kernel brings that row to
+    one scale. W_U x64 puts a random target's logit ~80 below its row maximum
+    (rows whose target is the argmax stay on the common path), and planted
+    rows in a later chunk exceed the maximum of the earlier chunks by ~200,
+    with their targets left elsewhere."""
+    base = I.CONFIGS[0] if dtype == "f32" else I.CONFIGS[1]
+    c = base.shrink(T=300, d=256, V=8200)
+    x, g = I.hidden(c), I.gain(c)
+    Wf = I.storage_to_f64(I.unembedding(c)).astype(np.float32) * 64
+    y = I.targets(c).copy()
+    W = I.to_storage(Wf, c.dtype)
+    ref0 = O.output_error(x, g, W, y)
+    y[::2] = ref0["argmax"][::2]
+    _, yy = O.rmsnorm_forward(x, g, 1e-6)
+    far = ref0["zmax"] - np.array([O.logit(x, g, W, t, int(y[t])) for t in range(c.T)])
+    assert np.sum(far > 70) > c.T // 4  # many rows take the own-scale path
+    got = run_gpu(x, g, W, y, dtype, dev, chunk=chunk)
+    check_against_oracle(x, g, W, y, dtype, got)
+    Wp = Wf.copy()
+    for t in range(1, c.T, 29):
+        Wp[6200 + t] = (300.0 * yy[t] / np.dot(yy[t], yy[t])).astype(np.float32)
+    W2 = I.to_storage(Wp, c.dtype)
+    got2 = run_gpu(x, g, W2, y, dtype, dev, chunk=chunk)
+    check_against_oracle(x, g, W2, y, dtype, got2)
+    for t in range(1, c.T, 29):
+        assert int(got2["argmax"][t]) == 6200 + t
 
 
 def test_out_of_range_targets_counted_and_zeroed(dev):
