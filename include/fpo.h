@@ -21,9 +21,17 @@
  *  - The calls allocate nothing, never synchronise the host and issue no
  *    memset, so they can be captured into a HIP graph (stream capture); the
  *    overlapped optimizer path's side stream joins a capture through its
- *    events (the first such call on a device creates that stream and its
- *    events: make it before capturing). Scalars passed by value (the optimizer step number, hence the
+ *    events. Scalars passed by value (the optimizer step number, hence the
  *    first-step and AdamW bias-correction terms) are fixed at capture.
+ *  - Library state: a thread-local error string; the static scratch array of
+ *    fpo_apply_update_noalloc; and, for fpo_pseudograd's overlapped optimizer
+ *    path when the caller passes no fpo_overlap, one side stream and two
+ *    events per device, created by the first such call on the device (make it
+ *    before any capture), kept until the process ends, and shared by every
+ *    such call on that device under a lock: such calls from several threads
+ *    are serialised while they enqueue, and one issued while another thread's
+ *    capture holds the shared side stream joins that capture. Passing an
+ *    fpo_overlap of the caller's own avoids all of this.
  *  - The caller owns every buffer. The library allocates no device memory;
  *    scratch space comes from the caller's workspace, whose size the
  *    matching *_workspace query returns (fpo_apply_update_noalloc instead
@@ -64,7 +72,7 @@
 extern "C" {
 #endif
 
-#define FPO_ABI_VERSION 5
+#define FPO_ABI_VERSION 6
 
 typedef enum {
   FPO_OK = 0,
@@ -221,6 +229,18 @@ typedef struct {
   float min_rms;
 } fpo_post_ffn;
 
+/* Caller-owned side stream and events for fpo_pseudograd's overlapped
+ * optimizer path (each layer's update runs on side_stream beside the next
+ * layer's outer products). All three are hipStream_t / hipEvent_t handles of
+ * the current device; the events should be created with
+ * hipEventDisableTiming. The library only records, waits on and launches into
+ * them; a set must not be used by two calls that run concurrently. */
+typedef struct {
+  void* side_stream;
+  void* ready_event;
+  void* done_event;
+} fpo_overlap;
+
 /* ---------------------------------------------------------------------------
  * fpo_pseudograd - per-layer token-summed outer products (eq. w3update, with
  * the App. A divisor supplied as desc->scale) and, in full-MLP mode, the
@@ -246,27 +266,32 @@ typedef struct {
  *              nullable (layer-viability diagnostic, eq. cosine)
  *   ref_dot, ref_sumsq  double [L] out (required when ref is given):
  *              <dW3_l, R_l> and ||R_l||_F^2
+ *   ref_cos    float [L] out, nullable (only with ref): the layer-viability
+ *              cosine <dW3_l, R_l> / (||dW3_l|| ||R_l||), 0 when either norm
+ *              is 0 (eq. cosine), from the same float64 sums
  *   post_ffn   required iff desc->mode has FPO_MODE_POST_FFN: compose each
  *              layer's post-FFN norm VJP (see fpo_post_ffn); g_tilde_lp is
  *              then unused and may be NULL
  *   opt, upd   both NULL, or both given: the call then also applies
  *              fpo_apply_update to the matrices in `sumsq` order, with the
  *              same result bit for bit as calling it separately
+ *   overlap    nullable: the side stream and events of the overlapped
+ *              optimizer path (see fpo_overlap); NULL uses the library's own
+ *              (see "Library state" above)
  *   stream     the work is ordered on this stream. With opt given on the
- *              FPO_BF16 / FPO_MODE_W3 path, each layer's update runs on a
- *              second, library-owned stream of the current device (default
- *              priority), overlapping the next layer's outer products, and is
- *              joined back to `stream` with an event before the call's last
- *              kernel; calls on one device from several host threads are
- *              serialized while they enqueue.
+ *              FPO_BF16 / FPO_MODE_W3 path with the gradient clip, each
+ *              layer's update runs on the side stream, overlapping the next
+ *              layer's outer products, and is joined back to `stream` with an
+ *              event before the call's last kernel.
  * Returns FPO_OK or an fpo_status. */
 size_t fpo_pseudograd_workspace(const fpo_pg_desc* desc);
 int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* const* a,
                    const void* const* W3_init, const void* const* gate, const void* const* up,
                    const void* const* x_in, float* const* dW3, float* const* dW1,
                    float* const* dW2, double* sumsq, const float* const* ref, double* ref_dot,
-                   double* ref_sumsq, const fpo_post_ffn* post_ffn, const fpo_opt* opt,
-                   const fpo_update_bufs* upd, void* ws, size_t ws_bytes, void* stream);
+                   double* ref_sumsq, float* ref_cos, const fpo_post_ffn* post_ffn,
+                   const fpo_opt* opt, const fpo_update_bufs* upd, const fpo_overlap* overlap,
+                   void* ws, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
  * fpo_apply_update - relative clip and optimizer step on fp32 masters

@@ -55,7 +55,11 @@ class PostFfn(C.Structure):
                 ("eps", C.c_float), ("min_rms", C.c_float)]
 
 
-ABI_VERSION = 5
+class Overlap(C.Structure):
+    _fields_ = [("side_stream", C.c_void_p), ("ready_event", C.c_void_p), ("done_event", C.c_void_p)]
+
+
+ABI_VERSION = 6
 PP = C.POINTER(C.c_void_p)
 VP = C.c_void_p
 _lib = None
@@ -92,8 +96,8 @@ def load() -> C.CDLL:
     lib.fpo_pseudograd_workspace.argtypes = [C.POINTER(PgDesc)]
     lib.fpo_pseudograd.restype = C.c_int
     lib.fpo_pseudograd.argtypes = [C.POINTER(PgDesc), VP, PP, PP, PP, PP, PP, PP, PP, PP, VP, PP, VP,
-                                   VP, C.POINTER(PostFfn), C.POINTER(Opt), C.POINTER(UpdateBufs), VP,
-                                   C.c_size_t, VP]
+                                   VP, VP, C.POINTER(PostFfn), C.POINTER(Opt), C.POINTER(UpdateBufs),
+                                   C.POINTER(Overlap), VP, C.c_size_t, VP]
     lib.fpo_apply_update_workspace.restype = C.c_size_t
     lib.fpo_apply_update_workspace.argtypes = [C.c_int64, C.POINTER(C.c_int64)]
     lib.fpo_apply_update.restype = C.c_int

@@ -18,7 +18,7 @@ from . import _lib as L
 
 __all__ = [
     "fpo_abi_version", "fpo_output_error", "fpo_output_error_workspace", "fpo_pseudograd", "PostFfn",
-    "fpo_pseudograd_workspace", "fpo_apply_update", "fpo_apply_update_workspace", "fpo_cosine",
+    "fpo_pseudograd_workspace", "fpo_apply_update", "fpo_apply_update_workspace", "fpo_cosine", "Overlap",
     "fpo_cosine_workspace", "OptConfig", "workspace", "dtype_code",
 ]
 
@@ -193,15 +193,34 @@ class PostFfn:
     min_rms: float = 0.5
 
 
+class Overlap:
+    """The caller's own side stream and two events for fpo_pseudograd's
+    overlapped optimizer path (fpo_overlap): a torch stream at the default
+    priority and two torch events (created here by recording them once).
+    Keep one per concurrent caller; it holds no device memory."""
+
+    def __init__(self, device=None):
+        self.stream = torch.cuda.Stream(device=device)
+        self.ready = torch.cuda.Event()
+        self.done = torch.cuda.Event()
+        self.ready.record(self.stream)
+        self.done.record(self.stream)
+
+    def c(self) -> L.Overlap:
+        return L.Overlap(self.stream.cuda_stream, self.ready.cuda_event, self.done.cuda_event)
+
+
 def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, ref_sumsq=None,
                    W3_init=None, gate=None, up=None, x_in=None, dW1=None, dW2=None, scale=None,
                    opt: Optional[OptConfig] = None, W_master=None, W_lp=None, state1=None,
                    state2=None, W_sumsq=None, clip_scale=None, ws=None, post_ffn: Optional[PostFfn] = None,
-                   grad_bf16: bool = False):
+                   grad_bf16: bool = False, ref_cos=None, overlap: Optional[Overlap] = None):
     """g_tilde_lp may be None when post_ffn is given (its left operands are
     then formed per layer from post_ffn.g_tilde). grad_bf16 (FPO_MODE_GRAD_BF16,
     fused update only, dW3 None): the pseudogradient is staged in bf16 in the
-    workspace instead of being returned."""
+    workspace instead of being returned. ref_cos (float32 [L]): the per-layer
+    cosine with ref, computed in the library. overlap: the side stream and
+    events of the overlapped optimizer path (default: the library's own)."""
     op = a[0].dtype
     dev = a[0].device
     T = a[0].shape[0]
@@ -220,6 +239,7 @@ def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, 
     numels = [d * d_ff] * nm
     ub = (_upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale, op, numels, dev)
           if opt is not None else None)
+    ov = overlap.c() if overlap is not None else None
     pf = None
     if post_ffn is not None:
         pf = L.PostFfn(_p(post_ffn.g_tilde, F32, (T, d), dev, "post_ffn.g_tilde"),
@@ -232,9 +252,10 @@ def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, 
         k.arr(dW3, F32, (d, d_ff), dev, Lyr, "dW3"), k.arr(dW1, F32, (d_ff, d), dev, Lyr, "dW1"),
         k.arr(dW2, F32, (d_ff, d), dev, Lyr, "dW2"), _p(sumsq, F64, nm, dev, "sumsq"),
         k.arr(ref, F32, (d, d_ff), dev, Lyr, "ref"), _p(ref_dot, F64, Lyr, dev, "ref_dot"),
-        _p(ref_sumsq, F64, Lyr, dev, "ref_sumsq"), C.byref(pf) if pf is not None else None,
+        _p(ref_sumsq, F64, Lyr, dev, "ref_sumsq"), _p(ref_cos, F32, Lyr, dev, "ref_cos"),
+        C.byref(pf) if pf is not None else None,
         C.byref(o) if o is not None else None, C.byref(ub) if ub is not None else None,
-        _p(ws, None, None, dev, "ws"), _nbytes(ws), _stream(dev)))
+        C.byref(ov) if ov is not None else None, _p(ws, None, None, dev, "ws"), _nbytes(ws), _stream(dev)))
     return ws
 
 

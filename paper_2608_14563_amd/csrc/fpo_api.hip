@@ -495,8 +495,9 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
                    const void* const* W3_init, const void* const* gate, const void* const* up,
                    const void* const* x_in, float* const* dW3, float* const* dW1, float* const* dW2,
                    double* sumsq, const float* const* ref, double* ref_dot, double* ref_sumsq,
-                   const fpo_post_ffn* post_ffn, const fpo_opt* opt, const fpo_update_bufs* upd,
-                   void* ws, size_t ws_bytes, void* stream) {
+                   float* ref_cos, const fpo_post_ffn* post_ffn, const fpo_opt* opt,
+                   const fpo_update_bufs* upd, const fpo_overlap* overlap, void* ws, size_t ws_bytes,
+                   void* stream) {
   if (int e = check_pg_desc(desc)) return e;
   const bool full = (desc->mode & FPO_MODE_FULL_MLP) != 0;
   const bool pffn = (desc->mode & FPO_MODE_POST_FFN) != 0;
@@ -526,6 +527,9 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
   if (!dW3 && !ref && !stage) return fail(FPO_ERR_NULL, "fpo_pseudograd: dW3 may be NULL only with ref");
   if (ref && (!ref_dot || !ref_sumsq))
     return fail(FPO_ERR_NULL, "fpo_pseudograd: ref needs ref_dot and ref_sumsq");
+  if (ref_cos && !ref) return fail(FPO_ERR_ARG, "fpo_pseudograd: ref_cos needs ref");
+  if (overlap && (!overlap->side_stream || !overlap->ready_event || !overlap->done_event))
+    return fail(FPO_ERR_NULL, "fpo_pseudograd: overlap needs side_stream, ready_event and done_event");
   if (full && (!W3_init || !gate || !up || !x_in || !dW1 || !dW2))
     return fail(FPO_ERR_NULL, "fpo_pseudograd: full-MLP mode needs W3_init, gate, up, x_in, dW1, dW2");
   if ((opt == nullptr) != (upd == nullptr))
@@ -580,6 +584,7 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
   P.sumsq = sumsq;
   P.ref_dot = ref_dot;
   P.ref_sumsq = ref_sumsq;
+  P.ref_cos = ref_cos;
   P.stream = stream;
   const PgPlan pl = plan_pg(*desc);
   P.Tp = pl.Tp;
@@ -610,7 +615,9 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
     // W3 only, bf16, gradient clip: layer l's update overlaps layer l+1's
     // outer products (clip-the-update needs every step's norm first: two
     // passes after the pseudogradient)
-    e = fpo::launch_pseudograd_update(P, U);
+    fpo::OverlapLaunch ov{};
+    if (overlap) ov = fpo::OverlapLaunch{overlap->side_stream, overlap->ready_event, overlap->done_event};
+    e = fpo::launch_pseudograd_update(P, U, overlap ? &ov : nullptr);
     if (e != hipSuccess) return hip_fail(e, "fpo_pseudograd overlapped launch");
     return FPO_OK;
   }

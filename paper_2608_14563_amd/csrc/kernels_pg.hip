@@ -358,11 +358,15 @@ __global__ __launch_bounds__(256, 1) void errh_kernel(const typename E::T* __res
   }
 }
 
+// Fixed-order float64 sums of one matrix's tile partials per workgroup:
+// ||C||^2 (into sumsq[mat_base + mat]) and, against a reference R, <C, R>,
+// ||R||^2 and cos = <C, R> / (||C|| ||R||) (0 when either norm is 0; eq. cosine).
 __global__ __launch_bounds__(256) void reduce_parts_kernel(const double* __restrict__ part,
                                                            int ntiles, int mat_base,
                                                            double* __restrict__ sumsq,
                                                            double* __restrict__ dot,
-                                                           double* __restrict__ refsq) {
+                                                           double* __restrict__ refsq,
+                                                           float* __restrict__ cos) {
   __shared__ double red[16];
   const int mat = blockIdx.x;
   const double* p = part + (int64_t)mat * ntiles * 3;
@@ -379,6 +383,7 @@ __global__ __launch_bounds__(256) void reduce_parts_kernel(const double* __restr
     if (sumsq) sumsq[mat_base + mat] = a;
     if (dot) dot[mat] = b;
     if (refsq) refsq[mat] = c;
+    if (cos) cos[mat] = (a == 0.0 || c == 0.0) ? 0.f : (float)(b / sqrt(a * c));
   }
 }
 
@@ -458,7 +463,7 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
     FPO_CHECK_LAUNCH();
     FPO_LAUNCH("reduce_parts", st,
                reduce_parts_kernel<<<dim3(a.L), dim3(256), 0, st>>>(a.part, ntiles, 0, a.sumsq, a.ref_dot,
-                                                         a.ref_sumsq));
+                                                         a.ref_sumsq, a.ref_cos));
     FPO_CHECK_LAUNCH();
   }
   if (!a.full_mlp) return hipSuccess;
@@ -484,11 +489,11 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
     if (a.sumsq) {
       FPO_LAUNCH("reduce_parts", st,
                  reduce_parts_kernel<<<dim3(1), dim3(256), 0, st>>>(a.part, ntiles2, a.L + l, a.sumsq,
-                                                         nullptr, nullptr));
+                                                         nullptr, nullptr, nullptr));
       FPO_CHECK_LAUNCH();
       FPO_LAUNCH("reduce_parts", st,
                  reduce_parts_kernel<<<dim3(1), dim3(256), 0, st>>>(a.part + (int64_t)ntiles2 * 3, ntiles2,
-                                                         2 * a.L + l, a.sumsq, nullptr, nullptr));
+                                                         2 * a.L + l, a.sumsq, nullptr, nullptr, nullptr));
       FPO_CHECK_LAUNCH();
     }
   }
@@ -527,16 +532,33 @@ static hipError_t pg_overlap_init(PgOverlap& p, int dev) {
 // while layer l+1's MFMAs run, with one workgroup per CU so that each CU holds
 // one outer-product workgroup and one update workgroup; the last layer's update
 // has the machine to itself. Same per-block arithmetic and reduction order as the
-// separate calls, so results are bit-identical to them.
-hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u) {
-  hipStream_t st = (hipStream_t)a.stream;
+// separate calls, so results are bit-identical to them. The side stream and its
+// two events are the caller's (ov) or, when ov is null, the device's
+// library-owned set, whose enqueue sequence is serialised by a lock.
+static hipError_t enqueue_pseudograd_update(const PgLaunch& a, const UpdLaunch& u, hipStream_t side,
+                                            hipEvent_t ready_l, hipEvent_t done, int cus);
+
+hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u, const OverlapLaunch* ov) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
   PgOverlap& po = g_pgo[dev];
+  if (ov) {
+    int cus = 0;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    return enqueue_pseudograd_update(a, u, (hipStream_t)ov->side, (hipEvent_t)ov->ready, (hipEvent_t)ov->done,
+                                     cus);
+  }
   std::lock_guard<std::mutex> lock(po.mu);
   if ((e = pg_overlap_init(po, dev)) != hipSuccess) return e;
+  return enqueue_pseudograd_update(a, u, po.side, po.ready_l, po.done, po.cus);
+}
+
+static hipError_t enqueue_pseudograd_update(const PgLaunch& a, const UpdLaunch& u, hipStream_t side,
+                                            hipEvent_t ready_l, hipEvent_t done, int cus) {
+  hipStream_t st = (hipStream_t)a.stream;
+  hipError_t e;
   if ((e = prepare_signals<uint16_t>(a, st)) != hipSuccess) return e;
   const int ntiles = (int)pseudograd_tiles(true, a.d, a.d_ff);
   int64_t blk_base = 0;
@@ -555,18 +577,18 @@ hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u) {
     FPO_LAUNCH("reduce_parts", st,
                reduce_parts_kernel<<<dim3(1), dim3(256), 0, st>>>(
         tpart, ntiles, l, a.sumsq, a.ref_dot ? a.ref_dot + l : nullptr,
-        a.ref_sumsq ? a.ref_sumsq + l : nullptr));
+        a.ref_sumsq ? a.ref_sumsq + l : nullptr, a.ref_cos ? a.ref_cos + l : nullptr));
     FPO_CHECK_LAUNCH();
     // layer l's dW and ||dW||^2 are complete: update it on the side stream
-    if ((e = hipEventRecord(po.ready_l, st)) != hipSuccess) return e;
-    if ((e = hipStreamWaitEvent(po.side, po.ready_l, 0)) != hipSuccess) return e;
+    if ((e = hipEventRecord(ready_l, st)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(side, ready_l, 0)) != hipSuccess) return e;
     // one workgroup per CU while the next layer's outer products run; the last
     // update runs alone and takes the whole machine
-    if ((e = launch_update_blocks(u, l, blk_base, po.side, l + 1 < a.L ? po.cus : 0)) != hipSuccess) return e;
+    if ((e = launch_update_blocks(u, l, blk_base, side, l + 1 < a.L ? cus : 0)) != hipSuccess) return e;
     blk_base += update_blocks(u.numel[l]);
   }
-  if ((e = hipEventRecord(po.done, po.side)) != hipSuccess) return e;
-  if ((e = hipStreamWaitEvent(st, po.done, 0)) != hipSuccess) return e;
+  if ((e = hipEventRecord(done, side)) != hipSuccess) return e;
+  if ((e = hipStreamWaitEvent(st, done, 0)) != hipSuccess) return e;
   // ||W'||^2 and the clip factors of every matrix
   return launch_update(u, false);
 }

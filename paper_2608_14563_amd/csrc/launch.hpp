@@ -82,6 +82,7 @@ struct PgLaunch {
   double* sumsq;                    // [n_mats] or null
   double* ref_dot;
   double* ref_sumsq;
+  float* ref_cos;
   // workspace
   void* gT;                         // [d, Tp] transposed signal
   void* g_row;                      // [T, d] per-layer signal (post-FFN composition, full-MLP)
@@ -125,9 +126,16 @@ hipError_t launch_update(const UpdLaunch& a, bool blocks = true);
 // The update blocks of matrix m of `a` on `stream` (partials at part + blk_base);
 // grid > 0: that many workgroups visit the blocks grid-stride.
 hipError_t launch_update_blocks(const UpdLaunch& a, int m, int64_t blk_base, void* stream, int grid = 0);
+// Caller-owned side stream and events of the overlapped path.
+struct OverlapLaunch {
+  void* side;
+  void* ready;
+  void* done;
+};
 // W3-only bf16 pseudogradients with the optimizer step overlapped (u: the
-// update of the same matrices, grad = the dW3 outputs, grad_sumsq = a.sumsq).
-hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u);
+// update of the same matrices, grad = the dW3 outputs, grad_sumsq = a.sumsq);
+// ov: the caller's side stream and events, or null for the library's own.
+hipError_t launch_pseudograd_update(const PgLaunch& a, const UpdLaunch& u, const OverlapLaunch* ov);
 int64_t update_blocks(int64_t numel);
 
 struct CosLaunch {

@@ -205,6 +205,7 @@ def fpo_launch(model: Transformer, c: Cache, tg: dict, op: torch.dtype, min_rms:
            "sumsq": torch.empty(3 * L if full else L, dtype=torch.float64, device=dev),
            "dot": torch.empty(L, dtype=torch.float64, device=dev),
            "rsq": torch.empty(L, dtype=torch.float64, device=dev),
+           "cos_w3": torch.empty(L, dtype=torch.float32, device=dev),
            "cos_out": torch.empty(L, dtype=torch.float32, device=dev)}
     kw = {}
     if full:
@@ -213,7 +214,7 @@ def fpo_launch(model: Transformer, c: Cache, tg: dict, op: torch.dtype, min_rms:
                   dW1=[torch.empty(d_ff, d, dtype=torch.float32, device=dev) for _ in range(L)],
                   dW2=[torch.empty(d_ff, d, dtype=torch.float32, device=dev) for _ in range(L)])
     api.fpo_pseudograd(sig, c.a, dW3=None, sumsq=out["sumsq"], ref=tg["dW3"], ref_dot=out["dot"],
-                       ref_sumsq=out["rsq"], scale=1.0 / T, post_ffn=post, **kw)
+                       ref_sumsq=out["rsq"], ref_cos=out["cos_w3"], scale=1.0 / T, post_ffn=post, **kw)
     api.fpo_cosine([g] * L, tg["dR"], cos=out["cos_out"])
     if full:
         out["D1"], out["D2"] = kw["dW1"], kw["dW2"]
@@ -224,14 +225,13 @@ def fpo_launch(model: Transformer, c: Cache, tg: dict, op: torch.dtype, min_rms:
 
 
 def fpo_finish(out: dict, keep: bool = False) -> dict:
-    """Copy fpo_launch's per-layer results to the host (synchronizes):
-    float64 arrays cos_w3 = dot / sqrt(||D||^2 ||R||^2), cos_out (cos_w1,
-    cos_w2), the reductions dot, sumsq_D, sumsq_R, and the device per-token
-    loss; with keep=True also g~ (and D1, D2)."""
+    """Copy fpo_launch's per-layer results to the host (synchronizes): the
+    library's cosines cos_w3, cos_out (cos_w1, cos_w2) as float64 arrays, the
+    reductions dot, sumsq_D, sumsq_R, and the device per-token loss; with
+    keep=True also g~ (and D1, D2)."""
     L = out["dot"].numel()
     dot_h, ss_h, rsq_h = out["dot"].cpu().numpy(), out["sumsq"].cpu().numpy()[:L], out["rsq"].cpu().numpy()
-    den = np.sqrt(ss_h * rsq_h)
-    res = {"cos_w3": np.where(den > 0, dot_h / np.where(den > 0, den, 1.0), 0.0),
+    res = {"cos_w3": out["cos_w3"].double().cpu().numpy(),
            "cos_out": out["cos_out"].double().cpu().numpy(), "dot": dot_h, "sumsq_D": ss_h, "sumsq_R": rsq_h,
            "loss_tok": out["loss_tok"]}
     for k in ("cos_w1", "cos_w2"):

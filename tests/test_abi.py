@@ -53,7 +53,7 @@ def test_library_exports_every_header_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert lib.fpo_abi_version() == 5 == L.ABI_VERSION
+    assert lib.fpo_abi_version() == 6 == L.ABI_VERSION
 
 
 def oe(T=128, d=256, V=4096, dtype=L.FPO_BF16, eps=1e-6, min_rms=0.5, chunk=0):
@@ -178,9 +178,11 @@ def test_pseudograd_validation(lib):
     a, ka = arr([FAKE, FAKE])
     dw, kd = arr([FAKE, FAKE])
 
-    def call(desc, A=a, dW3=dw, ref=None, ref_dot=None, opt=None, upd=None, ws_bytes=1 << 40, g=FAKE, pf=None):
+    def call(desc, A=a, dW3=dw, ref=None, ref_dot=None, opt=None, upd=None, ws_bytes=1 << 40, g=FAKE, pf=None,
+             ref_cos=None, ov=None):
         return lib.fpo_pseudograd(C.byref(desc) if desc is not None else None, g, A, None, None, None, None,
-                                  dW3, None, None, None, ref, ref_dot, None, pf, opt, upd, FAKE, ws_bytes, None)
+                                  dW3, None, None, None, ref, ref_dot, None, ref_cos, pf, opt, upd, ov, FAKE,
+                                  ws_bytes, None)
 
     good = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_W3, 1 / 128)
     assert call(None) == L.FPO_ERR_NULL
@@ -196,6 +198,13 @@ def test_pseudograd_validation(lib):
     assert call(good, dW3=None) == L.FPO_ERR_NULL
     r, kr = arr([FAKE, FAKE])
     assert call(good, dW3=None, ref=r) == L.FPO_ERR_NULL  # ref needs ref_dot / ref_sumsq
+    assert call(good, ref_cos=FAKE) == L.FPO_ERR_ARG          # a cosine needs a reference
+    # a caller-owned overlap set must name its stream and both events
+    for k in range(3):
+        h = [FAKE, FAKE, FAKE]
+        h[k] = None
+        assert call(good, ov=C.byref(L.Overlap(*h))) == L.FPO_ERR_NULL, k
+    assert call(good, ov=C.byref(L.Overlap(FAKE, FAKE, FAKE)), ws_bytes=16) == L.FPO_ERR_WORKSPACE
     o = L.Opt(0, 1e-4, 0.9, 0.9, 0.999, 1e-8, 0.01, 0.01, 1)
     assert call(good, opt=C.byref(o)) == L.FPO_ERR_ARG  # opt without upd
     full = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_FULL_MLP, 1 / 128)
@@ -254,7 +263,7 @@ def test_pseudograd_operand_alignment(lib):
         desc = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_W3, 1 / 128)
         a, ka = arr(good)
         return lib.fpo_pseudograd(C.byref(desc), FAKE, a, None, None, None, None, None, None, None, None, r,
-                                  FAKE, FAKE, None, None, None, FAKE, 16, None)
+                                  FAKE, FAKE, None, None, None, None, None, FAKE, 16, None)
 
     assert ref_call(good) == L.FPO_ERR_WORKSPACE
     assert ref_call(bad) == L.FPO_ERR_ARG
@@ -264,7 +273,7 @@ def test_pseudograd_operand_alignment(lib):
         p = [b[0] for b in bufs]
         desc = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_FULL_MLP, 1 / 128)
         return lib.fpo_pseudograd(C.byref(desc), FAKE, p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[6], None,
-                                  None, None, None, None, None, None, FAKE, 16, None)
+                                  None, None, None, None, None, None, None, None, FAKE, 16, None)
 
     assert full_call(-1) == L.FPO_ERR_WORKSPACE
     for k in range(1, 7):  # W3_init, gate, up, x_in, dW3 / dW1, dW2

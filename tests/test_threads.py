@@ -1,7 +1,8 @@
 """Concurrent callers: two host threads, each on its own stream with its own
-buffers, run the overlapped pseudogradient + SGD-momentum step three times.
-The library serialises their enqueue on the device and shares one side stream;
-each thread's results must equal the same steps run alone on one stream."""
+buffers, run the overlapped pseudogradient + SGD-momentum step three times,
+either with the library's shared side stream (enqueue serialised by its lock)
+or each with a side stream and events of its own (fpo_overlap); each thread's
+results must equal the same steps run alone on one stream."""
 import threading
 
 import pytest
@@ -25,14 +26,15 @@ def _case(c, dev, seed_layer):
                                  dev))
 
 
-def _steps(s, n=3):
+def _steps(s, n=3, overlap=None):
     for k in range(1, n + 1):
         api.fpo_pseudograd(s["g"], s["a"], dW3=None, sumsq=s["ss"], grad_bf16=True, ws=s["ws"],
                            opt=api.OptConfig(lr=1e-2, clip_frac=0.01, step=k), W_master=s["W"], W_lp=s["lp"],
-                           state1=s["s1"], W_sumsq=s["Wsq"])
+                           state1=s["s1"], W_sumsq=s["Wsq"], overlap=overlap)
 
 
-def test_two_threads_two_streams(dev):
+@pytest.mark.parametrize("own_side_stream", [False, True], ids=["library-side-stream", "caller-side-streams"])
+def test_two_threads_two_streams(dev, own_side_stream):
     c = I.CONFIGS[1].shrink(T=256, d=520, d_ff=1288, L=3)
     ref = [_case(c, dev, 0), _case(c, dev, 3)]
     for s in ref:
@@ -44,8 +46,9 @@ def test_two_threads_two_streams(dev):
     def run(s):
         try:
             st = torch.cuda.Stream()
+            ov = api.Overlap(dev) if own_side_stream else None
             with torch.cuda.stream(st):
-                _steps(s)
+                _steps(s, overlap=ov)
             st.synchronize()
         except Exception as e:  # pragma: no cover - reported below
             errors.append(e)
