@@ -6,11 +6,14 @@ fpo_output_error (final-norm recompute, vocabulary-chunked logits + online
 softmax + error, projection through W_U, clamped RMSNorm VJP) followed by
 fpo_pseudograd with the fused update (per-layer outer products for every
 target layer staged in bf16 as the paper's bf16 einsum produces them,
-relative 1% clip, SGD-momentum on fp32 masters, bf16 copy).
+relative 1% clip, SGD-momentum on fp32 masters, bf16 copy). The default
+workload is the Qwen3-8B-shaped training batch (config 2); config 4 is the
+layer-viability diagnostic (every layer's pseudogradient reduced against a
+reference gradient in the GEMM epilogue); --full-mlp also updates W1 and W2.
 Inputs are seeded synthetic tensors of the workload's shapes, resident in HBM
 before timing starts. Prints one JSON line on stdout; progress goes to stderr.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1]
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2] [--full-mlp]
 """
 from __future__ import annotations
 
@@ -43,12 +46,16 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=1, help="workload id (paper_2608_14563_amd.inputs.CONFIGS)")
+    ap.add_argument("--config", type=int, default=2,
+                    help="workload id (paper_2608_14563_amd.inputs.CONFIGS): 1-3 training steps, 4 the diagnostic")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--vocab-chunk", type=int, default=0,
                     help="vocabulary chunk width (0: the library's planner)")
     ap.add_argument("--cpu-tokens", type=int, default=0,
-                    help="tokens in the oracle's timed sample (0: the whole step)")
+                    help="tokens in the oracle's timed sample (0: about 10 TFLOP of float64 work, at most the "
+                         "whole batch)")
+    ap.add_argument("--full-mlp", action="store_true",
+                    help="update W1 and W2 too, through the fixed feedback W3_init (eq. errh)")
     ap.add_argument("--post-ffn", action="store_true",
                     help="compose each target layer's post-FFN RMSNorm VJP (OLMo-2 / Gemma 3 layout)")
     ap.add_argument("--grad-f32", action="store_true",
@@ -155,30 +162,32 @@ def profiled_traffic(workload: str, kernel: str):
     return None
 
 
-def kernel_work(name, c, steps, nchunk, opt="sgd-momentum", pffn=False, grad_bf16=False, clip_update=False):
+def kernel_work(name, c, steps, nchunk, opt="sgd-momentum", pffn=False, grad_bf16=False, clip_update=False,
+                full=False):
     """Algorithmic work of one kernel over `steps` steps: (amount, unit, bound).
     Flops count only the method's contractions; bytes count each operand once."""
     T, d, V, dff, L = c.T, c.d, c.V, c.d_ff, c.L
     if name in ("logits_chunk", "proj_chunk"):
         return 2.0 * T * V * d * steps, "flop", "mfma"
-    if name == "outer":
+    if name == "outer":  # W3 (and, full-MLP, W1 and W2) outer products of every layer
+        return 2.0 * T * d * dff * L * (3 if full else 1) * steps, "flop", "mfma"
+    if name == "errh":  # E = g~ W3_init per layer
         return 2.0 * T * d * dff * L * steps, "flop", "mfma"
+    nm = 3 * L if full else L
     gb = 2.0 if grad_bf16 else 4.0  # a staged bf16 pseudogradient reads 2 bytes instead of 4
     if name == "update" and clip_update:  # pass 2: W r/w, bf16 copy, the new state (or dW) read
         per = {"sgd-momentum": 14.0, "sgd": 10.0 + gb, "adamw": 18.0}[opt]
-        return per * L * d * dff * steps, "byte", "hbm"
+        return per * nm * d * dff * steps, "byte", "hbm"
     if name == "update_delta":  # pass 1: dW (and state, W for AdamW) read, new state written
         per = {"sgd-momentum": gb + 8.0, "sgd": gb, "adamw": gb + 20.0}[opt]
-        return per * L * d * dff * steps, "byte", "hbm"
+        return per * nm * d * dff * steps, "byte", "hbm"
     if name == "update":
-        return (OPT_BYTES[opt] - (4.0 - gb)) * L * d * dff * steps, "byte", "hbm"
+        return (OPT_BYTES[opt] - (4.0 - gb)) * nm * d * dff * steps, "byte", "hbm"
     if name == "chunk_stats":
-        # per-(token, 128-entry block) max / sum / argmax read; per-token state written
-        return (12.0 * T * ((V + 127) // 128) + 32.0 * T) * steps, "byte", "hbm"
-    if name == "rescale_p":
-        return 4.0 * T * V * steps, "byte", "hbm"  # staged p~ read + write (bf16)
+        # per-(token, 128-entry block) max / sum / argmax read; per-token state read and written
+        return (12.0 * T * ((V + 127) // 128) + 36.0 * T) * steps, "byte", "hbm"
     if name == "rms_forward":
-        return (4.0 * T * d) * steps, "byte", "hbm"  # x read, y written (bf16)
+        return (6.0 * T * d) * steps, "byte", "hbm"  # x read, y written, the target's W_U row read (bf16)
     if name == "pffn_stats":  # per layer: g~ fp32 and MLP output read
         return (6.0 * T * d * L) * steps, "byte", "hbm"
     if name == "signal_transpose":
@@ -190,14 +199,7 @@ def kernel_work(name, c, steps, nchunk, opt="sgd-momentum", pffn=False, grad_bf1
     return None
 
 
-def cpu_baseline(c, tokens, x, gam, W_U, y, acts, Wm):
-    """The oracle, timed on the host cores: the first `tokens` tokens (all T
-    by default) through the output error and every layer's outer product, then
-    every layer's clipped SGD-momentum step. With fewer than T tokens the full
-    step is estimated as per-token time x T + the measured updates."""
-    import numpy as np
-
-    import oracle as O
+def _cpu_info():
     blas = None
     try:
         from threadpoolctl import threadpool_info
@@ -214,25 +216,85 @@ def cpu_baseline(c, tokens, x, gam, W_U, y, acts, Wm):
                 break
     except OSError:  # pragma: no cover
         pass
-    ts = c.T if tokens <= 0 else min(tokens, c.T)
+    return thr, blas, cpu_model
+
+
+def auto_cpu_tokens(c, per_token_flop, budget=1.0e13):
+    """Token sample for the oracle: about 10 TFLOP of float64 work (10-20 s
+    on the GPU machine's 16 host cores), at most the whole batch."""
+    return max(1, min(c.T, int(budget // per_token_flop)))
+
+
+def cpu_baseline(c, tokens, x, gam, W_U, y, acts, Wm, full=None):
+    """The oracle, timed on the host cores: the first `tokens` tokens through
+    the output error and every layer's outer product (full-MLP: also the W1/W2
+    signals through W3_init), then every matrix's clipped SGD-momentum step.
+    With fewer than T tokens the full step is estimated as per-token time x T
+    + the measured updates."""
+    import numpy as np
+
+    import oracle as O
+    thr, blas, cpu_model = _cpu_info()
+    per_tok = 8.0 * c.V * c.d + 2.0 * c.d * c.d_ff * c.L * (4 if full else 1)
+    ts = auto_cpu_tokens(c, per_tok) if tokens <= 0 else min(tokens, c.T)
     t0 = time.perf_counter()
     out = O.output_error(x[:ts], gam, W_U, y[:ts], eps=c.eps, min_rms=c.min_rms, vocab_chunk=8192)
     Ds = [O.pseudograd(out["g_tilde"], a[:ts], scale=1.0 / c.T) for a in acts]
+    if full:
+        D1s, D2s = [], []
+        for l in range(c.L):
+            D1, D2 = O.full_mlp_grads(out["g_tilde"], full["W3i"][l], full["q"][l][:ts], full["u"][l][:ts],
+                                      full["x_in"][l][:ts], scale=1.0 / c.T)
+            D1s.append(D1)
+            D2s.append(D2)
+        Ds = Ds + D1s + D2s
     t1 = time.perf_counter()
     for D, W in zip(Ds, Wm):
         s = O.clip_scale(float((D * D).sum()), float((W.astype(np.float64) ** 2).sum()), c.clip_frac)
         O.sgd_momentum(W, np.zeros_like(D), s * D, c.lr, 0.9, step=2)
     t2 = time.perf_counter()
     est = (t1 - t0) / ts * c.T + (t2 - t1)
+    what = f"all {c.L} layers' {'W1, W2 and W3 pseudogradients' if full else 'outer products'}"
+    nm = len(Ds)
     if ts == c.T:
-        sample = (f"the whole step: {c.T} tokens through output error (full V={c.V}) and all {c.L} layer "
-                  f"outer products ({t1 - t0:.1f} s), then all {c.L} clipped SGD-momentum steps ({t2 - t1:.1f} s)")
+        sample = (f"the whole step: {c.T} tokens through output error (full V={c.V}) and {what} "
+                  f"({t1 - t0:.1f} s), then all {nm} clipped SGD-momentum steps ({t2 - t1:.1f} s)")
     else:
-        sample = (f"first {ts} of {c.T} tokens through output error (full V={c.V}) and all {c.L} layer outer "
-                  f"products ({t1 - t0:.1f} s), then all {c.L} clipped SGD-momentum steps ({t2 - t1:.1f} s); "
-                  f"full step estimated as per-token time x T + updates = {est:.1f} s")
+        sample = (f"first {ts} of {c.T} tokens through output error (full V={c.V}) and {what} ({t1 - t0:.1f} s), "
+                  f"then all {nm} clipped SGD-momentum steps ({t2 - t1:.1f} s); full step estimated as "
+                  f"per-token time x T + updates = {est:.1f} s")
     return {"value": c.T / est, "unit": "tokens/s", "cores": int(thr), "kind": "oracle", "sample": sample,
             "seconds": round(t2 - t0, 2), "affinity_cpus": len(os.sched_getaffinity(0)),
+            "cpu_model": cpu_model, "blas": blas}
+
+
+def cpu_baseline_diag(c, tokens, x, gam, W_U, y, tacts, refs):
+    """The oracle on a sample of the diagnostic workload: the first `tokens`
+    tokens through the output error and all layers' outer products (scaled to
+    T per token), and every layer's cosine against its full-size reference
+    (whose cost does not depend on T)."""
+    import numpy as np
+
+    import oracle as O
+    thr, blas, cpu_model = _cpu_info()
+    ts = min(tokens, c.T)
+    acts = [a[:ts].view(__import__("torch").int16).cpu().numpy().view(np.uint16) for a in tacts]
+    t0 = time.perf_counter()
+    out = O.output_error(x[:ts], gam, W_U, y[:ts], eps=c.eps, min_rms=c.min_rms, vocab_chunk=8192)
+    Ds = [O.pseudograd(out["g_tilde"], a, scale=1.0 / c.T) for a in acts]
+    t1 = time.perf_counter()
+    tc = 0.0
+    for D, R in zip(Ds, refs):
+        Rh = R.cpu().numpy()
+        tr = time.perf_counter()
+        O.cosine(D, Rh)
+        tc += time.perf_counter() - tr
+    est = (t1 - t0) / ts * c.T + tc
+    return {"value": c.T / est, "unit": "tokens/s", "cores": int(thr), "kind": "oracle",
+            "sample": (f"first {ts} of {c.T} tokens through output error (full V={c.V}) and all {c.L} layers' outer "
+                       f"products ({t1 - t0:.1f} s), then all {c.L} cosines against the full-size references "
+                       f"({tc:.1f} s); full job estimated as per-token time x T + cosines = {est:.1f} s"),
+            "seconds": round(t1 - t0 + tc, 2), "affinity_cpus": len(os.sched_getaffinity(0)),
             "cpu_model": cpu_model, "blas": blas}
 
 
@@ -378,6 +440,191 @@ def bench_e2e(args):
     print(json.dumps(out), flush=True)
 
 
+def _to_dev(dev):
+    import numpy as np
+    import torch
+
+    def t(a):
+        a = np.ascontiguousarray(a)
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+    return t
+
+
+def roofline_entry(dom, dom_stats, work, traffic):
+    """The line's roofline object for kernel `dom`: its algorithmic work over
+    the timed region divided by its summed event time."""
+    if work is None:
+        return None
+    amount, unit, bound = work
+    secs = dom_stats[0] / 1000.0
+    flop = unit == "flop"
+    ach = amount / secs / (1e12 if flop else 1e9)
+    peak = PEAK_BF16_TFLOPS if flop else PEAK_HBM_GBS
+    return {"bound": bound, "achieved": round(ach, 2 if flop else 1), "peak": peak,
+            "unit": "TFLOP/s" if flop else "GB/s", "frac": round(ach / peak, 4), "traffic": traffic,
+            "kernel": dom, "avg_launch_ms": round(dom_stats[0] / dom_stats[1], 4), "launches": dom_stats[1]}
+
+
+KERNEL_TIMING_NOTE = ("per-kernel figures from hipEvent pairs around every launch of one untimed step, on the "
+                      "stream each kernel runs on; microsecond-scale kernels include the launch gap, so their "
+                      "rates are lower bounds (the rocprofv3 durations are in profiles/)")
+
+
+def bench_diag(args, clk_mhz):
+    """Diagnostic workload hot path (eq. cosine; Sec. 2.2-2.3): one step is
+    fpo_output_error over the 16 x 512 calibration tokens and fpo_pseudograd
+    reducing every one of the 36 layers' outer products against a supplied
+    reference gradient R = D + sigma N (sigma so that E[cos] = 1/2) in the
+    GEMM epilogue: dot products, norms and cosines, no dW stored. The
+    activations and the noise are drawn on the device (seeded Philox); D for
+    the reference comes from one untimed fpo_pseudograd call."""
+    import numpy as np
+    import torch
+
+    from paper_2608_14563_amd import api
+    from paper_2608_14563_amd import inputs as I
+    dev = torch.device("cuda:0")
+    c = I.CONFIGS[4]
+    T, d, L = c.T, c.d, c.L
+    log(f"[bench] diagnostic workload {c.name}: T={T} d={d} d_ff={c.d_ff} V={c.V}, all {L} layers; generating inputs")
+    t = _to_dev(dev)
+    x, gam, W_U, y = I.hidden(c), I.gain(c), I.unembedding(c), I.targets(c)
+    tx, tgam, tW, ty = t(x), t(gam), t(W_U), t(y)
+    tacts = [I.device_activation(c, l, dev) for l in range(L)]
+    g_t = torch.empty(T, d, dtype=torch.float32, device=dev)
+    g_lp = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
+    loss = torch.empty(T, dtype=torch.float32, device=dev)
+    ws_oe = api.workspace(api.fpo_output_error_workspace(T, d, c.V, torch.bfloat16), dev)
+    ws_pg = api.workspace(api.fpo_pseudograd_workspace(T, d, c.d_ff, L, torch.bfloat16), dev)
+    ss = torch.empty(L, dtype=torch.float64, device=dev)
+    dot = torch.empty(L, dtype=torch.float64, device=dev)
+    rsq = torch.empty(L, dtype=torch.float64, device=dev)
+    cos = torch.empty(L, dtype=torch.float32, device=dev)
+    # reference gradients: the pseudogradient plus noise (expected cosine 1/2)
+    api.fpo_output_error(tx, tgam, tW, ty, g_t, g_tilde_lp=g_lp, ws=ws_oe, eps=c.eps, min_rms=c.min_rms)
+    refs = [torch.empty(d, c.d_ff, dtype=torch.float32, device=dev) for _ in range(L)]
+    api.fpo_pseudograd(g_lp, tacts, dW3=refs, sumsq=ss, ws=ws_pg)
+    torch.cuda.synchronize()
+    for l in range(L):
+        sigma = float(np.sqrt(3.0) * np.sqrt(float(ss[l])) / np.sqrt(d * c.d_ff))
+        refs[l].add_(I.device_noise(c, l, (d, c.d_ff), dev), alpha=sigma)
+    torch.cuda.synchronize()
+    log("[bench] inputs ready on the device")
+
+    def step(mid=None):
+        api.fpo_output_error(tx, tgam, tW, ty, g_t, g_tilde_lp=g_lp, loss=loss, ws=ws_oe, eps=c.eps,
+                             min_rms=c.min_rms)
+        if mid is not None:
+            mid.record()
+        api.fpo_pseudograd(g_lp, tacts, dW3=None, sumsq=ss, ref=refs, ref_dot=dot, ref_sumsq=rsq, ref_cos=cos,
+                           ws=ws_pg)
+
+    res = timed_run(args, step, lambda k: k not in ("update",), c, clk_mhz, T,
+                    flops_oe=4.0 * T * c.V * d, flops_pg=2.0 * T * d * c.d_ff * L,
+                    work=lambda k, n: kernel_work(k, c, n, None))
+    cos_h = cos.cpu().numpy().astype(np.float64)
+    k = int(round(L / 4))
+    res.update({
+        "metric": "FPO layer-viability diagnostic tokens/sec at 8B shapes (output error + every layer's "
+                  "pseudogradient reduced against a reference gradient); % bf16 MFMA peak",
+        "config": {"workload": f"{c.name}-shaped diagnostic hot path: T={T} tokens (16 x 512), d={d}, "
+                               f"d_ff={c.d_ff}, V={c.V}, all {L} layers scored against R = D + sigma N "
+                               f"(E[cos] = 1/2), bf16 operands / fp32 accumulate, cosines from float64 sums",
+                   "T": T, "d": d, "d_ff": c.d_ff, "V": c.V, "L": L},
+        "cos_per_layer": [round(float(v), 4) for v in cos_h],
+        "cos_summary_last_quarter": round(float(np.mean(cos_h[-k:])), 4),
+    })
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on a sample")
+        res["cpu_baseline"] = cpu_baseline_diag(c, args.cpu_tokens or 96, x, gam, W_U, y, tacts, refs)
+    else:
+        res["cpu_baseline"] = None
+    print(json.dumps(res), flush=True)
+
+
+def timed_run(args, step, on_step_stream, c, clk_mhz, T, flops_oe, flops_pg, work, traffic_name=None):
+    """Warm-up steps, one untimed fully instrumented step (per-kernel times;
+    the dominant kernel on the step's own stream), then args.steps timed steps
+    with the dominant kernel bracketed by events on its launch stream. Returns
+    the bench line's common fields."""
+    lib = prof_lib()
+    for _ in range(args.warmup):
+        step()
+    import torch
+    torch.cuda.synchronize()
+    lib.fpo_prof_reset()
+    lib.fpo_prof_enable(b"")
+    step()
+    torch.cuda.synchronize()
+    lib.fpo_prof_disable()
+    per_kernel = prof_read(lib)
+    lib.fpo_prof_reset()
+    dom = max((k for k in per_kernel if on_step_stream(k)), key=lambda k: per_kernel[k][0])
+    log("[bench] per-kernel ms in one step: " + ", ".join(f"{k}={v[0]:.3f}/{v[1]}" for k, v in sorted(per_kernel.items(), key=lambda kv: -kv[1][0])))
+    lib.fpo_prof_enable(dom.encode())
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    # per-step events: [start, output error done, pseudograd (+ update) done]
+    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    e0.record()
+    for k in range(args.steps):
+        marks[k][0].record()
+        step(marks[k][1])
+        marks[k][2].record()
+    e1.record()
+    torch.cuda.synchronize()
+    lib.fpo_prof_disable()
+    ms_total = e0.elapsed_time(e1)
+    per_step = sorted(m[0].elapsed_time(m[2]) for m in marks)
+    per_oe = sorted(m[0].elapsed_time(m[1]) for m in marks)
+    per_pg = sorted(m[1].elapsed_time(m[2]) for m in marks)
+    dom_stats = prof_read(lib)[dom]
+    lib.fpo_prof_reset()
+    ms_step = ms_total / args.steps
+    tok_s = T / (ms_step / 1000.0)
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step, {tok_s:.0f} tokens/s; dominant kernel {dom}: "
+        f"{dom_stats[0] / dom_stats[1]:.3f} ms avg over {dom_stats[1]} launches")
+    roof = roofline_entry(dom, dom_stats, work(dom, args.steps), profiled_traffic(traffic_name or c.name, dom))
+    kernels = {}
+    for k, (ms, n) in per_kernel.items():
+        wk = work(k, 1)
+        e = {"ms_per_step": round(ms, 4), "launches": n}
+        if wk is not None:
+            amount, unit, bound = wk
+            if unit == "flop":
+                e["tflops"] = round(amount / (ms / 1e3) / 1e12, 1)
+                e["mfma_frac"] = round(amount / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+            else:
+                e["gbs"] = round(amount / (ms / 1e3) / 1e9, 1)
+                e["hbm_frac"] = round(amount / (ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)
+        kernels[k] = e
+    med = lambda v: v[len(v) // 2]  # noqa: E731
+    props = torch.cuda.get_device_properties(0)
+    peak_clk = (props.multi_processor_count * clk_mhz * 1e6 * 4096 / 1e12) if clk_mhz else None
+    substeps = {
+        "step_ms_median": round(med(per_step), 4), "step_ms_min": round(per_step[0], 4),
+        "output_error_ms_median": round(med(per_oe), 4),
+        "pseudograd_update_ms_median": round(med(per_pg), 4),
+        "output_error_mfma_frac": round(flops_oe / (med(per_oe) / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "pseudograd_update_mfma_frac": round(flops_pg / (med(per_pg) / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "mfma_peak_tflops_nominal": PEAK_BF16_TFLOPS,
+        "mfma_peak_tflops_at_max_clock": round(peak_clk, 1) if peak_clk else None,
+        "max_engine_clock_mhz": clk_mhz,
+    }
+    log(f"[bench] median step {substeps['step_ms_median']:.3f} ms (min {substeps['step_ms_min']:.3f}): output error "
+        f"{substeps['output_error_ms_median']:.3f} ms, pseudograd {substeps['pseudograd_update_ms_median']:.3f} ms")
+    return {
+        "metric": METRIC, "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "step_mfma_frac": round((flops_oe + flops_pg) / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "substeps": substeps, "roofline": roof, "kernels": kernels, "kernels_timing": KERNEL_TIMING_NOTE,
+    }
+
+
 def main():
     args = parse()
     if args.calibrate_copy:
@@ -403,25 +650,42 @@ def main():
         sys.exit(1)
     dev = torch.device("cuda:0")
     c = I.CONFIGS[args.config]
-    if c.diag or c.dtype != "bf16":
-        print("bench workloads are the bf16 training configurations 1-3", file=sys.stderr)
+    if c.diag:
+        bench_diag(args, clk_mhz)
+        return
+    if c.dtype != "bf16":
+        print("bench workloads are the bf16 configurations 1-4", file=sys.stderr)
         sys.exit(2)
-    log(f"[bench] workload {c.name}: T={c.T} d={c.d} d_ff={c.d_ff} V={c.V} L={c.L}; generating inputs")
+    full = args.full_mlp
+    if full and (args.post_ffn or args.clip_target == "update"):
+        print("--full-mlp is timed with the final-norm signal and the gradient clip", file=sys.stderr)
+        sys.exit(2)
+    log(f"[bench] workload {c.name}: T={c.T} d={c.d} d_ff={c.d_ff} V={c.V} L={c.L}"
+        f"{' full-MLP' if full else ''}; generating inputs")
     tg0 = time.perf_counter()
     x, gam, W_U, y = I.hidden(c), I.gain(c), I.unembedding(c), I.targets(c)
-    acts = [I.activation(c, l) for l in range(c.L)]
+    if full:
+        caches = [I.mlp_cache(c, l) for l in range(c.L)]
+        acts = [cc[2] for cc in caches]
+        extras = [I.full_mlp_extra(c, l) for l in range(c.L)]
+    else:
+        acts = [I.activation(c, l) for l in range(c.L)]
     Wm_host = [I.master_weight(c, l) for l in range(c.L)]
+    if full:  # masters in the order of the pseudogradient's norms: W3(0..L-1), W1(..), W2(..)
+        Wm_host += [e[1] for e in extras] + [e[2] for e in extras]
     log(f"[bench] inputs generated in {time.perf_counter() - tg0:.1f} s; uploading")
-
-    def t(a):
-        a = np.ascontiguousarray(a)
-        if a.dtype == np.uint16:
-            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
-        return torch.from_numpy(a).to(dev)
-
+    t = _to_dev(dev)
     tx, tgam, tW, ty = t(x), t(gam), t(W_U), t(y)
     tacts = [t(a) for a in acts]
     Wm = [t(w) for w in Wm_host]
+    fkw = {}
+    if full:
+        fkw = dict(W3_init=[w.to(torch.bfloat16) for w in Wm[:c.L]], gate=[t(cc[0]) for cc in caches],
+                   up=[t(cc[1]) for cc in caches], x_in=[t(e[0]) for e in extras],
+                   dW1=[torch.empty(c.d_ff, c.d, dtype=torch.float32, device=dev) for _ in range(c.L)],
+                   dW2=[torch.empty(c.d_ff, c.d, dtype=torch.float32, device=dev) for _ in range(c.L)])
+        host_q, host_u = [cc[0] for cc in caches], [cc[1] for cc in caches]
+        del caches
     pffn = None
     if args.post_ffn:
         pf_host = [I.post_ffn(c, l) for l in range(c.L)]
@@ -442,15 +706,17 @@ def main():
     amax = torch.empty(T, dtype=torch.int32, device=dev)
     bad = torch.empty(1, dtype=torch.int32, device=dev)
     dW = [torch.empty(d, c.d_ff, dtype=torch.float32, device=dev) for _ in range(c.L)]
-    ss = torch.empty(c.L, dtype=torch.float64, device=dev)
+    ss = torch.empty(3 * c.L if full else c.L, dtype=torch.float64, device=dev)
     ws_oe = api.workspace(api.fpo_output_error_workspace(T, d, c.V, torch.bfloat16, args.vocab_chunk), dev)
-    stage = not args.grad_f32
-    ws_pg = api.workspace(api.fpo_pseudograd_workspace(T, d, c.d_ff, c.L, torch.bfloat16,
-                                                       post_ffn=args.post_ffn, grad_bf16=stage), dev)
+    stage_default = not args.grad_f32 and not full
+    ws_pg = api.workspace(max(api.fpo_pseudograd_workspace(T, d, c.d_ff, c.L, torch.bfloat16, full_mlp=full,
+                                                           post_ffn=args.post_ffn, grad_bf16=stg)
+                              for stg in ((False, True) if not full else (False,))), dev)
     if args.post_ffn:
         pffn = api.PostFfn(g_t, pffn_mo, pffn_g, c.eps, c.min_rms)
     torch.cuda.synchronize()
     step_no = [0]
+    stage = [stage_default]
 
     def step(mid=None):
         step_no[0] += 1
@@ -459,125 +725,59 @@ def main():
                              vocab_chunk=args.vocab_chunk)
         if mid is not None:
             mid.record()
-        api.fpo_pseudograd(g_lp, tacts, dW3=None if stage else dW, sumsq=ss, grad_bf16=stage,
+        api.fpo_pseudograd(g_lp, tacts, dW3=None if stage[0] else dW, sumsq=ss, grad_bf16=stage[0],
                            opt=api.OptConfig(kind=1 if adam else 0, lr=c.lr, momentum=0.0 if plain else 0.9,
                                              clip_frac=c.clip_frac, step=step_no[0],
                                              clip_target=1 if args.clip_target == "update" else 0),
-                           W_master=Wm, W_lp=Wlp, state1=s1, state2=s2, W_sumsq=Wsq, ws=ws_pg, post_ffn=pffn)
+                           W_master=Wm, W_lp=Wlp, state1=s1, state2=s2, W_sumsq=Wsq, ws=ws_pg, post_ffn=pffn,
+                           **fkw)
 
-    lib = prof_lib()
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    # one untimed step with every kernel timed, to find the dominant kernel
-    lib.fpo_prof_reset()
-    lib.fpo_prof_enable(b"")
-    step()
-    torch.cuda.synchronize()
-    lib.fpo_prof_disable()
-    per_kernel = prof_read(lib)
-    lib.fpo_prof_reset()
-    # The dominant kernel is taken on the step's own stream: on the overlapped
-    # path (bf16 W3 pseudogradient, gradient clip) every optimizer launch runs
-    # on the library's side stream beside the next layer's outer products, and
-    # at the OLMo-2 shapes the two summed times are within a few percent, so
-    # counting both would let the choice flip from run to run.
-    overlapped = args.clip_target != "update"
-    dom = max((k for k in per_kernel if not (overlapped and k == "update")), key=lambda k: per_kernel[k][0])
-    log("[bench] per-kernel ms in one step: " + ", ".join(f"{k}={v[0]:.3f}/{v[1]}" for k, v in sorted(per_kernel.items(), key=lambda kv: -kv[1][0])))
-    # timed region: K steps, the dominant kernel bracketed by events on its stream
-    lib.fpo_prof_enable(dom.encode())
-    torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    # per-step events: [start, output error done, pseudograd + update done]
-    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
-    e0.record()
-    for k in range(args.steps):
-        marks[k][0].record()
-        step(marks[k][1])
-        marks[k][2].record()
-    e1.record()
-    torch.cuda.synchronize()
-    lib.fpo_prof_disable()
-    ms_total = e0.elapsed_time(e1)
-    per_step = sorted(m[0].elapsed_time(m[2]) for m in marks)
-    per_oe = sorted(m[0].elapsed_time(m[1]) for m in marks)
-    per_pg = sorted(m[1].elapsed_time(m[2]) for m in marks)
-    dom_stats = prof_read(lib)[dom]
-    lib.fpo_prof_reset()
-    ms_step = ms_total / args.steps
-    tok_s = c.T / (ms_step / 1000.0)
-    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step, {tok_s:.0f} tokens/s; dominant kernel {dom}: "
-        f"{dom_stats[0] / dom_stats[1]:.3f} ms avg over {dom_stats[1]} launches")
-    nchunk = None
+    # On the overlapped path (bf16 W3 pseudogradient, gradient clip) every
+    # optimizer launch runs on a side stream beside the next layer's outer
+    # products, and at the OLMo-2 shapes the two summed times are within a few
+    # percent, so the dominant kernel is taken among the step stream's own.
+    overlapped = args.clip_target != "update" and not full
     cu = args.clip_target == "update"
-    w = kernel_work(dom, c, args.steps, nchunk, args.optimizer, args.post_ffn, stage, cu)
-    roof = None
-    traffic = profiled_traffic(c.name, dom)
-    if w is not None:
-        amount, unit, bound = w
-        secs = dom_stats[0] / 1000.0
-        if unit == "flop":
-            ach = amount / secs / 1e12
-            roof = {"bound": bound, "achieved": round(ach, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(ach / PEAK_BF16_TFLOPS, 4), "traffic": traffic, "kernel": dom,
-                    "avg_launch_ms": round(dom_stats[0] / dom_stats[1], 4), "launches": dom_stats[1]}
-        else:
-            ach = amount / secs / 1e9
-            roof = {"bound": bound, "achieved": round(ach, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                    "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": traffic, "kernel": dom,
-                    "avg_launch_ms": round(dom_stats[0] / dom_stats[1], 4), "launches": dom_stats[1]}
-    kernels = {}
-    for k, (ms, n) in per_kernel.items():
-        wk = kernel_work(k, c, 1, nchunk, args.optimizer, args.post_ffn, stage, cu)
-        e = {"ms_per_step": round(ms, 4), "launches": n}
-        if wk is not None:
-            amount, unit, bound = wk
-            if unit == "flop":
-                e["tflops"] = round(amount / (ms / 1e3) / 1e12, 1)
-                e["mfma_frac"] = round(amount / (ms / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)
-            else:
-                e["gbs"] = round(amount / (ms / 1e3) / 1e9, 1)
-                e["hbm_frac"] = round(amount / (ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)
-        kernels[k] = e
+
+    def work(k, n):
+        return kernel_work(k, c, n, None, args.optimizer, args.post_ffn, stage[0], cu, full)
+
     flops_oe = 4.0 * c.T * c.V * c.d
-    flops_pg = 2.0 * c.T * c.d * c.d_ff * c.L
-    flops_step = flops_oe + flops_pg
-    med = lambda v: v[len(v) // 2]  # noqa: E731
-    props = torch.cuda.get_device_properties(0)
-    peak_clk = (props.multi_processor_count * clk_mhz * 1e6 * 4096 / 1e12) if clk_mhz else None
-    substeps = {
-        "step_ms_median": round(med(per_step), 4), "step_ms_min": round(per_step[0], 4),
-        "output_error_ms_median": round(med(per_oe), 4),
-        "pseudograd_update_ms_median": round(med(per_pg), 4),
-        "output_error_mfma_frac": round(flops_oe / (med(per_oe) / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-        "pseudograd_update_mfma_frac": round(flops_pg / (med(per_pg) / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-        "mfma_peak_tflops_nominal": PEAK_BF16_TFLOPS,
-        "mfma_peak_tflops_at_max_clock": round(peak_clk, 1) if peak_clk else None,
-        "max_engine_clock_mhz": clk_mhz,
-    }
-    log(f"[bench] median step {substeps['step_ms_median']:.3f} ms (min {substeps['step_ms_min']:.3f}): output error "
-        f"{substeps['output_error_ms_median']:.3f} ms, pseudograd + update {substeps['pseudograd_update_ms_median']:.3f} ms")
-    res = {
-        "metric": METRIC, "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": f"{c.name}-shaped FPO step: T={c.T} tokens, d={c.d}, d_ff={c.d_ff}, V={c.V}, "
-                               f"{c.L} target layers (W3{', post-FFN norm VJP per layer' if args.post_ffn else ''}), bf16 operands / fp32 "
-                               f"accumulate, pseudogradient handed to the update in {'fp32' if args.grad_f32 else 'bf16'}, "
-                               f"{OPT_NAME[args.optimizer]} "
-                               f"on fp32 masters, 1% relative clip", "T": c.T, "d": c.d, "d_ff": c.d_ff, "V": c.V, "L": c.L,
-                   "optimizer": args.optimizer, "post_ffn_norm": bool(args.post_ffn),
-                   "pseudogradient_staging": "f32" if args.grad_f32 else "bf16", "clip_target": args.clip_target},
-        "step_mfma_frac": round(flops_step / (ms_step / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
-        "substeps": substeps,
-        "roofline": roof,
-        "kernels": kernels,
-    }
+    flops_pg = 2.0 * c.T * c.d * c.d_ff * c.L * (4 if full else 1)
+    res = timed_run(args, step, lambda k: not (overlapped and k == "update"), c, clk_mhz, T, flops_oe, flops_pg,
+                    work)
+    res["config"] = {"workload": f"{c.name}-shaped FPO step: T={c.T} tokens, d={c.d}, d_ff={c.d_ff}, V={c.V}, "
+                                 f"{c.L} target layers ({'W1, W2 and W3 (full-MLP)' if full else 'W3'}"
+                                 f"{', post-FFN norm VJP per layer' if args.post_ffn else ''}), bf16 operands / fp32 "
+                                 f"accumulate, pseudogradient handed to the update in "
+                                 f"{'bf16' if stage_default else 'fp32'}, {OPT_NAME[args.optimizer]} "
+                                 f"on fp32 masters, 1% relative clip", "T": c.T, "d": c.d, "d_ff": c.d_ff,
+                     "V": c.V, "L": c.L, "optimizer": args.optimizer, "post_ffn_norm": bool(args.post_ffn),
+                     "full_mlp": bool(full), "pseudogradient_staging": "bf16" if stage_default else "f32",
+                     "clip_target": args.clip_target}
+    if stage_default and overlapped:
+        # the same step with the pseudogradient handed to the optimizer in fp32
+        stage[0] = False
+        for _ in range(2):
+            step()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ev[0].record()
+        for _ in range(args.steps):
+            step()
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms32 = ev[0].elapsed_time(ev[1]) / args.steps
+        res["substeps"]["grad_f32_ms_per_step"] = round(ms32, 4)
+        res["substeps"]["grad_f32_tokens_per_s"] = round(c.T / (ms32 / 1e3), 1)
+        log(f"[bench] with the pseudogradient handed over in fp32: {ms32:.3f} ms/step")
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle")
-        res["cpu_baseline"] = cpu_baseline(c, args.cpu_tokens, x, gam, W_U, y, acts, Wm_host)
+        fb = None
+        if full:
+            fb = {"W3i": [I.to_storage(w, "bf16") for w in Wm_host[:c.L]], "q": host_q, "u": host_u,
+                  "x_in": [e[0] for e in extras]}
+        res["cpu_baseline"] = cpu_baseline(c, args.cpu_tokens, x, gam, W_U, y, acts, Wm_host, fb)
     else:
         res["cpu_baseline"] = None
     print(json.dumps(res), flush=True)

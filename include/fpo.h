@@ -72,7 +72,7 @@
 extern "C" {
 #endif
 
-#define FPO_ABI_VERSION 6
+#define FPO_ABI_VERSION 7
 
 typedef enum {
   FPO_OK = 0,
@@ -90,7 +90,8 @@ typedef enum {
   FPO_MODE_W3 = 0,
   FPO_MODE_FULL_MLP = 1,
   FPO_MODE_POST_FFN = 2,
-  FPO_MODE_GRAD_BF16 = 4
+  FPO_MODE_GRAD_BF16 = 4,
+  FPO_MODE_PRE_MLP = 8
 } fpo_mode; /* bit flags */
 typedef enum { FPO_OPT_SGD = 0, FPO_OPT_ADAMW = 1 } fpo_opt_kind;
 typedef enum { FPO_CLIP_GRADIENT = 0, FPO_CLIP_UPDATE = 1 } fpo_clip_target;
@@ -115,7 +116,14 @@ typedef struct {
  *          also the gate (W1) and up (W2) signals through the fixed feedback
  *          W3_init (eq. errh); FPO_MODE_POST_FFN (bit 1): compose each layer's
  *          post-FFN RMSNorm VJP (the call's post_ffn argument is then
- *          required; the workspace holds every layer's composed signal)
+ *          required; the workspace holds every layer's composed signal);
+ *          FPO_MODE_PRE_MLP (bit 3): compose each layer's pre-MLP RMSNorm
+ *          VJP after it (pre_mlp argument; see fpo_pre_mlp);
+ *          FPO_MODE_GRAD_BF16 (bit 2, FPO_BF16 W3-only path with the
+ *          fused update): each dW3 tile is rounded once to bf16 (RNE) into
+ *          the workspace and the update reads that (the precision of the
+ *          paper's bf16 einsum); sumsq is then of the rounded values and dW3
+ *          must be NULL
  *   scale  multiplier of the token sum; the paper divides by the token count
  *          (App. A pseudocode), so callers pass 1/T */
 typedef struct {
@@ -229,6 +237,29 @@ typedef struct {
   float min_rms;
 } fpo_post_ffn;
 
+/* Pre-MLP RMSNorm composition (Sec. 3.2 "Pre-MLP RMSNorm (Qwen3, Gemma 3)";
+ * the per-architecture composition appendix and its table). The paper says
+ * these families also compose "the pre-MLP RMSNorm Jacobian at each target
+ * layer" without placing it on the W3 path; the library applies it as the
+ * App. A pseudocode applies the post-FFN norm's: the clamped RMSNorm VJP at
+ * the norm's cached input x (the residual stream entering the layer's MLP
+ * sub-block) and gain, after the post-FFN VJP when both are composed (Gemma 3):
+ *   rho~ = max(sqrt(mean x_t^2 + eps), min_rms); x^ = x_t / rho~;
+ *   c = (1/d) <x^, gamma * v_t>;  g_l,t = (gamma * v_t - c x^) / rho~
+ * with v the fp32 g~ (or its post-FFN composition), rounded once to the
+ * operand dtype, then used for dW3_l and (full-MLP mode) E_l.
+ *   g_tilde  float [T, d]: fpo_output_error's g_tilde (the same pointer as
+ *            post_ffn->g_tilde when both are given)
+ *   x        [host] L pointers to [T, d] (dtype): cached pre-MLP norm inputs
+ *   gamma    [host] L pointers to [d] (dtype): pre-MLP norm gains */
+typedef struct {
+  const float* g_tilde;
+  const void* const* x;
+  const void* const* gamma;
+  float eps;
+  float min_rms;
+} fpo_pre_mlp;
+
 /* Caller-owned side stream and events for fpo_pseudograd's overlapped
  * optimizer path (each layer's update runs on side_stream beside the next
  * layer's outer products). All three are hipStream_t / hipEvent_t handles of
@@ -272,6 +303,9 @@ typedef struct {
  *   post_ffn   required iff desc->mode has FPO_MODE_POST_FFN: compose each
  *              layer's post-FFN norm VJP (see fpo_post_ffn); g_tilde_lp is
  *              then unused and may be NULL
+ *   pre_mlp    required iff desc->mode has FPO_MODE_PRE_MLP: compose each
+ *              layer's pre-MLP norm VJP (see fpo_pre_mlp); g_tilde_lp is
+ *              then unused and may be NULL
  *   opt, upd   both NULL, or both given: the call then also applies
  *              fpo_apply_update to the matrices in `sumsq` order, with the
  *              same result bit for bit as calling it separately
@@ -290,8 +324,8 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
                    const void* const* x_in, float* const* dW3, float* const* dW1,
                    float* const* dW2, double* sumsq, const float* const* ref, double* ref_dot,
                    double* ref_sumsq, float* ref_cos, const fpo_post_ffn* post_ffn,
-                   const fpo_opt* opt, const fpo_update_bufs* upd, const fpo_overlap* overlap,
-                   void* ws, size_t ws_bytes, void* stream);
+                   const fpo_pre_mlp* pre_mlp, const fpo_opt* opt, const fpo_update_bufs* upd,
+                   const fpo_overlap* overlap, void* ws, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
  * fpo_apply_update - relative clip and optimizer step on fp32 masters

@@ -34,8 +34,12 @@ Readings of points the paper leaves open (each listed in the design notes):
   * a cosine with a zero-norm side is 0; the model summary averages the last
     round(N/4) layers;
   * the post-FFN composition uses the fp32 g~ (before any bf16 rounding) and
-    the same eps and min-RMS clamp as the final norm.
-Parity status: every function below is pinned by tests/test_oracle_pins.py,
+    the same eps and min-RMS clamp as the final norm;
+  * the pre-MLP composition (layer_signal) is the same VJP at the pre-MLP
+    norm's input and gain, after the post-FFN one when both apply.
+Parity status: every function below is pinned by tests/test_oracle_pins.py
+(layer_signal's arithmetic by autograd; its placement on the W3 path is a
+reading of the paper, "parity unpinned"),
 the clamp branch of rmsnorm_vjp (rho < min_rms, shared by post_ffn_signal)
 included: it equals the autograd VJP of a plain RMSNorm whose epsilon is
 raised, per row, so that the row's RMS is exactly the floor.
@@ -183,6 +187,32 @@ def post_ffn_signal(g_tilde, mlp_out, gamma_pffn, eps=1e-6, min_rms=0.5):
     """g_l = rmsnorm_vjp(g~, mlp_out_l, gamma_pffn_l) [T, d]: the layer's left
     operand (for the W3 outer product and, in full-MLP mode, E = g_l W3_init)."""
     return rmsnorm_vjp(g_tilde, mlp_out, gamma_pffn, eps, min_rms)
+
+
+# --------------------------------------------------------------------------
+# Pre-MLP RMSNorm composition (Sec. 3.2 "Pre-MLP RMSNorm (Qwen3, Gemma 3)";
+# the per-architecture composition appendix and its summary table): the
+# families that apply it also pass each target layer's signal through the
+# closed-form VJP of that layer's pre-MLP RMSNorm. The paper does not say
+# where on the W3 path it enters; the reading taken here applies it the way
+# the App. A pseudocode applies the post-FFN norm's: rmsnorm_vjp at the norm's
+# cached input (the residual stream entering the MLP sub-block) with its gain
+# and the same eps and min-RMS clamp, after the post-FFN composition when a
+# family has both (Gemma 3), i.e. in the order the chain of norms from the
+# output meets them. Each factor is an exact RMSNorm VJP (pinned by autograd);
+# the placement itself has no value or identity in the paper to pin it
+# ("parity unpinned" for the placement).
+def layer_signal(g_tilde, mlp_out=None, gamma_pffn=None, pre_in=None, gamma_pre=None, eps=1e-6,
+                 min_rms=0.5):
+    """Left operand of a target layer's outer product (and of E = g W3_init):
+    g~, then the post-FFN VJP when mlp_out is given, then the pre-MLP VJP when
+    pre_in is given. [T, d]"""
+    g = _f64(g_tilde)
+    if mlp_out is not None:
+        g = rmsnorm_vjp(g, mlp_out, gamma_pffn, eps, min_rms)
+    if pre_in is not None:
+        g = rmsnorm_vjp(g, pre_in, gamma_pre, eps, min_rms)
+    return g
 
 
 # --------------------------------------------------------------------------

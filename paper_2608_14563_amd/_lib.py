@@ -13,7 +13,7 @@ LIB_PATH = os.path.join(_HERE, "libfpo.so")
 
 FPO_OK, FPO_ERR_NULL, FPO_ERR_SHAPE, FPO_ERR_DTYPE, FPO_ERR_ARG, FPO_ERR_WORKSPACE, FPO_ERR_UNSUPPORTED, FPO_ERR_HIP = range(8)
 FPO_F32, FPO_BF16 = 0, 1
-FPO_MODE_W3, FPO_MODE_FULL_MLP, FPO_MODE_POST_FFN, FPO_MODE_GRAD_BF16 = 0, 1, 2, 4  # bit flags
+FPO_MODE_W3, FPO_MODE_FULL_MLP, FPO_MODE_POST_FFN, FPO_MODE_GRAD_BF16, FPO_MODE_PRE_MLP = 0, 1, 2, 4, 8  # bit flags
 FPO_OPT_SGD, FPO_OPT_ADAMW = 0, 1
 FPO_CLIP_GRADIENT, FPO_CLIP_UPDATE = 0, 1
 
@@ -55,11 +55,16 @@ class PostFfn(C.Structure):
                 ("eps", C.c_float), ("min_rms", C.c_float)]
 
 
+class PreMlp(C.Structure):
+    _fields_ = [("g_tilde", C.c_void_p), ("x", C.POINTER(C.c_void_p)), ("gamma", C.POINTER(C.c_void_p)),
+                ("eps", C.c_float), ("min_rms", C.c_float)]
+
+
 class Overlap(C.Structure):
     _fields_ = [("side_stream", C.c_void_p), ("ready_event", C.c_void_p), ("done_event", C.c_void_p)]
 
 
-ABI_VERSION = 6
+ABI_VERSION = 7
 PP = C.POINTER(C.c_void_p)
 VP = C.c_void_p
 _lib = None
@@ -96,8 +101,8 @@ def load() -> C.CDLL:
     lib.fpo_pseudograd_workspace.argtypes = [C.POINTER(PgDesc)]
     lib.fpo_pseudograd.restype = C.c_int
     lib.fpo_pseudograd.argtypes = [C.POINTER(PgDesc), VP, PP, PP, PP, PP, PP, PP, PP, PP, VP, PP, VP,
-                                   VP, VP, C.POINTER(PostFfn), C.POINTER(Opt), C.POINTER(UpdateBufs),
-                                   C.POINTER(Overlap), VP, C.c_size_t, VP]
+                                   VP, VP, C.POINTER(PostFfn), C.POINTER(PreMlp), C.POINTER(Opt),
+                                   C.POINTER(UpdateBufs), C.POINTER(Overlap), VP, C.c_size_t, VP]
     lib.fpo_apply_update_workspace.restype = C.c_size_t
     lib.fpo_apply_update_workspace.argtypes = [C.c_int64, C.POINTER(C.c_int64)]
     lib.fpo_apply_update.restype = C.c_int

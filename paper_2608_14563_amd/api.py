@@ -17,7 +17,7 @@ import torch
 from . import _lib as L
 
 __all__ = [
-    "fpo_abi_version", "fpo_output_error", "fpo_output_error_workspace", "fpo_pseudograd", "PostFfn",
+    "fpo_abi_version", "fpo_output_error", "fpo_output_error_workspace", "fpo_pseudograd", "PostFfn", "PreMlp",
     "fpo_pseudograd_workspace", "fpo_apply_update", "fpo_apply_update_workspace", "fpo_cosine", "Overlap",
     "fpo_cosine_workspace", "OptConfig", "workspace", "dtype_code",
 ]
@@ -170,14 +170,14 @@ def _upd_bufs(keep: _Keep, W_master, W_lp, state1, state2, W_sumsq, clip_scale, 
 
 
 # --------------------------------------------------------------------- pseudograd
-def _mode(full_mlp: bool, post_ffn: bool, grad_bf16: bool = False) -> int:
+def _mode(full_mlp: bool, post_ffn: bool, grad_bf16: bool = False, pre_mlp: bool = False) -> int:
     return ((L.FPO_MODE_FULL_MLP if full_mlp else L.FPO_MODE_W3) | (L.FPO_MODE_POST_FFN if post_ffn else 0)
-            | (L.FPO_MODE_GRAD_BF16 if grad_bf16 else 0))
+            | (L.FPO_MODE_GRAD_BF16 if grad_bf16 else 0) | (L.FPO_MODE_PRE_MLP if pre_mlp else 0))
 
 
 def fpo_pseudograd_workspace(T, d, d_ff, Lyr, dtype: torch.dtype, full_mlp=False, post_ffn=False,
-                             grad_bf16=False) -> int:
-    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(dtype), _mode(full_mlp, post_ffn, grad_bf16), 1.0)
+                             grad_bf16=False, pre_mlp=False) -> int:
+    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(dtype), _mode(full_mlp, post_ffn, grad_bf16, pre_mlp), 1.0)
     return L.load().fpo_pseudograd_workspace(C.byref(desc))
 
 
@@ -188,6 +188,18 @@ class PostFfn:
     [d] (operand dtype)."""
     g_tilde: torch.Tensor
     mlp_out: Sequence[torch.Tensor]
+    gamma: Sequence[torch.Tensor]
+    eps: float = 1e-6
+    min_rms: float = 0.5
+
+
+@dataclass
+class PreMlp:
+    """Per-layer pre-MLP RMSNorm composition (fpo_pre_mlp): the fp32 g~ [T, d]
+    (the same tensor as PostFfn.g_tilde when both are given), each target
+    layer's cached pre-MLP norm input [T, d] and gain [d] (operand dtype)."""
+    g_tilde: torch.Tensor
+    x: Sequence[torch.Tensor]
     gamma: Sequence[torch.Tensor]
     eps: float = 1e-6
     min_rms: float = 0.5
@@ -214,7 +226,8 @@ def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, 
                    W3_init=None, gate=None, up=None, x_in=None, dW1=None, dW2=None, scale=None,
                    opt: Optional[OptConfig] = None, W_master=None, W_lp=None, state1=None,
                    state2=None, W_sumsq=None, clip_scale=None, ws=None, post_ffn: Optional[PostFfn] = None,
-                   grad_bf16: bool = False, ref_cos=None, overlap: Optional[Overlap] = None):
+                   grad_bf16: bool = False, ref_cos=None, overlap: Optional[Overlap] = None,
+                   pre_mlp: Optional[PreMlp] = None):
     """g_tilde_lp may be None when post_ffn is given (its left operands are
     then formed per layer from post_ffn.g_tilde). grad_bf16 (FPO_MODE_GRAD_BF16,
     fused update only, dW3 None): the pseudogradient is staged in bf16 in the
@@ -224,11 +237,12 @@ def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, 
     op = a[0].dtype
     dev = a[0].device
     T = a[0].shape[0]
-    d = (g_tilde_lp if g_tilde_lp is not None else post_ffn.g_tilde).shape[1]
+    d = (g_tilde_lp if g_tilde_lp is not None else (post_ffn or pre_mlp).g_tilde).shape[1]
     Lyr = len(a)
     d_ff = a[0].shape[1]
     full = W3_init is not None
-    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(op), _mode(full, post_ffn is not None, grad_bf16),
+    desc = L.PgDesc(T, d, d_ff, Lyr, dtype_code(op),
+                    _mode(full, post_ffn is not None, grad_bf16, pre_mlp is not None),
                     (1.0 / T) if scale is None else scale)
     lib = L.load()
     if ws is None:
@@ -240,6 +254,11 @@ def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, 
     ub = (_upd_bufs(k, W_master, W_lp, state1, state2, W_sumsq, clip_scale, op, numels, dev)
           if opt is not None else None)
     ov = overlap.c() if overlap is not None else None
+    pm = None
+    if pre_mlp is not None:
+        pm = L.PreMlp(_p(pre_mlp.g_tilde, F32, (T, d), dev, "pre_mlp.g_tilde"),
+                      k.arr(pre_mlp.x, op, (T, d), dev, Lyr, "pre_mlp.x"),
+                      k.arr(pre_mlp.gamma, op, (d,), dev, Lyr, "pre_mlp.gamma"), pre_mlp.eps, pre_mlp.min_rms)
     pf = None
     if post_ffn is not None:
         pf = L.PostFfn(_p(post_ffn.g_tilde, F32, (T, d), dev, "post_ffn.g_tilde"),
@@ -253,7 +272,7 @@ def fpo_pseudograd(g_tilde_lp, a, dW3=None, sumsq=None, ref=None, ref_dot=None, 
         k.arr(dW2, F32, (d_ff, d), dev, Lyr, "dW2"), _p(sumsq, F64, nm, dev, "sumsq"),
         k.arr(ref, F32, (d, d_ff), dev, Lyr, "ref"), _p(ref_dot, F64, Lyr, dev, "ref_dot"),
         _p(ref_sumsq, F64, Lyr, dev, "ref_sumsq"), _p(ref_cos, F32, Lyr, dev, "ref_cos"),
-        C.byref(pf) if pf is not None else None,
+        C.byref(pf) if pf is not None else None, C.byref(pm) if pm is not None else None,
         C.byref(o) if o is not None else None, C.byref(ub) if ub is not None else None,
         C.byref(ov) if ov is not None else None, _p(ws, None, None, dev, "ws"), _nbytes(ws), _stream(dev)))
     return ws

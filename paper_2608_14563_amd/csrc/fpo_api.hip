@@ -247,13 +247,13 @@ size_t carve_pg(const fpo_pg_desc& d, const PgPlan& p, void* ws, fpo::PgLaunch* 
                 double** upd_part, double** upd_dsq = nullptr) {
   const int64_t esz = d.dtype == FPO_BF16 ? 2 : 4;
   const bool full = (d.mode & FPO_MODE_FULL_MLP) != 0;
-  const bool pffn = (d.mode & FPO_MODE_POST_FFN) != 0;
+  const bool chain = (d.mode & (FPO_MODE_POST_FFN | FPO_MODE_PRE_MLP)) != 0;
   Carver c(ws);
-  // token-contiguous left operand(s): shared, or one per layer (post-FFN)
-  void* gT = c.take<char>((pffn ? d.L : 1) * d.d * p.Tp * esz);
-  // post-FFN + full-MLP: each layer's signal row-major too (error GEMM operand)
-  void* grow = (pffn && full) ? c.take<char>(d.L * d.T * d.d * esz) : nullptr;
-  float* pstats = pffn ? c.take<float>(2 * d.T) : nullptr;  // per-token norm statistics
+  // token-contiguous left operand(s): shared, or one per layer (norm chain)
+  void* gT = c.take<char>((chain ? d.L : 1) * d.d * p.Tp * esz);
+  // norm chain + full-MLP: each layer's signal row-major too (error GEMM operand)
+  void* grow = (chain && full) ? c.take<char>(d.L * d.T * d.d * esz) : nullptr;
+  float* pstats = chain ? c.take<float>(4 * d.T) : nullptr;  // per-token norm-chain statistics
   void* dq = full ? c.take<char>(d.d_ff * p.Tp * esz) : nullptr;
   void* du = full ? c.take<char>(d.d_ff * p.Tp * esz) : nullptr;
   double* part = c.take<double>(std::max<int64_t>(d.L, 2) * p.ntiles * 3);
@@ -268,7 +268,7 @@ size_t carve_pg(const fpo_pg_desc& d, const PgPlan& p, void* ws, fpo::PgLaunch* 
   if (L) {
     L->gT = gT;
     L->g_row = grow;
-    L->pffn_stats = pstats;
+    L->chain_stats = pstats;
     L->dq_T = dq;
     L->du_T = du;
     L->part = part;
@@ -282,7 +282,7 @@ int check_pg_desc(const fpo_pg_desc* d) {
   if (!d) return fail(FPO_ERR_NULL, "fpo_pseudograd: desc is NULL");
   if (d->dtype != FPO_F32 && d->dtype != FPO_BF16)
     return fail(FPO_ERR_DTYPE, "fpo_pseudograd: unknown dtype %d", (int)d->dtype);
-  if (d->mode < 0 || d->mode > (FPO_MODE_FULL_MLP | FPO_MODE_POST_FFN | FPO_MODE_GRAD_BF16))
+  if (d->mode < 0 || d->mode > (FPO_MODE_FULL_MLP | FPO_MODE_POST_FFN | FPO_MODE_GRAD_BF16 | FPO_MODE_PRE_MLP))
     return fail(FPO_ERR_ARG, "fpo_pseudograd: unknown mode %d", (int)d->mode);
   if ((d->mode & FPO_MODE_GRAD_BF16) && (d->dtype != FPO_BF16 || (d->mode & FPO_MODE_FULL_MLP)))
     return fail(FPO_ERR_UNSUPPORTED,
@@ -495,18 +495,37 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
                    const void* const* W3_init, const void* const* gate, const void* const* up,
                    const void* const* x_in, float* const* dW3, float* const* dW1, float* const* dW2,
                    double* sumsq, const float* const* ref, double* ref_dot, double* ref_sumsq,
-                   float* ref_cos, const fpo_post_ffn* post_ffn, const fpo_opt* opt,
-                   const fpo_update_bufs* upd, const fpo_overlap* overlap, void* ws, size_t ws_bytes,
-                   void* stream) {
+                   float* ref_cos, const fpo_post_ffn* post_ffn, const fpo_pre_mlp* pre_mlp,
+                   const fpo_opt* opt, const fpo_update_bufs* upd, const fpo_overlap* overlap, void* ws,
+                   size_t ws_bytes, void* stream) {
   if (int e = check_pg_desc(desc)) return e;
   const bool full = (desc->mode & FPO_MODE_FULL_MLP) != 0;
   const bool pffn = (desc->mode & FPO_MODE_POST_FFN) != 0;
+  const bool pre = (desc->mode & FPO_MODE_PRE_MLP) != 0;
   const int L = (int)desc->L;
   if (!a) return fail(FPO_ERR_NULL, "fpo_pseudograd: a is required");
   if (pffn != (post_ffn != nullptr))
     return fail(FPO_ERR_ARG, "fpo_pseudograd: post_ffn must be given exactly when mode has FPO_MODE_POST_FFN");
-  if (!g_tilde_lp && !post_ffn)
-    return fail(FPO_ERR_NULL, "fpo_pseudograd: g_tilde_lp is required (unless post_ffn is given)");
+  if (pre != (pre_mlp != nullptr))
+    return fail(FPO_ERR_ARG, "fpo_pseudograd: pre_mlp must be given exactly when mode has FPO_MODE_PRE_MLP");
+  if (!g_tilde_lp && !post_ffn && !pre_mlp)
+    return fail(FPO_ERR_NULL, "fpo_pseudograd: g_tilde_lp is required (unless post_ffn or pre_mlp is given)");
+  if (pre_mlp) {
+    if (!pre_mlp->g_tilde || !pre_mlp->x || !pre_mlp->gamma)
+      return fail(FPO_ERR_NULL, "fpo_pseudograd: pre_mlp needs g_tilde, x and gamma");
+    if (post_ffn && post_ffn->g_tilde != pre_mlp->g_tilde)
+      return fail(FPO_ERR_ARG, "fpo_pseudograd: post_ffn and pre_mlp must name the same g_tilde");
+    if (!aligned(pre_mlp->g_tilde, 16)) return fail(FPO_ERR_ARG, "fpo_pseudograd: pre_mlp->g_tilde not aligned");
+    if (!(pre_mlp->eps >= 0.f) || !std::isfinite(pre_mlp->eps) || !(pre_mlp->min_rms >= 0.f) ||
+        !std::isfinite(pre_mlp->min_rms))
+      return fail(FPO_ERR_ARG, "fpo_pseudograd: pre_mlp eps and min_rms must be finite and >= 0");
+    for (int l = 0; l < L; ++l) {
+      if (!pre_mlp->x[l] || !pre_mlp->gamma[l])
+        return fail(FPO_ERR_NULL, "fpo_pseudograd: pre_mlp buffers of layer %d are NULL", l);
+      if (!aligned(pre_mlp->x[l], 16) || !aligned(pre_mlp->gamma[l], 16))
+        return fail(FPO_ERR_ARG, "fpo_pseudograd: pre_mlp buffers of layer %d not 16-byte aligned", l);
+    }
+  }
   if (post_ffn) {
     if (!post_ffn->g_tilde || !post_ffn->mlp_out || !post_ffn->gamma)
       return fail(FPO_ERR_NULL, "fpo_pseudograd: post_ffn needs g_tilde, mlp_out and gamma");
@@ -579,6 +598,16 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
     for (int l = 0; l < L; ++l) {
       P.mlp_out[l] = post_ffn->mlp_out[l];
       P.gamma_pffn[l] = post_ffn->gamma[l];
+    }
+  }
+  if (pre_mlp) {
+    P.pre = true;
+    P.g_f32 = pre_mlp->g_tilde;
+    P.pre_eps = pre_mlp->eps;
+    P.pre_min_rms = pre_mlp->min_rms;
+    for (int l = 0; l < L; ++l) {
+      P.pre_in[l] = pre_mlp->x[l];
+      P.gamma_pre[l] = pre_mlp->gamma[l];
     }
   }
   P.sumsq = sumsq;

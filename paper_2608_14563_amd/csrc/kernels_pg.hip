@@ -23,44 +23,75 @@
 
 namespace fpo {
 
-// Per-token statistics of the post-FFN norm composition (one workgroup per
-// token): irt = 1 / max(sqrt(mean x^2 + eps), min_rms) and
-// c = (1/d) <x * irt, gamma * g>, with x the cached MLP output, gamma the
-// layer's post-FFN gain and g the fp32 signal g~.
-template <typename T>
-__global__ __launch_bounds__(256) void pffn_stats_kernel(int d, const float* __restrict__ g,
-                                                         const T* __restrict__ x,
-                                                         const T* __restrict__ gamma, float eps,
-                                                         float min_rms, float2* __restrict__ stats) {
+// Per-token statistics of a layer's norm chain (one workgroup per token),
+// with g the fp32 signal g~:
+//   post-FFN (POST): irt1 = 1 / max(sqrt(mean x1^2 + eps1), min_rms1),
+//                    c1 = (1/d) <x1 irt1, gamma1 g>;  v1 = (gamma1 g - c1 x1 irt1) irt1
+//   pre-MLP (PRE):   irt2, c2 the same with x2, gamma2 and v1 (g without POST)
+// where x1 is the cached MLP output and x2 the cached pre-MLP norm input.
+// stats[t] = {irt1, c1, irt2, c2}; signal_transpose forms the composed signal
+// from them elementwise with the same float expressions.
+template <typename T, bool POST, bool PRE>
+__global__ __launch_bounds__(256) void chain_stats_kernel(int d, const float* __restrict__ g,
+                                                          const T* __restrict__ x1,
+                                                          const T* __restrict__ gamma1, float eps1,
+                                                          float mr1, const T* __restrict__ x2,
+                                                          const T* __restrict__ gamma2, float eps2,
+                                                          float mr2, float4* __restrict__ stats) {
   __shared__ float red[16];
   const int64_t row = blockIdx.x;
   const float* gr = g + row * d;
-  const T* xr = x + row * d;
-  float ss = 0.f, cd = 0.f;
-  for (int k = threadIdx.x * 4; k < d; k += 1024) {
-    const f32x4 xv = ld4(xr, k), gm = ld4(gamma, k), gv = *reinterpret_cast<const f32x4*>(gr + k);
-    ss += xv.x * xv.x + xv.y * xv.y + xv.z * xv.z + xv.w * xv.w;
-    cd += xv.x * gm.x * gv.x + xv.y * gm.y * gv.y + xv.z * gm.z * gv.z + xv.w * gm.w * gv.w;
+  float irt1 = 1.f, c1 = 0.f, irt2 = 1.f, c2 = 0.f;
+  if constexpr (POST) {
+    const T* xr = x1 + row * d;
+    float ss = 0.f, cd = 0.f;
+    for (int k = threadIdx.x * 4; k < d; k += 1024) {
+      const f32x4 xv = ld4(xr, k), gm = ld4(gamma1, k), gv = *reinterpret_cast<const f32x4*>(gr + k);
+      ss += xv.x * xv.x + xv.y * xv.y + xv.z * xv.z + xv.w * xv.w;
+      cd += xv.x * gm.x * gv.x + xv.y * gm.y * gv.y + xv.z * gm.z * gv.z + xv.w * gm.w * gv.w;
+    }
+    ss = block_sum(ss, red);
+    cd = block_sum(cd, red);
+    irt1 = 1.0f / fmaxf(sqrtf(ss / (float)d + eps1), mr1);
+    c1 = cd * irt1 / (float)d;
   }
-  ss = block_sum(ss, red);
-  cd = block_sum(cd, red);
-  if (threadIdx.x == 0) {
-    const float irt = 1.0f / fmaxf(sqrtf(ss / (float)d + eps), min_rms);
-    stats[row] = float2{irt, cd * irt / (float)d};
+  if constexpr (PRE) {
+    const T* x1r = x1 + row * d;
+    const T* xr = x2 + row * d;
+    float ss = 0.f, cd = 0.f;
+    for (int k = threadIdx.x * 4; k < d; k += 1024) {
+      f32x4 v = *reinterpret_cast<const f32x4*>(gr + k);
+      if constexpr (POST) {
+        const f32x4 xv = ld4(x1r, k), gm = ld4(gamma1, k);
+        v.x = (gm.x * v.x - c1 * xv.x * irt1) * irt1;
+        v.y = (gm.y * v.y - c1 * xv.y * irt1) * irt1;
+        v.z = (gm.z * v.z - c1 * xv.z * irt1) * irt1;
+        v.w = (gm.w * v.w - c1 * xv.w * irt1) * irt1;
+      }
+      const f32x4 xv = ld4(xr, k), gm = ld4(gamma2, k);
+      ss += xv.x * xv.x + xv.y * xv.y + xv.z * xv.z + xv.w * xv.w;
+      cd += xv.x * gm.x * v.x + xv.y * gm.y * v.y + xv.z * gm.z * v.z + xv.w * gm.w * v.w;
+    }
+    ss = block_sum(ss, red);
+    cd = block_sum(cd, red);
+    irt2 = 1.0f / fmaxf(sqrtf(ss / (float)d + eps2), mr2);
+    c2 = cd * irt2 / (float)d;
   }
+  if (threadIdx.x == 0) stats[row] = float4{irt1, c1, irt2, c2};
 }
 
 // The token-contiguous copy of a layer's left operand: dst [C, ldd] with
 // dst[c, r] = v(r, c) for r < R and 0 for R <= r < Rp, where v is src[r, c]
-// (shared signal) or, for the post-FFN composition, the clamped VJP
-//   v = (gamma_c g[r, c] - c_r x[r, c] irt_r) irt_r
-// in the operand dtype (also stored row-major to row_out when given). 64 x 64
-// tiles through LDS, 16-byte loads and 8- / 16-byte stores.
-template <typename T, bool PFFN>
+// (the shared signal, CHAIN == 0) or the fp32 src passed through the layer's
+// norm chain (CHAIN bit 0: post-FFN VJP, bit 1: pre-MLP VJP, in that order;
+// statistics from chain_stats_kernel), in the operand dtype (also stored
+// row-major to row_out when given). 64 x 64 tiles through LDS, 16-byte loads
+// and 8- / 16-byte stores.
+template <typename T, int CHAIN>
 __global__ __launch_bounds__(256) void signal_transpose_kernel(
-    const void* __restrict__ src, const T* __restrict__ x, const T* __restrict__ gamma,
-    const float2* __restrict__ stats, int64_t R, int64_t C, T* __restrict__ dst, int64_t ldd,
-    int64_t Rp, T* __restrict__ row_out) {
+    const void* __restrict__ src, const T* __restrict__ x1, const T* __restrict__ gamma1,
+    const T* __restrict__ x2, const T* __restrict__ gamma2, const float4* __restrict__ stats, int64_t R,
+    int64_t C, T* __restrict__ dst, int64_t ldd, int64_t Rp, T* __restrict__ row_out) {
   __shared__ float tile[64][65];
   const int64_t r0 = (int64_t)blockIdx.x * 64, c0 = (int64_t)blockIdx.y * 64;
   // 64 rows x 16 column quads
@@ -70,14 +101,23 @@ __global__ __launch_bounds__(256) void signal_transpose_kernel(
     const int64_t r = r0 + rr, c = c0 + cq;
     f32x4 v = {0.f, 0.f, 0.f, 0.f};
     if (r < R && c < C) {  // C % 8 == 0: a quad is all in or all out
-      if constexpr (PFFN) {
-        const f32x4 gv = *reinterpret_cast<const f32x4*>((const float*)src + r * C + c);
-        const f32x4 xv = ld4(x, r * C + c), gm = ld4(gamma, c);
-        const float2 st = stats[r];
-        v.x = (gm.x * gv.x - st.y * xv.x * st.x) * st.x;
-        v.y = (gm.y * gv.y - st.y * xv.y * st.x) * st.x;
-        v.z = (gm.z * gv.z - st.y * xv.z * st.x) * st.x;
-        v.w = (gm.w * gv.w - st.y * xv.w * st.x) * st.x;
+      if constexpr (CHAIN != 0) {
+        v = *reinterpret_cast<const f32x4*>((const float*)src + r * C + c);
+        const float4 st = stats[r];
+        if constexpr (CHAIN & 1) {
+          const f32x4 xv = ld4(x1, r * C + c), gm = ld4(gamma1, c);
+          v.x = (gm.x * v.x - st.y * xv.x * st.x) * st.x;
+          v.y = (gm.y * v.y - st.y * xv.y * st.x) * st.x;
+          v.z = (gm.z * v.z - st.y * xv.z * st.x) * st.x;
+          v.w = (gm.w * v.w - st.y * xv.w * st.x) * st.x;
+        }
+        if constexpr (CHAIN & 2) {
+          const f32x4 xv = ld4(x2, r * C + c), gm = ld4(gamma2, c);
+          v.x = (gm.x * v.x - st.w * xv.x * st.z) * st.z;
+          v.y = (gm.y * v.y - st.w * xv.y * st.z) * st.z;
+          v.z = (gm.z * v.z - st.w * xv.z * st.z) * st.z;
+          v.w = (gm.w * v.w - st.w * xv.w * st.z) * st.z;
+        }
         if (row_out) st4(row_out, r * C + c, v);
       } else {
         v = ld4((const T*)src, r * C + c);
@@ -400,42 +440,53 @@ int64_t pseudograd_tiles(bool bf16, int64_t M, int64_t N) {
 
 // Left operands of every layer, formed before any outer product (while HBM is
 // otherwise idle): the shared signal's token-contiguous copy in a.gT, or, with
-// the post-FFN composition, each layer's composed signal in a.gT + l * d * Tp
-// (and row-major in a.g_row + l * T * d for the full-MLP error GEMM).
-template <typename T>
-static hipError_t prepare_signals(const PgLaunch& a, hipStream_t st) {
-  const dim3 grid((unsigned)(a.Tp / 64), (unsigned)((a.d + 63) / 64));
-  if (!a.pffn) {
-    FPO_LAUNCH("signal_transpose", st,
-               signal_transpose_kernel<T, false><<<grid, dim3(256), 0, st>>>(
-        a.g_lp, nullptr, nullptr, nullptr, a.T, a.d, (T*)a.gT, a.Tp, a.Tp, nullptr));
-    FPO_CHECK_LAUNCH();
-    return hipSuccess;
-  }
+// a norm chain (post-FFN and / or pre-MLP composition), each layer's composed
+// signal in a.gT + l * d * Tp (and row-major in a.g_row + l * T * d for the
+// full-MLP error GEMM).
+template <typename T, bool POST, bool PRE>
+static hipError_t prepare_chain(const PgLaunch& a, hipStream_t st, dim3 grid) {
+  constexpr int CHAIN = (POST ? 1 : 0) | (PRE ? 2 : 0);
   for (int l = 0; l < a.L; ++l) {
-    FPO_LAUNCH("pffn_stats", st,
-               pffn_stats_kernel<T><<<dim3((unsigned)a.T), dim3(256), 0, st>>>(
-        (int)a.d, a.g_f32, (const T*)a.mlp_out[l], (const T*)a.gamma_pffn[l], a.pffn_eps, a.pffn_min_rms,
-        (float2*)a.pffn_stats));
+    const T* x1 = POST ? (const T*)a.mlp_out[l] : nullptr;
+    const T* g1 = POST ? (const T*)a.gamma_pffn[l] : nullptr;
+    const T* x2 = PRE ? (const T*)a.pre_in[l] : nullptr;
+    const T* g2 = PRE ? (const T*)a.gamma_pre[l] : nullptr;
+    FPO_LAUNCH("chain_stats", st,
+               chain_stats_kernel<T, POST, PRE><<<dim3((unsigned)a.T), dim3(256), 0, st>>>(
+        (int)a.d, a.g_f32, x1, g1, a.pffn_eps, a.pffn_min_rms, x2, g2, a.pre_eps, a.pre_min_rms,
+        (float4*)a.chain_stats));
     FPO_CHECK_LAUNCH();
     T* row = a.full_mlp ? (T*)a.g_row + (int64_t)l * a.T * a.d : nullptr;
     FPO_LAUNCH("signal_transpose", st,
-               signal_transpose_kernel<T, true><<<grid, dim3(256), 0, st>>>(
-        a.g_f32, (const T*)a.mlp_out[l], (const T*)a.gamma_pffn[l], (const float2*)a.pffn_stats, a.T, a.d,
-        (T*)a.gT + (int64_t)l * a.d * a.Tp, a.Tp, a.Tp, row));
+               signal_transpose_kernel<T, CHAIN><<<grid, dim3(256), 0, st>>>(
+        a.g_f32, x1, g1, x2, g2, (const float4*)a.chain_stats, a.T, a.d, (T*)a.gT + (int64_t)l * a.d * a.Tp,
+        a.Tp, a.Tp, row));
     FPO_CHECK_LAUNCH();
   }
+  return hipSuccess;
+}
+
+template <typename T>
+static hipError_t prepare_signals(const PgLaunch& a, hipStream_t st) {
+  const dim3 grid((unsigned)(a.Tp / 64), (unsigned)((a.d + 63) / 64));
+  if (a.pffn && a.pre) return prepare_chain<T, true, true>(a, st, grid);
+  if (a.pffn) return prepare_chain<T, true, false>(a, st, grid);
+  if (a.pre) return prepare_chain<T, false, true>(a, st, grid);
+  FPO_LAUNCH("signal_transpose", st,
+             signal_transpose_kernel<T, 0><<<grid, dim3(256), 0, st>>>(
+      a.g_lp, nullptr, nullptr, nullptr, nullptr, nullptr, a.T, a.d, (T*)a.gT, a.Tp, a.Tp, nullptr));
+  FPO_CHECK_LAUNCH();
   return hipSuccess;
 }
 
 // Layer l's token-contiguous left operand [d, Tp] and its row-major form [T, d].
 template <typename T>
 static const T* signal_T(const PgLaunch& a, int l) {
-  return (const T*)a.gT + (a.pffn ? (int64_t)l * a.d * a.Tp : 0);
+  return (const T*)a.gT + ((a.pffn || a.pre) ? (int64_t)l * a.d * a.Tp : 0);
 }
 template <typename T>
 static const T* signal_rows(const PgLaunch& a, int l) {
-  return a.pffn ? (const T*)a.g_row + (int64_t)l * a.T * a.d : (const T*)a.g_lp;
+  return (a.pffn || a.pre) ? (const T*)a.g_row + (int64_t)l * a.T * a.d : (const T*)a.g_lp;
 }
 
 template <class E>

@@ -73,12 +73,17 @@ struct PgLaunch {
   float* dW1[kMaxMats];
   float* dW2[kMaxMats];
   const float* ref[kMaxMats];
-  // post-FFN composition: per layer, g_l = VJP(g~ fp32; mlp_out_l, gamma_l)
+  // norm chain: per layer, g_l = VJP_pre(VJP_post(g~ fp32; mlp_out_l, gamma_l); pre_in_l, gamma_pre_l),
+  // either factor optional
   bool pffn;
   const float* g_f32;               // [T, d]
   const void* mlp_out[kMaxMats];    // [T, d]
   const void* gamma_pffn[kMaxMats]; // [d]
   float pffn_eps, pffn_min_rms;
+  bool pre;
+  const void* pre_in[kMaxMats];     // [T, d] cached pre-MLP norm input
+  const void* gamma_pre[kMaxMats];  // [d]
+  float pre_eps, pre_min_rms;
   double* sumsq;                    // [n_mats] or null
   double* ref_dot;
   double* ref_sumsq;
@@ -86,7 +91,7 @@ struct PgLaunch {
   // workspace
   void* gT;                         // [d, Tp] transposed signal
   void* g_row;                      // [T, d] per-layer signal (post-FFN composition, full-MLP)
-  float* pffn_stats;                // [T, 2] its per-token norm statistics
+  float* chain_stats;               // [T, 4] per-token norm-chain statistics
   void* dq_T;                       // [d_ff, Tp] full-MLP gate error (transposed)
   void* du_T;                       // [d_ff, Tp] full-MLP up error (transposed)
   double* part;                     // per-tile partials

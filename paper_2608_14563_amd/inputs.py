@@ -40,7 +40,7 @@ BLOCK = 1 << 20
 
 # tensor ids inside the spawn key
 T_X, T_GAMMA, T_WU, T_TARGETS, T_Q, T_U, T_W, T_OUTLIER, T_REFNOISE, T_XIN, T_W1, T_W2, T_G, T_STATE, T_MISC, T_REF1, \
-    T_PFFN, T_MODEL = range(18)
+    T_PFFN, T_MODEL, T_PRE = range(19)
 
 
 @dataclass(frozen=True)
@@ -244,12 +244,62 @@ def post_ffn(cfg: Config, layer: int):
     return to_storage(out, cfg.dtype), to_storage(gam, cfg.dtype)
 
 
+def pre_mlp(cfg: Config, layer: int):
+    """Cached pre-MLP norm input (the residual stream entering the layer's MLP
+    sub-block) [T, d] and the layer's pre-MLP norm gain [d], storage dtype.
+    The paper prints no statistics for this norm; the stand-in follows the
+    usual growth of the residual stream with depth: per-token RMS around a
+    layer mean rising from 2 (first target layer) to 8 (last), log-normal
+    spread (sigma 0.3), with 1% of tokens (token 0 included) at RMS 0.3 so the
+    min-RMS clamp is active; gain 1 + N(0, 0.1^2) like the final norm's."""
+    frac = layer / max(1, cfg.L - 1)
+    mean_rms = 2.0 + 6.0 * frac
+    r = mean_rms * np.exp(0.3 * normal(cfg.cid, T_PRE, 4 * layer, cfg.T))
+    k = max(1, int(round(0.01 * cfg.T)))
+    idx = np.unique(np.concatenate([[0], _rng(cfg.cid, T_PRE, 4 * layer + 1, 0).choice(cfg.T, k, replace=False)]))
+    r[idx] = 0.3
+    z = normal(cfg.cid, T_PRE, 4 * layer + 2, cfg.T * cfg.d).reshape(cfg.T, cfg.d)
+    x = (z * r[:, None].astype(np.float32)).astype(np.float32)
+    gam = normal(cfg.cid, T_PRE, 4 * layer + 3, cfg.d, std=0.1, mean=1.0)
+    return to_storage(x, cfg.dtype), to_storage(gam, cfg.dtype)
+
+
 def rank1_reference(cfg: Config, layer: int = 0):
     """u [d], v [d_ff] float32 N(0,1): factors of a rank-1 reference gradient
     R = u v^T, whose inner product with any outer product has a closed form."""
     u = normal(cfg.cid, T_REF1, 2 * layer, cfg.d)
     v = normal(cfg.cid, T_REF1, 2 * layer + 1, cfg.d_ff)
     return u, v
+
+
+def _device_generator(cfg: Config, tensor: int, layer: int, device):
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(((ENTROPY * 64 + cfg.cid) * 64 + tensor) * 4096 + layer)
+    return g
+
+
+def device_activation(cfg: Config, layer: int, device):
+    """Cached MLP activation a = SiLU(q) * u [T, d_ff] (bf16) drawn on the
+    device from torch's seeded Philox stream of (cfg, layer): q, u ~ N(0,1)
+    rounded to bf16 first, as in mlp_cache. For workloads whose activations
+    take too long to draw on the host (the diagnostic's 36 x 8192 x 12288);
+    the values differ from mlp_cache's (another generator), the distribution
+    does not."""
+    import torch
+    g = _device_generator(cfg, T_Q, layer, device)
+    q = torch.randn(cfg.T, cfg.d_ff, generator=g, device=device).to(torch.bfloat16).float()
+    u = torch.randn(cfg.T, cfg.d_ff, generator=g, device=device).to(torch.bfloat16).float()
+    a = (q / (1.0 + torch.exp(-q)) * u).to(torch.bfloat16)
+    del q, u
+    return a
+
+
+def device_noise(cfg: Config, layer: int, shape, device):
+    """N(0,1) float32 noise of `shape` drawn on the device (seeded Philox
+    stream of (cfg, layer)): the diagnostic reference's noise term."""
+    import torch
+    return torch.randn(*shape, generator=_device_generator(cfg, T_REFNOISE, layer, device), device=device)
 
 
 def synthetic_signal(cfg: Config, std: float = 0.02, tensor: int = T_G) -> np.ndarray:

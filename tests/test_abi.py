@@ -53,7 +53,7 @@ def test_library_exports_every_header_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert lib.fpo_abi_version() == 6 == L.ABI_VERSION
+    assert lib.fpo_abi_version() == 7 == L.ABI_VERSION
 
 
 def oe(T=128, d=256, V=4096, dtype=L.FPO_BF16, eps=1e-6, min_rms=0.5, chunk=0):
@@ -179,9 +179,9 @@ def test_pseudograd_validation(lib):
     dw, kd = arr([FAKE, FAKE])
 
     def call(desc, A=a, dW3=dw, ref=None, ref_dot=None, opt=None, upd=None, ws_bytes=1 << 40, g=FAKE, pf=None,
-             ref_cos=None, ov=None):
+             ref_cos=None, ov=None, pm=None):
         return lib.fpo_pseudograd(C.byref(desc) if desc is not None else None, g, A, None, None, None, None,
-                                  dW3, None, None, None, ref, ref_dot, None, ref_cos, pf, opt, upd, ov, FAKE,
+                                  dW3, None, None, None, ref, ref_dot, None, ref_cos, pf, pm, opt, upd, ov, FAKE,
                                   ws_bytes, None)
 
     good = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_W3, 1 / 128)
@@ -220,7 +220,20 @@ def test_pseudograd_validation(lib):
     assert call(pmode, g=None, pf=pf, ws_bytes=16) == L.FPO_ERR_WORKSPACE
     assert call(pmode, g=None) == L.FPO_ERR_ARG          # mode without the argument
     assert call(good, pf=pf) == L.FPO_ERR_ARG            # argument without the mode
-    assert call(L.PgDesc(128, 256, 688, 2, 1, 8, 1.0)) == L.FPO_ERR_ARG  # unknown mode bit
+    assert call(L.PgDesc(128, 256, 688, 2, 1, 16, 1.0)) == L.FPO_ERR_ARG  # unknown mode bit
+    # pre-MLP composition (mode flag + argument), alone or after the post-FFN one
+    qmode = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_PRE_MLP, 1 / 128)
+    pm = C.byref(L.PreMlp(FAKE, mo, gm, 1e-6, 0.5))
+    assert call(qmode, g=None, pm=pm, ws_bytes=16) == L.FPO_ERR_WORKSPACE
+    assert call(qmode, g=None) == L.FPO_ERR_ARG          # mode without the argument
+    assert call(good, pm=pm) == L.FPO_ERR_ARG            # argument without the mode
+    assert call(qmode, g=None, pm=C.byref(L.PreMlp(None, mo, gm, 1e-6, 0.5))) == L.FPO_ERR_NULL
+    assert call(qmode, g=None, pm=C.byref(L.PreMlp(FAKE, mo, None, 1e-6, 0.5))) == L.FPO_ERR_NULL
+    assert call(qmode, g=None, pm=C.byref(L.PreMlp(FAKE, mo, gm, -1.0, 0.5))) == L.FPO_ERR_ARG
+    both = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_POST_FFN | L.FPO_MODE_PRE_MLP, 1 / 128)
+    assert call(both, g=None, pf=pf, pm=pm, ws_bytes=16) == L.FPO_ERR_WORKSPACE
+    assert call(both, g=None, pf=pf, pm=C.byref(L.PreMlp(FAKE + 256, mo, gm, 1e-6, 0.5))) == L.FPO_ERR_ARG
+    assert lib.fpo_pseudograd_workspace(C.byref(qmode)) == lib.fpo_pseudograd_workspace(C.byref(pmode))
     assert call(pmode, g=None, pf=C.byref(L.PostFfn(None, mo, gm, 1e-6, 0.5))) == L.FPO_ERR_NULL
     assert call(pmode, g=None, pf=C.byref(L.PostFfn(FAKE, None, gm, 1e-6, 0.5))) == L.FPO_ERR_NULL
     m1, km1 = arr([FAKE, None])
@@ -263,7 +276,7 @@ def test_pseudograd_operand_alignment(lib):
         desc = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_W3, 1 / 128)
         a, ka = arr(good)
         return lib.fpo_pseudograd(C.byref(desc), FAKE, a, None, None, None, None, None, None, None, None, r,
-                                  FAKE, FAKE, None, None, None, None, None, FAKE, 16, None)
+                                  FAKE, FAKE, None, None, None, None, None, None, FAKE, 16, None)
 
     assert ref_call(good) == L.FPO_ERR_WORKSPACE
     assert ref_call(bad) == L.FPO_ERR_ARG
@@ -273,7 +286,7 @@ def test_pseudograd_operand_alignment(lib):
         p = [b[0] for b in bufs]
         desc = L.PgDesc(128, 256, 688, 2, L.FPO_BF16, L.FPO_MODE_FULL_MLP, 1 / 128)
         return lib.fpo_pseudograd(C.byref(desc), FAKE, p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[6], None,
-                                  None, None, None, None, None, None, None, None, FAKE, 16, None)
+                                  None, None, None, None, None, None, None, None, None, FAKE, 16, None)
 
     assert full_call(-1) == L.FPO_ERR_WORKSPACE
     for k in range(1, 7):  # W3_init, gate, up, x_in, dW3 / dW1, dW2

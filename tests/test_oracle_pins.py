@@ -396,6 +396,64 @@ def test_post_ffn_signal_scale_and_gain_properties():
     np.testing.assert_allclose(O.post_ffn_signal(g, x, 2.0 * gam, eps=0.0, min_rms=0.5), 2.0 * base, rtol=1e-12)
 
 
+def _rmsnorm_vjp_autograd(g, x, gam, eps, floor):
+    """The VJP of a plain RMSNorm at x by torch autograd, with a row's epsilon
+    raised to floor^2 - mean(x^2) where its RMS is below the floor (the clamp,
+    as pinned above)."""
+    ms = (x * x).mean(1)
+    rho = np.sqrt(ms + eps)
+    eps_row = np.where(rho < floor, floor ** 2 - ms, eps)
+    X = torch.tensor(x, requires_grad=True)
+    Y = torch.tensor(gam) * X / torch.sqrt((X * X).mean(1, keepdim=True) + torch.tensor(eps_row)[:, None])
+    (gx,) = torch.autograd.grad((Y * torch.tensor(g)).sum(), X)
+    return gx.numpy()
+
+
+@pytest.mark.parametrize("post", [False, True], ids=["pre-MLP only (Qwen3)", "post-FFN then pre-MLP (Gemma 3)"])
+def test_layer_signal_is_the_chain_of_rmsnorm_vjps(post):
+    """Sec. 3.2 pre-MLP RMSNorm: layer_signal applies the VJP of the pre-MLP
+    norm at its own cached input and gain after the post-FFN one, each an
+    exact RMSNorm VJP (autograd), clamp active on some rows of each norm. A
+    swapped order or swapped inputs / gains do not match."""
+    r = np.random.default_rng(51)
+    T, d = 7, 10
+    g = r.standard_normal((T, d))
+    x_post = 2.0 * r.standard_normal((T, d))
+    x_post[2] *= 0.1                      # RMS ~0.2: clamp active on this row of the post-FFN norm
+    x_pre = 4.0 * r.standard_normal((T, d))
+    x_pre[5] *= 0.05                      # RMS ~0.2: clamp active on this row of the pre-MLP norm
+    gp = 0.3 + 0.05 * r.standard_normal(d)
+    gq = 1.0 + 0.1 * r.standard_normal(d)
+    eps, floor = 1e-6, 0.5
+    want = _rmsnorm_vjp_autograd(g, x_post, gp, eps, floor) if post else g
+    want = _rmsnorm_vjp_autograd(want, x_pre, gq, eps, floor)
+    got = O.layer_signal(g, x_post if post else None, gp if post else None, x_pre, gq, eps=eps, min_rms=floor)
+    np.testing.assert_allclose(got, want, rtol=1e-11, atol=1e-13)
+    if post:
+        swapped = _rmsnorm_vjp_autograd(_rmsnorm_vjp_autograd(g, x_pre, gq, eps, floor), x_post, gp, eps, floor)
+        assert not np.allclose(got, swapped, rtol=1e-3)
+        np.testing.assert_allclose(O.layer_signal(g, x_post, gp, eps=eps, min_rms=floor),
+                                   O.post_ffn_signal(g, x_post, gp, eps=eps, min_rms=floor), rtol=0, atol=0)
+    assert not np.allclose(got, O.layer_signal(g, x_post if post else None, gp if post else None, x_pre, gp,
+                                               eps=eps, min_rms=floor), rtol=1e-3)
+    np.testing.assert_array_equal(O.layer_signal(g), g)
+
+
+def test_pre_mlp_signal_scale_invariance():
+    """The pre-MLP norm's output does not depend on the scale of its input, so
+    its VJP at k x is the VJP at x divided by k (RMS above the clamp): the
+    composed signal shrinks as the residual stream grows; eps = 0."""
+    r = np.random.default_rng(52)
+    g = r.standard_normal((4, 8))
+    x = 3.0 * r.standard_normal((4, 8))
+    gam = 1.0 + 0.1 * r.standard_normal(8)
+    base = O.layer_signal(g, pre_in=x, gamma_pre=gam, eps=0.0, min_rms=0.5)
+    np.testing.assert_allclose(O.layer_signal(g, pre_in=5.0 * x, gamma_pre=gam, eps=0.0, min_rms=0.5), base / 5.0,
+                               rtol=1e-12)
+    # the signal is orthogonal to its own input row (scale invariance of RMSNorm, eps = 0)
+    np.testing.assert_allclose(np.sum(base * x, axis=1), 0.0, atol=1e-12)
+
+
 def test_full_mlp_step0_feedback_is_exact_gradient():
     """eq. errh: at step 0 (W3 = W3_init) the W1/W2 signals are the exact gradients."""
     r = np.random.default_rng(31)

@@ -27,7 +27,8 @@ def run_w3(c, g, acts, dev, refs=None, store=True):
     kw = {}
     if refs is not None:
         kw = dict(ref=[dev_tensor(r, dev) for r in refs], ref_dot=torch.empty(len(acts), dtype=torch.float64, device=dev),
-                  ref_sumsq=torch.empty(len(acts), dtype=torch.float64, device=dev))
+                  ref_sumsq=torch.empty(len(acts), dtype=torch.float64, device=dev),
+                  ref_cos=torch.full((len(acts),), -7.0, dtype=torch.float32, device=dev))
     api.fpo_pseudograd(tg, ta, dW3=dW, sumsq=ss, **kw)
     torch.cuda.synchronize()
     out = dict(sumsq=ss.cpu().numpy())
@@ -36,6 +37,7 @@ def run_w3(c, g, acts, dev, refs=None, store=True):
     if refs is not None:
         out["dot"] = kw["ref_dot"].cpu().numpy()
         out["refsq"] = kw["ref_sumsq"].cpu().numpy()
+        out["cos"] = kw["ref_cos"].cpu().numpy()
     return out
 
 
@@ -76,6 +78,9 @@ def test_fused_diagnostic_cosine(dev, cid):
             cg = out["dot"][l] / np.sqrt(out["sumsq"][l] * out["refsq"][l])
             assert abs(cg - cs) <= 1e-3
             assert abs(cs - 0.5) < 0.05
+            # the library's own cosine: the same float64 sums, rounded once to float32
+            assert abs(float(out["cos"][l]) - cg) <= 1e-6 * abs(cg) + 1e-7
+            assert abs(float(out["cos"][l]) - cs) <= 1e-3
         assert np.array_equal(with_store["dot"], fused["dot"])
 
 
@@ -108,6 +113,54 @@ def test_full_mlp(dev, cid, T, d, d_ff, L):
         assert_close("sumsq W2", s[2 * L + l], float((D2 ** 2).sum()), c.dtype)
 
 
+@pytest.mark.slow
+@pytest.mark.parametrize("cid,L", [(1, 8), (3, 3)], ids=["olmo2-7b-8-layers", "falcon3-7b-3-layers"])
+def test_full_size_full_mlp(dev, cid, L):
+    """Full-MLP mode (eq. errh) at the 7-8B shapes: OLMo-2 with all 8 target
+    layers, Falcon3 (d_ff 23040, the widest operand bands of the error GEMM
+    and its transposed dq / du stores) with 3. Per layer, 66 sampled rows of
+    dW1 and dW2 (all d columns; at Falcon3 shapes half of them outlier
+    channels) against oracle.full_mlp_grads on those d_ff columns of W3_init,
+    q and u, sampled columns of dW3 against oracle.pseudograd, and for the
+    first and last layer the reported squared norms against the oracle's
+    full matrices."""
+    c = I.CONFIGS[cid].shrink(L=L)
+    g = signal(c)
+    caches = [I.mlp_cache(c, l) for l in range(L)]
+    extras = [I.full_mlp_extra(c, l) for l in range(L)]
+    W3i = [I.to_storage(I.master_weight(c, l), c.dtype) for l in range(L)]
+    dW3 = [torch.empty(c.d, c.d_ff, dtype=torch.float32, device=dev) for _ in range(L)]
+    dW1 = [torch.empty(c.d_ff, c.d, dtype=torch.float32, device=dev) for _ in range(L)]
+    dW2 = [torch.empty(c.d_ff, c.d, dtype=torch.float32, device=dev) for _ in range(L)]
+    ss = torch.empty(3 * L, dtype=torch.float64, device=dev)
+    print(f"[pg] full-size full-MLP config {cid} L={L}", flush=True)
+    api.fpo_pseudograd(dev_tensor(g, dev), [dev_tensor(cc[2], dev) for cc in caches], dW3=dW3, sumsq=ss,
+                       W3_init=[dev_tensor(w, dev) for w in W3i], gate=[dev_tensor(cc[0], dev) for cc in caches],
+                       up=[dev_tensor(cc[1], dev) for cc in caches], x_in=[dev_tensor(e[0], dev) for e in extras],
+                       dW1=dW1, dW2=dW2)
+    torch.cuda.synchronize()
+    gf = I.storage_to_f64(g)
+    r = np.random.default_rng(500 + cid)
+    for l in range(L):
+        q, u, a = caches[l]
+        x_in = extras[l][0]
+        rows = [r.integers(0, c.d_ff, 64), [0, c.d_ff - 1]]
+        if c.outliers:
+            rows.append(I.outlier_channels(c, l)[:64])
+        ii = np.concatenate(rows)
+        D1s, D2s = O.full_mlp_grads(gf, W3i[l][:, ii], q[:, ii], u[:, ii], x_in)
+        assert_close(f"dW1[{l}] rows", dW1[l][ii].cpu().numpy().astype(np.float64), D1s, "bf16")
+        assert_close(f"dW2[{l}] rows", dW2[l][ii].cpu().numpy().astype(np.float64), D2s, "bf16")
+        jj = np.concatenate([r.integers(0, c.d_ff, 64), [c.d_ff - 1, 0]])
+        D3s = O.pseudograd(gf, a[:, jj])
+        assert_close(f"dW3[{l}] columns", dW3[l][:, jj].cpu().numpy().astype(np.float64), D3s, "bf16")
+        if l in (0, L - 1):
+            D1, D2 = O.full_mlp_grads(gf, W3i[l], q, u, x_in)
+            assert_close(f"sumsq W1[{l}]", float(ss[L + l]), float(np.sum(D1 * D1)), "bf16")
+            assert_close(f"sumsq W2[{l}]", float(ss[2 * L + l]), float(np.sum(D2 * D2)), "bf16")
+            del D1, D2
+
+
 def test_deterministic(dev):
     c = I.CONFIGS[1].shrink(T=700, d=512, d_ff=1024, L=2)
     g = signal(c)
@@ -119,42 +172,46 @@ def test_deterministic(dev):
         assert np.array_equal(x, y)
 
 
+def oracle_layer(gf, act):
+    """The oracle's pseudogradient of one layer at full size (float64 on the
+    host: 2 T d d_ff flops through BLAS) and its squared Frobenius norm."""
+    D = O.pseudograd(gf, act)
+    return D, float(np.sum(D * D))
+
+
 @pytest.mark.slow
 @pytest.mark.parametrize("cid", [1, 2, 3])
-def test_full_size_sampled(dev, cid):
-    """Full workload shapes: sampled entries of every layer against the oracle,
-    and layer 0's squared norm through the Gram identity
-    ||G^T A||_F^2 = <G G^T, A A^T> (exact in fp64 at any size)."""
+def test_full_size_w3(dev, cid):
+    """Full workload shapes: every layer's whole dW against oracle.pseudograd
+    and its reported squared norm against the oracle's."""
     c = I.CONFIGS[cid]
     g = signal(c)
+    tg = dev_tensor(g, dev)
     acts = [I.activation(c, l) for l in range(c.L)]
-    got = run_w3(c, g, acts, dev)
+    ta = [dev_tensor(a, dev) for a in acts]
+    dW = [torch.empty(c.d, c.d_ff, dtype=torch.float32, device=dev) for _ in range(c.L)]
+    ss = torch.empty(c.L, dtype=torch.float64, device=dev)
+    print(f"[pg] full-size W3 config {cid}", flush=True)
+    api.fpo_pseudograd(tg, ta, dW3=dW, sumsq=ss)
+    torch.cuda.synchronize()
     gf = I.storage_to_f64(g)
-    r = np.random.default_rng(cid)
     for l in range(c.L):
-        af = I.storage_to_f64(acts[l])
-        ii = r.integers(0, c.d, 64)
-        jj = r.integers(0, c.d_ff, 64)
-        ii = np.concatenate([ii, [0, c.d - 1]])
-        jj = np.concatenate([jj, [c.d_ff - 1, 0]])
-        ref = np.einsum("ti,ti->i", gf[:, ii], af[:, jj]) / c.T
-        assert_close(f"dW[{l}] samples", got["dW"][l][ii, jj], ref, "bf16")
-        if l == 0:
-            G = gf @ gf.T
-            A = af @ af.T
-            n2 = float(np.sum(G * A)) / c.T ** 2
-            assert_close("sumsq[0] (Gram)", got["sumsq"][0], n2, "bf16")
+        D, n2 = oracle_layer(gf, acts[l])
+        assert_close(f"dW[{l}]", host64(dW[l]), D, "bf16")
+        assert_close(f"sumsq[{l}]", float(ss[l]), n2, "bf16")
+        del D
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("cid,stage", [(1, False), (2, False), (3, False), (1, True), (3, True)])
+@pytest.mark.parametrize("cid,stage", [(1, False), (2, False), (3, False), (1, True), (2, True), (3, True)])
 def test_full_size_fused_update(dev, cid, stage):
     """The benchmark's launch configuration at full size: pseudogradient with
     the SGD-momentum step overlapped (first step), its pseudogradient returned
-    in fp32 or staged in bf16 (FPO_MODE_GRAD_BF16). Sampled momentum entries
-    against the oracle's clipped pseudogradient s * D (s from the reported
-    norms), W' and the bf16 copy exactly as fp32 / RNE from the GPU momentum,
-    and the reported clip factor."""
+    in fp32 or staged in bf16 (FPO_MODE_GRAD_BF16). For every layer: the
+    reported ||dW||^2 against the oracle's ||D||^2, the clip factor against
+    the oracle's clip of D, the whole momentum buffer against the oracle's
+    clipped pseudogradient s * D, W' within one ulp of fp32(W - lr * b) from
+    the GPU's momentum and its bf16 copy exactly RNE of W'."""
     c = I.CONFIGS[cid]
     g = signal(c)
     acts = [I.activation(c, l) for l in range(c.L)]
@@ -170,26 +227,34 @@ def test_full_size_fused_update(dev, cid, stage):
     ss = torch.empty(c.L, dtype=torch.float64, device=dev)
     cs = torch.empty(c.L, dtype=torch.float32, device=dev)
     opt = api.OptConfig(lr=c.lr, clip_frac=c.clip_frac, step=1)
+    print(f"[pg] full-size fused update config {cid} staged={stage}", flush=True)
     api.fpo_pseudograd(tg, ta, dW3=None if stage else dW, sumsq=ss, opt=opt, W_master=W, W_lp=lp, state1=s1,
                        W_sumsq=Wsq, clip_scale=cs, grad_bf16=stage)
     torch.cuda.synchronize()
-    ssh = ss.cpu().numpy()
     gf = I.storage_to_f64(g)
-    r = np.random.default_rng(100 + cid)
+    active = 0
     for l in range(c.L):
-        s = min(1.0, c.clip_frac * np.sqrt(wsq[l]) / np.sqrt(ssh[l]))
-        assert abs(float(cs[l]) - s) <= 1e-6 * s
-        ii = np.concatenate([r.integers(0, c.d, 64), [0, c.d - 1]])
-        jj = np.concatenate([r.integers(0, c.d_ff, 64), [c.d_ff - 1, 0]])
-        af = I.storage_to_f64(acts[l][:, jj])
-        D = np.einsum("ti,ti->i", gf[:, ii], af) / c.T
-        m = s1[l][ii, jj].cpu().numpy()
-        assert_close(f"momentum[{l}] samples", m.astype(np.float64), s * D, "bf16")
-        w_new = W[l][ii, jj].cpu().numpy()
-        w_exp = (Wh[l][ii, jj].astype(np.float32) - np.float32(c.lr) * m).astype(np.float32)
+        D, n2 = oracle_layer(gf, acts[l])
+        assert_close(f"sumsq[{l}]", float(ss[l]), n2, "bf16")
+        assert abs(float(ss[l]) - n2) <= 1e-4 * n2, (l, float(ss[l]), n2)
+        s = O.clip_scale(n2, wsq[l], c.clip_frac)
+        active += s < 1.0
+        assert abs(float(cs[l]) - s) <= 1e-4 * s, (l, float(cs[l]), s)
+        m = s1[l].cpu().numpy()
+        assert_close(f"momentum[{l}]", m.astype(np.float64), s * D, "bf16")
+        if not stage:
+            assert_close(f"dW[{l}]", host64(dW[l]), D, "bf16")
+        del D
+        w_new = W[l].cpu().numpy()
+        # the kernel's single-rounding fma(-lr, b, W): the product of two floats is
+        # exact in float64, so W - lr b there is within one float64 rounding
+        w_exp = (Wh[l].astype(np.float64) - np.float64(np.float32(c.lr)) * m.astype(np.float64)).astype(np.float32)
         assert np.all(ulp_diff_f32(w_new, w_exp) <= 1), l
-        lpv = lp[l][ii, jj].view(torch.int16).cpu().numpy().view(np.uint16)
+        lpv = lp[l].view(torch.int16).cpu().numpy().view(np.uint16)
         assert np.array_equal(lpv, bf16_rne_bits(w_new)), l
+    # the workload's clip is active on the OLMo-2 and Falcon3 shapes (||D|| / ||W|| ~ 1.3% and 2.1%)
+    if cid in (1, 3):
+        assert active == c.L, active
     # ||W'||^2 reported for the next step's clip
     for l in (0, c.L - 1):
         wn = W[l].double()
@@ -201,11 +266,12 @@ def test_full_size_fused_update(dev, cid, stage):
 def test_full_size_fused_adamw(dev, cid):
     """AdamW in the benchmark's launch configuration (--optimizer adamw): the
     bf16-staged pseudogradient, the step overlapped with the next layer's
-    outer products, first step. Sampled moments against the oracle's AdamW on
-    the clipped pseudogradient s * D (s from the reported norms); W' against
-    the kernel's float32 formula applied to the GPU's own moments (a few ulp:
-    the step ~ lr sign(D) makes the oracle's W' sensitive to near-zero D);
-    the bf16 copy exactly RNE of W'; the reported ||W'||^2."""
+    outer products, first step. Per layer: the reported ||dW||^2 and the clip
+    factor against the oracle's, both moments in full against the oracle's
+    AdamW on its clipped pseudogradient s * D; W' (sampled) against the
+    kernel's float32 formula applied to the GPU's own moments (a few ulp: the
+    step ~ lr sign(D) makes the oracle's W' sensitive to near-zero D); the
+    bf16 copy exactly RNE of W'; the reported ||W'||^2."""
     c = I.CONFIGS[cid]
     g = signal(c)
     acts = [I.activation(c, l) for l in range(c.L)]
@@ -223,22 +289,25 @@ def test_full_size_fused_adamw(dev, cid):
     api.fpo_pseudograd(dev_tensor(g, dev), [dev_tensor(a, dev) for a in acts], dW3=None, sumsq=ss, opt=opt,
                        W_master=W, W_lp=lp, state1=m1, state2=m2, W_sumsq=Wsq, clip_scale=cs, grad_bf16=True)
     torch.cuda.synchronize()
-    ssh = ss.cpu().numpy()
     gf = I.storage_to_f64(g)
     f32 = lambda v: np.float64(np.float32(v))  # noqa: E731
     r = np.random.default_rng(200 + cid)
     for l in range(c.L):
-        s = min(1.0, c.clip_frac * np.sqrt(wsq[l]) / np.sqrt(ssh[l]))
-        assert abs(float(cs[l]) - s) <= 1e-6 * s
+        Df, n2 = oracle_layer(gf, acts[l])
+        assert abs(float(ss[l]) - n2) <= 1e-4 * n2, (l, float(ss[l]), n2)
+        s = O.clip_scale(n2, wsq[l], c.clip_frac)
+        assert abs(float(cs[l]) - s) <= 1e-4 * s, (l, float(cs[l]), s)
+        _, om_f, ov_f = O.adamw(Wh[l], 0.0, 0.0, s * Df, opt.lr, 1, opt.beta1, opt.beta2, opt.adam_eps,
+                                opt.weight_decay)
+        del Df
+        assert_close(f"exp_avg[{l}]", m1[l].cpu().numpy().astype(np.float64), om_f, "bf16")
+        assert_close(f"exp_avg_sq[{l}]", m2[l].cpu().numpy().astype(np.float64), ov_f, "bf16")
+        del om_f, ov_f
         ii = np.concatenate([r.integers(0, c.d, 64), [0, c.d - 1]])
         jj = np.concatenate([r.integers(0, c.d_ff, 64), [c.d_ff - 1, 0]])
-        D = np.einsum("ti,ti->i", gf[:, ii], I.storage_to_f64(acts[l][:, jj])) / c.T
         w0 = Wh[l][ii, jj].astype(np.float64)
-        _, om, ov = O.adamw(w0, 0.0, 0.0, s * D, opt.lr, 1, opt.beta1, opt.beta2, opt.adam_eps, opt.weight_decay)
         mg = m1[l][ii, jj].cpu().numpy().astype(np.float64)
         vg = m2[l][ii, jj].cpu().numpy().astype(np.float64)
-        assert_close(f"exp_avg[{l}]", mg, om, "bf16")
-        assert_close(f"exp_avg_sq[{l}]", vg, ov, "bf16")
         step = f32(opt.lr) * (mg * f32(1.0 / (1.0 - opt.beta1))) / (
             np.sqrt(vg) * f32(1.0 / np.sqrt(1.0 - opt.beta2)) + f32(opt.adam_eps))
         expect = w0 * f32(1.0 - opt.lr * opt.weight_decay) - step
@@ -257,11 +326,12 @@ def test_full_size_fused_adamw(dev, cid):
 def test_full_size_fused_update_clip(dev, lr):
     """The clip-the-update reading at full size (--clip-target update, OLMo-2
     shapes, bf16-staged pseudogradient): SGD-momentum state advances on the
-    unclipped pseudogradient (sampled against the oracle's D), the applied
-    step -lr b is scaled by s = min(1, 0.01 ||W|| / ||lr b||) (checked against
-    the oracle's formula on the GPU's own norm), and W' equals W + s (-lr b)
-    from the GPU's state within fp32 rounding. At the workload's lr (1e-4)
-    the bound is idle (s = 1); lr = 2 makes it bite on every layer."""
+    unclipped pseudogradient (the whole buffer against the oracle's D), the
+    applied step -lr b is scaled by s = min(1, 0.01 ||W|| / ||lr b||), checked
+    against the oracle's clip-the-update step on its own D, and W' equals
+    W + s (-lr b) from the GPU's state within fp32 rounding. At the
+    workload's lr (1e-4) the bound is idle (s = 1); lr = 2 makes it bite on
+    every layer."""
     c = I.CONFIGS[1]
     g = signal(c)
     acts = [I.activation(c, l) for l in range(c.L)]
@@ -283,16 +353,16 @@ def test_full_size_fused_update_clip(dev, lr):
     f32 = lambda v: np.float64(np.float32(v))  # noqa: E731
     r = np.random.default_rng(300)
     for l in range(c.L):
-        bl = b1[l].double()
-        dsq = float(((f32(lr) * bl) ** 2).sum())  # ||delta||^2 of the GPU's step
-        s = O.clip_scale(dsq, wsq[l], c.clip_frac)
-        assert abs(float(cs[l]) - s) <= 1e-5 * s, (l, float(cs[l]), s)
+        Df, _ = oracle_layer(gf, acts[l])
+        _, ob, s = O.sgd_momentum_update_clip(Wh[l], None, Df, lr, 0.9, step=1, frac=c.clip_frac)
+        del Df
+        assert abs(float(cs[l]) - s) <= 1e-4 * s, (l, float(cs[l]), s)
         assert (s < 1.0) == (lr > 1.0), (l, s)
+        assert_close(f"momentum[{l}]", b1[l].cpu().numpy().astype(np.float64), ob, "bf16")  # unclipped state
+        del ob
         ii = np.concatenate([r.integers(0, c.d, 64), [0, c.d - 1]])
         jj = np.concatenate([r.integers(0, c.d_ff, 64), [c.d_ff - 1, 0]])
-        D = np.einsum("ti,ti->i", gf[:, ii], I.storage_to_f64(acts[l][:, jj])) / c.T
         bg = b1[l][ii, jj].cpu().numpy().astype(np.float64)
-        assert_close(f"momentum[{l}] samples", bg, D, "bf16")  # unclipped state
         w0 = Wh[l][ii, jj].astype(np.float64)
         delta = -f32(lr) * bg
         expect = w0 + float(cs[l]) * delta
@@ -327,7 +397,8 @@ def test_full_size_diagnostic_rank1_reference(dev):
     ss = torch.empty(c.L, dtype=torch.float64, device=dev)
     dot = torch.empty(c.L, dtype=torch.float64, device=dev)
     rsq = torch.empty(c.L, dtype=torch.float64, device=dev)
-    api.fpo_pseudograd(tg, ta, dW3=dW, sumsq=ss, ref=[R] * c.L, ref_dot=dot, ref_sumsq=rsq)
+    cosl = torch.empty(c.L, dtype=torch.float32, device=dev)
+    api.fpo_pseudograd(tg, ta, dW3=dW, sumsq=ss, ref=[R] * c.L, ref_dot=dot, ref_sumsq=rsq, ref_cos=cosl)
     torch.cuda.synchronize()
     gf = I.storage_to_f64(g)
     ug = gf @ u.astype(np.float64)                      # u . g~_t
@@ -347,6 +418,8 @@ def test_full_size_diagnostic_rank1_reference(dev):
             assert_close(f"dW[{l}] samples", dW[l][ii, jj].cpu().numpy().astype(np.float64), D, "bf16")
             # the reported norm is that of the stored matrix (layers of one activation agree exactly)
             assert float(ss[l]) == float(ss[k])
+            cg = float(dot[l]) / np.sqrt(float(ss[l]) * float(rsq[l]))
+            assert abs(float(cosl[l]) - cg) <= 1e-6 * abs(cg) + 1e-7
         del af
 
 
@@ -415,6 +488,115 @@ def test_post_ffn_full_mlp(dev, cid, T, d, d_ff, L):
         assert_close("dW1", host64(store["dW1"][l]), D1, c.dtype)
         assert_close("dW2", host64(store["dW2"][l]), D2, c.dtype)
         assert_close("sumsq W1", float(ss[L + l]), float((D1 ** 2).sum()), c.dtype)
+
+
+def run_chain(c, g32, acts, dev, pf=None, pre=None, extra=None, **kw):
+    """fpo_pseudograd with the post-FFN (pf) and / or pre-MLP (pre) composition."""
+    tg = torch.from_numpy(g32).to(dev)
+    ta = [dev_tensor(a, dev) for a in acts]
+    dW = [torch.empty(c.d, c.d_ff, dtype=torch.float32, device=dev) for _ in acts]
+    ss = torch.empty(len(acts) * (3 if extra else 1), dtype=torch.float64, device=dev)
+    args = dict(dW3=dW, sumsq=ss, **kw)
+    if pf is not None:
+        args["post_ffn"] = api.PostFfn(tg, [dev_tensor(m, dev) for m, _ in pf], [dev_tensor(g, dev) for _, g in pf],
+                                       c.eps, c.min_rms)
+    if pre is not None:
+        args["pre_mlp"] = api.PreMlp(tg, [dev_tensor(x, dev) for x, _ in pre], [dev_tensor(g, dev) for _, g in pre],
+                                     c.eps, c.min_rms)
+    if extra is not None:
+        args.update(extra(dev))
+    api.fpo_pseudograd(None, ta, **args)
+    torch.cuda.synchronize()
+    return dW, ss, args
+
+
+@pytest.mark.parametrize("post", [False, True], ids=["pre-MLP", "post-FFN+pre-MLP"])
+@pytest.mark.parametrize("cid,T,d,d_ff,L", [(0, 128, 256, 688, 2), (0, 300, 264, 520, 3), (1, 300, 264, 520, 2),
+                                            (1, 1000, 512, 1032, 2)])
+def test_pre_mlp_w3(dev, cid, T, d, d_ff, L, post):
+    """Pre-MLP RMSNorm composition (Qwen3 layout; with the post-FFN one first,
+    the Gemma 3 layout): each layer's left operand is oracle.layer_signal of
+    the fp32 g~, 1% of tokens below the min-RMS floor in each norm."""
+    c = I.CONFIGS[cid].shrink(T=T, d=d, d_ff=d_ff, L=L)
+    g32, pf = pffn_case(c, L)
+    pre = [I.pre_mlp(c, l) for l in range(L)]
+    acts = [I.activation(c, l) for l in range(L)]
+    dW, ss, _ = run_chain(c, g32, acts, dev, pf=pf if post else None, pre=pre)
+    for l in range(L):
+        gl = O.layer_signal(g32, pf[l][0] if post else None, pf[l][1] if post else None, pre[l][0], pre[l][1],
+                            eps=c.eps, min_rms=c.min_rms)
+        D = O.pseudograd(gl, acts[l])
+        assert_close(f"dW[{l}] (pre-MLP)", host64(dW[l]), D, c.dtype)
+        assert_close(f"sumsq[{l}]", float(ss[l]), float((D * D).sum()), c.dtype)
+        # the composition matters: skipping the pre-MLP VJP is far outside the tolerance
+        g0 = O.layer_signal(g32, pf[l][0] if post else None, pf[l][1] if post else None, eps=c.eps,
+                            min_rms=c.min_rms)
+        assert np.linalg.norm(O.pseudograd(g0, acts[l]) - D) > 0.2 * np.linalg.norm(D)
+
+
+@pytest.mark.parametrize("cid,T,d,d_ff,L", [(0, 128, 256, 688, 2), (1, 200, 256, 520, 2)])
+def test_pre_mlp_full_mlp(dev, cid, T, d, d_ff, L):
+    """Full-MLP mode with both norms composed: W1 / W2 through W3_init take
+    the composed signal too."""
+    c = I.CONFIGS[cid].shrink(T=T, d=d, d_ff=d_ff, L=L)
+    g32, pf = pffn_case(c, L)
+    pre = [I.pre_mlp(c, l) for l in range(L)]
+    caches = [I.mlp_cache(c, l) for l in range(L)]
+    extras = [I.full_mlp_extra(c, l) for l in range(L)]
+    W3i = [I.to_storage(I.master_weight(c, l), c.dtype) for l in range(L)]
+    store = {}
+
+    def extra(dev):
+        store["dW1"] = [torch.empty(c.d_ff, c.d, dtype=torch.float32, device=dev) for _ in range(L)]
+        store["dW2"] = [torch.empty(c.d_ff, c.d, dtype=torch.float32, device=dev) for _ in range(L)]
+        return dict(W3_init=[dev_tensor(w, dev) for w in W3i], gate=[dev_tensor(q, dev) for q, _, _ in caches],
+                    up=[dev_tensor(u, dev) for _, u, _ in caches], x_in=[dev_tensor(e[0], dev) for e in extras],
+                    dW1=store["dW1"], dW2=store["dW2"])
+
+    dW3, ss, _ = run_chain(c, g32, [a for _, _, a in caches], dev, pf=pf, pre=pre, extra=extra)
+    for l in range(L):
+        gl = O.layer_signal(g32, pf[l][0], pf[l][1], pre[l][0], pre[l][1], eps=c.eps, min_rms=c.min_rms)
+        q, u, a = caches[l]
+        D1, D2 = O.full_mlp_grads(gl, W3i[l], q, u, extras[l][0])
+        assert_close("dW3", host64(dW3[l]), O.pseudograd(gl, a), c.dtype)
+        assert_close("dW1", host64(store["dW1"][l]), D1, c.dtype)
+        assert_close("dW2", host64(store["dW2"][l]), D2, c.dtype)
+        assert_close("sumsq W2", float(ss[2 * L + l]), float((D2 ** 2).sum()), c.dtype)
+
+
+@pytest.mark.slow
+def test_full_size_pre_mlp_fused_update(dev):
+    """Qwen3-8B shapes (a pre-MLP-norm family) at full size with the pre-MLP
+    composition and the overlapped SGD-momentum step: the composed signal
+    against oracle.layer_signal in full, sampled columns of every layer's
+    momentum against the oracle's clipped s * D (s from the oracle's norm of
+    those layers' full D for the first and last layer)."""
+    c = I.CONFIGS[2]
+    g32 = I.normal(c.cid, I.T_G, 7, c.T * c.d, std=0.02).reshape(c.T, c.d)
+    pre = [I.pre_mlp(c, l) for l in range(c.L)]
+    acts = [I.activation(c, l) for l in range(c.L)]
+    Wh = [I.master_weight(c, l) for l in range(c.L)]
+    W = [torch.from_numpy(w).to(dev) for w in Wh]
+    wsq = np.array([float((w.astype(np.float64) ** 2).sum()) for w in Wh])
+    s1 = [torch.zeros_like(w) for w in W]
+    cs = torch.empty(c.L, dtype=torch.float32, device=dev)
+    print("[pg] full-size pre-MLP fused update (Qwen3-8B shapes)", flush=True)
+    dW, ss, _ = run_chain(c, g32, acts, dev, pre=pre,
+                          opt=api.OptConfig(lr=c.lr, clip_frac=c.clip_frac, step=1), W_master=W,
+                          W_lp=[torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in W], state1=s1,
+                          W_sumsq=torch.tensor(wsq, dtype=torch.float64, device=dev), clip_scale=cs)
+    r = np.random.default_rng(8)
+    for l in range(c.L):
+        gl = O.layer_signal(g32, pre_in=pre[l][0], gamma_pre=pre[l][1], eps=c.eps, min_rms=c.min_rms)
+        jj = np.concatenate([r.integers(0, c.d_ff, 96), [c.d_ff - 1, 0]])
+        Ds = O.pseudograd(gl, acts[l][:, jj])
+        assert_close(f"dW[{l}] columns", dW[l][:, jj].cpu().numpy().astype(np.float64), Ds, "bf16")
+        if l in (0, c.L - 1):
+            D, n2 = oracle_layer(gl, acts[l])
+            s = O.clip_scale(n2, wsq[l], c.clip_frac)
+            assert abs(float(cs[l]) - s) <= 1e-3 * s, (l, float(cs[l]), s)
+            assert_close(f"momentum[{l}]", s1[l].cpu().numpy().astype(np.float64), s * D, "bf16")
+            del D
 
 
 @pytest.mark.slow
