@@ -744,8 +744,13 @@ def main():
 
     flops_oe = 4.0 * c.T * c.V * c.d
     flops_pg = 2.0 * c.T * c.d * c.d_ff * c.L * (4 if full else 1)
+    # the committed counter profiles cover the default step and the full-MLP step; other variants (post-FFN,
+    # optimizer, clip target, fp32 staging, chunk width) change the dominant kernel's traffic: none is looked up
+    variant = (args.post_ffn or args.optimizer != "sgd-momentum" or args.clip_target != "gradient" or args.grad_f32
+               or args.vocab_chunk)
+    tname = c.name + ("-full-mlp" if full else "") + ("-variant" if variant else "")
     res = timed_run(args, step, lambda k: not (overlapped and k == "update"), c, clk_mhz, T, flops_oe, flops_pg,
-                    work)
+                    work, traffic_name=tname)
     res["config"] = {"workload": f"{c.name}-shaped FPO step: T={c.T} tokens, d={c.d}, d_ff={c.d_ff}, V={c.V}, "
                                  f"{c.L} target layers ({'W1, W2 and W3 (full-MLP)' if full else 'W3'}"
                                  f"{', post-FFN norm VJP per layer' if args.post_ffn else ''}), bf16 operands / fp32 "

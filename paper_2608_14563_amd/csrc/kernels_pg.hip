@@ -251,12 +251,17 @@ __global__ __launch_bounds__(256, 1) void outer_kernel(OuterArgs args, int M, in
   using TT = Tile<E>;
   using T = typename E::T;
   __shared__ double red[12];
-  // one flat grid over (matrix, tile); each XCD takes a contiguous range
+  // one flat grid over (matrix, tile), matrix-major in dispatch order, each
+  // matrix's tiles spread over the 8 XCDs (a contiguous group per XCD): every
+  // XCD works on the same matrix at the same time, so the matrix's operand
+  // panels are fetched into the Infinity Cache once for all of them. (A
+  // contiguous range of the whole flat grid per XCD put eight different
+  // matrices in flight: 83 GB fetched for 14.5 GB of operands in the
+  // 36-layer diagnostic launch.)
   const int ntm = (M + TT::BM - 1) / TT::BM, ntn = (N + TT::BN - 1) / TT::BN;
   const int ntiles = ntm * ntn;
-  const int id = xcd_remap(blockIdx.x, gridDim.x);
-  const int mat = id / ntiles;
-  const int tile = id % ntiles;
+  const int mat = blockIdx.x / ntiles;
+  const int tile = xcd_remap(blockIdx.x - mat * ntiles, ntiles);
   int tm, tn;
   grouped_tile(tile, ntm, ntn, 8, tm, tn);
   const int m0 = tm * TT::BM, n0 = tn * TT::BN;
@@ -625,14 +630,15 @@ static hipError_t enqueue_pseudograd_update(const PgLaunch& a, const UpdLaunch& 
                outer_kernel<TileBF16><<<dim3(ntiles), dim3(256), 0, st>>>(oa, (int)a.d, (int)a.d_ff, (int)a.T,
                                                                  a.Tp, a.d_ff, a.scale, tpart));
     FPO_CHECK_LAUNCH();
-    FPO_LAUNCH("reduce_parts", st,
-               reduce_parts_kernel<<<dim3(1), dim3(256), 0, st>>>(
+    // layer l's tiles are complete: its norm reduction and update follow on the
+    // side stream, so the next layer's outer products start right away
+    if ((e = hipEventRecord(ready_l, st)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(side, ready_l, 0)) != hipSuccess) return e;
+    FPO_LAUNCH("reduce_parts", side,
+               reduce_parts_kernel<<<dim3(1), dim3(256), 0, side>>>(
         tpart, ntiles, l, a.sumsq, a.ref_dot ? a.ref_dot + l : nullptr,
         a.ref_sumsq ? a.ref_sumsq + l : nullptr, a.ref_cos ? a.ref_cos + l : nullptr));
     FPO_CHECK_LAUNCH();
-    // layer l's dW and ||dW||^2 are complete: update it on the side stream
-    if ((e = hipEventRecord(ready_l, st)) != hipSuccess) return e;
-    if ((e = hipStreamWaitEvent(side, ready_l, 0)) != hipSuccess) return e;
     // one workgroup per CU while the next layer's outer products run; the last
     // update runs alone and takes the whole machine
     if ((e = launch_update_blocks(u, l, blk_base, side, l + 1 < a.L ? cus : 0)) != hipSuccess) return e;
