@@ -18,7 +18,11 @@
 // one wait + barrier per tile (after MFMA group 13 of 16) makes tile j+1
 // visible and releases stage j % 2; the last two groups then overlap the next
 // tile's first operand reads. Out-of-range rows / K chunks are given a buffer
-// offset beyond the resource and read as zero.
+// offset beyond the resource and read as zero. Kernels instantiated with FAST
+// (launched only when M and N are multiples of 256 and K of 64) copy with the
+// lane's offset fixed in a register and the rest in the scalar offset, so a
+// copy costs no vector instructions: the bounds selects of the general form
+// were most of the core's non-MFMA vector issue.
 //
 // LDS layouts (16-byte chunks):
 //   K-contiguous tile: [rows][8 chunks], chunk c of row r stored at position
@@ -72,6 +76,18 @@ __device__ __forceinline__ void dma16(u32x4 rsrc, uint32_t lds_addr, uint32_t vo
       : "memory", "m0");
 }
 
+// The same copy with a uniform byte offset in soffset: lane l reads
+// rsrc + soffset + voff. The buffer range check covers voff only, so this form
+// is used only where every lane's address is known to lie inside the operand.
+__device__ __forceinline__ void dma16s(u32x4 rsrc, uint32_t lds_addr, uint32_t voff, uint32_t soff) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "buffer_load_dwordx4 %1, %2, %3 offen lds"
+      :
+      : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff)
+      : "memory", "m0");
+}
 
 // s_waitcnt vmcnt(n) leaving lgkmcnt / expcnt unconstrained (gfx9 encoding:
 // vmcnt[3:0] at bits 3:0, vmcnt[5:4] at bits 15:14).
@@ -140,6 +156,7 @@ struct Pipe2 {
   // columns 8*(l&31) .. +7.
   uint32_t offBn;
   bool okBn;
+  int klast;                   // last K tile (fast form: later copies are clamped to it)
 
   __device__ __forceinline__ void setup(const u32x4* smem, const Operand& A, const Operand& B,
                                         int M_rem_, int N_rem_, int K_) {
@@ -164,6 +181,39 @@ struct Pipe2 {
     }
     offBn = (uint32_t)((int64_t)(l >> 5) * ldB2 + 16 * (l & 31));
     okBn = 8 * (l & 31) < N_rem;
+    klast = (K + G2::BK - 1) / G2::BK - 1;
+  }
+
+  // Copy j of K tile kt in the fast form, for operands whose tiles are all
+  // whole (M and N multiples of the tile, K of BK): the lane's offset is fixed,
+  // the rest is uniform (soffset), so a copy needs no vector arithmetic and no
+  // bounds selects. Every address lies inside the operand (copies issued past
+  // the last K tile are clamped to it by the caller).
+  __device__ __forceinline__ void issue_fast(int st, int kt, int j) const {
+    const int k0 = kt * G2::BK;
+    const uint32_t sbase = lds_wave + (uint32_t)st * (G2::STAGE_CHUNKS * 16);
+    const int q = j & 7, inst = 8 * w + q;
+    if (j < 8) {
+      dma16s(ra, sbase + 1024u * inst, offA[q & 1], (uint32_t)((int64_t)8 * inst * ldA2 + k0 * 2));
+    } else if constexpr (BNC) {
+      dma16s(rb, sbase + G2::A_CHUNKS * 16 + 1024u * inst, offBn, (uint32_t)((int64_t)(k0 + 2 * inst) * ldB2));
+    } else {
+      dma16s(rb, sbase + G2::A_CHUNKS * 16 + 1024u * inst, offBt[q & 1],
+             (uint32_t)((int64_t)8 * inst * ldB2 + k0 * 2));
+    }
+  }
+
+  template <bool FAST>
+  __device__ __forceinline__ void issue(int st, int kt, int j) const {
+    if constexpr (FAST)
+      issue_fast(st, kt, j);
+    else
+      issue_one(st, kt, j);
+  }
+  // K tile whose copies go out as tile kt (fast form: clamped to the last)
+  template <bool FAST>
+  __device__ __forceinline__ int copy_tile(int kt) const {
+    return FAST ? min(kt, klast) : kt;
   }
 
   // DMA copy j (0..7: A, 8..15: B) of K tile kt into ring stage st; rows,
@@ -267,31 +317,31 @@ __device__ __forceinline__ void mfma_group(f32x16 (&acc)[4][4], int f, u32x4 a, 
 // barrier). After group 13: wait for tile j+1's copies, barrier. Groups 14, 15
 // read tile j+1's first operands and issue tile j+2's copies 0..3 into the
 // stage just released.
-template <bool BNC>
+template <bool BNC, bool FAST>
 __device__ __forceinline__ void gemm2_iter(const Pipe2<BNC>& p, G2Smem& sm, f32x16 (&acc)[4][4],
                                            u32x4 (&bc)[4], u32x4 (&a)[2], int j, int kt0) {
   const u32x4* cur = sm.s + (j & 1) * G2::STAGE_CHUNKS;
   const u32x4* nxt = sm.s + ((j + 1) & 1) * G2::STAGE_CHUNKS;
-  const int s1 = (j + 1) & 1, t1 = kt0 + j + 1;  // tile j+1: copies 4..15 now
-  const int s2 = j & 1, t2 = kt0 + j + 2;        // tile j+2: copies 0..3 after the barrier
+  const int s1 = (j + 1) & 1, t1 = p.template copy_tile<FAST>(kt0 + j + 1);  // tile j+1: copies 4..15 now
+  const int s2 = j & 1, t2 = p.template copy_tile<FAST>(kt0 + j + 2);        // tile j+2: copies 0..3 after the barrier
   auto nop = [] {};
   u32x2 raw[8];
   u32x4 bq[4], bn[4];
   u32x4 a2, a3, a4, a5, a6, a7, a8, a9, a10, a11, a12, a13, a14, a15;
   // ---- K step 0
-  mfma_group(acc, 0, a[0], bc, [&] { a2 = p.read_a(cur, 2, 0); }, [&] { p.issue_one(s1, t1, 4); },
-             [&] { p.read_b(cur, 1, 0, raw, bq); }, [&] { p.issue_one(s1, t1, 5); });
-  mfma_group(acc, 1, a[1], bc, [&] { a3 = p.read_a(cur, 3, 0); }, [&] { p.issue_one(s1, t1, 6); },
-             [&] { p.read_b(cur, 1, 1, raw, bq); }, [&] { p.issue_one(s1, t1, 7); });
-  mfma_group(acc, 2, a2, bc, [&] { a4 = p.read_a(cur, 0, 1); }, [&] { p.issue_one(s1, t1, 8); },
-             [&] { Pipe2<BNC>::pack_b(raw, bq, bn, 0); }, [&] { p.issue_one(s1, t1, 9); });
-  mfma_group(acc, 3, a3, bc, [&] { a5 = p.read_a(cur, 1, 1); }, [&] { p.issue_one(s1, t1, 10); },
-             [&] { Pipe2<BNC>::pack_b(raw, bq, bn, 1); }, [&] { p.issue_one(s1, t1, 11); });
+  mfma_group(acc, 0, a[0], bc, [&] { a2 = p.read_a(cur, 2, 0); }, [&] { p.template issue<FAST>(s1, t1, 4); },
+             [&] { p.read_b(cur, 1, 0, raw, bq); }, [&] { p.template issue<FAST>(s1, t1, 5); });
+  mfma_group(acc, 1, a[1], bc, [&] { a3 = p.read_a(cur, 3, 0); }, [&] { p.template issue<FAST>(s1, t1, 6); },
+             [&] { p.read_b(cur, 1, 1, raw, bq); }, [&] { p.template issue<FAST>(s1, t1, 7); });
+  mfma_group(acc, 2, a2, bc, [&] { a4 = p.read_a(cur, 0, 1); }, [&] { p.template issue<FAST>(s1, t1, 8); },
+             [&] { Pipe2<BNC>::pack_b(raw, bq, bn, 0); }, [&] { p.template issue<FAST>(s1, t1, 9); });
+  mfma_group(acc, 3, a3, bc, [&] { a5 = p.read_a(cur, 1, 1); }, [&] { p.template issue<FAST>(s1, t1, 10); },
+             [&] { Pipe2<BNC>::pack_b(raw, bq, bn, 1); }, [&] { p.template issue<FAST>(s1, t1, 11); });
   // ---- K step 1
-  mfma_group(acc, 0, a4, bn, [&] { a6 = p.read_a(cur, 2, 1); }, [&] { p.issue_one(s1, t1, 12); },
-             [&] { p.read_b(cur, 2, 0, raw, bq); }, [&] { p.issue_one(s1, t1, 13); });
-  mfma_group(acc, 1, a5, bn, [&] { a7 = p.read_a(cur, 3, 1); }, [&] { p.issue_one(s1, t1, 14); },
-             [&] { p.read_b(cur, 2, 1, raw, bq); }, [&] { p.issue_one(s1, t1, 15); });
+  mfma_group(acc, 0, a4, bn, [&] { a6 = p.read_a(cur, 2, 1); }, [&] { p.template issue<FAST>(s1, t1, 12); },
+             [&] { p.read_b(cur, 2, 0, raw, bq); }, [&] { p.template issue<FAST>(s1, t1, 13); });
+  mfma_group(acc, 1, a5, bn, [&] { a7 = p.read_a(cur, 3, 1); }, [&] { p.template issue<FAST>(s1, t1, 14); },
+             [&] { p.read_b(cur, 2, 1, raw, bq); }, [&] { p.template issue<FAST>(s1, t1, 15); });
   mfma_group(acc, 2, a6, bn, [&] { a8 = p.read_a(cur, 0, 2); }, nop,
              [&] { Pipe2<BNC>::pack_b(raw, bq, bc, 0); }, nop);
   mfma_group(acc, 3, a7, bn, [&] { a9 = p.read_a(cur, 1, 2); }, nop,
@@ -314,9 +364,9 @@ __device__ __forceinline__ void gemm2_iter(const Pipe2<BNC>& p, G2Smem& sm, f32x
     stage_barrier();
   });
   mfma_group(acc, 2, a14, bn, [&] { p.read_b(nxt, 0, 0, raw, bq); }, [&] { a[0] = p.read_a(nxt, 0, 0); },
-             [&] { p.read_b(nxt, 0, 1, raw, bq); }, [&] { p.issue_one(s2, t2, 0); });
-  mfma_group(acc, 3, a15, bn, [&] { a[1] = p.read_a(nxt, 1, 0); }, [&] { p.issue_one(s2, t2, 1); },
-             [&] { p.issue_one(s2, t2, 2); }, [&] { p.issue_one(s2, t2, 3); });
+             [&] { p.read_b(nxt, 0, 1, raw, bq); }, [&] { p.template issue<FAST>(s2, t2, 0); });
+  mfma_group(acc, 3, a15, bn, [&] { a[1] = p.read_a(nxt, 1, 0); }, [&] { p.template issue<FAST>(s2, t2, 1); },
+             [&] { p.template issue<FAST>(s2, t2, 2); }, [&] { p.template issue<FAST>(s2, t2, 3); });
   Pipe2<BNC>::pack_b(raw, bq, bc, 0);
   Pipe2<BNC>::pack_b(raw, bq, bc, 1);
 }
@@ -327,7 +377,7 @@ __device__ __forceinline__ void gemm2_iter(const Pipe2<BNC>& p, G2Smem& sm, f32x
 // Copies are issued for every iteration (beyond the last tile they read
 // zeros, or the next split's data, into a stage no longer needed), so every
 // wait is the same: vmcnt(0) at the barrier of each tile.
-template <bool BNC>
+template <bool BNC, bool FAST = false>
 __device__ __forceinline__ void gemm2_mainloop(G2Smem& sm, f32x16 (&acc)[4][4], const Operand& A,
                                                const Operand& B, int M_rem, int N_rem, int K,
                                                int kt0, int kt1) {
@@ -336,11 +386,12 @@ __device__ __forceinline__ void gemm2_mainloop(G2Smem& sm, f32x16 (&acc)[4][4], 
   Pipe2<BNC> p;
   p.setup(sm.s, A, B, M_rem, N_rem, K);
 #pragma unroll
-  for (int q = 0; q < 16; ++q) p.issue_one(0, kt0, q);
+  for (int q = 0; q < 16; ++q) p.template issue<FAST>(0, kt0, q);
   wait_vmcnt<0>();
   stage_barrier();
+  const int kt1c = p.template copy_tile<FAST>(kt0 + 1);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) p.issue_one(1, kt0 + 1, q);
+  for (int q = 0; q < 4; ++q) p.template issue<FAST>(1, kt1c, q);
   u32x2 raw[8];
   u32x4 bq[4], bc[4], a[2];
   p.read_b(sm.s, 0, 0, raw, bq);
@@ -349,7 +400,7 @@ __device__ __forceinline__ void gemm2_mainloop(G2Smem& sm, f32x16 (&acc)[4][4], 
   a[1] = p.read_a(sm.s, 1, 0);
   Pipe2<BNC>::pack_b(raw, bq, bc, 0);
   Pipe2<BNC>::pack_b(raw, bq, bc, 1);
-  for (int j = 0; j < n; ++j) gemm2_iter<BNC>(p, sm, acc, bc, a, j, kt0);
+  for (int j = 0; j < n; ++j) gemm2_iter<BNC, FAST>(p, sm, acc, bc, a, j, kt0);
   wait_vmcnt<0>();
   __syncthreads();
 }

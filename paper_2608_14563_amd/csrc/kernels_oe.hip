@@ -270,7 +270,7 @@ __device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], G2
   }
 }
 
-template <class E>
+template <class E, bool FAST>
 __global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
     const typename E::T* __restrict__ y, const typename E::T* __restrict__ Wc, int T, int d,
     int vc_valid, int v0, const float* __restrict__ ref, typename E::T* __restrict__ P, int64_t ldp,
@@ -287,7 +287,7 @@ __global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
     zero_acc2(acc);
     const Operand A{Wc + (int64_t)n0 * d, d, band_bytes(vc_valid - n0, d)};
     const Operand B{y + (int64_t)m0 * d, d, band_bytes(T - m0, d)};
-    gemm2_mainloop<false>(sm, acc, A, B, vc_valid - n0, T - m0, d, 0, (d + G2::BK - 1) / G2::BK);
+    gemm2_mainloop<false, FAST>(sm, acc, A, B, vc_valid - n0, T - m0, d, 0, (d + G2::BK - 1) / G2::BK);
     if (n0 + ((threadIdx.x >> 7) + 1) * G2::WTM <= vc_valid)  // wave-uniform
       logits_epilogue_vt<false>(acc, sm, n0, m0, T, vc_valid, v0, ref, P, ldp, nb, blk_m, blk_s, blk_i);
     else
@@ -476,7 +476,7 @@ __device__ __forceinline__ void proj_epilogue2(f32x16 (&acc)[4][4], G2Smem& sm, 
   }
 }
 
-template <class E>
+template <class E, bool FAST>
 __global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
     const typename E::T* __restrict__ P, int64_t ldp, const typename E::T* __restrict__ Wc,
     int T, int d, int vc_valid, int nb, int bps, int blkw, int first, int nsplit,
@@ -499,7 +499,7 @@ __global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
     const int kt0 = min(sp * bps * tpb, nkt), kt1 = min(min(nb, (sp + 1) * bps) * tpb, nkt);
     const Operand A{P + (int64_t)m0 * ldp, ldp, band_bytes(T - m0, ldp)};
     const Operand B{Wc + n0, d, band_bytes(vc_valid, d, n0)};
-    gemm2_mainloop<true>(sm, acc, A, B, T - m0, d - n0, vc_valid, kt0, kt1);
+    gemm2_mainloop<true, FAST>(sm, acc, A, B, T - m0, d - n0, vc_valid, kt0, kt1);
     proj_epilogue2(acc, sm, m0, n0, T, d, first, fout, alpha, Gs);
   } else {
     __shared__ GemmSmem<E> sm;
@@ -634,10 +634,18 @@ static hipError_t run_output_error(const OeLaunch& a) {
     const int vc_valid = (int)width;
     const int gn = (vc_valid + TT::BN - 1) / TT::BN;
     const int nbv = (vc_valid + TT::WTN - 1) / TT::WTN;  // blocks holding a valid column
-    FPO_LAUNCH("logits_chunk", st,
-               logits_chunk_kernel<E><<<dim3(gm * gn), dim3(256), 0, st>>>(
-        y, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, (int)v0, a.ref, P, a.ldp, nbv, a.blk_m, a.blk_s,
-        a.blk_i));
+    // whole 256 x 256 tiles and 64-deep K tiles: the copy form without bounds
+    const bool fast_l = vc_valid % TT::BM == 0 && a.T % TT::BN == 0 && a.d % 64 == 0;
+    if (fast_l)
+      FPO_LAUNCH("logits_chunk", st,
+                 logits_chunk_kernel<E, true><<<dim3(gm * gn), dim3(256), 0, st>>>(
+          y, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, (int)v0, a.ref, P, a.ldp, nbv, a.blk_m, a.blk_s,
+          a.blk_i));
+    else
+      FPO_LAUNCH("logits_chunk", st,
+                 logits_chunk_kernel<E, false><<<dim3(gm * gn), dim3(256), 0, st>>>(
+          y, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, (int)v0, a.ref, P, a.ldp, nbv, a.blk_m, a.blk_s,
+          a.blk_i));
     FPO_CHECK_LAUNCH();
     FPO_LAUNCH("chunk_stats", st,
                chunk_stats_kernel<T><<<dim3((unsigned)((a.T + 3) / 4)), dim3(256), 0, st>>>(
@@ -645,10 +653,18 @@ static hipError_t run_output_error(const OeLaunch& a) {
         P, a.ldp));
     FPO_CHECK_LAUNCH();
     const int bps = (nbv + a.nsplit - 1) / a.nsplit;
-    FPO_LAUNCH("proj_chunk", st,
-               proj_chunk_kernel<E><<<dim3(gm * (unsigned)((a.d + TT::BN - 1) / TT::BN) * a.nsplit), dim3(256), 0, st>>>(
-        P, a.ldp, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, nbv, bps, TT::WTN, c == 0, a.nsplit,
-        a.fout, a.alpha, a.G, a.T * a.d));
+    const bool fast_p = a.T % TT::BM == 0 && a.d % TT::BN == 0 && vc_valid % 64 == 0;
+    const dim3 gp(gm * (unsigned)((a.d + TT::BN - 1) / TT::BN) * a.nsplit);
+    if (fast_p)
+      FPO_LAUNCH("proj_chunk", st,
+                 proj_chunk_kernel<E, true><<<gp, dim3(256), 0, st>>>(
+          P, a.ldp, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, nbv, bps, TT::WTN, c == 0, a.nsplit,
+          a.fout, a.alpha, a.G, a.T * a.d));
+    else
+      FPO_LAUNCH("proj_chunk", st,
+                 proj_chunk_kernel<E, false><<<gp, dim3(256), 0, st>>>(
+          P, a.ldp, W + v0 * a.d, (int)a.T, (int)a.d, vc_valid, nbv, bps, TT::WTN, c == 0, a.nsplit,
+          a.fout, a.alpha, a.G, a.T * a.d));
     FPO_CHECK_LAUNCH();
   }
   FPO_LAUNCH("finalize_vjp", st,

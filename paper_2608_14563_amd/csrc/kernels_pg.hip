@@ -244,7 +244,7 @@ __device__ __forceinline__ void outer_epilogue2(const f32x16 (&acc)[4][4], int m
   }
 }
 
-template <class E>
+template <class E, bool FAST>
 __global__ __launch_bounds__(256, 1) void outer_kernel(OuterArgs args, int M, int N, int K,
                                                        int64_t lda, int64_t ldb, float scale,
                                                        double* __restrict__ part) {
@@ -274,7 +274,7 @@ __global__ __launch_bounds__(256, 1) void outer_kernel(OuterArgs args, int M, in
     zero_acc2(acc);
     const Operand A{Am + (int64_t)m0 * lda, lda, band_bytes(M - m0, lda)};
     const Operand B{Bm + n0, ldb, band_bytes(K, ldb, n0)};
-    gemm2_mainloop<true>(sm, acc, A, B, M - m0, N - n0, K, 0, (K + G2::BK - 1) / G2::BK);
+    gemm2_mainloop<true, FAST>(sm, acc, A, B, M - m0, N - n0, K, 0, (K + G2::BK - 1) / G2::BK);
     outer_epilogue2(acc, m0, n0, M, N, scale, args.C[mat], args.Cb[mat], args.R[mat], red, po);
   } else {
     __shared__ GemmSmem<E> sm;
@@ -372,7 +372,7 @@ __device__ __forceinline__ void errh_epilogue2(const f32x16 (&acc)[4][4], int m0
     }
 }
 
-template <class E>
+template <class E, bool FAST>
 __global__ __launch_bounds__(256, 1) void errh_kernel(const typename E::T* __restrict__ g,
                                                       const typename E::T* __restrict__ W3i,
                                                       const typename E::T* __restrict__ q,
@@ -391,7 +391,7 @@ __global__ __launch_bounds__(256, 1) void errh_kernel(const typename E::T* __res
     zero_acc2(acc);
     const Operand A{g + (int64_t)m0 * d, d, band_bytes(T - m0, d)};
     const Operand B{W3i + n0, d_ff, band_bytes(d, d_ff, n0)};
-    gemm2_mainloop<true>(sm, acc, A, B, T - m0, d_ff - n0, d, 0, (d + G2::BK - 1) / G2::BK);
+    gemm2_mainloop<true, FAST>(sm, acc, A, B, T - m0, d_ff - n0, d, 0, (d + G2::BK - 1) / G2::BK);
     errh_epilogue2(acc, m0, n0, q, u, T, Tp, d_ff, dq_T, du_T);
   } else {
     __shared__ GemmSmem<E> sm;
@@ -494,6 +494,31 @@ static const T* signal_rows(const PgLaunch& a, int l) {
   return (a.pffn || a.pre) ? (const T*)a.g_row + (int64_t)l * a.T * a.d : (const T*)a.g_lp;
 }
 
+// Whole 256 x 256 tiles and 64-deep K tiles (M, N multiples of 256, K of 64)
+// take the GEMM core's copy form without bounds selects.
+static bool whole_tiles(int64_t M, int64_t N, int64_t K) {
+  return M % 256 == 0 && N % 256 == 0 && K % 64 == 0;
+}
+
+template <class E>
+static void launch_outer(dim3 grid, hipStream_t st, const OuterArgs& oa, int M, int N, int K, int64_t lda,
+                         int64_t ldb, float scale, double* part) {
+  if (whole_tiles(M, N, K))
+    outer_kernel<E, true><<<grid, dim3(256), 0, st>>>(oa, M, N, K, lda, ldb, scale, part);
+  else
+    outer_kernel<E, false><<<grid, dim3(256), 0, st>>>(oa, M, N, K, lda, ldb, scale, part);
+}
+
+template <class E>
+static void launch_errh(dim3 grid, hipStream_t st, const typename E::T* g, const typename E::T* W3i,
+                        const typename E::T* q, const typename E::T* u, int T, int Tp, int d, int d_ff,
+                        typename E::T* dq_T, typename E::T* du_T) {
+  if (whole_tiles(T, d_ff, d))
+    errh_kernel<E, true><<<grid, dim3(256), 0, st>>>(g, W3i, q, u, T, Tp, d, d_ff, dq_T, du_T);
+  else
+    errh_kernel<E, false><<<grid, dim3(256), 0, st>>>(g, W3i, q, u, T, Tp, d, d_ff, dq_T, du_T);
+}
+
 template <class E>
 static hipError_t run_pseudograd(const PgLaunch& a) {
   using T = typename E::T;
@@ -514,8 +539,8 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
       oa.R[l] = a.ref[l];
     }
     FPO_LAUNCH("outer", st,
-               outer_kernel<E><<<dim3(ntiles * a.L), dim3(256), 0, st>>>(oa, (int)a.d, (int)a.d_ff, (int)a.T,
-                                                           a.Tp, a.d_ff, a.scale, a.part));
+               launch_outer<E>(dim3(ntiles * a.L), st, oa, (int)a.d, (int)a.d_ff, (int)a.T, a.Tp, a.d_ff,
+                               a.scale, a.part));
     FPO_CHECK_LAUNCH();
     FPO_LAUNCH("reduce_parts", st,
                reduce_parts_kernel<<<dim3(a.L), dim3(256), 0, st>>>(a.part, ntiles, 0, a.sumsq, a.ref_dot,
@@ -526,9 +551,10 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
   // W1/W2 signals through W3_init (eq. errh), one layer at a time
   for (int l = 0; l < a.L; ++l) {
     FPO_LAUNCH("errh", st,
-               errh_kernel<E><<<dim3((unsigned)(((a.Tp + TT::BM - 1) / TT::BM) * ((a.d_ff + TT::BN - 1) / TT::BN))), dim3(256), 0, st>>>(
-        signal_rows<T>(a, l), (const T*)a.W3i[l], (const T*)a.q[l], (const T*)a.u[l], (int)a.T, (int)a.Tp,
-        (int)a.d, (int)a.d_ff, (T*)a.dq_T, (T*)a.du_T));
+               launch_errh<E>(dim3((unsigned)(((a.Tp + TT::BM - 1) / TT::BM) * ((a.d_ff + TT::BN - 1) / TT::BN))),
+                              st, signal_rows<T>(a, l), (const T*)a.W3i[l], (const T*)a.q[l],
+                              (const T*)a.u[l], (int)a.T, (int)a.Tp, (int)a.d, (int)a.d_ff, (T*)a.dq_T,
+                              (T*)a.du_T));
     FPO_CHECK_LAUNCH();
     OuterArgs oa{};
     oa.A[0] = a.dq_T;
@@ -538,8 +564,8 @@ static hipError_t run_pseudograd(const PgLaunch& a) {
     oa.B[1] = a.x_in[l];
     oa.C[1] = a.dW2[l];
     FPO_LAUNCH("outer", st,
-               outer_kernel<E><<<dim3(ntiles2 * 2), dim3(256), 0, st>>>(oa, (int)a.d_ff, (int)a.d, (int)a.T,
-                                                         a.Tp, a.d, a.scale, a.part));
+               launch_outer<E>(dim3(ntiles2 * 2), st, oa, (int)a.d_ff, (int)a.d, (int)a.T, a.Tp, a.d, a.scale,
+                               a.part));
     FPO_CHECK_LAUNCH();
     // matrices W1(l) and W2(l) sit at a.L + l and 2 a.L + l of sumsq
     if (a.sumsq) {
@@ -627,8 +653,8 @@ static hipError_t enqueue_pseudograd_update(const PgLaunch& a, const UpdLaunch& 
     oa.R[0] = a.ref[l];
     double* tpart = a.part + (int64_t)l * ntiles * 3;
     FPO_LAUNCH("outer", st,
-               outer_kernel<TileBF16><<<dim3(ntiles), dim3(256), 0, st>>>(oa, (int)a.d, (int)a.d_ff, (int)a.T,
-                                                                 a.Tp, a.d_ff, a.scale, tpart));
+               launch_outer<TileBF16>(dim3(ntiles), st, oa, (int)a.d, (int)a.d_ff, (int)a.T, a.Tp, a.d_ff,
+                                      a.scale, tpart));
     FPO_CHECK_LAUNCH();
     // layer l's tiles are complete: its norm reduction and update follow on the
     // side stream, so the next layer's outer products start right away

@@ -69,8 +69,11 @@ def test_fp32_ragged(dev, T, d, V, chunk):
     check_against_oracle(x, g, W, y, "f32", got)
 
 
+# (512, 512, 4224, 1024) and (512, 256, 2048, 0) are whole 256 x 256 tiles (the
+# GEMM core's copy form without bounds), the first with a ragged last chunk
 @pytest.mark.parametrize("T,d,V,chunk", [(300, 264, 4104, 1024), (600, 512, 10000, 0), (256, 256, 4096, 2048), (1, 128, 1024, 0),
-                                         (5, 8200, 264, 0), (16, 64, 200000, 0)])
+                                         (5, 8200, 264, 0), (16, 64, 200000, 0), (512, 512, 4224, 1024),
+                                         (512, 256, 2048, 0)])
 def test_bf16_ragged(dev, T, d, V, chunk):
     c, x, g, W, y = small_case(I.CONFIGS[1], T, d, V)
     got = run_gpu(x, g, W, y, "bf16", dev, chunk=chunk)

@@ -41,8 +41,10 @@ def run_w3(c, g, acts, dev, refs=None, store=True):
     return out
 
 
+# (1, 256, 256, 512, 2) and (1, 512, 512, 768, 3): whole tiles (copy form without bounds)
 @pytest.mark.parametrize("cid,T,d,d_ff,L", [(0, 128, 256, 688, 2), (0, 300, 264, 520, 3), (1, 300, 264, 520, 2),
-                                            (1, 1000, 512, 1032, 2), (1, 1, 256, 512, 1), (3, 333, 256, 1000, 2)])
+                                            (1, 1000, 512, 1032, 2), (1, 1, 256, 512, 1), (3, 333, 256, 1000, 2),
+                                            (1, 256, 256, 512, 2), (1, 512, 512, 768, 3)])
 def test_w3_outer_products(dev, cid, T, d, d_ff, L):
     c = I.CONFIGS[cid].shrink(T=T, d=d, d_ff=d_ff, L=L)
     g = signal(c)
@@ -84,7 +86,7 @@ def test_fused_diagnostic_cosine(dev, cid):
         assert np.array_equal(with_store["dot"], fused["dot"])
 
 
-@pytest.mark.parametrize("cid,T,d,d_ff,L", [(0, 128, 256, 688, 2), (1, 200, 256, 520, 2)])
+@pytest.mark.parametrize("cid,T,d,d_ff,L", [(0, 128, 256, 688, 2), (1, 200, 256, 520, 2), (1, 256, 256, 512, 2)])
 def test_full_mlp(dev, cid, T, d, d_ff, L):
     c = I.CONFIGS[cid].shrink(T=T, d=d, d_ff=d_ff, L=L)
     g = signal(c)
