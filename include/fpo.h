@@ -261,8 +261,8 @@ typedef struct {
 } fpo_pre_mlp;
 
 /* Caller-owned side stream and events for fpo_pseudograd's overlapped
- * optimizer path (each layer's update runs on side_stream beside the next
- * layer's outer products). All three are hipStream_t / hipEvent_t handles of
+ * optimizer path (each matrix's update runs on side_stream beside the GEMM
+ * launches that follow its outer products). All three are hipStream_t / hipEvent_t handles of
  * the current device; the events should be created with
  * hipEventDisableTiming. The library only records, waits on and launches into
  * them; a set must not be used by two calls that run concurrently. */
@@ -313,10 +313,12 @@ typedef struct {
  *              optimizer path (see fpo_overlap); NULL uses the library's own
  *              (see "Library state" above)
  *   stream     the work is ordered on this stream. With opt given on the
- *              FPO_BF16 / FPO_MODE_W3 path with the gradient clip, each
- *              layer's update runs on the side stream, overlapping the next
- *              layer's outer products, and is joined back to `stream` with an
- *              event before the call's last kernel.
+ *              FPO_BF16 path with the gradient clip (W3 only or FULL_MLP),
+ *              each matrix's norm reduction and update run on the side
+ *              stream once its outer products are done, overlapping the GEMM
+ *              launches that follow (the next layer's outer products; with
+ *              FULL_MLP the W1/W2 launches too), and are joined back to
+ *              `stream` with an event before the call's last kernel.
  * Returns FPO_OK or an fpo_status. */
 size_t fpo_pseudograd_workspace(const fpo_pg_desc* desc);
 int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* const* a,

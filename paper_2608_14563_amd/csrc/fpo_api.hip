@@ -256,7 +256,9 @@ size_t carve_pg(const fpo_pg_desc& d, const PgPlan& p, void* ws, fpo::PgLaunch* 
   float* pstats = chain ? c.take<float>(4 * d.T) : nullptr;  // per-token norm-chain statistics
   void* dq = full ? c.take<char>(d.d_ff * p.Tp * esz) : nullptr;
   void* du = full ? c.take<char>(d.d_ff * p.Tp * esz) : nullptr;
-  double* part = c.take<double>(std::max<int64_t>(d.L, 2) * p.ntiles * 3);
+  // tile partials: a region per matrix (3 L with the full MLP: the overlapped
+  // update reduces each matrix's partials while later launches run)
+  double* part = c.take<double>((full ? 3 * d.L : std::max<int64_t>(d.L, 2)) * p.ntiles * 3);
   double* up = c.take<double>(p.upd_blocks);
   double* dsq = c.take<double>(p.nmats);  // ||delta||^2 per matrix (clip-the-update mode)
   // staged bf16 pseudogradients (FPO_MODE_GRAD_BF16), one 256-aligned matrix per layer
@@ -640,10 +642,10 @@ int fpo_pseudograd(const fpo_pg_desc* desc, const void* g_tilde_lp, const void* 
     U.stream = stream;
   }
   hipError_t e;
-  if (opt && P.bf16 && !full && !U.clip_update) {
-    // W3 only, bf16, gradient clip: layer l's update overlaps layer l+1's
-    // outer products (clip-the-update needs every step's norm first: two
-    // passes after the pseudogradient)
+  if (opt && P.bf16 && !U.clip_update) {
+    // bf16, gradient clip: each matrix's update overlaps the GEMM launches
+    // that follow its outer products (clip-the-update needs every step's norm
+    // first: two passes after the pseudogradient)
     fpo::OverlapLaunch ov{};
     if (overlap) ov = fpo::OverlapLaunch{overlap->side_stream, overlap->ready_event, overlap->done_event};
     e = fpo::launch_pseudograd_update(P, U, overlap ? &ov : nullptr);

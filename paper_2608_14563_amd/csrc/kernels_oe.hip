@@ -228,6 +228,9 @@ __device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], G2
       }
     }
     const float base = block_base(m, R[i]);
+    // exp(z - base) as 2^(z log2 e - base log2 e): one fma ahead of the exp
+    // instead of a subtract and a multiply (the staged value is bf16)
+    const float nb2 = -base * 1.44269504088896341f;
     float s = 0.f;
     // LDS token row of this lane and the tile column of its entries at f = q = 0
     const int lrow = (w & 1) * G2::WTN + 32 * i + lc;
@@ -241,7 +244,8 @@ __device__ __forceinline__ void logits_epilogue_vt(const f32x16 (&acc)[4][4], G2
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int o = 32 * f + 8 * q + j;
-          p[j] = (!RAGGED || o < lim) ? __expf(acc[f][i][4 * q + j] - base) : 0.f;
+          p[j] = (!RAGGED || o < lim) ? __builtin_amdgcn_exp2f(fmaf(acc[f][i][4 * q + j], 1.44269504088896341f, nb2))
+                                      : 0.f;
           s += p[j];
         }
         const int chunk = ((col0 + 32 * f + 8 * q) >> 3) ^ lc;  // lrow & 31 == lc
@@ -288,7 +292,7 @@ __global__ __launch_bounds__(256, 1) void logits_chunk_kernel(
     const Operand A{Wc + (int64_t)n0 * d, d, band_bytes(vc_valid - n0, d)};
     const Operand B{y + (int64_t)m0 * d, d, band_bytes(T - m0, d)};
     gemm2_mainloop<false, FAST>(sm, acc, A, B, vc_valid - n0, T - m0, d, 0, (d + G2::BK - 1) / G2::BK);
-    if (n0 + ((threadIdx.x >> 7) + 1) * G2::WTM <= vc_valid)  // wave-uniform
+    if (FAST || n0 + ((threadIdx.x >> 7) + 1) * G2::WTM <= vc_valid)  // wave-uniform; FAST: whole tiles
       logits_epilogue_vt<false>(acc, sm, n0, m0, T, vc_valid, v0, ref, P, ldp, nb, blk_m, blk_s, blk_i);
     else
       logits_epilogue_vt<true>(acc, sm, n0, m0, T, vc_valid, v0, ref, P, ldp, nb, blk_m, blk_s, blk_i);

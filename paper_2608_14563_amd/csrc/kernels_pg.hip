@@ -11,9 +11,9 @@
 //   errh_kernel   : E = g~ W3_init (MFMA); du = E*SiLU(q), dq = E*u*SiLU'(q),
 //                   stored token-contiguous for the W1/W2 outer products
 //   reduce_parts  : fixed-order float64 sums of the tile partials
-// With the optimizer fused (bf16, W3 only), launch_pseudograd_update runs the
-// outer products one layer per launch and each layer's update on a side stream,
-// overlapping the next layer's outer products.
+// With the optimizer fused (bf16), launch_pseudograd_update runs the outer
+// products one layer per launch and each matrix's update on a side stream,
+// overlapping the GEMM launches that follow.
 #include "gemm.hpp"
 #include "gemm2.hpp"
 #include "launch.hpp"
@@ -607,13 +607,16 @@ static hipError_t pg_overlap_init(PgOverlap& p, int dev) {
   return hipSuccess;
 }
 
-// W3-only bf16 pseudogradient with the optimizer step overlapped: the outer
-// products run one layer per launch on the caller's stream; once layer l's
-// tiles and norm are done, its update (few registers and no LDS, so its
-// workgroups sit beside the GEMM's on the same CUs) streams on a side stream
-// while layer l+1's MFMAs run, with one workgroup per CU so that each CU holds
-// one outer-product workgroup and one update workgroup; the last layer's update
-// has the machine to itself. Same per-block arithmetic and reduction order as the
+// bf16 pseudogradient with the optimizer step overlapped: the outer products
+// run one layer per launch on the caller's stream; once a matrix's tiles are
+// done, its norm and update (few registers and no LDS, so its workgroups sit
+// beside an outer-product GEMM's on the same CUs) stream on a side stream while
+// the following launches run, with one workgroup per CU so that each CU holds
+// one GEMM workgroup and one update workgroup; the updates released by the last
+// launch have the machine to itself. With the full MLP, the W3 launches come
+// first, then per layer the W1/W2 signal GEMM (eq. errh: all registers, so an
+// update workgroup and an errh workgroup take turns on a CU) and one launch of
+// both W1/W2 outer products, which releases both updates. Same per-block arithmetic and reduction order as the
 // separate calls, so results are bit-identical to them. The side stream and its
 // two events are the caller's (ov) or, when ov is null, the device's
 // library-owned set, whose enqueue sequence is serialised by a lock.
@@ -643,7 +646,36 @@ static hipError_t enqueue_pseudograd_update(const PgLaunch& a, const UpdLaunch& 
   hipError_t e;
   if ((e = prepare_signals<uint16_t>(a, st)) != hipSuccess) return e;
   const int ntiles = (int)pseudograd_tiles(true, a.d, a.d_ff);
-  int64_t blk_base = 0;
+  const int ntiles2 = (int)pseudograd_tiles(true, a.d_ff, a.d);
+  // matrix m: W3 of layer m (m < L), then W1 and W2 of layer l at L + l and
+  // 2 L + l; its update blocks start at the sum of the earlier matrices'
+  // blocks. Tile partials have a region per matrix (the side stream reads them
+  // while later launches run): slot l for W3 of layer l, slots L + 2l and
+  // L + 2l + 1 for W1 and W2 of layer l (one launch writes both, the second
+  // matrix's partials right after the first's).
+  const int nm = a.full_mlp ? 3 * a.L : a.L;
+  int64_t blk_base[kMaxMats + 1];
+  blk_base[0] = 0;
+  for (int m = 0; m < nm; ++m) blk_base[m + 1] = blk_base[m] + update_blocks(u.numel[m]);
+  auto tpart = [&](int slot) { return a.part + (int64_t)slot * ntiles * 3; };
+  // the norm reduction and the update of matrix m (partials in `slot`) on the
+  // side stream, after the launch just enqueued on st; `alone`: no GEMM
+  // follows to share the CUs
+  auto release = [&](int m, int slot, int nt, bool ref, bool alone) -> hipError_t {
+    FPO_LAUNCH("reduce_parts", side,
+               reduce_parts_kernel<<<dim3(1), dim3(256), 0, side>>>(
+        tpart(slot), nt, m, a.sumsq, ref && a.ref_dot ? a.ref_dot + m : nullptr,
+        ref && a.ref_sumsq ? a.ref_sumsq + m : nullptr, ref && a.ref_cos ? a.ref_cos + m : nullptr));
+    FPO_CHECK_LAUNCH();
+    // one workgroup per CU beside the next GEMM launch; the last updates run
+    // alone and take the whole machine
+    return launch_update_blocks(u, m, blk_base[m], side, alone ? 0 : cus);
+  };
+  auto handoff = [&]() -> hipError_t {
+    hipError_t r;
+    if ((r = hipEventRecord(ready_l, st)) != hipSuccess) return r;
+    return hipStreamWaitEvent(side, ready_l, 0);
+  };
   for (int l = 0; l < a.L; ++l) {
     OuterArgs oa{};
     oa.A[0] = signal_T<uint16_t>(a, l);
@@ -651,24 +683,41 @@ static hipError_t enqueue_pseudograd_update(const PgLaunch& a, const UpdLaunch& 
     oa.C[0] = a.dW3[l];
     oa.Cb[0] = a.dW3_bf16[l];
     oa.R[0] = a.ref[l];
-    double* tpart = a.part + (int64_t)l * ntiles * 3;
     FPO_LAUNCH("outer", st,
                launch_outer<TileBF16>(dim3(ntiles), st, oa, (int)a.d, (int)a.d_ff, (int)a.T, a.Tp, a.d_ff,
-                                      a.scale, tpart));
+                                      a.scale, tpart(l)));
     FPO_CHECK_LAUNCH();
     // layer l's tiles are complete: its norm reduction and update follow on the
     // side stream, so the next layer's outer products start right away
-    if ((e = hipEventRecord(ready_l, st)) != hipSuccess) return e;
-    if ((e = hipStreamWaitEvent(side, ready_l, 0)) != hipSuccess) return e;
-    FPO_LAUNCH("reduce_parts", side,
-               reduce_parts_kernel<<<dim3(1), dim3(256), 0, side>>>(
-        tpart, ntiles, l, a.sumsq, a.ref_dot ? a.ref_dot + l : nullptr,
-        a.ref_sumsq ? a.ref_sumsq + l : nullptr, a.ref_cos ? a.ref_cos + l : nullptr));
+    if ((e = handoff()) != hipSuccess) return e;
+    if ((e = release(l, l, ntiles, true, !a.full_mlp && l + 1 == a.L)) != hipSuccess) return e;
+  }
+  // full MLP: W1/W2 signals through W3_init (eq. errh), then both outer
+  // products of the layer in one launch, their updates released together
+  for (int l = 0; a.full_mlp && l < a.L; ++l) {
+    FPO_LAUNCH("errh", st,
+               launch_errh<TileBF16>(dim3((unsigned)(((a.Tp + 255) / 256) * ((a.d_ff + 255) / 256))), st,
+                                     signal_rows<uint16_t>(a, l), (const uint16_t*)a.W3i[l],
+                                     (const uint16_t*)a.q[l], (const uint16_t*)a.u[l], (int)a.T, (int)a.Tp,
+                                     (int)a.d, (int)a.d_ff, (uint16_t*)a.dq_T, (uint16_t*)a.du_T));
     FPO_CHECK_LAUNCH();
-    // one workgroup per CU while the next layer's outer products run; the last
-    // update runs alone and takes the whole machine
-    if ((e = launch_update_blocks(u, l, blk_base, side, l + 1 < a.L ? cus : 0)) != hipSuccess) return e;
-    blk_base += update_blocks(u.numel[l]);
+    const int m1 = a.L + l, m2 = 2 * a.L + l;
+    OuterArgs oa{};
+    oa.A[0] = a.dq_T;
+    oa.B[0] = a.x_in[l];
+    oa.C[0] = a.dW1[l];
+    oa.A[1] = a.du_T;
+    oa.B[1] = a.x_in[l];
+    oa.C[1] = a.dW2[l];
+    const int slot = a.L + 2 * l;  // ntiles2 == ntiles (256 x 256 tiles of d x d_ff or d_ff x d)
+    FPO_LAUNCH("outer", st,
+               launch_outer<TileBF16>(dim3(ntiles2 * 2), st, oa, (int)a.d_ff, (int)a.d, (int)a.T, a.Tp, a.d,
+                                      a.scale, tpart(slot)));
+    FPO_CHECK_LAUNCH();
+    if ((e = handoff()) != hipSuccess) return e;
+    const bool last = l + 1 == a.L;
+    if ((e = release(m1, slot, ntiles2, false, last)) != hipSuccess) return e;
+    if ((e = release(m2, slot + 1, ntiles2, false, last)) != hipSuccess) return e;
   }
   if ((e = hipEventRecord(done, side)) != hipSuccess) return e;
   if ((e = hipStreamWaitEvent(st, done, 0)) != hipSuccess) return e;

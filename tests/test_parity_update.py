@@ -286,6 +286,60 @@ def test_fused_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip, pff
 
 
 @pytest.mark.parametrize("target", [0, 1], ids=["clip-grad", "clip-update"])
+@pytest.mark.parametrize("kind", ["sgd", "adamw"])
+@pytest.mark.parametrize("T,d,d_ff,L,clip", [(256, 256, 512, 2, 0.01), (300, 264, 1000, 3, 0.01),
+                                             (200, 1032, 1288, 2, 1e-5)])
+def test_fused_full_mlp_update_matches_separate_calls(dev, kind, T, d, d_ff, L, clip, target):
+    """Full-MLP pseudogradient with the optimizer fused (bf16, gradient clip:
+    each matrix's update released on the side stream once its outer products
+    are done, beside the W1/W2 signal and outer-product launches that follow)
+    is bit-identical to the pseudogradient followed by fpo_apply_update over
+    the 3 L matrices (W3, W1, W2), over two steps; whole tiles, a ragged shape,
+    and matrices of more update blocks than compute units with an active clip."""
+    c = I.CONFIGS[1].shrink(T=T, d=d, d_ff=d_ff, L=L)
+    g = dev_tensor(I.synthetic_signal(c), dev)
+    caches = [I.mlp_cache(c, l) for l in range(L)]
+    extras = [I.full_mlp_extra(c, l) for l in range(L)]
+    acts = [dev_tensor(cc[2], dev) for cc in caches]
+    W0 = [torch.from_numpy(I.master_weight(c, l)).to(dev) for l in range(L)]
+    W0 += [torch.from_numpy(e[1]).to(dev) for e in extras] + [torch.from_numpy(e[2]).to(dev) for e in extras]
+    fkw = dict(W3_init=[w.to(torch.bfloat16) for w in W0[:L]], gate=[dev_tensor(cc[0], dev) for cc in caches],
+               up=[dev_tensor(cc[1], dev) for cc in caches], x_in=[dev_tensor(e[0], dev) for e in extras])
+    adam = kind == "adamw"
+    n = 3 * L
+
+    def fresh():
+        W = [w.clone() for w in W0]
+        return dict(W=W, s1=[torch.zeros_like(w) for w in W], s2=[torch.zeros_like(w) for w in W] if adam else None,
+                    lp=[torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in W],
+                    Wsq=torch.tensor([float((w.double() ** 2).sum()) for w in W], dtype=torch.float64, device=dev),
+                    dW3=[torch.empty(d, d_ff, dtype=torch.float32, device=dev) for _ in range(L)],
+                    dW1=[torch.empty(d_ff, d, dtype=torch.float32, device=dev) for _ in range(L)],
+                    dW2=[torch.empty(d_ff, d, dtype=torch.float32, device=dev) for _ in range(L)],
+                    ss=torch.empty(n, dtype=torch.float64, device=dev),
+                    cs=torch.empty(n, dtype=torch.float32, device=dev))
+
+    sep, fus = fresh(), fresh()
+    for step in (1, 2):
+        opt = api.OptConfig(kind=L_.FPO_OPT_ADAMW if adam else L_.FPO_OPT_SGD, lr=1e-2, clip_frac=clip, step=step,
+                            momentum=0.9, clip_target=target)
+        api.fpo_pseudograd(g, acts, dW3=sep["dW3"], dW1=sep["dW1"], dW2=sep["dW2"], sumsq=sep["ss"], **fkw)
+        api.fpo_apply_update(opt, sep["dW3"] + sep["dW1"] + sep["dW2"], sep["ss"], sep["W"], sep["s1"], sep["Wsq"],
+                             W_lp=sep["lp"], state2=sep["s2"], clip_scale=sep["cs"])
+        api.fpo_pseudograd(g, acts, dW3=fus["dW3"], dW1=fus["dW1"], dW2=fus["dW2"], sumsq=fus["ss"], opt=opt,
+                           W_master=fus["W"], W_lp=fus["lp"], state1=fus["s1"], state2=fus["s2"],
+                           W_sumsq=fus["Wsq"], clip_scale=fus["cs"], **fkw)
+        torch.cuda.synchronize()
+        for key in ("W", "lp", "s1", "dW3", "dW1", "dW2") + (("s2",) if adam else ()):
+            for i, (a, b) in enumerate(zip(sep[key], fus[key])):
+                assert torch.equal(a, b), (key, i, step)
+        for key in ("Wsq", "ss", "cs"):
+            assert torch.equal(sep[key], fus[key]), (key, step)
+    if clip < 1e-4:
+        assert float(fus["cs"].max()) < 1.0  # the clip was active
+
+
+@pytest.mark.parametrize("target", [0, 1], ids=["clip-grad", "clip-update"])
 @pytest.mark.parametrize("kind", ["sgd", "adamw", "sgd-plain"])
 @pytest.mark.parametrize("T,d,d_ff,L,clip,pffn", [(300, 264, 1000, 3, 0.01, False), (200, 1032, 1288, 3, 1e-5, False),
                                                   (300, 264, 1000, 2, 0.01, True)])
