@@ -732,11 +732,12 @@ def main():
                            W_master=Wm, W_lp=Wlp, state1=s1, state2=s2, W_sumsq=Wsq, ws=ws_pg, post_ffn=pffn,
                            **fkw)
 
-    # On the overlapped path (bf16 W3 pseudogradient, gradient clip) every
-    # optimizer launch runs on a side stream beside the next layer's outer
-    # products, and at the OLMo-2 shapes the two summed times are within a few
-    # percent, so the dominant kernel is taken among the step stream's own.
-    overlapped = args.clip_target != "update" and not full
+    # On the overlapped path (bf16 pseudogradient, gradient clip; W3 only or
+    # the full MLP) every optimizer launch runs on a side stream beside the
+    # GEMM launches that follow, and the two summed times are close (OLMo-2
+    # shapes: within a few percent), so the dominant kernel is taken among the
+    # step stream's own.
+    overlapped = args.clip_target != "update"
     cu = args.clip_target == "update"
 
     def work(k, n):
