@@ -372,6 +372,89 @@ __device__ __forceinline__ void errh_epilogue2(const f32x16 (&acc)[4][4], int m0
     }
 }
 
+// bf16 form for whole tiles (T and d_ff multiples of 256: no bounds), the
+// transposed outputs staged through LDS one output per pass (pass 0: dq;
+// pass 1: du, q loaded again; the accumulators are only read, so no register
+// holds a second output): the lane's values for 4 consecutive tokens x 4
+// consecutive columns go into the idle LDS ring as the 256 column x 256 token
+// tile [column][32 chunks of 8 tokens] (chunk c of column j at position
+// c ^ ((j >> 2) & 31)), then whole 512-byte token-contiguous rows of dq^T /
+// du^T are stored. (Stored directly, each lane's 8-byte runs of 4 tokens land
+// Tp apart: about 60 us of a 170 us tile at the OLMo-2 shapes; ragged tiles
+// still take that form.) q and u are read as 8-byte runs of the lane's 4
+// columns, one fragment group ahead of their use.
+__device__ __forceinline__ void errh_epilogue_lds(f32x16 (&acc)[4][4], G2Smem& sm, int m0, int n0,
+                                                  const uint16_t* __restrict__ q,
+                                                  const uint16_t* __restrict__ u, int Tp,
+                                                  int d_ff, uint16_t* __restrict__ dq_T,
+                                                  uint16_t* __restrict__ du_T) {
+  const AccMap2<true> mp;
+  const int jl0 = mp.col(0);  // tile-relative first of the lane's 4 columns
+  const int j0 = n0 + jl0;
+  const int tr0 = mp.row(0, 0);  // tile-relative first token of the lane
+  const int64_t lane_off = (int64_t)(m0 + tr0) * d_ff + j0;  // element (token m0 + tr0, column j0)
+  char* lds = reinterpret_cast<char*>(sm.s);
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    // group k = 4 f + g: tokens m0 + tr0 + 32 f + 8 g .. + 3 (a uniform step from the lane's first)
+    auto load = [&](int k, u32x2 (&qv)[4], u32x2 (&uv)[4]) {
+      const int dt = 32 * (k >> 2) + 8 * (k & 3);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t o = lane_off + (int64_t)(dt + r) * d_ff;
+        qv[r] = *reinterpret_cast<const u32x2*>(q + o);
+        uv[r] = pass == 0 ? *reinterpret_cast<const u32x2*>(u + o) : u32x2{0u, 0u};
+      }
+    };
+    u32x2 qn[4], un[4];
+    load(0, qn, un);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int f = k >> 2, g = k & 3;
+      u32x2 qv[4], uv[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        qv[r] = qn[r];
+        uv[r] = un[r];
+      }
+      if (k + 1 < 16) load(k + 1, qn, un);
+      const int tl0 = mp.row(f, 4 * g);  // tile-relative tokens tl0 .. tl0 + 3
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const uint32_t qw = qv[r][i >> 1], uw = uv[r][i >> 1];
+          const float qq = (i & 1) ? bf16_hi(qw) : bf16_lo(qw);
+          const float uu = (i & 1) ? bf16_hi(uw) : bf16_lo(uw);
+          // read from its accumulator register at each use (both passes),
+          // so no pass keeps a copy of the whole tile in vector registers
+          float e;
+          asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(e) : "a"(acc[f][i][4 * g + r]));
+          // SiLU(q) = q sg, SiLU'(q) = sg (1 + q (1 - sg)); the reciprocal to
+          // about 1 ulp (the values are rounded to bf16 next)
+          const float sg = __builtin_amdgcn_rcpf(1.0f + __expf(-qq));
+          v[r] = pass == 0 ? e * uu * sg * (1.0f + qq * (1.0f - sg)) : e * qq * sg;
+        }
+        const int jl = jl0 + i;
+        const int pos = ((tl0 >> 3) ^ ((jl >> 2) & 31)) * 16 + ((tl0 >> 2) & 1) * 8;
+        *reinterpret_cast<u32x2*>(lds + jl * 512 + pos) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+      }
+    }
+    __syncthreads();
+    uint16_t* dst = pass == 0 ? dq_T : du_T;
+    const int c = threadIdx.x & 31;
+#pragma unroll 4
+    for (int kk = 0; kk < 32; ++kk) {
+      const int jl = (int)(threadIdx.x >> 5) + 8 * kk;
+      const int t = m0 + 8 * c;
+      *reinterpret_cast<u32x4*>(dst + (int64_t)(n0 + jl) * Tp + t) =
+            *reinterpret_cast<const u32x4*>(lds + jl * 512 + ((c ^ ((jl >> 2) & 31)) * 16));
+    }
+    __syncthreads();
+  }
+}
+
 template <class E, bool FAST>
 __global__ __launch_bounds__(256, 1) void errh_kernel(const typename E::T* __restrict__ g,
                                                       const typename E::T* __restrict__ W3i,
@@ -392,7 +475,10 @@ __global__ __launch_bounds__(256, 1) void errh_kernel(const typename E::T* __res
     const Operand A{g + (int64_t)m0 * d, d, band_bytes(T - m0, d)};
     const Operand B{W3i + n0, d_ff, band_bytes(d, d_ff, n0)};
     gemm2_mainloop<true, FAST>(sm, acc, A, B, T - m0, d_ff - n0, d, 0, (d + G2::BK - 1) / G2::BK);
-    errh_epilogue2(acc, m0, n0, q, u, T, Tp, d_ff, dq_T, du_T);
+    if constexpr (FAST)
+      errh_epilogue_lds(acc, sm, m0, n0, q, u, Tp, d_ff, dq_T, du_T);
+    else
+      errh_epilogue2(acc, m0, n0, q, u, T, Tp, d_ff, dq_T, du_T);
   } else {
     __shared__ GemmSmem<E> sm;
     f32x4 acc[E::FM][E::FN];
