@@ -221,7 +221,7 @@ def _cpu_info():
 
 def auto_cpu_tokens(c, per_token_flop, budget=1.0e13):
     """Token sample for the oracle: about 10 TFLOP of float64 work (10-20 s
-    on the GPU machine's 16 host cores), at most the whole batch."""
+    on 16 host cores), at most the whole batch."""
     return max(1, min(c.T, int(budget // per_token_flop)))
 
 
