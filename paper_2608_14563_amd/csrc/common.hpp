@@ -93,6 +93,26 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   for (int i = 0; i < nw; ++i) s += red[i];  // fixed order
   return s;
 }
+// Two block sums in one exchange (two barriers instead of four); each value
+// is summed exactly as block_sum sums it. red holds 2 * (waves) floats.
+__device__ __forceinline__ void block_sum2(float& a, float& b, float* red) {
+  a = wave_sum(a);
+  b = wave_sum(b);
+  const int w = threadIdx.x / kWave, l = threadIdx.x % kWave, nw = blockDim.x / kWave;
+  __syncthreads();
+  if (l == 0) {
+    red[w] = a;
+    red[nw + w] = b;
+  }
+  __syncthreads();
+  float sa = 0.f, sb = 0.f;
+  for (int i = 0; i < nw; ++i) {  // fixed order
+    sa += red[i];
+    sb += red[nw + i];
+  }
+  a = sa;
+  b = sb;
+}
 // One thread's share of sum_b v[b], b in [begin, end), of a 256-lane
 // workgroup: elements begin + tid + 256k in a fixed order, with four
 // independent accumulators so that four loads are in flight.

@@ -178,6 +178,7 @@ size_t carve_oe(const fpo_oe_desc& d, const OePlan& p, void* ws, fpo::OeLaunch* 
   float* fout = c.take<float>(d.T);
   float* alpha = c.take<float>(d.T);
   float* ref = c.take<float>(d.T);
+  float* zt = c.take<float>(d.T);
   float* runM = c.take<float>(d.T);
   float* runS = c.take<float>(d.T);
   int32_t* runA = c.take<int32_t>(d.T);
@@ -191,6 +192,7 @@ size_t carve_oe(const fpo_oe_desc& d, const OePlan& p, void* ws, fpo::OeLaunch* 
     L->fout = fout;
     L->alpha = alpha;
     L->ref = ref;
+    L->zt = zt;
     L->runM = runM;
     L->runS = runS;
     L->runA = runA;

@@ -41,6 +41,7 @@ __global__ __launch_bounds__(256) void rms_forward_kernel(const T* __restrict__ 
                                                           const T* __restrict__ W_U,
                                                           const int32_t* __restrict__ targets, int V,
                                                           float* __restrict__ ref,
+                                                          float* __restrict__ zt,
                                                           int32_t* __restrict__ bad) {
   __shared__ float red[16];
   const int64_t row = blockIdx.x;
@@ -77,7 +78,10 @@ __global__ __launch_bounds__(256) void rms_forward_kernel(const T* __restrict__ 
   }
   for (int k = threadIdx.x * 4 + kRowRegIters * 1024; k < d; k += 1024) out(k, ld4(xr, k));
   zr = block_sum(zr, red);
-  if (threadIdx.x == 0) ref[row] = zr;
+  if (threadIdx.x == 0) {
+    ref[row] = zr;
+    zt[row] = zr;  // the loss's target logit (valid targets), for finalize_vjp
+  }
   if (bad && row == 0 && threadIdx.x == 0) *bad = 0;
 }
 
@@ -522,16 +526,19 @@ __global__ __launch_bounds__(256, 1) void proj_chunk_kernel(
 // outside [0, V)), then the clamped VJP
 //   rho~ = max(sqrt(mean x^2 + eps), min_rms); x^ = x / rho~;
 //   c = (1/d) <x^, gamma * g>;  g~ = (gamma * g - c x^) / rho~.
+// The loss takes the target logit that rms_forward formed from the stored y
+// (the same products and summation order as a second pass here would use),
+// so the row of y is not read again.
 template <typename T>
 __global__ __launch_bounds__(256) void finalize_vjp_kernel(
     int d, int V, int nsplit, int64_t split_stride, const float* __restrict__ G,
     const float* __restrict__ runM, const float* __restrict__ runS,
-    const int32_t* __restrict__ runA, const T* __restrict__ y,
+    const int32_t* __restrict__ runA, const float* __restrict__ zt,
     const int32_t* __restrict__ targets, const T* __restrict__ W_U, const T* __restrict__ x,
     const T* __restrict__ gamma, float eps, float min_rms, float* __restrict__ g_tilde,
     T* __restrict__ g_tilde_lp, float* __restrict__ g_pre, float* __restrict__ lse,
     float* __restrict__ loss, int32_t* __restrict__ argmax, int32_t* __restrict__ bad) {
-  __shared__ float red[16];
+  __shared__ float red[32];
   const int64_t row = blockIdx.x;
   const int tg = targets[row];
   const bool valid = tg >= 0 && tg < V;
@@ -539,7 +546,7 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
   const float invS = 1.0f / S;
   const T* xr = x + row * d;
   float* gt = g_tilde + row * d;
-  float ss = 0.f, cd = 0.f, zt = 0.f;
+  float ss = 0.f, cd = 0.f;
   // pass 1: g = sum_s G_s / S - W_U[y] and the row reductions. Rows of up to
   // kRowRegIters * 1024 entries keep g and x in registers for pass 2; longer
   // rows park the rest of g in the g~ row (rewritten in pass 2).
@@ -548,12 +555,7 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int s = 0; s < nsplit; ++s) acc += *reinterpret_cast<const f32x4*>(G + s * split_stride + row * d + k);
     f32x4 g = {0.f, 0.f, 0.f, 0.f};
-    if (valid) {
-      f32x4 wy = ld4(W_U + (int64_t)tg * d, k);
-      f32x4 yv = ld4(y + row * d, k);
-      g = acc * invS - wy;
-      zt += yv.x * wy.x + yv.y * wy.y + yv.z * wy.z + yv.w * wy.w;  // target logit z_y
-    }
+    if (valid) g = acc * invS - ld4(W_U + (int64_t)tg * d, k);
     if (g_pre) *reinterpret_cast<f32x4*>(g_pre + row * d + k) = g;
     return g;
   };
@@ -576,9 +578,7 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
     *reinterpret_cast<f32x4*>(gt + k) = g;
     reduce(g, xv, ld4(gamma, k));
   }
-  ss = block_sum(ss, red);
-  cd = block_sum(cd, red);
-  zt = block_sum(zt, red);
+  block_sum2(ss, cd, red);
   const float rho = sqrtf(ss / (float)d + eps);
   const float rt = fmaxf(rho, min_rms);
   const float irt = 1.0f / rt;
@@ -604,7 +604,7 @@ __global__ __launch_bounds__(256) void finalize_vjp_kernel(
   if (threadIdx.x == 0) {
     const float l_se = runM[row] + logf(S);
     if (lse) lse[row] = l_se;
-    if (loss) loss[row] = valid ? l_se - zt : 0.f;
+    if (loss) loss[row] = valid ? l_se - zt[row] : 0.f;  // target logit from rms_forward
     if (argmax) argmax[row] = runA[row];
     if (!valid && bad) atomicAdd(bad, 1);
   }
@@ -629,7 +629,7 @@ static hipError_t run_output_error(const OeLaunch& a) {
   T* P = (T*)a.P;
   FPO_LAUNCH("rms_forward", st,
              rms_forward_kernel<T><<<dim3((unsigned)a.T), dim3(256), 0, st>>>(
-      x, gamma, (int)a.d, a.eps, y, W, a.targets, (int)a.V, a.ref, a.bad_targets));
+      x, gamma, (int)a.d, a.eps, y, W, a.targets, (int)a.V, a.ref, a.zt, a.bad_targets));
   FPO_CHECK_LAUNCH();
   const int gm = (int)((a.T + TT::BM - 1) / TT::BM);
   for (int c = 0; c < a.nchunk; ++c) {
@@ -673,7 +673,7 @@ static hipError_t run_output_error(const OeLaunch& a) {
   }
   FPO_LAUNCH("finalize_vjp", st,
              finalize_vjp_kernel<T><<<dim3((unsigned)a.T), dim3(256), 0, st>>>(
-      (int)a.d, (int)a.V, a.nsplit, a.T * a.d, a.G, a.runM, a.runS, a.runA, y, a.targets, W,
+      (int)a.d, (int)a.V, a.nsplit, a.T * a.d, a.G, a.runM, a.runS, a.runA, a.zt, a.targets, W,
       x, gamma, a.eps, a.min_rms, a.g_tilde, (T*)a.g_tilde_lp, a.g_pre, a.lse, a.loss, a.argmax,
       a.bad_targets));
   FPO_CHECK_LAUNCH();

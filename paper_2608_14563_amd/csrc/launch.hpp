@@ -48,6 +48,7 @@ struct OeLaunch {
   float* fout;   // [T] exp(Ref - M_new) of the current chunk
   float* alpha;  // [T] exp(M_old - M_new)
   float* ref;    // [T] staging reference of the current chunk
+  float* zt;     // [T] target logit <y_t, W_U[y_t]> (from the stored y)
   float* runM;
   float* runS;
   int32_t* runA;

@@ -141,7 +141,9 @@ def test_staged_p_pitch_padding_and_band(lib):
     T, d, V, ns = 2048, 4096, 100352, 2
     vc = 26624
     nb = vc // 128
-    want = (a256(T * d * 2) + a256(T * (vc + 128) * 2) + 3 * a256(T * nb * 4) + 6 * a256(T * 4)
+    # y, p~, block max / sum / argmax, seven per-token arrays (output factors, staging reference,
+    # target logit, running max / partition / argmax), the projection's split accumulators
+    want = (a256(T * d * 2) + a256(T * (vc + 128) * 2) + 3 * a256(T * nb * 4) + 7 * a256(T * 4)
             + a256(ns * T * d * 4))
     assert lib.fpo_output_error_workspace(C.byref(oe(T=T, d=d, V=V))) == want
     T, V = 8192, 131072
