@@ -74,3 +74,60 @@ def test_step_graph_replays_match_eager(dev, variant):
                 assert torch.equal(a, b), (key, k)
         for key in ("Wsq", "ss", "g", "glp"):
             assert torch.equal(eager[key], graphed[key]), (key, k)
+
+
+def test_full_mlp_step_graph_replays_match_eager(dev):
+    """The full-MLP step with the overlapped optimizer (each of the 3 L
+    matrices' norm and update released on the side stream after its outer
+    products) replays from a graph bit-identically to eager execution."""
+    c = I.CONFIGS[1].shrink(T=256, d=256, d_ff=512, V=4104, L=2)
+    x, gam, WU, y = (dev_tensor(a, dev) for a in (I.hidden(c), I.gain(c), I.unembedding(c), I.targets(c)))
+    caches = [I.mlp_cache(c, l) for l in range(c.L)]
+    extras = [I.full_mlp_extra(c, l) for l in range(c.L)]
+    acts = [dev_tensor(cc[2], dev) for cc in caches]
+    W0 = [torch.from_numpy(I.master_weight(c, l)).to(dev) for l in range(c.L)]
+    W0 += [torch.from_numpy(e[1]).to(dev) for e in extras] + [torch.from_numpy(e[2]).to(dev) for e in extras]
+    fkw = dict(W3_init=[w.to(torch.bfloat16) for w in W0[:c.L]], gate=[dev_tensor(cc[0], dev) for cc in caches],
+               up=[dev_tensor(cc[1], dev) for cc in caches], x_in=[dev_tensor(e[0], dev) for e in extras])
+    n = 3 * c.L
+
+    def state():
+        W = [w.clone() for w in W0]
+        return dict(W=W, s1=[torch.zeros_like(w) for w in W],
+                    lp=[torch.empty(w.shape, dtype=torch.bfloat16, device=dev) for w in W],
+                    Wsq=torch.tensor([float((w.double() ** 2).sum()) for w in W], dtype=torch.float64, device=dev),
+                    ss=torch.empty(n, dtype=torch.float64, device=dev),
+                    dW3=[torch.empty(c.d, c.d_ff, device=dev) for _ in range(c.L)],
+                    dW1=[torch.empty(c.d_ff, c.d, device=dev) for _ in range(c.L)],
+                    dW2=[torch.empty(c.d_ff, c.d, device=dev) for _ in range(c.L)],
+                    g=torch.empty(c.T, c.d, device=dev), glp=torch.empty(c.T, c.d, dtype=torch.bfloat16, device=dev),
+                    ws_oe=api.workspace(api.fpo_output_error_workspace(c.T, c.d, c.V, torch.bfloat16), dev),
+                    ws_pg=api.workspace(api.fpo_pseudograd_workspace(c.T, c.d, c.d_ff, c.L, torch.bfloat16,
+                                                                     full_mlp=True), dev))
+
+    def step(s, k):
+        api.fpo_output_error(x, gam, WU, y, s["g"], s["glp"], ws=s["ws_oe"])
+        api.fpo_pseudograd(s["glp"], acts, dW3=s["dW3"], dW1=s["dW1"], dW2=s["dW2"], sumsq=s["ss"], ws=s["ws_pg"],
+                           opt=api.OptConfig(kind=0, lr=1e-2, clip_frac=0.01, step=k),
+                           W_master=s["W"], W_lp=s["lp"], state1=s["s1"], W_sumsq=s["Wsq"], **fkw)
+
+    eager, graphed = state(), state()
+    for k in (1, 2):
+        step(eager, k)
+        step(graphed, k)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=torch.cuda.Stream()):
+        step(graphed, 3)  # recorded, not run
+    torch.cuda.synchronize()
+    for k in (3, 4, 5):
+        step(eager, k)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        x.add_(0)  # the program's own eager work between replays
+        for key in ("W", "s1", "lp", "dW3", "dW1", "dW2"):
+            for i, (a, b) in enumerate(zip(eager[key], graphed[key])):
+                assert torch.equal(a, b), (key, i, k)
+        for key in ("Wsq", "ss", "g", "glp"):
+            assert torch.equal(eager[key], graphed[key]), (key, k)
