@@ -252,12 +252,11 @@ __global__ __launch_bounds__(256, 1) void outer_kernel(OuterArgs args, int M, in
   using T = typename E::T;
   __shared__ double red[12];
   // one flat grid over (matrix, tile), matrix-major in dispatch order, each
-  // matrix's tiles spread over the 8 XCDs (a contiguous group per XCD): every
-  // XCD works on the same matrix at the same time, so the matrix's operand
-  // panels are fetched into the Infinity Cache once for all of them. (A
-  // contiguous range of the whole flat grid per XCD put eight different
-  // matrices in flight: 83 GB fetched for 14.5 GB of operands in the
-  // 36-layer diagnostic launch.)
+  // matrix's tiles spread over the 8 XCDs (a contiguous group per XCD), so
+  // that the XCDs tend to work on the same matrix at the same time rather
+  // than on eight different ones (how closely depends on dispatch timing: the
+  // 36-layer diagnostic launch reads 65-91 GB beyond L2 from run to run, for
+  // 14.5 GB of operands, which the Infinity Cache serves)
   const int ntm = (M + TT::BM - 1) / TT::BM, ntn = (N + TT::BN - 1) / TT::BN;
   const int ntiles = ntm * ntn;
   const int mat = blockIdx.x / ntiles;
