@@ -7,8 +7,12 @@
 //
 // Why these shapes (measured on MI355X with random bf16 operands, where the
 // chip runs at its power limit and the clock, not the issue rate, decides):
-//  * 32x32x16 sustains ~70% of the bf16 peak in a pure MFMA loop, 16x16x32
-//    ~64%;
+//  * in a pure MFMA loop over random operands 16x16x32 costs less power per
+//    flop (~80% of the bf16 peak at ~1.95 GHz against ~71% at ~1.74 GHz for
+//    32x32x16), but a 16x16x32 version of this core (same ring, tiles and
+//    copies) turned the higher clock into no speed: its MFMA pipe sat idle
+//    more of the time (twice the instructions to issue per flop from the one
+//    wave each SIMD holds), so the core keeps the larger instruction;
 //  * a 64-deep K stage makes every copy of a K-contiguous row a full 128-byte
 //    line: at 32 deep each row gave a half line, twice the L2 requests for the
 //    same bytes, and the extra request traffic cost ~25% of the clock.
