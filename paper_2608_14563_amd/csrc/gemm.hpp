@@ -1,22 +1,20 @@
-// MFMA tile core for the three contractions of the FPO hot path on gfx950:
-// the logits Y W_U^T, the projection P W_U and the per-layer outer product
-// g~^T a. One workgroup of 4 waves (2 x 2) computes a BM x BN tile of
-// C = A B with A stored K-contiguous ([M][K] row-major) and B stored either
-// K-contiguous ([N][K], "Bt") or N-contiguous ([K][N]).
-//
-// bf16 operands use v_mfma_f32_16x16x32_bf16 on a 256 x 256 x 64 tile (each
-// wave 128 x 128 = 8 x 8 MFMA blocks); fp32 operands use
-// v_mfma_f32_16x16x4_f32 on a 128 x 128 x 32 tile (each wave 64 x 64), exact
-// fp32 products with fp32 accumulation.
+// fp32 MFMA tile core for the three contractions of the FPO hot path on
+// gfx950 (the logits Y W_U^T, the projection P W_U and the per-layer outer
+// product g~^T a) when the operands are fp32: one workgroup of 4 waves (2 x 2)
+// computes a 128 x 128 tile of C = A B with v_mfma_f32_16x16x4_f32 (exact
+// fp32 products, fp32 accumulation), A stored K-contiguous ([M][K]
+// row-major) and B either K-contiguous ([N][K], "Bt") or N-contiguous
+// ([K][N]); 32-deep K tiles, register-staged double buffering. bf16 operands
+// run on the LDS-DMA core of gemm2.hpp; TileBF16 here only carries their tile
+// constants.
 //
 // Lane layout. Within one 32-wide K step every lane l owns the eight K
-// indices 8*(l>>4) + s, s = 0..7, for both operands (the K order inside an
-// MFMA is a summation order only). Output columns are interleaved: the lane
+// indices 8*(l>>4) + s, s = 0..7, for both operands (the K order inside the
+// sum is a summation order only). Output columns are interleaved: the lane
 // owns columns FN*(l&15) + i, i = 0..FN-1, of its wave's tile, so that its
 // FN accumulator blocks hold FN consecutive output columns (16-byte epilogue
 // stores) and an N-contiguous B tile is read with one 16-byte LDS load per K
-// row. For bf16 the eight K rows are then packed pairwise with v_perm into
-// the MFMA's B registers; no LDS transpose is needed.
+// row.
 //
 // Accumulator acc[f][i][r] holds C[row, col] with
 //   row = m0 + wm*WTM + 16*f + 4*(l>>4) + r,  col = n0 + wn*WTN + FN*(l&15) + i.
@@ -139,59 +137,6 @@ struct TileLoader {
 };
 
 // ---------------------------------------------------------------- compute
-// Pack K rows (2j, 2j+1) of column i from eight 16-byte bf16 rows.
-__device__ __forceinline__ uint32_t pair_col(uint32_t w_even, uint32_t w_odd, int i) {
-  // v_perm: (w_odd.half << 16) | w_even.half, half = i & 1
-  return (i & 1) ? __builtin_amdgcn_perm(w_odd, w_even, 0x07060302u)
-                 : __builtin_amdgcn_perm(w_odd, w_even, 0x05040100u);
-}
-
-template <bool BNC>
-__device__ __forceinline__ void mma_tile_bf16(const u32x4* __restrict__ sa,
-                                              const u32x4* __restrict__ sb,
-                                              f32x4 (&acc)[8][8], int wm, int wn) {
-  using TT = Tile<TileBF16>;
-  const int l = threadIdx.x & 63;
-  const int lr = l & 15, lg = l >> 4;
-#pragma unroll
-  for (int ks = 0; ks < TT::KSTEPS; ++ks) {
-    u32x4 af[8];
-#pragma unroll
-    for (int f = 0; f < 8; ++f) {
-      const int row = wm * TT::WTM + 16 * f + lr;
-      af[f] = sa[row * 8 + ((ks * 4 + lg) ^ swz(row))];
-    }
-    u32x4 bo[8];
-    if constexpr (BNC) {
-      u32x4 raw[8];
-#pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const int k = ks * 32 + 8 * lg + s;
-        raw[s] = sb[k * 32 + wn * (TT::WTN / 8) + lr];
-      }
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int w = i >> 1;
-        bo[i] = u32x4{pair_col(raw[0][w], raw[1][w], i), pair_col(raw[2][w], raw[3][w], i),
-                      pair_col(raw[4][w], raw[5][w], i), pair_col(raw[6][w], raw[7][w], i)};
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int row = wn * TT::WTN + 8 * lr + i;
-        bo[i] = sb[row * 8 + ((ks * 4 + lg) ^ swz(row))];
-      }
-    }
-#pragma unroll
-    for (int f = 0; f < 8; ++f)
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-        acc[f][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, af[f]),
-                                                            __builtin_bit_cast(bf16x8, bo[i]),
-                                                            acc[f][i], 0, 0, 0);
-  }
-}
-
 template <bool BNC>
 __device__ __forceinline__ void mma_tile_f32(const u32x4* __restrict__ sa,
                                              const u32x4* __restrict__ sb,
@@ -246,10 +191,8 @@ __device__ __forceinline__ void mma_tile_f32(const u32x4* __restrict__ sa,
 template <class E, bool BNC>
 __device__ __forceinline__ void mma_tile(const u32x4* sa, const u32x4* sb,
                                          f32x4 (&acc)[E::FM][E::FN], int wm, int wn) {
-  if constexpr (E::EPC == 8)
-    mma_tile_bf16<BNC>(sa, sb, acc, wm, wn);
-  else
-    mma_tile_f32<BNC>(sa, sb, acc, wm, wn);
+  static_assert(E::EPC == 4, "this core computes fp32 tiles only");
+  mma_tile_f32<BNC>(sa, sb, acc, wm, wn);
 }
 
 struct NoHook {
