@@ -7,8 +7,8 @@
 //                  next chunk's reference R_t <- running max; the rare rows
 //                  with a block far above R_t rescaled in place
 //   proj_chunk   : G_s <- rescale(G_s) + p~ W_c (MFMA), one partial per split
-//   finalize_vjp : g = sum_s G_s / S - W_U[y], the target logit, the clamped
-//                  RMSNorm VJP                                         (HBM bound)
+//   finalize_vjp : g = sum_s G_s / S - W_U[y], the loss (from rms_forward's
+//                  target logit), the clamped RMSNorm VJP              (HBM bound)
 // The T x V logits are never stored: only one vocabulary chunk of p~ (bf16,
 // at most 2^26 entries by default, so it stays in the 256 MB Infinity Cache)
 // is staged between the logits and projection launches of that chunk.
